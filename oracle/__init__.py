@@ -1,0 +1,310 @@
+"""CPU oracle for the Ozaki Scheme II emulated DGEMM -- TEST INFRASTRUCTURE.
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg may use
+this package.  It shares no code with the HIP library: the arithmetic lives in
+``ozaki_oracle.c`` (plain scalar C, exact integer arithmetic, one IEEE
+rounding), built with gcc into ``liboracle.so`` next to it; this module only
+marshals numpy arrays into it and chains its steps in the paper's order
+(Eq. (scale) -> Eq. (residueprod) -> Eq. (pieces)/Lemma 1 -> Eq. (garner),
+Eq. (horner) -> single rounding).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "ozaki_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+R = 12
+NPLANES = 30
+NONFINITE = -(2 ** 31)
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (plain -O2, single thread)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-std=gnu11", "-shared", "-fPIC", "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        L = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        i64, i32 = ctypes.c_int64, ctypes.c_int32
+        L.oracle_scale_bits.argtypes = [i64]
+        L.oracle_scale_bits.restype = ctypes.c_int
+        L.oracle_modulus.argtypes = [ctypes.c_int]
+        L.oracle_modulus.restype = i64
+        L.oracle_planes_of.argtypes = [ctypes.c_int]
+        L.oracle_plane_base.argtypes = [ctypes.c_int]
+        L.oracle_product_of_moduli.argtypes = [P, P]
+        L.oracle_exponents.argtypes = [i64, i64, P, i64, i64, ctypes.c_int, P]
+        L.oracle_quantise.argtypes = [ctypes.c_double, i32]
+        L.oracle_quantise.restype = i64
+        L.oracle_quantise_vectors.argtypes = [i64, i64, P, i64, i64, P, P]
+        L.oracle_centred_mod.argtypes = [i64, i64]
+        L.oracle_centred_mod.restype = i64
+        L.oracle_residues.argtypes = [i64, i64, P, P]
+        L.oracle_in_e4m3.argtypes = [i64]
+        L.oracle_limbs.argtypes = [ctypes.c_int, i64, P]
+        L.oracle_split16.argtypes = [i64, P]
+        L.oracle_limb_product_table.argtypes = [ctypes.c_int, P]
+        L.oracle_limb_product.argtypes = [ctypes.c_int, P, P]
+        L.oracle_limb_product.restype = i64
+        L.oracle_planes.argtypes = [i64, i64, i64, P, P]
+        L.oracle_residue_gemm.argtypes = [i64, i64, i64, P, P, P]
+        L.oracle_garner_constants.argtypes = [P]
+        L.oracle_garner.argtypes = [i64, i64, P, P, P]
+        L.oracle_exact_product.argtypes = [i64, i64, i64, P, P, P, P]
+        L.oracle_round_scaled.argtypes = [i64, ctypes.c_uint64, ctypes.c_int]
+        L.oracle_round_scaled.restype = ctypes.c_double
+        L.oracle_reconstruct.argtypes = [i64, i64, P, P, P, P, ctypes.c_int, P, i64]
+        _lib = L
+    return _lib
+
+
+def _p(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+# ---------------------------------------------------------------- constants
+def moduli() -> list[int]:
+    return [int(lib().oracle_modulus(i)) for i in range(R)]
+
+
+def planes_of(i: int) -> int:
+    return int(lib().oracle_planes_of(i))
+
+
+def plane_base(i: int) -> int:
+    return int(lib().oracle_plane_base(i))
+
+
+def product_of_moduli() -> int:
+    hi = np.zeros(1, np.uint64)
+    lo = np.zeros(1, np.uint64)
+    lib().oracle_product_of_moduli(_p(hi), _p(lo))
+    return (int(hi[0]) << 64) | int(lo[0])
+
+
+def scale_bits(k: int) -> int:
+    return int(lib().oracle_scale_bits(k))
+
+
+def garner_constants() -> list[int]:
+    w = np.zeros(R, np.int64)
+    lib().oracle_garner_constants(_p(w))
+    return [int(x) for x in w]
+
+
+def k_pad(k: int) -> int:
+    return (k + 63) // 64 * 64
+
+
+# ---------------------------------------------------------------- scalars
+def centred_mod(z: int, x: int) -> int:
+    return int(lib().oracle_centred_mod(z, x))
+
+
+def in_e4m3(v: int) -> bool:
+    return bool(lib().oracle_in_e4m3(v))
+
+
+def limbs(i: int, d: int) -> list[int]:
+    out = np.zeros(3, np.int8)
+    n = lib().oracle_limbs(i, d, _p(out))
+    return [int(x) for x in out[:n]]
+
+
+def limb_product(i: int, dl, el) -> int:
+    a = np.zeros(3, np.int8)
+    b = np.zeros(3, np.int8)
+    a[: len(dl)] = dl
+    b[: len(el)] = el
+    return int(lib().oracle_limb_product(i, _p(a), _p(b)))
+
+
+def split16(d: int) -> list[int]:
+    out = np.zeros(3, np.int64)
+    lib().oracle_split16(d, _p(out))
+    return [int(x) for x in out]
+
+
+def limb_product_table(i: int) -> np.ndarray:
+    m = moduli()[i]
+    out = np.zeros((m, m), np.int32)
+    lib().oracle_limb_product_table(i, _p(out))
+    return out
+
+
+def quantise(x: float, sigma: int) -> int:
+    return int(lib().oracle_quantise(x, sigma))
+
+
+def round_scaled(X: int, e: int) -> float:
+    hi = X >> 64
+    lo = X & ((1 << 64) - 1)
+    return float(lib().oracle_round_scaled(hi, lo, e))
+
+
+# ---------------------------------------------------------------- vectors
+def _vec_view(X: np.ndarray, side: int):
+    """(nvec, k, sv, sk) element strides for A rows (side 0) or B columns (1)."""
+    X = np.ascontiguousarray(X, dtype=np.float64)
+    if side == 0:
+        nvec, k = X.shape
+        return X, nvec, k, X.strides[0] // 8, 1
+    k, nvec = X.shape
+    return X, nvec, k, 1, X.strides[0] // 8
+
+
+def exponents(X: np.ndarray, side: int, t: int) -> np.ndarray:
+    """sigma (side 0: rows of A) or tau (side 1: columns of B)."""
+    X, nvec, k, sv, sk = _vec_view(X, side)
+    out = np.zeros(nvec, np.int32)
+    lib().oracle_exponents(nvec, k, _p(X), sv, sk, t, _p(out))
+    return out
+
+
+def quantise_vectors(X: np.ndarray, side: int, exps: np.ndarray) -> np.ndarray:
+    """Z[v][l]: the scaled, rounded integers of each row of A / column of B."""
+    X, nvec, k, sv, sk = _vec_view(X, side)
+    exps = np.ascontiguousarray(exps, dtype=np.int32)
+    Z = np.zeros((nvec, k), np.int64)
+    lib().oracle_quantise_vectors(nvec, k, _p(X), sv, sk, _p(exps), _p(Z))
+    return Z
+
+
+def residues(Z: np.ndarray) -> np.ndarray:
+    Z = np.ascontiguousarray(Z, dtype=np.int64)
+    nvec, k = Z.shape
+    out = np.zeros((R, nvec, k), np.int16)
+    lib().oracle_residues(nvec, k, _p(Z), _p(out))
+    return out
+
+
+def planes(Z: np.ndarray, kp: int | None = None) -> np.ndarray:
+    Z = np.ascontiguousarray(Z, dtype=np.int64)
+    nvec, k = Z.shape
+    kp = k_pad(k) if kp is None else kp
+    out = np.zeros((NPLANES, nvec, kp), np.int8)
+    lib().oracle_planes(nvec, k, kp, _p(Z), _p(out))
+    return out
+
+
+def residue_gemm(resA: np.ndarray, resB: np.ndarray) -> np.ndarray:
+    resA = np.ascontiguousarray(resA, dtype=np.int16)
+    resB = np.ascontiguousarray(resB, dtype=np.int16)
+    _, m, k = resA.shape
+    _, n, k2 = resB.shape
+    assert k == k2
+    C = np.zeros((R, m, n), np.int32)
+    lib().oracle_residue_gemm(m, n, k, _p(resA), _p(resB), _p(C))
+    return C
+
+
+def garner(Cres: np.ndarray):
+    """Returns (Xhi int64, Xlo uint64) of the reconstructed integers."""
+    Cres = np.ascontiguousarray(Cres, dtype=np.int32)
+    _, m, n = Cres.shape
+    hi = np.zeros((m, n), np.int64)
+    lo = np.zeros((m, n), np.uint64)
+    lib().oracle_garner(m, n, _p(Cres), _p(hi), _p(lo))
+    return hi, lo
+
+
+def exact_product(ZA: np.ndarray, ZB: np.ndarray):
+    ZA = np.ascontiguousarray(ZA, dtype=np.int64)
+    ZB = np.ascontiguousarray(ZB, dtype=np.int64)
+    m, k = ZA.shape
+    n, _ = ZB.shape
+    hi = np.zeros((m, n), np.int64)
+    lo = np.zeros((m, n), np.uint64)
+    lib().oracle_exact_product(m, n, k, _p(ZA), _p(ZB), _p(hi), _p(lo))
+    return hi, lo
+
+
+def reconstruct(Xhi, Xlo, expsA, expsB, C_in: np.ndarray | None = None) -> np.ndarray:
+    Xhi = np.ascontiguousarray(Xhi, dtype=np.int64)
+    Xlo = np.ascontiguousarray(Xlo, dtype=np.uint64)
+    expsA = np.ascontiguousarray(expsA, dtype=np.int32)
+    expsB = np.ascontiguousarray(expsB, dtype=np.int32)
+    m, n = Xhi.shape
+    if C_in is None:
+        C = np.zeros((m, n), np.float64)
+        sub = 0
+    else:
+        C = np.array(C_in, dtype=np.float64, copy=True, order="C")
+        sub = 1
+    lib().oracle_reconstruct(m, n, _p(Xhi), _p(Xlo), _p(expsA), _p(expsB), sub, _p(C), n)
+    return C
+
+
+def to_int(hi, lo) -> np.ndarray:
+    """Object array of Python ints from (hi, lo) words."""
+    hi = np.asarray(hi)
+    lo = np.asarray(lo)
+    out = np.empty(hi.shape, dtype=object)
+    for idx in np.ndindex(hi.shape):
+        out[idx] = (int(hi[idx]) << 64) | int(lo[idx])
+    return out
+
+
+# ---------------------------------------------------------------- pipeline
+class Result:
+    """Every intermediate of one oracle run (for parity on each stage)."""
+
+    def __init__(self, **kw):
+        self.__dict__.update(kw)
+
+
+def dgemm(A: np.ndarray, B: np.ndarray, C_in: np.ndarray | None = None,
+          rows=None, cols=None, want_planes: bool = True, check_exact: bool = True) -> Result:
+    """Oracle emulated DGEMM on the full k, for all outputs or for the sampled
+    rows of A and columns of B (each output depends only on its row and
+    column).  Steps in the order of Alg. 1: exponent scan, quantise, residues
+    and limbs, per-modulus products, Garner, single rounding.  With
+    ``check_exact`` the CRT result is compared with the direct integer
+    product (they must be equal, since |A'B'| < M/2)."""
+    m, k = A.shape
+    k2, n = B.shape
+    assert k == k2
+    rows = np.arange(m) if rows is None else np.asarray(rows)
+    cols = np.arange(n) if cols is None else np.asarray(cols)
+    t = scale_bits(k)
+    As = np.ascontiguousarray(A[rows])
+    Bs = np.ascontiguousarray(B[:, cols])
+    sigma = exponents(As, 0, t)
+    tau = exponents(Bs, 1, t)
+    ZA = quantise_vectors(As, 0, sigma)
+    ZB = quantise_vectors(Bs, 1, tau)
+    resA = residues(ZA)
+    resB = residues(ZB)
+    Cres = residue_gemm(resA, resB)
+    Xhi, Xlo = garner(Cres)
+    if check_exact:
+        Ehi, Elo = exact_product(ZA, ZB)
+        if not (np.array_equal(Ehi, Xhi) and np.array_equal(Elo, Xlo)):
+            raise AssertionError("oracle: CRT reconstruction differs from the exact integer product")
+    Cs = None if C_in is None else np.ascontiguousarray(C_in[np.ix_(rows, cols)])
+    C = reconstruct(Xhi, Xlo, sigma, tau, Cs)
+    r = Result(t=t, sigma=sigma, tau=tau, ZA=ZA, ZB=ZB, Cres=Cres, Xhi=Xhi, Xlo=Xlo, C=C,
+               rows=rows, cols=cols)
+    if want_planes:
+        r.planesA = planes(ZA)
+        r.planesB = planes(ZB)
+    return r

@@ -1,0 +1,359 @@
+/*
+ * CPU oracle for the Ozaki Scheme II emulated DGEMM (round-to-nearest variant,
+ * published twelve-modulus set).  TEST INFRASTRUCTURE ONLY: the tests, the
+ * smoke check and the benchmark's CPU-baseline leg call it; the product path
+ * never does.  It shares no code, header, table or constant generator with the
+ * HIP library: every constant below is derived here from the moduli.
+ *
+ * Plain, slow, obviously correct: scalar loops, int64/__int128 exact integer
+ * arithmetic and one IEEE rounding at the end.  Each function names the
+ * passage of the paper it writes out.
+ *
+ *  - Eq. (scale): per-row (A) / per-column (B) power-of-two scaling and the
+ *    integer quantiser (round to nearest, ties to even).
+ *  - Eq. (moduli): the residue system, M > 2 mu with mu = k 2^{2t}.
+ *  - Eq. (residueprod) and the centred residue convention [-x/2, x/2).
+ *  - Eq. (pieces), the square-modulus two-plane split and Lemma 1 (the
+ *    carry-corrected three-plane layout for the nonsquare moduli).
+ *  - Eq. (garner) and Eq. (horner): mixed-radix reconstruction, symmetric
+ *    lift, single rounding.
+ *
+ * Pin status: every function here is checked in the CPU tests against the
+ * paper's worked values, closed forms or brute force with Python integers /
+ * fractions.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#define OR_R 12
+#define OR_NPLANES 30
+#define OR_NONFINITE INT32_MIN
+
+typedef __int128 i128;
+typedef unsigned __int128 u128;
+
+/* Published set S in its published order (Eq. (moduli)): six squares
+ * 33^2, 32^2, 31^2, 29^2, 25^2, 23^2, then six nonsquares. */
+static const int64_t OR_MODULI[OR_R] = {1089, 1024, 961, 841, 625, 529,
+                                        511,  509,  503, 499, 491, 487};
+
+/* Integer square root of m when m is a perfect square, else 0. */
+static int64_t or_square_root(int64_t m) {
+  for (int64_t s = 1; s * s <= m; ++s)
+    if (s * s == m) return s;
+  return 0;
+}
+
+int oracle_num_moduli(void) { return OR_R; }
+int oracle_num_planes(void) { return OR_NPLANES; }
+int64_t oracle_modulus(int i) { return OR_MODULI[i]; }
+int oracle_planes_of(int i) { return or_square_root(OR_MODULI[i]) ? 2 : 3; }
+
+/* M = prod m_i (Eq. (moduli)), returned as two 64-bit halves. */
+void oracle_product_of_moduli(uint64_t* hi, uint64_t* lo) {
+  u128 M = 1;
+  for (int i = 0; i < OR_R; ++i) M *= (u128)OR_MODULI[i];
+  *hi = (uint64_t)(M >> 64);
+  *lo = (uint64_t)M;
+}
+
+/* t(k): the largest t with k * 2^{2t} <= M/2 - 1, so that every entry of
+ * A'B' (bounded by k 2^{2t}, Eq. (moduli)) lies strictly inside the symmetric
+ * range [-M/2, M/2).  Returns -1 for k < 1. */
+int oracle_scale_bits(int64_t k) {
+  if (k < 1) return -1;
+  u128 M = 1;
+  for (int i = 0; i < OR_R; ++i) M *= (u128)OR_MODULI[i];
+  u128 q = (M / 2 - 1) / (u128)k; /* 2^{2t} <= q */
+  int t = 0;
+  while (((u128)1 << (2 * (t + 1))) <= q) ++t;
+  return t;
+}
+
+/* a1 (Eq. (scale) and the exponent scan of Alg. 1): for each of nvec vectors
+ * of length k, element l of vector v at X[v*sv + l*sk], the exponent e of the
+ * vector's largest magnitude in frexp form (max in [2^{e-1}, 2^e); e = 0 for
+ * an all-zero vector) gives sigma = t - e.  A vector holding a NaN or an
+ * infinity gets the sentinel INT32_MIN. */
+void oracle_exponents(int64_t nvec, int64_t k, const double* X, int64_t sv,
+                      int64_t sk, int t, int32_t* exps) {
+  for (int64_t v = 0; v < nvec; ++v) {
+    double mx = 0.0;
+    int nonfinite = 0;
+    for (int64_t l = 0; l < k; ++l) {
+      double x = X[v * sv + l * sk];
+      if (!isfinite(x)) nonfinite = 1;
+      else if (fabs(x) > mx) mx = fabs(x);
+    }
+    if (nonfinite) {
+      exps[v] = OR_NONFINITE;
+    } else {
+      int e = 0;
+      (void)frexp(mx, &e);
+      exps[v] = t - e;
+    }
+  }
+}
+
+/* a2 (Eq. (scale), round-to-nearest variant): z = RN_even(x * 2^sigma).  The
+ * power-of-two scaling is exact here (|x 2^sigma| < 2^t), so rint is the only
+ * rounding.  Rows flagged non-finite quantise to zero. */
+int64_t oracle_quantise(double x, int32_t sigma) {
+  if (sigma == OR_NONFINITE) return 0;
+  return (int64_t)rint(ldexp(x, sigma));
+}
+
+void oracle_quantise_vectors(int64_t nvec, int64_t k, const double* X, int64_t sv,
+                             int64_t sk, const int32_t* exps, int64_t* Z) {
+  for (int64_t v = 0; v < nvec; ++v)
+    for (int64_t l = 0; l < k; ++l)
+      Z[v * k + l] = oracle_quantise(X[v * sv + l * sk], exps[v]);
+}
+
+/* The centred residue convention: z mod x in [-x/2, x/2), for even x the
+ * endpoint -x/2 included and +x/2 excluded; for odd x the range
+ * [-(x-1)/2, (x-1)/2]. */
+int64_t oracle_centred_mod(int64_t z, int64_t x) {
+  int64_t r = z % x;
+  if (r < 0) r += x;           /* r in [0, x) */
+  if (r > (x - 1) / 2) r -= x; /* upper half wraps to the negative side */
+  return r;
+}
+
+/* a3 (Eq. (residueprod)): residues of quantised vectors, out[i][v][l]. */
+void oracle_residues(int64_t nvec, int64_t k, const int64_t* Z, int16_t* out) {
+  for (int i = 0; i < OR_R; ++i)
+    for (int64_t v = 0; v < nvec; ++v)
+      for (int64_t l = 0; l < k; ++l)
+        out[(i * nvec + v) * k + l] = (int16_t)oracle_centred_mod(Z[v * k + l], OR_MODULI[i]);
+}
+
+/* Membership in the e4m3 integer set: integers M 2^e with |M| <= 15 and
+ * magnitude at most 448 (Lemma 1's set).  Written as a direct search. */
+int oracle_in_e4m3(int64_t v) {
+  if (v < -448 || v > 448) return 0;
+  for (int64_t M = -15; M <= 15; ++M)
+    for (int e = 0; e <= 9; ++e)
+      if (M * ((int64_t)1 << e) == v) return 1;
+  return 0;
+}
+
+/* Lemma 1's rule on its own (it depends on d only, not on the modulus):
+ * canonical balanced base-16 split, then the one carry when d0 + d1 is not
+ * e4m3-exact.  out = (d0, d1, d0 + d1) as int64. */
+void oracle_split16(int64_t d, int64_t* out) {
+  int64_t d0 = oracle_centred_mod(d, 16);
+  int64_t d1 = (d - d0) / 16;
+  if (!oracle_in_e4m3(d0 + d1)) {
+    int64_t sg = (d0 > 0) - (d0 < 0);
+    d0 -= 16 * sg;
+    d1 += sg;
+  }
+  out[0] = d0;
+  out[1] = d1;
+  out[2] = d0 + d1;
+}
+
+/* a4: the stored limbs of one centred residue d modulo the i-th modulus.
+ *  - square m = s^2 (Eq. (pieces) with base s; d1 e1 vanishes mod s^2):
+ *    d0 is the balanced base-s digit (the centred residue of d mod s) and
+ *    d1 = (d - d0)/s; stored (d0, d1).
+ *  - nonsquare (Lemma 1): canonical balanced base-16 digit d0 in [-8, 7],
+ *    d1 = (d - d0)/16; if d0 + d1 is not e4m3-exact, move one unit of 16
+ *    between the limbs against the sign of d0; stored (d0, d1, d0 + d1).
+ * Returns the number of limbs written (2 or 3). */
+int oracle_limbs(int i, int64_t d, int8_t* out) {
+  int64_t m = OR_MODULI[i];
+  int64_t s = or_square_root(m);
+  if (s) {
+    int64_t d0 = oracle_centred_mod(d, s);
+    int64_t d1 = (d - d0) / s;
+    out[0] = (int8_t)d0;
+    out[1] = (int8_t)d1;
+    return 2;
+  }
+  int64_t l[3];
+  oracle_split16(d, l);
+  out[0] = (int8_t)l[0];
+  out[1] = (int8_t)l[1];
+  out[2] = (int8_t)l[2];
+  return 3;
+}
+
+/* Product of two residues from their limbs, following the epilogues the
+ * paper gives: square moduli d e = d0 e0 + s (d0 e1 + d1 e0) + s^2 d1 e1,
+ * whose last term vanishes mod s^2; nonsquare moduli Eq. (karcarry):
+ * d e = (1-16) d0 e0 + 16 (d0+d1)(e0+e1) + (16^2-16) d1 e1.  Returns the
+ * centred residue of the limb combination modulo m_i. */
+int64_t oracle_limb_product(int i, const int8_t* dl, const int8_t* el) {
+  int64_t m = OR_MODULI[i];
+  int64_t s = or_square_root(m);
+  int64_t v;
+  if (s)
+    v = (int64_t)dl[0] * el[0] + s * ((int64_t)dl[0] * el[1] + (int64_t)dl[1] * el[0]);
+  else
+    v = -15 * (int64_t)dl[0] * el[0] + 16 * (int64_t)dl[2] * el[2] + 240 * (int64_t)dl[1] * el[1];
+  return oracle_centred_mod(v, m);
+}
+
+/* The limb-product epilogue over every ordered pair of centred residues of
+ * modulus i: out[a * m + b] = oracle_limb_product(limbs(d_a), limbs(e_b))
+ * with d_a = a - floor(m/2), e_b = b - floor(m/2). */
+void oracle_limb_product_table(int i, int32_t* out) {
+  int64_t m = OR_MODULI[i];
+  int64_t lo = -(m / 2);
+  for (int64_t a = 0; a < m; ++a) {
+    int8_t dl[3] = {0, 0, 0};
+    oracle_limbs(i, lo + a, dl);
+    for (int64_t b = 0; b < m; ++b) {
+      int8_t el[3] = {0, 0, 0};
+      oracle_limbs(i, lo + b, el);
+      out[a * m + b] = (int32_t)oracle_limb_product(i, dl, el);
+    }
+  }
+}
+
+/* Index of the first stored plane of modulus i (2 per square, 3 per
+ * nonsquare, in the order of the set). */
+int oracle_plane_base(int i) {
+  int q = 0;
+  for (int j = 0; j < i; ++j) q += oracle_planes_of(j);
+  return q;
+}
+
+/* a2-a4 for whole vectors: planes[q][v][kp], kp >= k, zero padded. */
+void oracle_planes(int64_t nvec, int64_t k, int64_t kp, const int64_t* Z, int8_t* planes) {
+  memset(planes, 0, (size_t)OR_NPLANES * (size_t)nvec * (size_t)kp);
+  for (int i = 0; i < OR_R; ++i) {
+    int q0 = oracle_plane_base(i);
+    for (int64_t v = 0; v < nvec; ++v)
+      for (int64_t l = 0; l < k; ++l) {
+        int8_t limbs[3];
+        int np = oracle_limbs(i, oracle_centred_mod(Z[v * k + l], OR_MODULI[i]), limbs);
+        for (int p = 0; p < np; ++p) planes[((int64_t)(q0 + p) * nvec + v) * kp + l] = limbs[p];
+      }
+  }
+}
+
+/* a5 (Eq. (residueprod)): C^(i) = centred(sum_l d_il e_lj mod m_i) from the
+ * residues themselves (not the limbs), in plain int64 loops.  resA is
+ * [12][m][k] (rows of A), resB is [12][n][k] (columns of B), C is [12][m][n]. */
+void oracle_residue_gemm(int64_t m, int64_t n, int64_t k, const int16_t* resA,
+                         const int16_t* resB, int32_t* C) {
+  for (int i = 0; i < OR_R; ++i)
+    for (int64_t r = 0; r < m; ++r)
+      for (int64_t c = 0; c < n; ++c) {
+        const int16_t* a = resA + (i * m + r) * k;
+        const int16_t* b = resB + (i * n + c) * k;
+        int64_t acc = 0;
+        for (int64_t l = 0; l < k; ++l) acc += (int64_t)a[l] * b[l];
+        C[(i * m + r) * n + c] = (int32_t)oracle_centred_mod(acc, OR_MODULI[i]);
+      }
+}
+
+/* Modular inverse by the extended Euclidean algorithm (a, m coprime). */
+static int64_t or_inverse(int64_t a, int64_t m) {
+  int64_t r0 = m, r1 = ((a % m) + m) % m, t0 = 0, t1 = 1;
+  while (r1 != 0) {
+    int64_t q = r0 / r1, tmp;
+    tmp = r0 - q * r1; r0 = r1; r1 = tmp;
+    tmp = t0 - q * t1; t0 = t1; t1 = tmp;
+  }
+  return ((t0 % m) + m) % m;
+}
+
+/* Garner constants w_j = (m_1 ... m_{j-1})^{-1} mod m_j (Eq. (garner)). */
+void oracle_garner_constants(int64_t* w) {
+  w[0] = 1;
+  for (int j = 1; j < OR_R; ++j) {
+    int64_t p = 1;
+    for (int l = 0; l < j; ++l) p = (p * (OR_MODULI[l] % OR_MODULI[j])) % OR_MODULI[j];
+    w[j] = or_inverse(p, OR_MODULI[j]);
+  }
+}
+
+/* a6 (Eq. (garner), Eq. (horner) and the symmetric lift): the integer X in
+ * [-M/2, M/2) with X = c[i] (mod m_i) for all i.  Digits v_j in [0, m_j). */
+static i128 or_garner(const int64_t* c) {
+  int64_t w[OR_R], v[OR_R];
+  oracle_garner_constants(w);
+  u128 M = 1;
+  for (int i = 0; i < OR_R; ++i) M *= (u128)OR_MODULI[i];
+  for (int j = 0; j < OR_R; ++j) {
+    int64_t mj = OR_MODULI[j];
+    /* partial = v_1 + v_2 m_1 + ... + v_{j-1} m_1...m_{j-2} */
+    u128 partial = 0, radix = 1;
+    for (int l = 0; l < j; ++l) {
+      partial += (u128)v[l] * radix;
+      radix *= (u128)OR_MODULI[l];
+    }
+    int64_t cj = ((c[j] % mj) + mj) % mj;
+    int64_t pm = (int64_t)(partial % (u128)mj);
+    int64_t diff = ((cj - pm) % mj + mj) % mj;
+    v[j] = (diff * w[j]) % mj;
+  }
+  /* Horner: v_1 + m_1 (v_2 + m_2 (v_3 + ... + m_{r-1} v_r)) */
+  u128 X = (u128)v[OR_R - 1];
+  for (int j = OR_R - 2; j >= 0; --j) X = X * (u128)OR_MODULI[j] + (u128)v[j];
+  if (X >= M / 2) return (i128)X - (i128)M;
+  return (i128)X;
+}
+
+/* Garner over a block of outputs: Cres [12][m][n] -> X as (hi, lo) words of
+ * the two's-complement 128-bit value, X = hi * 2^64 + lo. */
+void oracle_garner(int64_t m, int64_t n, const int32_t* Cres, int64_t* Xhi, uint64_t* Xlo) {
+  for (int64_t e = 0; e < m * n; ++e) {
+    int64_t c[OR_R];
+    for (int i = 0; i < OR_R; ++i) c[i] = Cres[(int64_t)i * m * n + e];
+    i128 X = or_garner(c);
+    Xhi[e] = (int64_t)(X >> 64);
+    Xlo[e] = (uint64_t)X;
+  }
+}
+
+/* The exact integer product X = sum_l a'_il b'_lj directly (the quantity CRT
+ * reconstruction must reproduce).  ZA is [m][k], ZB is [n][k]. */
+void oracle_exact_product(int64_t m, int64_t n, int64_t k, const int64_t* ZA,
+                          const int64_t* ZB, int64_t* Xhi, uint64_t* Xlo) {
+  for (int64_t r = 0; r < m; ++r)
+    for (int64_t c = 0; c < n; ++c) {
+      i128 acc = 0;
+      for (int64_t l = 0; l < k; ++l) acc += (i128)ZA[r * k + l] * (i128)ZB[c * k + l];
+      Xhi[r * n + c] = (int64_t)(acc >> 64);
+      Xlo[r * n + c] = (uint64_t)acc;
+    }
+}
+
+/* Single rounding (Alg. 3, last step): RN_even(X * 2^e) for a signed integer
+ * X of at most 113 bits.  X converts exactly to binary128 (113-bit
+ * significand), the power-of-two scaling is exact in binary128's exponent
+ * range, and the conversion to double rounds once, to nearest even,
+ * including the subnormal and overflow ranges.  X = 0 gives +0.0. */
+double oracle_round_scaled(int64_t Xhi, uint64_t Xlo, int e) {
+  i128 X = (i128)(((u128)(uint64_t)Xhi << 64) | (u128)Xlo);
+  if (X == 0) return 0.0;
+  __float128 q = (__float128)X;
+  __float128 p = 1;
+  for (int i = 0; i < e; ++i) p *= 2;
+  for (int i = 0; i > e; --i) p /= 2;
+  return (double)(q * p);
+}
+
+/* Output element: C_ij = RN(X 2^{-sigma_i - tau_j}); NaN when row i of A or
+ * column j of B held a non-finite value.  With subtract, C_ij = C_ij - that
+ * (two roundings: the product is rounded, then the IEEE subtraction). */
+void oracle_reconstruct(int64_t m, int64_t n, const int64_t* Xhi, const uint64_t* Xlo,
+                        const int32_t* expsA, const int32_t* expsB, int subtract,
+                        double* C, int64_t ldc) {
+  for (int64_t r = 0; r < m; ++r)
+    for (int64_t c = 0; c < n; ++c) {
+      double v;
+      if (expsA[r] == OR_NONFINITE || expsB[c] == OR_NONFINITE)
+        v = NAN;
+      else
+        v = oracle_round_scaled(Xhi[r * n + c], Xlo[r * n + c], -expsA[r] - expsB[c]);
+      if (subtract) C[r * ldc + c] = C[r * ldc + c] - v;
+      else C[r * ldc + c] = v;
+    }
+}
