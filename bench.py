@@ -1,0 +1,222 @@
+#!/usr/bin/env python3
+"""Benchmark: emulated FP64 GEMM (Ozaki Scheme II, published 12-modulus set,
+round to nearest) on one MI355X, through the C ABI.
+
+One step = one full ozaki25_dgemm_ex call: exponent scans, deconstruction of
+both operands into int8 planes, the 36 int8-MFMA limb products with the
+modular epilogue, and the CRT reconstruction, on synthetic seeded inputs that
+are already resident in HBM.  Prints one JSON line.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload square]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import workloads  # noqa: E402
+
+# MI355X published peaks
+HBM_PEAK_GBS = 8000.0
+INT8_PEAK_TOPS = 5000.0
+FP64_PEAK_TFLOPS = 78.6
+PRODUCTS = 36               # 3 limb products for each of the 12 moduli
+PLANE_BYTES = 30            # stored int8 planes per element
+COUNTER_FILE = os.path.join(ROOT, "profiles", "residue_gemm_square_counters.txt")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2609_09095_amd", "csrc", "residue_gemm.hip")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def source_hash(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(w):
+    """HBM bytes per residue-GEMM launch from the committed rocprofv3 counter
+    summary, or None if it is absent, for another workload, or taken on an
+    older version of the kernel source."""
+    if not os.path.exists(COUNTER_FILE):
+        return None
+    kv = {}
+    with open(COUNTER_FILE) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                key, val = line.split(":", 1)
+                kv[key.strip()] = val.strip()
+    try:
+        if kv.get("workload") != w.name or kv.get("source_sha256_16") != source_hash(GEMM_SOURCE):
+            return None
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(A, B, w, rows, cols):
+    import oracle
+    oracle.build(force=False)
+    ridx = np.arange(rows)
+    cidx = np.arange(cols)
+    t0 = time.perf_counter()
+    oracle.dgemm(A, B, rows=ridx, cols=cidx, want_planes=False)
+    dt = time.perf_counter() - t0
+    flops = 2.0 * rows * cols * w.k
+    return {"value": flops / dt / 1e12, "unit": "TFLOPS", "cores": 1, "kind": "oracle",
+            "sample": f"{rows} rows of A x {cols} columns of B of the {w.name} workload, full k={w.k} "
+                      f"(exponent scan, quantise, residues, 12 int64 residue GEMMs, Garner, rounding, "
+                      f"exact-product check), {dt:.1f} s single-threaded"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="square", choices=sorted(workloads.WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-native", action="store_true")
+    ap.add_argument("--baseline-sample", type=int, default=512)
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the emulated DGEMM shards by output panels, but this build measures one GPU)",
+              file=sys.stderr)
+        return 2
+
+    import torch
+    import paper_2609_09095_amd as oz
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    oz.lib()
+
+    w = workloads.WORKLOADS[args.workload]
+    log(f"[bench] generating {w.name} inputs m={w.m} n={w.n} k={w.k} s={w.s}")
+    A, B, C0 = workloads.make_inputs(w)
+    dev = torch.device("cuda:0")
+    Ad = torch.from_numpy(A).to(dev)
+    Bd = torch.from_numpy(B).to(dev)
+    Cd = torch.from_numpy(C0).to(dev) if C0 is not None else torch.empty((w.m, w.n), dtype=torch.float64, device=dev)
+    ws = torch.empty(oz.ozaki25_dgemm_workspace_size(w.m, w.n, w.k), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+
+    def step(events=None):
+        oz.ozaki25_dgemm_ex(Ad, Bd, Cd, subtract=w.subtract, workspace=ws, stage_events=events)
+
+    log(f"[bench] warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(oz.NUM_STAGE_EVENTS)] for _ in range(args.steps)]
+    for row in ev:
+        for e in row:
+            e.record()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    log(f"[bench] timing {args.steps} steps")
+    start.record()
+    for i in range(args.steps):
+        step(ev[i])
+    end.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    ms = total_ms / args.steps
+    stage = np.array([[row[j].elapsed_time(row[j + 1]) for j in range(oz.NUM_STAGE_EVENTS - 1)] for row in ev])
+    scan_ms, dec_ms, gemm_ms, rec_ms = stage.mean(axis=0).tolist()
+    log(f"[bench] {ms:.3f} ms/step; scan {scan_ms:.3f} deconstruct {dec_ms:.3f} gemm {gemm_ms:.3f} "
+        f"reconstruct {rec_ms:.3f} ms")
+
+    tflops = w.flops / (ms * 1e-3) / 1e12
+    gemm_ops = 2.0 * PRODUCTS * w.m * w.n * w.k
+    gemm_tops = gemm_ops / (gemm_ms * 1e-3) / 1e12
+    elems = w.m * w.k + w.k * w.n
+    dec_bytes = elems * (8 + PLANE_BYTES)
+    scan_bytes = elems * 8
+    dec_gbs = dec_bytes / (dec_ms * 1e-3) / 1e9
+    stage_gbs = (dec_bytes + scan_bytes) / ((dec_ms + scan_ms) * 1e-3) / 1e9
+    rec_bytes = w.m * w.n * (12 * 2 + 8 + (8 if w.subtract else 0))
+    rec_gbs = rec_bytes / (rec_ms * 1e-3) / 1e9
+    roof = INT8_PEAK_TOPS / PRODUCTS
+
+    native = None
+    if not args.no_native and not w.subtract and w.m * w.n * w.k <= 8192 ** 3:
+        log("[bench] native FP64 matmul")
+        Cn = torch.matmul(Ad, Bd)
+        torch.cuda.synchronize()
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s0.record()
+        for _ in range(3):
+            torch.matmul(Ad, Bd, out=Cn)
+        s1.record()
+        torch.cuda.synchronize()
+        native = w.flops / (s0.elapsed_time(s1) / 3 * 1e-3) / 1e12
+        del Cn
+
+    traffic = measured_traffic(w)
+    result = {
+        "metric": "emulated FP64 TFLOPS (2mnk/s) + deconstruction GB/s vs HBM/MFMA roofs",
+        "value": round(tflops, 3),
+        "unit": "TFLOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int8",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: C {'-=' if w.subtract else '='} A.B, m={w.m} n={w.n} k={w.k}, "
+                               f"entries (U-0.5)exp({w.s} N), seed {w.seed}",
+                   "m": w.m, "n": w.n, "k": w.k, "moduli": "published 12-modulus set", "quantiser": "RN",
+                   "route": "int8 MFMA, i32 accumulate"},
+        "roofline": {"bound": "mfma", "kernel": "residue_gemm_kernel<int16>",
+                     "achieved": round(gemm_tops, 2), "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
+                     "frac": round(gemm_tops / INT8_PEAK_TOPS, 4),
+                     "traffic": traffic,
+                     "ops_per_launch": gemm_ops,
+                     "note": "int8 ops (1 MAC = 2 ops): 36 limb products x 2mnk per launch; peak is the dense int8 rate"},
+        "roofline_deconstruct": {"bound": "hbm", "kernel": "deconstruct_kernel<0>+<1>",
+                                 "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                 "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
+                                 "bytes_per_call": dec_bytes,
+                                 "stage_with_scan_gbs": round(stage_gbs, 1)},
+        "roofline_reconstruct": {"bound": "hbm", "achieved": round(rec_gbs, 1), "peak": HBM_PEAK_GBS,
+                                 "unit": "GB/s", "frac": round(rec_gbs / HBM_PEAK_GBS, 4)},
+        "stage_ms": {"scan": round(scan_ms, 4), "deconstruct": round(dec_ms, 4), "residue_gemm": round(gemm_ms, 4),
+                     "reconstruct": round(rec_ms, 4)},
+        "emulation_roof_tflops": round(roof, 2),
+        "emulation_roof_frac": round(tflops / roof, 4),
+        "native_fp64_tflops": round(native, 2) if native else None,
+        "native_fp64_peak_tflops": FP64_PEAK_TFLOPS,
+        "paper_context": "modelled Rubin projections (no measurement in the paper): 473 TFLOPS roof, 182-235 TFLOPS floors",
+    }
+    del Ad, Bd, Cd, ws
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        rows = min(args.baseline_sample, w.m)
+        cols = min(args.baseline_sample, w.n)
+        log(f"[bench] cpu baseline: oracle on {rows}x{cols} outputs")
+        result["cpu_baseline"] = cpu_baseline(A, B, w, rows, cols)
+    else:
+        result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

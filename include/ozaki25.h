@@ -1,0 +1,172 @@
+/*
+ * ozaki25.h -- emulated FP64 matrix multiplication by Ozaki Scheme II on the
+ * int8 matrix cores of an AMD Instinct MI355X (gfx950).
+ *
+ * The method (Ozaki Scheme II, Sec. 2 of "Ozaki 2.5: Engineering the
+ * Deconstruction Path of FP64-Emulated Dense Matrix Multiplication on FP8
+ * Tensor Cores"):
+ *   1. scale each row of A and each column of B by a power of two and round to
+ *      integers, A' = RN(diag(2^sigma) A), B' = RN(B diag(2^tau))   Eq. (scale)
+ *   2. reduce the integers to centred residues modulo the published twelve
+ *      moduli and split each residue into low-precision limbs      Eq. (residueprod),
+ *      Eq. (pieces), Lemma 1, Alg. 2
+ *   3. form the per-modulus products C^(i) = A^(i) B^(i) mod m_i    Eq. (residueprod)
+ *   4. recover A'B' by Garner's mixed-radix CRT, unscale and round once to
+ *      FP64                                                          Eq. (garner),
+ *      Eq. (horner), Alg. 3
+ *
+ * Conventions shared by every entry point:
+ *  - Matrices are row-major FP64.  A is m x k with leading dimension lda >= k,
+ *    B is k x n with ldb >= n, C is m x n with ldc >= n.
+ *  - Every data pointer is a DEVICE pointer (memory of the current HIP device).
+ *    The caller owns all memory; no entry point frees or keeps a pointer.
+ *  - `stream` is a hipStream_t passed as void* (NULL: the null stream).  Work is
+ *    enqueued asynchronously on it; nothing synchronises the host.
+ *  - Argument errors are detected synchronously, before anything is enqueued,
+ *    and nothing is written then.  No exception crosses this interface.
+ *  - Residues are centred: r in [-m/2, m/2), the endpoint -m/2 included for
+ *    even m (Sec. 2, the convention stated with Eq. (moduli)).
+ *  - Exponents: sigma_i = t(k) - e_i where e_i is the frexp exponent of
+ *    max_l |a_il| (max in [2^(e-1), 2^e); e = 0 for a zero row); likewise
+ *    tau_j for the columns of B.  A row or column holding a NaN or an infinity
+ *    gets OZAKI25_EXP_NONFINITE, its planes are zero and every output it
+ *    touches is NaN (the non-finite contract of the validation plan, Sec. 7).
+ *  - Rounding: the quantiser rounds to nearest, ties to even (the RN variant of
+ *    Eq. (scale)); the final rescale rounds once to nearest even, subnormal and
+ *    overflow ranges included; an exact zero gives +0.0.
+ */
+#ifndef OZAKI25_H
+#define OZAKI25_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  OZAKI25_SUCCESS = 0,
+  OZAKI25_ERR_INVALID_VALUE = 1, /* bad dimension, leading dimension, pointer or enum */
+  OZAKI25_ERR_UNSUPPORTED = 2,   /* k beyond OZAKI25_MAX_K */
+  OZAKI25_ERR_WORKSPACE = 3,     /* workspace too small, or its allocation failed */
+  OZAKI25_ERR_HIP = 4            /* a HIP launch or runtime call failed */
+} ozaki25_status;
+
+/* The modulus sets.  OZAKI25_MODULI_S12 is the published set of Eq. (moduli),
+ * in its published order: 1089, 1024, 961, 841, 625, 529 (squares of 33, 32,
+ * 31, 29, 25, 23), then 511, 509, 503, 499, 491, 487.  log2(prod) = 111.84. */
+typedef enum { OZAKI25_MODULI_S12 = 0 } ozaki25_moduli_set;
+
+#define OZAKI25_NUM_MODULI 12
+#define OZAKI25_NUM_PLANES 30          /* 2 per square modulus + 3 per nonsquare */
+#define OZAKI25_K_ALIGN 64             /* planes are zero padded to a multiple of this */
+#define OZAKI25_MAX_K 4194304          /* int32 limb accumulators: 22^2 * k < 2^31 */
+#define OZAKI25_EXP_NONFINITE INT32_MIN
+#define OZAKI25_NUM_STAGE_EVENTS 5     /* see ozaki25_dgemm_ex */
+
+/* Text for a status code (static storage, never NULL). */
+const char* ozaki25_status_string(ozaki25_status status);
+
+/* Number of moduli r of a set (12 for S12), or -1 for an unknown set. */
+int ozaki25_num_moduli(ozaki25_moduli_set set);
+
+/* Number of stored limb planes of a set (30 for S12), or -1. */
+int ozaki25_num_planes(ozaki25_moduli_set set);
+
+/* The i-th modulus of a set (0-based, published order), or -1. */
+int64_t ozaki25_modulus(ozaki25_moduli_set set, int i);
+
+/* t(k): the largest t with k 2^(2t) <= M/2 - 1 (M the product of the
+ * moduli), so that every entry of A'B' lies inside [-M/2, M/2) (Eq. (moduli):
+ * M > 2 mu with mu = k 2^(2t)).  Returns -1 for k < 1 or an unknown set. */
+int ozaki25_scale_bits(int64_t k, ozaki25_moduli_set set);
+
+/* k rounded up to OZAKI25_K_ALIGN (the plane row length k_pad); 0 for k <= 0. */
+int64_t ozaki25_k_pad(int64_t k);
+
+/* Bytes of the stored planes of `vecs` rows (or columns) of length k:
+ * num_planes * vecs * k_pad.  0 on invalid input. */
+size_t ozaki25_planes_bytes(int64_t vecs, int64_t k, ozaki25_moduli_set set);
+
+/* Deconstruction of one operand (Alg. 2 with the exponent scan of Alg. 1):
+ * exponent scan, scale, round to nearest, twelve centred residues and the
+ * limb split of Eq. (pieces) -- squares m = s^2: balanced base-s digits
+ * (d0, d1) with d0 the centred residue of d mod s; nonsquares: Lemma 1's
+ * carry-corrected base-16 layout (d0, d1, d0 + d1).
+ *  side 0: X is A (vecs x k, row-major, ldx >= k); vector v is row v.
+ *  side 1: X is B (k x vecs, row-major, ldx >= vecs); vector v is column v.
+ * Outputs (device, caller-allocated):
+ *  planes: int8 [num_planes][vecs][k_pad]; plane q of modulus i is at
+ *          q = (2 per earlier square + 3 per earlier nonsquare) + limb index;
+ *          entries with l >= k are zero.
+ *  exps:   int32 [vecs], sigma (side 0) or tau (side 1), or
+ *          OZAKI25_EXP_NONFINITE.
+ * vecs == 0 or k == 0 is a no-op.  Errors: INVALID_VALUE (side, sizes, null
+ * pointers with nonzero sizes, set), UNSUPPORTED (k > OZAKI25_MAX_K), HIP. */
+ozaki25_status ozaki25_deconstruct(int side, int64_t vecs, int64_t k, const double* X,
+                                   int64_t ldx, ozaki25_moduli_set set, int8_t* planes,
+                                   int32_t* exps, void* stream);
+
+/* Per-modulus products (Eq. (residueprod)) from stored planes, on int8 MFMA
+ * with int32 accumulation: for modulus i the limb products are combined with
+ * the square epilogue {1, s, s} (d1 e1 vanishes mod s^2) or Eq. (karcarry)'s
+ * {-15, 16, 240}, and reduced to the centred residue.
+ *  planesA: int8 [num_planes][m][k_pad] (side 0 of ozaki25_deconstruct)
+ *  planesB: int8 [num_planes][n][k_pad] (side 1)
+ *  Cres:    int32 [r][m][n], centred C^(i) (written, caller-allocated)
+ * m == 0 or n == 0 is a no-op; k == 0 writes zeros.  Errors as above. */
+ozaki25_status ozaki25_residue_gemm(int64_t m, int64_t n, int64_t k, const int8_t* planesA,
+                                    const int8_t* planesB, ozaki25_moduli_set set,
+                                    int32_t* Cres, void* stream);
+
+/* Reconstruction (Alg. 3, Eq. (garner), Eq. (horner)): Garner's mixed-radix
+ * digits of the r centred residues, the integer X in [-M/2, M/2), and
+ * C_ij = RN(X 2^(-sigma_i - tau_j)) rounded once; NaN where expsA[i] or
+ * expsB[j] is OZAKI25_EXP_NONFINITE.  With subtract != 0:
+ * C_ij <- C_ij - RN(X 2^(-sigma_i - tau_j)) (the product rounded, then the
+ * IEEE subtraction).
+ *  Cres: int32 [r][m][n]; expsA: int32 [m]; expsB: int32 [n]; C: m x n, ldc.
+ * m == 0 or n == 0 is a no-op. */
+ozaki25_status ozaki25_reconstruct(int64_t m, int64_t n, const int32_t* Cres,
+                                   const int32_t* expsA, const int32_t* expsB,
+                                   ozaki25_moduli_set set, double* C, int64_t ldc,
+                                   int subtract, void* stream);
+
+/* Device workspace that ozaki25_dgemm_ex needs for an m x n x k product. */
+size_t ozaki25_dgemm_workspace_size(int64_t m, int64_t n, int64_t k, ozaki25_moduli_set set);
+
+/* Emulated DGEMM C = A B (Alg. 1): both operands deconstructed once into
+ * planes in the workspace (storage mode M), the residue products, then the
+ * reconstruction.  The workspace is allocated and released stream-ordered on
+ * `stream` (hipMallocAsync / hipFreeAsync).  m == 0 or n == 0: no-op;
+ * k == 0: C = +0.  A and B must not overlap C.  Errors: INVALID_VALUE,
+ * UNSUPPORTED, WORKSPACE (allocation failed), HIP. */
+ozaki25_status ozaki25_dgemm(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
+                             const double* B, int64_t ldb, double* C, int64_t ldc,
+                             ozaki25_moduli_set set, void* stream);
+
+/* HPL trailing update C <- C - A B, same conventions (k == 0: C unchanged). */
+ozaki25_status ozaki25_dgemm_sub(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
+                                 const double* B, int64_t ldb, double* C, int64_t ldc,
+                                 ozaki25_moduli_set set, void* stream);
+
+/* Full form.  subtract: 0 for C = A B, 1 for C <- C - A B.
+ * workspace: NULL to allocate stream-ordered, else a device buffer of at least
+ *   ozaki25_dgemm_workspace_size() bytes (256-byte aligned), owned by the
+ *   caller and not used by anything else until the stream has passed this call.
+ * stage_events: NULL, or OZAKI25_NUM_STAGE_EVENTS hipEvent_t handles (passed as
+ *   void*) that are recorded on `stream` before the first kernel and after the
+ *   exponent scans, the deconstruction, the residue products and the
+ *   reconstruction, for per-stage timing. */
+ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
+                                const double* B, int64_t ldb, double* C, int64_t ldc,
+                                ozaki25_moduli_set set, int subtract, void* workspace,
+                                size_t workspace_bytes, void* const* stage_events,
+                                void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OZAKI25_H */

@@ -1,0 +1,249 @@
+"""MI355X-native emulated FP64 GEMM by Ozaki Scheme II on int8 MFMA.
+
+Python binding of ``libozaki25.so`` (the C ABI declared in
+``include/ozaki25.h``).  Argument marshalling only: every step of the
+computation runs in the library's HIP kernels.  PyTorch supplies device memory
+and the current stream.  The binding fails loudly when the library has not
+been built -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+__all__ = [
+    "Ozaki25Error", "lib", "library_path", "exported_symbols",
+    "ozaki25_status_string", "ozaki25_num_moduli", "ozaki25_num_planes", "ozaki25_modulus",
+    "ozaki25_scale_bits", "ozaki25_k_pad", "ozaki25_planes_bytes", "ozaki25_dgemm_workspace_size",
+    "ozaki25_deconstruct", "ozaki25_residue_gemm", "ozaki25_reconstruct",
+    "ozaki25_dgemm", "ozaki25_dgemm_sub", "ozaki25_dgemm_ex",
+]
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_PKG, "libozaki25.so")
+_HEADER = os.path.join(os.path.dirname(_PKG), "include", "ozaki25.h")
+
+S12 = 0
+NUM_MODULI = 12
+NUM_PLANES = 30
+K_ALIGN = 64
+MAX_K = 4194304
+EXP_NONFINITE = -(2 ** 31)
+NUM_STAGE_EVENTS = 5
+
+SUCCESS, ERR_INVALID_VALUE, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
+
+
+class Ozaki25Error(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {ozaki25_status_string(status)} (status {status})")
+        self.status = status
+
+
+_lib = None
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def lib():
+    """The loaded C library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise ImportError(f"{_LIB_PATH} is not built: run `python -m paper_2609_09095_amd.build`")
+        L = ctypes.CDLL(_LIB_PATH)
+        P, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t
+        sig = {
+            "ozaki25_status_string": ([i32], ctypes.c_char_p),
+            "ozaki25_num_moduli": ([i32], i32),
+            "ozaki25_num_planes": ([i32], i32),
+            "ozaki25_modulus": ([i32, i32], i64),
+            "ozaki25_scale_bits": ([i64, i32], i32),
+            "ozaki25_k_pad": ([i64], i64),
+            "ozaki25_planes_bytes": ([i64, i64, i32], sz),
+            "ozaki25_deconstruct": ([i32, i64, i64, P, i64, i32, P, P, P], i32),
+            "ozaki25_residue_gemm": ([i64, i64, i64, P, P, i32, P, P], i32),
+            "ozaki25_reconstruct": ([i64, i64, P, P, P, i32, P, i64, i32, P], i32),
+            "ozaki25_dgemm_workspace_size": ([i64, i64, i64, i32], sz),
+            "ozaki25_dgemm": ([i64, i64, i64, P, i64, P, i64, P, i64, i32, P], i32),
+            "ozaki25_dgemm_sub": ([i64, i64, i64, P, i64, P, i64, P, i64, i32, P], i32),
+            "ozaki25_dgemm_ex": ([i64, i64, i64, P, i64, P, i64, P, i64, i32, i32, P, sz, P, P], i32),
+        }
+        for name, (args, res) in sig.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = res
+        _lib = L
+    return _lib
+
+
+def exported_symbols() -> list[str]:
+    """Function names that include/ozaki25.h declares."""
+    with open(_HEADER) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ozaki25_[a-z0-9_]+)\s*\(", text)))
+
+
+# ----------------------------------------------------------------- helpers
+def _check(status: int, what: str):
+    if status != SUCCESS:
+        raise Ozaki25Error(status, what)
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _matrix(t, name):
+    import torch
+    if not (isinstance(t, torch.Tensor) and t.is_cuda and t.dtype == torch.float64 and t.dim() == 2):
+        raise ValueError(f"{name} must be a 2-D float64 CUDA tensor")
+    if t.stride(1) != 1 and t.shape[1] > 1:
+        raise ValueError(f"{name} must be row-major (unit column stride)")
+    return t, max(t.stride(0), t.shape[1], 1)
+
+
+# ----------------------------------------------------------------- host-only
+def ozaki25_status_string(status: int) -> str:
+    return lib().ozaki25_status_string(status).decode()
+
+
+def ozaki25_num_moduli(set: int = S12) -> int:
+    return lib().ozaki25_num_moduli(set)
+
+
+def ozaki25_num_planes(set: int = S12) -> int:
+    return lib().ozaki25_num_planes(set)
+
+
+def ozaki25_modulus(i: int, set: int = S12) -> int:
+    return lib().ozaki25_modulus(set, i)
+
+
+def ozaki25_scale_bits(k: int, set: int = S12) -> int:
+    return lib().ozaki25_scale_bits(k, set)
+
+
+def ozaki25_k_pad(k: int) -> int:
+    return lib().ozaki25_k_pad(k)
+
+
+def ozaki25_planes_bytes(vecs: int, k: int, set: int = S12) -> int:
+    return lib().ozaki25_planes_bytes(vecs, k, set)
+
+
+def ozaki25_dgemm_workspace_size(m: int, n: int, k: int, set: int = S12) -> int:
+    return lib().ozaki25_dgemm_workspace_size(m, n, k, set)
+
+
+# ----------------------------------------------------------------- stages
+def ozaki25_deconstruct(side: int, X, planes=None, exps=None, set: int = S12, stream=None):
+    """side 0: X is A (rows); side 1: X is B (columns).  Returns (planes, exps):
+    planes int8 [30][vecs][k_pad], exps int32 [vecs]."""
+    import torch
+    X, ldx = _matrix(X, "X")
+    vecs, k = (X.shape[0], X.shape[1]) if side == 0 else (X.shape[1], X.shape[0])
+    kp = ozaki25_k_pad(k)
+    if planes is None:
+        planes = torch.empty((NUM_PLANES, vecs, kp), dtype=torch.int8, device=X.device)
+    if exps is None:
+        exps = torch.empty((vecs,), dtype=torch.int32, device=X.device)
+    if planes.numel() < NUM_PLANES * vecs * kp or exps.numel() < vecs:
+        raise ValueError("output buffers too small")
+    _check(lib().ozaki25_deconstruct(side, vecs, k, _ptr(X), ldx, set, _ptr(planes), _ptr(exps),
+                                     _stream(stream)), "ozaki25_deconstruct")
+    return planes, exps
+
+
+def ozaki25_residue_gemm(m: int, n: int, k: int, planesA, planesB, Cres=None, set: int = S12,
+                         stream=None):
+    """Centred per-modulus products, int32 [12][m][n]."""
+    import torch
+    dev = planesA.device
+    if Cres is None:
+        Cres = torch.empty((NUM_MODULI, m, n), dtype=torch.int32, device=dev)
+    if Cres.numel() < NUM_MODULI * m * n:
+        raise ValueError("Cres too small")
+    _check(lib().ozaki25_residue_gemm(m, n, k, _ptr(planesA), _ptr(planesB), set, _ptr(Cres),
+                                      _stream(stream)), "ozaki25_residue_gemm")
+    return Cres
+
+
+def ozaki25_reconstruct(Cres, expsA, expsB, C=None, subtract: bool = False, set: int = S12,
+                        stream=None):
+    """C (m x n float64) from int32 residues [12][m][n] and the exponents."""
+    import torch
+    m, n = expsA.numel(), expsB.numel()
+    if C is None:
+        C = torch.empty((m, n), dtype=torch.float64, device=Cres.device)
+    C, ldc = _matrix(C, "C")
+    _check(lib().ozaki25_reconstruct(m, n, _ptr(Cres), _ptr(expsA), _ptr(expsB), set, _ptr(C), ldc,
+                                     1 if subtract else 0, _stream(stream)), "ozaki25_reconstruct")
+    return C
+
+
+# ----------------------------------------------------------------- GEMM
+def ozaki25_dgemm_ex(A, B, C, subtract: bool = False, workspace=None, stage_events=None,
+                     set: int = S12, stream=None):
+    A, lda = _matrix(A, "A")
+    B, ldb = _matrix(B, "B")
+    C, ldc = _matrix(C, "C")
+    m, k = A.shape
+    k2, n = B.shape
+    if k2 != k or tuple(C.shape) != (m, n):
+        raise ValueError("shape mismatch")
+    ev = None
+    if stage_events is not None:
+        handles = []
+        for e in stage_events:
+            if not hasattr(e, "cuda_event") or not e.cuda_event:
+                raise ValueError("stage events must be recorded torch.cuda.Event objects")
+            handles.append(e.cuda_event)
+        ev = (ctypes.c_void_p * NUM_STAGE_EVENTS)(*handles)
+    ws_ptr = _ptr(workspace) if workspace is not None else ctypes.c_void_p(0)
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().ozaki25_dgemm_ex(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, set,
+                                  1 if subtract else 0, ws_ptr, ws_bytes,
+                                  ctypes.cast(ev, ctypes.c_void_p) if ev is not None else None,
+                                  _stream(stream)), "ozaki25_dgemm_ex")
+    return C
+
+
+def ozaki25_dgemm(A, B, C=None, set: int = S12, stream=None):
+    """C = A B (float64, row-major CUDA tensors)."""
+    import torch
+    A, lda = _matrix(A, "A")
+    B, ldb = _matrix(B, "B")
+    m, k = A.shape
+    k2, n = B.shape
+    if k2 != k:
+        raise ValueError("shape mismatch")
+    if C is None:
+        C = torch.empty((m, n), dtype=torch.float64, device=A.device)
+    C, ldc = _matrix(C, "C")
+    _check(lib().ozaki25_dgemm(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, set,
+                               _stream(stream)), "ozaki25_dgemm")
+    return C
+
+
+def ozaki25_dgemm_sub(A, B, C, set: int = S12, stream=None):
+    """C <- C - A B in place."""
+    A, lda = _matrix(A, "A")
+    B, ldb = _matrix(B, "B")
+    C, ldc = _matrix(C, "C")
+    m, k = A.shape
+    _, n = B.shape
+    _check(lib().ozaki25_dgemm_sub(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, set,
+                                   _stream(stream)), "ozaki25_dgemm_sub")
+    return C

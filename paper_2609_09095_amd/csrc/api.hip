@@ -1,0 +1,223 @@
+// The C ABI of ozaki25.h: argument checks, the scale-bit rule, workspace
+// layout and the launch sequence of Alg. 1 on one stream.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstring>
+
+#include "kernels.hpp"
+#include "moduli.hpp"
+#include "ozaki25.h"
+
+namespace {
+
+using u128 = unsigned __int128;
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool known_set(ozaki25_moduli_set set) { return set == OZAKI25_MODULI_S12; }
+
+// t(k) = max{t : k 2^(2t) <= M/2 - 1} (Eq. (moduli) with mu = k 2^(2t)).
+int scale_bits(int64_t k) {
+  if (k < 1) return -1;
+  u128 M = 1;
+  for (int i = 0; i < oz::kR; ++i) M *= (u128)oz::kModulus[i];
+  const u128 q = (M / 2 - 1) / (u128)k;
+  int t = 0;
+  while (((u128)1 << (2 * (t + 1))) <= q) ++t;
+  return t;
+}
+
+int64_t k_pad(int64_t k) { return k <= 0 ? 0 : (k + oz::kKAlign - 1) / oz::kKAlign * oz::kKAlign; }
+
+// Byte range [p, p + bytes) overlaps [q, q + qbytes)?
+bool overlaps(const void* p, size_t bytes, const void* q, size_t qbytes) {
+  const uintptr_t a = (uintptr_t)p, b = (uintptr_t)q;
+  return bytes && qbytes && a < b + qbytes && b < a + bytes;
+}
+
+size_t matrix_bytes(int64_t rows, int64_t cols, int64_t ld) {
+  if (rows <= 0 || cols <= 0) return 0;
+  return ((size_t)(rows - 1) * (size_t)ld + (size_t)cols) * sizeof(double);
+}
+
+ozaki25_status hip_status(hipError_t e) { return e == hipSuccess ? OZAKI25_SUCCESS : OZAKI25_ERR_HIP; }
+
+struct Workspace {
+  size_t planes_a, planes_b, exps_a, exps_b, cres, total;
+};
+
+Workspace layout(int64_t m, int64_t n, int64_t k) {
+  Workspace w;
+  const int64_t kp = k_pad(k);
+  size_t off = 0;
+  w.planes_a = off;
+  off = align_up(off + (size_t)oz::kPlanes * m * kp);
+  w.planes_b = off;
+  off = align_up(off + (size_t)oz::kPlanes * n * kp);
+  w.exps_a = off;
+  off = align_up(off + (size_t)m * sizeof(int32_t));
+  w.exps_b = off;
+  off = align_up(off + (size_t)n * sizeof(int32_t));
+  w.cres = off;
+  off = align_up(off + (size_t)oz::kR * m * n * sizeof(int16_t));
+  w.total = off;
+  return w;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ozaki25_status_string(ozaki25_status s) {
+  switch (s) {
+    case OZAKI25_SUCCESS: return "success";
+    case OZAKI25_ERR_INVALID_VALUE: return "invalid value";
+    case OZAKI25_ERR_UNSUPPORTED: return "unsupported (k beyond the exactness bound)";
+    case OZAKI25_ERR_WORKSPACE: return "workspace too small or allocation failed";
+    case OZAKI25_ERR_HIP: return "HIP runtime or launch error";
+  }
+  return "unknown status";
+}
+
+int ozaki25_num_moduli(ozaki25_moduli_set set) { return known_set(set) ? oz::kR : -1; }
+
+int ozaki25_num_planes(ozaki25_moduli_set set) { return known_set(set) ? oz::kPlanes : -1; }
+
+int64_t ozaki25_modulus(ozaki25_moduli_set set, int i) {
+  return known_set(set) && i >= 0 && i < oz::kR ? oz::kModulus[i] : -1;
+}
+
+int ozaki25_scale_bits(int64_t k, ozaki25_moduli_set set) { return known_set(set) ? scale_bits(k) : -1; }
+
+int64_t ozaki25_k_pad(int64_t k) { return k_pad(k); }
+
+size_t ozaki25_planes_bytes(int64_t vecs, int64_t k, ozaki25_moduli_set set) {
+  if (!known_set(set) || vecs < 0 || k < 0) return 0;
+  return (size_t)oz::kPlanes * (size_t)vecs * (size_t)k_pad(k);
+}
+
+ozaki25_status ozaki25_deconstruct(int side, int64_t vecs, int64_t k, const double* X, int64_t ldx,
+                                   ozaki25_moduli_set set, int8_t* planes, int32_t* exps,
+                                   void* stream) {
+  if (!known_set(set) || (side != 0 && side != 1) || vecs < 0 || k < 0)
+    return OZAKI25_ERR_INVALID_VALUE;
+  if (k > OZAKI25_MAX_K) return OZAKI25_ERR_UNSUPPORTED;
+  if (vecs == 0 || k == 0) return OZAKI25_SUCCESS;
+  if (ldx < (side == 0 ? k : vecs)) return OZAKI25_ERR_INVALID_VALUE;
+  if (!X || !planes || !exps) return OZAKI25_ERR_INVALID_VALUE;
+  if (((uintptr_t)planes & 15) || ((uintptr_t)exps & 3) || ((uintptr_t)X & 7))
+    return OZAKI25_ERR_INVALID_VALUE;
+  hipStream_t s = (hipStream_t)stream;
+  const int t = scale_bits(k);
+  hipError_t e = oz::launch_scan(side, vecs, k, X, ldx, t, exps, s);
+  if (e == hipSuccess) e = oz::launch_deconstruct(side, vecs, k, k_pad(k), X, ldx, exps, planes, s);
+  return hip_status(e);
+}
+
+ozaki25_status ozaki25_residue_gemm(int64_t m, int64_t n, int64_t k, const int8_t* planesA,
+                                    const int8_t* planesB, ozaki25_moduli_set set, int32_t* Cres,
+                                    void* stream) {
+  if (!known_set(set) || m < 0 || n < 0 || k < 0) return OZAKI25_ERR_INVALID_VALUE;
+  if (k > OZAKI25_MAX_K) return OZAKI25_ERR_UNSUPPORTED;
+  if (m == 0 || n == 0) return OZAKI25_SUCCESS;
+  if (!Cres || (k > 0 && (!planesA || !planesB))) return OZAKI25_ERR_INVALID_VALUE;
+  if (((uintptr_t)planesA & 15) || ((uintptr_t)planesB & 15) || ((uintptr_t)Cres & 3))
+    return OZAKI25_ERR_INVALID_VALUE;
+  return hip_status(oz::launch_residue_gemm_i32(m, n, k_pad(k), planesA, planesB, Cres,
+                                                (hipStream_t)stream));
+}
+
+ozaki25_status ozaki25_reconstruct(int64_t m, int64_t n, const int32_t* Cres, const int32_t* expsA,
+                                   const int32_t* expsB, ozaki25_moduli_set set, double* C,
+                                   int64_t ldc, int subtract, void* stream) {
+  if (!known_set(set) || m < 0 || n < 0) return OZAKI25_ERR_INVALID_VALUE;
+  if (m == 0 || n == 0) return OZAKI25_SUCCESS;
+  if (!Cres || !expsA || !expsB || !C || ldc < n) return OZAKI25_ERR_INVALID_VALUE;
+  if (((uintptr_t)Cres & 3) || ((uintptr_t)expsA & 3) || ((uintptr_t)expsB & 3) || ((uintptr_t)C & 7))
+    return OZAKI25_ERR_INVALID_VALUE;
+  return hip_status(oz::launch_reconstruct_i32(m, n, Cres, expsA, expsB, C, ldc, subtract ? 1 : 0,
+                                               (hipStream_t)stream));
+}
+
+size_t ozaki25_dgemm_workspace_size(int64_t m, int64_t n, int64_t k, ozaki25_moduli_set set) {
+  if (!known_set(set) || m < 0 || n < 0 || k < 0) return 0;
+  return layout(m, n, k).total;
+}
+
+ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
+                                const double* B, int64_t ldb, double* C, int64_t ldc,
+                                ozaki25_moduli_set set, int subtract, void* workspace,
+                                size_t workspace_bytes, void* const* stage_events, void* stream) {
+  if (!known_set(set) || m < 0 || n < 0 || k < 0) return OZAKI25_ERR_INVALID_VALUE;
+  if (k > OZAKI25_MAX_K) return OZAKI25_ERR_UNSUPPORTED;
+  if (m == 0 || n == 0) return OZAKI25_SUCCESS;
+  if (!C || ldc < n || ((uintptr_t)C & 7)) return OZAKI25_ERR_INVALID_VALUE;
+  if (k > 0) {
+    if (!A || !B || lda < k || ldb < n || ((uintptr_t)A & 7) || ((uintptr_t)B & 7))
+      return OZAKI25_ERR_INVALID_VALUE;
+    const size_t cb = matrix_bytes(m, n, ldc);
+    if (overlaps(A, matrix_bytes(m, k, lda), C, cb) || overlaps(B, matrix_bytes(k, n, ldb), C, cb))
+      return OZAKI25_ERR_INVALID_VALUE;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  hipEvent_t* ev = (hipEvent_t*)stage_events;
+  hipError_t e = hipSuccess;
+  if (k == 0) {
+    if (ev) e = hipEventRecord(ev[0], s);
+    if (e == hipSuccess && !subtract) e = oz::launch_zero_c(m, n, C, ldc, s);
+    for (int i = 1; ev && e == hipSuccess && i < OZAKI25_NUM_STAGE_EVENTS; ++i) e = hipEventRecord(ev[i], s);
+    return hip_status(e);
+  }
+
+  const Workspace w = layout(m, n, k);
+  void* ws = workspace;
+  bool owned = false;
+  if (ws) {
+    if (workspace_bytes < w.total || ((uintptr_t)ws & (kAlign - 1))) return OZAKI25_ERR_WORKSPACE;
+  } else {
+    if (hipMallocAsync(&ws, w.total, s) != hipSuccess || !ws) return OZAKI25_ERR_WORKSPACE;
+    owned = true;
+  }
+  char* base = (char*)ws;
+  int8_t* pa = (int8_t*)(base + w.planes_a);
+  int8_t* pb = (int8_t*)(base + w.planes_b);
+  int32_t* ea = (int32_t*)(base + w.exps_a);
+  int32_t* eb = (int32_t*)(base + w.exps_b);
+  int16_t* cres = (int16_t*)(base + w.cres);
+  const int t = scale_bits(k);
+  const int64_t kp = k_pad(k);
+
+  if (ev) e = hipEventRecord(ev[0], s);
+  if (e == hipSuccess) e = oz::launch_scan(0, m, k, A, lda, t, ea, s);
+  if (e == hipSuccess) e = oz::launch_scan(1, n, k, B, ldb, t, eb, s);
+  if (ev && e == hipSuccess) e = hipEventRecord(ev[1], s);
+  if (e == hipSuccess) e = oz::launch_deconstruct(0, m, k, kp, A, lda, ea, pa, s);
+  if (e == hipSuccess) e = oz::launch_deconstruct(1, n, k, kp, B, ldb, eb, pb, s);
+  if (ev && e == hipSuccess) e = hipEventRecord(ev[2], s);
+  if (e == hipSuccess) e = oz::launch_residue_gemm_i16(m, n, kp, pa, pb, cres, s);
+  if (ev && e == hipSuccess) e = hipEventRecord(ev[3], s);
+  if (e == hipSuccess) e = oz::launch_reconstruct_i16(m, n, cres, ea, eb, C, ldc, subtract ? 1 : 0, s);
+  if (ev && e == hipSuccess) e = hipEventRecord(ev[4], s);
+  if (owned) {
+    const hipError_t f = hipFreeAsync(ws, s);
+    if (e == hipSuccess) e = f;
+  }
+  return hip_status(e);
+}
+
+ozaki25_status ozaki25_dgemm(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
+                             const double* B, int64_t ldb, double* C, int64_t ldc,
+                             ozaki25_moduli_set set, void* stream) {
+  return ozaki25_dgemm_ex(m, n, k, A, lda, B, ldb, C, ldc, set, 0, nullptr, 0, nullptr, stream);
+}
+
+ozaki25_status ozaki25_dgemm_sub(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
+                                 const double* B, int64_t ldb, double* C, int64_t ldc,
+                                 ozaki25_moduli_set set, void* stream) {
+  return ozaki25_dgemm_ex(m, n, k, A, lda, B, ldb, C, ldc, set, 1, nullptr, 0, nullptr, stream);
+}
+
+}  // extern "C"

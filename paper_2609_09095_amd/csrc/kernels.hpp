@@ -1,0 +1,38 @@
+// Launchers of the gfx950 kernels (internal to the library; the C ABI in
+// ozaki25.h is the public surface).  Every launcher enqueues on `stream` and
+// returns the HIP error of the launch.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+namespace oz {
+
+// Exponent scan of A's rows (side 0) or B's columns (side 1), Alg. 1 setup:
+// exps[v] = t - e_v, or INT32_MIN for a vector holding a NaN or infinity.
+hipError_t launch_scan(int side, int64_t vecs, int64_t k, const double* X, int64_t ldx, int t,
+                       int32_t* exps, hipStream_t stream);
+
+// Alg. 2: scale, round, residues and limb planes of one operand, given exps.
+hipError_t launch_deconstruct(int side, int64_t vecs, int64_t k, int64_t kp, const double* X,
+                              int64_t ldx, const int32_t* exps, int8_t* planes,
+                              hipStream_t stream);
+
+// Eq. (residueprod) on int8 MFMA: r centred per-modulus products [r][m][n].
+hipError_t launch_residue_gemm_i32(int64_t m, int64_t n, int64_t kp, const int8_t* pa,
+                                   const int8_t* pb, int32_t* cres, hipStream_t stream);
+hipError_t launch_residue_gemm_i16(int64_t m, int64_t n, int64_t kp, const int8_t* pa,
+                                   const int8_t* pb, int16_t* cres, hipStream_t stream);
+
+// Alg. 3: Garner, Horner, lift, single rounding (C = or C -= ).
+hipError_t launch_reconstruct_i32(int64_t m, int64_t n, const int32_t* cres, const int32_t* ea,
+                                  const int32_t* eb, double* C, int64_t ldc, int subtract,
+                                  hipStream_t stream);
+hipError_t launch_reconstruct_i16(int64_t m, int64_t n, const int16_t* cres, const int32_t* ea,
+                                  const int32_t* eb, double* C, int64_t ldc, int subtract,
+                                  hipStream_t stream);
+
+// C = +0.0 over an m x n block (the k == 0 product).
+hipError_t launch_zero_c(int64_t m, int64_t n, double* C, int64_t ldc, hipStream_t stream);
+
+}  // namespace oz
