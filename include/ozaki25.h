@@ -60,7 +60,7 @@ typedef enum { OZAKI25_MODULI_S12 = 0 } ozaki25_moduli_set;
 
 #define OZAKI25_NUM_MODULI 12
 #define OZAKI25_NUM_PLANES 30          /* 2 per square modulus + 3 per nonsquare */
-#define OZAKI25_K_ALIGN 64             /* planes are zero padded to a multiple of this */
+#define OZAKI25_K_ALIGN 128            /* planes are zero padded to a multiple of this */
 #define OZAKI25_MAX_K 4194304          /* int32 limb accumulators: 22^2 * k < 2^31 */
 #define OZAKI25_EXP_NONFINITE INT32_MIN
 #define OZAKI25_NUM_STAGE_EVENTS 5     /* see ozaki25_dgemm_ex */

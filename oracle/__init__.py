@@ -112,7 +112,7 @@ def garner_constants() -> list[int]:
 
 
 def k_pad(k: int) -> int:
-    return (k + 63) // 64 * 64
+    return (k + 127) // 128 * 128
 
 
 # ---------------------------------------------------------------- scalars

@@ -27,7 +27,7 @@ _HEADER = os.path.join(os.path.dirname(_PKG), "include", "ozaki25.h")
 S12 = 0
 NUM_MODULI = 12
 NUM_PLANES = 30
-K_ALIGN = 64
+K_ALIGN = 128
 MAX_K = 4194304
 EXP_NONFINITE = -(2 ** 31)
 NUM_STAGE_EVENTS = 5

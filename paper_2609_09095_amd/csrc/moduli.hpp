@@ -11,7 +11,7 @@ namespace oz {
 
 constexpr int kR = 12;
 constexpr int kPlanes = 30;
-constexpr int kKAlign = 64;
+constexpr int kKAlign = 128;
 
 // Published order: six squares, then the six nonsquares near 2^9.
 constexpr int kModulus[kR] = {1089, 1024, 961, 841, 625, 529, 511, 509, 503, 499, 491, 487};

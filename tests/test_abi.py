@@ -57,8 +57,9 @@ def test_scale_bits_invalid():
 
 def test_size_helpers():
     assert oz.ozaki25_k_pad(0) == 0
-    assert oz.ozaki25_k_pad(1) == 64 and oz.ozaki25_k_pad(64) == 64 and oz.ozaki25_k_pad(65) == 128
+    assert oz.ozaki25_k_pad(1) == 128 and oz.ozaki25_k_pad(128) == 128 and oz.ozaki25_k_pad(129) == 256
     assert oz.ozaki25_planes_bytes(10, 70) == 30 * 10 * 128
+    assert oz.ozaki25_planes_bytes(10, 130) == 30 * 10 * 256
     assert oz.ozaki25_planes_bytes(-1, 70) == 0
     ws = oz.ozaki25_dgemm_workspace_size(100, 50, 70)
     assert ws >= 30 * 100 * 128 + 30 * 50 * 128 + 4 * 150 + 12 * 100 * 50 * 2

@@ -460,7 +460,7 @@ def test_planes_layout_and_padding():
     res = oracle.dgemm(A, workloads.random_matrix(70, 2, 1.0, 7))
     P = res.planesA
     assert P.shape == (30, 3, 128)
-    assert not P[:, :, 70:].any()
+    assert not P[:, :, 70:].any()   # zero padding up to the 128-byte plane row
     mods = oracle.moduli()
     for i, m in enumerate(mods):
         q = oracle.plane_base(i)
