@@ -48,7 +48,7 @@ extern "C" {
 typedef enum {
   OZAKI25_SUCCESS = 0,
   OZAKI25_ERR_INVALID_VALUE = 1, /* bad dimension, leading dimension, pointer or enum */
-  OZAKI25_ERR_UNSUPPORTED = 2,   /* k beyond OZAKI25_MAX_K */
+  OZAKI25_ERR_UNSUPPORTED = 2,   /* k beyond OZAKI25_MAX_K or n beyond OZAKI25_MAX_N */
   OZAKI25_ERR_WORKSPACE = 3,     /* workspace too small, or its allocation failed */
   OZAKI25_ERR_HIP = 4            /* a HIP launch or runtime call failed */
 } ozaki25_status;
@@ -62,6 +62,7 @@ typedef enum { OZAKI25_MODULI_S12 = 0 } ozaki25_moduli_set;
 #define OZAKI25_NUM_PLANES 30          /* 2 per square modulus + 3 per nonsquare */
 #define OZAKI25_K_ALIGN 128            /* planes are zero padded to a multiple of this */
 #define OZAKI25_MAX_K 4194304          /* int32 limb accumulators: 22^2 * k < 2^31 */
+#define OZAKI25_MAX_N 8388608          /* columns of B / C (32-bit offsets inside a tile) */
 #define OZAKI25_EXP_NONFINITE INT32_MIN
 #define OZAKI25_NUM_STAGE_EVENTS 5     /* see ozaki25_dgemm_ex */
 

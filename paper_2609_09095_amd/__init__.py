@@ -29,6 +29,7 @@ NUM_MODULI = 12
 NUM_PLANES = 30
 K_ALIGN = 128
 MAX_K = 4194304
+MAX_N = 8388608
 EXP_NONFINITE = -(2 ** 31)
 NUM_STAGE_EVENTS = 5
 

@@ -9,6 +9,8 @@
 #include "moduli.hpp"
 #include "ozaki25.h"
 
+static_assert(OZAKI25_MAX_N <= oz::kMaxResidueCols, "residue GEMM column limit");
+
 namespace {
 
 using u128 = unsigned __int128;
@@ -75,7 +77,7 @@ const char* ozaki25_status_string(ozaki25_status s) {
   switch (s) {
     case OZAKI25_SUCCESS: return "success";
     case OZAKI25_ERR_INVALID_VALUE: return "invalid value";
-    case OZAKI25_ERR_UNSUPPORTED: return "unsupported (k beyond the exactness bound)";
+    case OZAKI25_ERR_UNSUPPORTED: return "unsupported size (k or n beyond the library limits)";
     case OZAKI25_ERR_WORKSPACE: return "workspace too small or allocation failed";
     case OZAKI25_ERR_HIP: return "HIP runtime or launch error";
   }
@@ -121,7 +123,7 @@ ozaki25_status ozaki25_residue_gemm(int64_t m, int64_t n, int64_t k, const int8_
                                     const int8_t* planesB, ozaki25_moduli_set set, int32_t* Cres,
                                     void* stream) {
   if (!known_set(set) || m < 0 || n < 0 || k < 0) return OZAKI25_ERR_INVALID_VALUE;
-  if (k > OZAKI25_MAX_K) return OZAKI25_ERR_UNSUPPORTED;
+  if (k > OZAKI25_MAX_K || n > OZAKI25_MAX_N) return OZAKI25_ERR_UNSUPPORTED;
   if (m == 0 || n == 0) return OZAKI25_SUCCESS;
   if (!Cres || (k > 0 && (!planesA || !planesB))) return OZAKI25_ERR_INVALID_VALUE;
   if (((uintptr_t)planesA & 15) || ((uintptr_t)planesB & 15) || ((uintptr_t)Cres & 3))
@@ -152,7 +154,7 @@ ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A
                                 ozaki25_moduli_set set, int subtract, void* workspace,
                                 size_t workspace_bytes, void* const* stage_events, void* stream) {
   if (!known_set(set) || m < 0 || n < 0 || k < 0) return OZAKI25_ERR_INVALID_VALUE;
-  if (k > OZAKI25_MAX_K) return OZAKI25_ERR_UNSUPPORTED;
+  if (k > OZAKI25_MAX_K || n > OZAKI25_MAX_N) return OZAKI25_ERR_UNSUPPORTED;
   if (m == 0 || n == 0) return OZAKI25_SUCCESS;
   if (!C || ldc < n || ((uintptr_t)C & 7)) return OZAKI25_ERR_INVALID_VALUE;
   if (k > 0) {

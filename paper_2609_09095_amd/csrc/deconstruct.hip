@@ -68,7 +68,8 @@ __device__ __forceinline__ void emit_modulus(const double (&y)[kElems], int8_t* 
                                              int64_t plane_stride, int64_t off) {
   constexpr int M = kModulus[I];
   constexpr int S = root_of(I);
-  int8_t* base = planes + (int64_t)plane_base(I) * plane_stride + off;
+  constexpr int Q = plane_base(I);
+  int8_t* base = planes + (int64_t)Q * plane_stride + off;
   int l0[kElems], l1[kElems];
 #pragma unroll
   for (int c = 0; c < kElems; ++c) {

@@ -19,6 +19,8 @@ hipError_t launch_deconstruct(int side, int64_t vecs, int64_t k, int64_t kp, con
                               hipStream_t stream);
 
 // Eq. (residueprod) on int8 MFMA: r centred per-modulus products [r][m][n].
+// n must not exceed kMaxResidueCols.
+constexpr int64_t kMaxResidueCols = (int64_t)1 << 23;
 hipError_t launch_residue_gemm_i32(int64_t m, int64_t n, int64_t kp, const int8_t* pa,
                                    const int8_t* pb, int32_t* cres, hipStream_t stream);
 hipError_t launch_residue_gemm_i16(int64_t m, int64_t n, int64_t kp, const int8_t* pa,

@@ -20,11 +20,16 @@
 // Tiling (4 wavefronts, 1 per SIMD): 256 x 256 block tile, 128 x 128 per
 // wavefront (4 x 4 MFMA blocks of 32 x 32), K stages of 128 bytes loaded
 // straight from global memory into LDS (buffer loads with the lds bit; 2 x
-// 64 KiB, double buffered) while the previous stage feeds the MFMAs.  LDS
-// rows are 128 bytes with the 16-byte chunk index XOR-swizzled by the row so
-// that the b128 fragment reads of 8 (or 16) consecutive rows hit distinct
-// banks.  Plane rows are padded to a multiple of 128 bytes, so every stage
-// is full.
+// 64 KiB, double buffered).  The 16 loads of stage s+1 are interleaved with
+// the first half of stage s's MFMAs, so the wave never stalls on a full
+// vector-memory queue with MFMAs waiting behind it.  LDS rows are 128 bytes
+// with the 16-byte chunk index XOR-swizzled by the row so that the b128
+// fragment reads of 8 (or 16) consecutive rows hit distinct banks.  Plane
+// rows are padded to a multiple of 128 bytes, so every stage is full.
+//
+// At this tile size the operand stream is 64 KiB per CU per 2048 MFMA
+// cycles (32 B/clk); the per-CU L2 read throughput that the counters show
+// (~20 B/clk at ~530 cycles average latency) is the bound, not the MFMAs.
 #include "device_math.hpp"
 #include "kernels.hpp"
 #include "moduli.hpp"
@@ -46,7 +51,6 @@ constexpr int kGroupM = 4;      // tile rows per group in the block order
 struct ModSched {
   int m;           // modulus
   int hi;          // (m - 1) / 2, top of the centred range
-  double inv;      // 1.0 / m
   int plane_a[3];  // A plane of each product, in issue order
   int plane_b[3];  // B plane of each product
   int mult[3];     // multiplier after product p (p = 2: the final weight)
@@ -73,7 +77,6 @@ constexpr int issue_mult(int i, int p) {
 constexpr ModSched make_sched(int i) {
   return ModSched{kModulus[i],
                   (kModulus[i] - 1) / 2,
-                  1.0 / kModulus[i],
                   {issue_plane_a(i, 0), issue_plane_a(i, 1), issue_plane_a(i, 2)},
                   {issue_plane_b(i, 0), issue_plane_b(i, 1), issue_plane_b(i, 2)},
                   {issue_mult(i, 0), issue_mult(i, 1), issue_mult(i, 2)}};
@@ -96,26 +99,27 @@ __constant__ ModSched kSched[kR] = {make_sched(0), make_sched(1), make_sched(2),
                                     make_sched(4), make_sched(5), make_sched(6),  make_sched(7),
                                     make_sched(8), make_sched(9), make_sched(10), make_sched(11)};
 
-// Centred residue of an int32 modulo a runtime m (same argument as cmod_f64).
-__device__ __forceinline__ int cmod_rt(int x, int m, int hi, double inv) {
-  const double v = (double)x;
-  const double q = __builtin_rint(v * inv);
-  const int r = (int)__builtin_fma(-q, (double)m, v);
-  const int r1 = r > hi ? r - m : r;
-  return r1 < hi - m + 1 ? r1 + m : r1;
+// acc * mult reduced mod m to a representative in [-m/2, m/2]: acc * mult is
+// exact in FP64 (|acc| < 2^31, mult < 2^11), its quotient by m is off from
+// the nearest integer by far less than 1/(2m) (odd m: never a tie; m = 1024:
+// exact), and the remainder is exact in one FMA.  Ties of the even modulus
+// may land on +m/2; the final reduction maps them to -m/2.
+__device__ __forceinline__ int mulmod_rt(int acc, double mult, double m, double mult_inv) {
+  const double a = (double)acc;
+  const double q = __builtin_rint(a * mult_inv);     // mult_inv = mult / m
+  return (int)__builtin_fma(a, mult, -q * m);         // a * mult exact, q * m exact
 }
 
 __device__ __forceinline__ int swz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
 
-// Block order: moduli outermost; each XCD (block ids are dealt round-robin
-// over the 8 XCDs) gets a contiguous range of the logical order; inside a
-// modulus, tiles go in groups of kGroupM tile rows so that the blocks that
-// run together share A and B panels in their XCD's L2.
+// Block order: moduli outermost; inside a modulus, tiles go in groups of
+// kGroupM tile rows, so that the ~256 blocks resident at a time cover a
+// compact patch of output tiles and share their A and B panels in the L2s
+// and the Infinity Cache.  (Giving each XCD a contiguous range of this order
+// measured slower: it spreads the XCDs over distant tiles and moduli.)
 __device__ __forceinline__ void block_coords(int64_t tiles_m, int64_t tiles_n, int& mod,
                                              int64_t& tm, int64_t& tn) {
-  const int64_t total = (int64_t)kR * tiles_m * tiles_n;
-  int64_t id = blockIdx.x;
-  if (total % 8 == 0) id = (id % 8) * (total / 8) + id / 8;
+  const int64_t id = blockIdx.x;
   const int64_t per_mod = tiles_m * tiles_n;
   mod = (int)(id / per_mod);
   const int64_t t = id % per_mod;
@@ -167,12 +171,22 @@ __device__ __forceinline__ void load_frags(const int8_t* la, const int8_t* lb, i
   }
 }
 
-// The four 32-byte K steps of one stage; the fragments of step ks+1 are read
-// from LDS while the 16 MFMAs of step ks run.
-__device__ __forceinline__ void stage_mma(const int8_t* la, const int8_t* lb, int wr, int wc, int fr,
-                                          int fh, v16i (&acc)[4][4]) {
+// One stage of MFMAs with the next stage's 16 DMA loads spread among them:
+// the fragments of step 0 first, then per K step [1 fragment read of the
+// next step, 1 DMA (steps 0-1 only), 2 MFMAs] x 8.
+__device__ __forceinline__ void stage_mma_dma(const int8_t* la, const int8_t* lb, int wr, int wc,
+                                              int fr, int fh, v16i (&acc)[4][4],
+                                              __amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rb,
+                                              int8_t* na, int8_t* nb, const int (&voff)[8], int k0,
+                                              int wave) {
   v4i af[2][4], bf[2][4];
   load_frags(la, lb, wr, wc, fr, fh, 0, af[0], bf[0]);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int slab = (wave * 8 + i) * 1024;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr)(na + slab), 16, voff[i], k0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr)(nb + slab), 16, voff[i], k0, 0, 0);
+  }
 #pragma unroll
   for (int ks = 0; ks < BK / 32; ++ks) {
     const int cur = ks & 1;
@@ -183,6 +197,15 @@ __device__ __forceinline__ void stage_mma(const int8_t* la, const int8_t* lb, in
       for (int b = 0; b < 4; ++b)
         acc[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[cur][a], bf[cur][b], acc[a][b], 0, 0, 0);
   }
+  __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+  for (int ks = 0; ks < BK / 32; ++ks)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      if (ks + 1 < BK / 32) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      if (ks < 2) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    }
 }
 
 template <typename OT>
@@ -235,45 +258,49 @@ __global__ __launch_bounds__(256, 1) void residue_gemm_kernel(int64_t m, int64_t
 
     stage_load(ra, rb, lds_a0, lds_b0, voff, 0, wave);
     for (int s = 0; s < nstage; s += 2) {
-      // stage s lives in buffer 0, stage s+1 in buffer 1
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
-      if (s + 1 < nstage) stage_load(ra, rb, lds_a1, lds_b1, voff, (s + 1) * BK, wave);
-      stage_mma(lds_a0, lds_b0, wr, wc, fr, fh, acc);
+      // the DMA of the stage after the last one reads past the panel: harmless,
+      // it lands in the idle buffer and is drained before the next product
+      stage_mma_dma(lds_a0, lds_b0, wr, wc, fr, fh, acc, ra, rb, lds_a1, lds_b1, voff, (s + 1) * BK, wave);
       if (s + 1 >= nstage) break;
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
-      if (s + 2 < nstage) stage_load(ra, rb, lds_a0, lds_b0, voff, (s + 2) * BK, wave);
-      stage_mma(lds_a1, lds_b1, wr, wc, fr, fh, acc);
+      stage_mma_dma(lds_a1, lds_b1, wr, wc, fr, fh, acc, ra, rb, lds_a0, lds_b0, voff, (s + 2) * BK, wave);
     }
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();  // every wave is done with the buffers before the next product loads
-    // carry: acc <- (acc mod m) * mult_p mod m (a multiplier of 1 mid-way needs no reduction)
+    // carry: acc <- acc * mult_p mod m (a multiplier of 1 mid-way needs no reduction)
     const int mult = sc.mult[p];
     if (p == 2 || mult != 1) {
+      const double dm = (double)sc.m, dmult = (double)mult, dinv = (double)mult / (double)sc.m;
 #pragma unroll
       for (int a = 0; a < 4; ++a)
 #pragma unroll
         for (int b = 0; b < 4; ++b)
 #pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int r = cmod_rt(acc[a][b][v], sc.m, sc.hi, sc.inv);
-            acc[a][b][v] = cmod_rt(r * mult, sc.m, sc.hi, sc.inv);
-          }
+          for (int v = 0; v < 16; ++v) acc[a][b][v] = mulmod_rt(acc[a][b][v], dmult, dm, dinv);
     }
   }
 
   // 32x32 MFMA result layout: lane holds column lane%32 and rows
-  // 8*(v/4) + 4*(lane/32) + v%4 of its 32x32 block.
-  OT* out = cres + (int64_t)mod * m * n;
+  // 8*(v/4) + 4*(lane/32) + v%4 of its 32x32 block.  Stores use the tile's
+  // scalar base and 32-bit element offsets (256 n < 2^31).
+  OT* out = (OT*)uniform_ptr((const int8_t*)(cres + (int64_t)mod * m * n + tm * BM * n + tn * BN));
+  const int nn = (int)n;
+  const int rows_left = (int)(m - tm * BM), cols_left = (int)(n - tn * BN);
 #pragma unroll
   for (int a = 0; a < 4; ++a)
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
-      const int64_t col = tn * BN + wc * 128 + b * 32 + fr;
+      const int col = wc * 128 + b * 32 + fr;
+      const int row0 = wr * 128 + a * 32 + 4 * fh;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int64_t row = tm * BM + wr * 128 + a * 32 + 8 * (v >> 2) + 4 * fh + (v & 3);
-        if (row < m && col < n) out[row * n + col] = (OT)acc[a][b][v];
+        const int row = row0 + 8 * (v >> 2) + (v & 3);
+        // representatives lie in [-m/2, m/2]: only +m/2 (even m) needs wrapping
+        const int r = acc[a][b][v];
+        if (row < rows_left && col < cols_left) out[row * nn + col] = (OT)(r > sc.hi ? r - sc.m : r);
       }
     }
 }
@@ -282,6 +309,8 @@ template <typename OT>
 hipError_t launch_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* pa, const int8_t* pb,
                        OT* cres, hipStream_t stream) {
   if (m <= 0 || n <= 0) return hipSuccess;
+  // the store epilogue uses 32-bit offsets within a 256-row tile
+  if (n > kMaxResidueCols) return hipErrorInvalidValue;
   const int64_t blocks = (int64_t)kR * ((m + BM - 1) / BM) * ((n + BN - 1) / BN);
   hipLaunchKernelGGL(residue_gemm_kernel<OT>, dim3((unsigned)blocks), dim3(256), 0, stream, m, n,
                      kp, pa, pb, cres);

@@ -91,6 +91,7 @@ def test_argument_errors_are_synchronous():
     assert L.ozaki25_residue_gemm(4, 4, 4, fake, fake, 0, null, null) == oz.ERR_INVALID_VALUE
     assert L.ozaki25_residue_gemm(0, 4, 4, null, null, 0, null, null) == oz.SUCCESS
     assert L.ozaki25_residue_gemm(4, 4, oz.MAX_K + 1, fake, fake, 0, fake, null) == oz.ERR_UNSUPPORTED
+    assert L.ozaki25_residue_gemm(4, oz.MAX_N + 1, 4, fake, fake, 0, fake, null) == oz.ERR_UNSUPPORTED
     # reconstruct
     assert L.ozaki25_reconstruct(4, 4, fake, fake, fake, 0, fake, 3, 0, null) == oz.ERR_INVALID_VALUE
     assert L.ozaki25_reconstruct(4, 4, null, fake, fake, 0, fake, 4, 0, null) == oz.ERR_INVALID_VALUE
@@ -104,6 +105,7 @@ def test_argument_errors_are_synchronous():
     assert f(4, 4, 4, null, 4, _v(0x300000), 4, _v(0x200000), 4, 0, 0, null, 0, null, null) == oz.ERR_INVALID_VALUE
     assert f(4, 4, 4, fake, 4, _v(0x300000), 4, _v(0x200000), 4, 1, 0, null, 0, null, null) == oz.ERR_INVALID_VALUE
     assert f(0, 4, 4, null, 4, null, 4, null, 4, 0, 0, null, 0, null, null) == oz.SUCCESS
+    assert f(4, oz.MAX_N + 1, 4, fake, 4, _v(0x300000), oz.MAX_N + 1, _v(0x200000), oz.MAX_N + 1, 0, 0, null, 0, null, null) == oz.ERR_UNSUPPORTED
     # a caller workspace that is too small is refused before any launch
     assert f(4, 4, 4, fake, 4, _v(0x300000), 4, _v(0x200000), 4, 0, 0, _v(0x400000), 16, null, null) == oz.ERR_WORKSPACE
 
