@@ -1,0 +1,94 @@
+"""Parity at the full workload sizes, through the same entry points the
+benchmark times (ozaki25_dgemm_ex with a caller workspace), on sampled
+outputs that the oracle computes one by one.
+
+Per workload: every exponent of A's rows and B's columns, the planes of a
+sample of rows and columns, the per-modulus products and the final C on the
+sampled rows x columns (which always include the first and last row and
+column, i.e. the ragged tiles), all bit for bit."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2609_09095_amd as oz
+import workloads
+from gpu_util import assert_bits_equal, assert_int_equal, log, require_gpu, sample_indices
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    require_gpu()
+
+
+def _run(name, nsample=96):
+    import torch
+    w = workloads.WORKLOADS[name]
+    log(f"[large] {name}: generating m={w.m} n={w.n} k={w.k}")
+    A, B, C0 = workloads.make_inputs(w)
+    rows = sample_indices(w.m, nsample, 11)
+    cols = sample_indices(w.n, nsample, 12)
+    Ad = torch.from_numpy(A).cuda()
+    Bd = torch.from_numpy(B).cuda()
+    Cd = torch.from_numpy(C0).cuda() if C0 is not None else torch.empty((w.m, w.n), dtype=torch.float64, device="cuda")
+    ws = torch.empty(oz.ozaki25_dgemm_workspace_size(w.m, w.n, w.k), dtype=torch.uint8, device="cuda")
+    log(f"[large] {name}: ozaki25_dgemm_ex")
+    oz.ozaki25_dgemm_ex(Ad, Bd, Cd, subtract=w.subtract, workspace=ws)
+    torch.cuda.synchronize()
+    ri = torch.from_numpy(rows).cuda()
+    ci = torch.from_numpy(cols).cuda()
+    C_s = Cd.index_select(0, ri).index_select(1, ci).cpu().numpy()
+    del ws, Cd
+    torch.cuda.empty_cache()
+
+    log(f"[large] {name}: stage API (exponents, planes, products)")
+    planesA, expsA = oz.ozaki25_deconstruct(0, Ad)
+    planesB, expsB = oz.ozaki25_deconstruct(1, Bd)
+    torch.cuda.synchronize()
+    del Ad, Bd
+    pA_s = planesA.index_select(1, ri).cpu().numpy()
+    pB_s = planesB.index_select(1, ci).cpu().numpy()
+    Cres = oz.ozaki25_residue_gemm(w.m, w.n, w.k, planesA, planesB)
+    torch.cuda.synchronize()
+    Cres_s = Cres.index_select(1, ri).index_select(2, ci).cpu().numpy()
+    eA, eB = expsA.cpu().numpy(), expsB.cpu().numpy()
+    del planesA, planesB, Cres
+    torch.cuda.empty_cache()
+
+    log(f"[large] {name}: oracle on {len(rows)} x {len(cols)} outputs")
+    t = oracle.scale_bits(w.k)
+    assert_int_equal(eA, oracle.exponents(A, 0, t), "sigma (all rows)")
+    assert_int_equal(eB, oracle.exponents(B, 1, t), "tau (all columns)")
+    r = oracle.dgemm(A, B, C_in=C0, rows=rows, cols=cols)
+    assert_int_equal(pA_s, r.planesA, "planes of sampled rows of A")
+    assert_int_equal(pB_s, r.planesB, "planes of sampled columns of B")
+    assert_int_equal(Cres_s, r.Cres, "per-modulus products (sampled)")
+    assert_bits_equal(C_s, r.C, "C (sampled)")
+    log(f"[large] {name}: ok")
+
+
+def test_square_8192():
+    _run("square")
+
+
+def test_ragged_8191_8209_7937():
+    _run("ragged")
+
+
+def test_hpl_trailing_update_32768_1024():
+    _run("hpl", nsample=64)
+
+
+def test_block_krylov_262144_128_4096():
+    _run("krylov", nsample=128)
+
+
+def test_long_k_single_output():
+    """k far beyond the workloads (1024 K stages), one output row/column."""
+    import torch
+    A = workloads.random_matrix(3, 131072, 1.0, 91)
+    B = workloads.random_matrix(131072, 2, 1.0, 92)
+    C = oz.ozaki25_dgemm(torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda())
+    torch.cuda.synchronize()
+    assert_bits_equal(C.cpu().numpy(), oracle.dgemm(A, B, want_planes=False).C, "C")
