@@ -88,6 +88,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-native", action="store_true")
     ap.add_argument("--baseline-sample", type=int, default=512)
+    ap.add_argument("--calibration-copy", action="store_true",
+                    help="copy 1 GiB device to device once before the run (a known-size kernel "
+                         "for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -115,6 +118,14 @@ def main():
 
     def step(events=None):
         oz.ozaki25_dgemm_ex(Ad, Bd, Cd, subtract=w.subtract, workspace=ws, stage_events=events)
+
+    if args.calibration_copy:
+        src = torch.ones(1 << 27, dtype=torch.float64, device=dev)   # 1 GiB
+        dst = torch.empty_like(src)
+        torch.mul(src, 1.0, out=dst)   # an elementwise kernel: 1 GiB in, 1 GiB out
+        torch.cuda.synchronize()
+        del src, dst
+        log("[bench] calibration copy: 1 GiB read, 1 GiB written")
 
     log(f"[bench] warmup {args.warmup}")
     for _ in range(args.warmup):
