@@ -3,8 +3,8 @@
 round to nearest) on one MI355X, through the C ABI.
 
 One step = one full ozaki25_dgemm_ex call: exponent scans, deconstruction of
-both operands into int8 planes, the 36 int8-MFMA limb products with the
-modular epilogue, and the CRT reconstruction, on synthetic seeded inputs that
+both operands into e4m3 planes, the 36 FP8-MFMA limb products (FP32
+accumulation) with the modular epilogue, and the CRT reconstruction, on synthetic seeded inputs that
 are already resident in HBM.  Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload square]
@@ -27,10 +27,10 @@ import workloads  # noqa: E402
 
 # MI355X published peaks
 HBM_PEAK_GBS = 8000.0
-INT8_PEAK_TOPS = 5000.0
+FP8_PEAK_TOPS = 5000.0
 FP64_PEAK_TFLOPS = 78.6
 PRODUCTS = 36               # 3 limb products for each of the 12 moduli
-PLANE_BYTES = 30            # stored int8 planes per element
+PLANE_BYTES = 30            # stored e4m3 plane bytes per element
 COUNTER_FILE = os.path.join(ROOT, "profiles", "residue_gemm_square_counters.txt")
 GEMM_SOURCE = os.path.join(ROOT, "paper_2609_09095_amd", "csrc", "residue_gemm.hip")
 
@@ -161,7 +161,7 @@ def main():
     stage_gbs = (dec_bytes + scan_bytes) / ((dec_ms + scan_ms) * 1e-3) / 1e9
     rec_bytes = w.m * w.n * (12 * 2 + 8 + (8 if w.subtract else 0))
     rec_gbs = rec_bytes / (rec_ms * 1e-3) / 1e9
-    roof = INT8_PEAK_TOPS / PRODUCTS
+    roof = FP8_PEAK_TOPS / PRODUCTS
 
     native = None
     if not args.no_native and not w.subtract and w.m * w.n * w.k <= 8192 ** 3:
@@ -189,18 +189,18 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "int8",
+        "dtype": "fp8",
         "data": "synthetic",
         "config": {"workload": f"{w.name}: C {'-=' if w.subtract else '='} A.B, m={w.m} n={w.n} k={w.k}, "
                                f"entries (U-0.5)exp({w.s} N), seed {w.seed}",
                    "m": w.m, "n": w.n, "k": w.k, "moduli": "published 12-modulus set", "quantiser": "RN",
-                   "route": "int8 MFMA, i32 accumulate"},
+                   "route": "e4m3 MFMA, fp32 accumulate"},
         "roofline": {"bound": "mfma", "kernel": "residue_gemm_kernel<int16>",
-                     "achieved": round(gemm_tops, 2), "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
-                     "frac": round(gemm_tops / INT8_PEAK_TOPS, 4),
+                     "achieved": round(gemm_tops, 2), "peak": FP8_PEAK_TOPS, "unit": "TFLOP/s",
+                     "frac": round(gemm_tops / FP8_PEAK_TOPS, 4),
                      "traffic": traffic,
                      "ops_per_launch": gemm_ops,
-                     "note": "int8 ops (1 MAC = 2 ops): 36 limb products x 2mnk per launch; peak is the dense int8 rate"},
+                     "note": "fp8 ops (1 MAC = 2 ops): 36 limb products x 2mnk per launch; peak is the dense fp8 rate"},
         "roofline_deconstruct": {"bound": "hbm", "kernel": "deconstruct_kernel<0>+<1>",
                                  "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                  "frac": round(dec_gbs / HBM_PEAK_GBS, 4),

@@ -1,6 +1,6 @@
 /*
  * ozaki25.h -- emulated FP64 matrix multiplication by Ozaki Scheme II on the
- * int8 matrix cores of an AMD Instinct MI355X (gfx950).
+ * FP8 matrix cores of an AMD Instinct MI355X (gfx950).
  *
  * The method (Ozaki Scheme II, Sec. 2 of "Ozaki 2.5: Engineering the
  * Deconstruction Path of FP64-Emulated Dense Matrix Multiplication on FP8
@@ -61,7 +61,7 @@ typedef enum { OZAKI25_MODULI_S12 = 0 } ozaki25_moduli_set;
 #define OZAKI25_NUM_MODULI 12
 #define OZAKI25_NUM_PLANES 30          /* 2 per square modulus + 3 per nonsquare */
 #define OZAKI25_K_ALIGN 128            /* planes are zero padded to a multiple of this */
-#define OZAKI25_MAX_K 4194304          /* int32 limb accumulators: 22^2 * k < 2^31 */
+#define OZAKI25_MAX_K 4194304          /* 256-row plane panels: 32-bit byte offsets */
 #define OZAKI25_MAX_N 8388608          /* columns of B / C (32-bit offsets inside a tile) */
 #define OZAKI25_EXP_NONFINITE INT32_MIN
 #define OZAKI25_NUM_STAGE_EVENTS 5     /* see ozaki25_dgemm_ex */
@@ -98,7 +98,9 @@ size_t ozaki25_planes_bytes(int64_t vecs, int64_t k, ozaki25_moduli_set set);
  *  side 0: X is A (vecs x k, row-major, ldx >= k); vector v is row v.
  *  side 1: X is B (k x vecs, row-major, ldx >= vecs); vector v is column v.
  * Outputs (device, caller-allocated):
- *  planes: int8 [num_planes][vecs][k_pad]; plane q of modulus i is at
+ *  planes: uint8 [num_planes][vecs][k_pad], each byte a limb (an integer in
+ *          [-22, 22]) encoded as OCP FP8 E4M3FN -- every limb is e4m3-exact
+ *          (Lemma 1), zero is 0x00; plane q of modulus i is at
  *          q = (2 per earlier square + 3 per earlier nonsquare) + limb index;
  *          entries with l >= k are zero.
  *  exps:   int32 [vecs], sigma (side 0) or tau (side 1), or
@@ -106,19 +108,21 @@ size_t ozaki25_planes_bytes(int64_t vecs, int64_t k, ozaki25_moduli_set set);
  * vecs == 0 or k == 0 is a no-op.  Errors: INVALID_VALUE (side, sizes, null
  * pointers with nonzero sizes, set), UNSUPPORTED (k > OZAKI25_MAX_K), HIP. */
 ozaki25_status ozaki25_deconstruct(int side, int64_t vecs, int64_t k, const double* X,
-                                   int64_t ldx, ozaki25_moduli_set set, int8_t* planes,
+                                   int64_t ldx, ozaki25_moduli_set set, uint8_t* planes,
                                    int32_t* exps, void* stream);
 
-/* Per-modulus products (Eq. (residueprod)) from stored planes, on int8 MFMA
- * with int32 accumulation: for modulus i the limb products are combined with
- * the square epilogue {1, s, s} (d1 e1 vanishes mod s^2) or Eq. (karcarry)'s
- * {-15, 16, 240}, and reduced to the centred residue.
- *  planesA: int8 [num_planes][m][k_pad] (side 0 of ozaki25_deconstruct)
- *  planesB: int8 [num_planes][n][k_pad] (side 1)
+/* Per-modulus products (Eq. (residueprod)) from stored planes, on FP8 MFMA
+ * with FP32 accumulation, reduced mod m_i at least every 16384 k so that every
+ * partial sum is an integer below 2^24 and exact: for modulus i the limb
+ * products are combined with the square epilogue {1, s, s} (d1 e1 vanishes
+ * mod s^2) or Eq. (karcarry)'s {-15, 16, 240}, and reduced to the centred
+ * residue.
+ *  planesA: uint8 e4m3 [num_planes][m][k_pad] (side 0 of ozaki25_deconstruct)
+ *  planesB: uint8 e4m3 [num_planes][n][k_pad] (side 1)
  *  Cres:    int32 [r][m][n], centred C^(i) (written, caller-allocated)
  * m == 0 or n == 0 is a no-op; k == 0 writes zeros.  Errors as above. */
-ozaki25_status ozaki25_residue_gemm(int64_t m, int64_t n, int64_t k, const int8_t* planesA,
-                                    const int8_t* planesB, ozaki25_moduli_set set,
+ozaki25_status ozaki25_residue_gemm(int64_t m, int64_t n, int64_t k, const uint8_t* planesA,
+                                    const uint8_t* planesB, ozaki25_moduli_set set,
                                     int32_t* Cres, void* stream);
 
 /* Reconstruction (Alg. 3, Eq. (garner), Eq. (horner)): Garner's mixed-radix

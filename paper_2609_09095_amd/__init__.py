@@ -1,4 +1,4 @@
-"""MI355X-native emulated FP64 GEMM by Ozaki Scheme II on int8 MFMA.
+"""MI355X-native emulated FP64 GEMM by Ozaki Scheme II on FP8 MFMA.
 
 Python binding of ``libozaki25.so`` (the C ABI declared in
 ``include/ozaki25.h``).  Argument marshalling only: every step of the
@@ -151,13 +151,13 @@ def ozaki25_dgemm_workspace_size(m: int, n: int, k: int, set: int = S12) -> int:
 # ----------------------------------------------------------------- stages
 def ozaki25_deconstruct(side: int, X, planes=None, exps=None, set: int = S12, stream=None):
     """side 0: X is A (rows); side 1: X is B (columns).  Returns (planes, exps):
-    planes int8 [30][vecs][k_pad], exps int32 [vecs]."""
+    planes uint8 [30][vecs][k_pad] (limbs as OCP e4m3 bytes), exps int32 [vecs]."""
     import torch
     X, ldx = _matrix(X, "X")
     vecs, k = (X.shape[0], X.shape[1]) if side == 0 else (X.shape[1], X.shape[0])
     kp = ozaki25_k_pad(k)
     if planes is None:
-        planes = torch.empty((NUM_PLANES, vecs, kp), dtype=torch.int8, device=X.device)
+        planes = torch.empty((NUM_PLANES, vecs, kp), dtype=torch.uint8, device=X.device)
     if exps is None:
         exps = torch.empty((vecs,), dtype=torch.int32, device=X.device)
     if planes.numel() < NUM_PLANES * vecs * kp or exps.numel() < vecs:

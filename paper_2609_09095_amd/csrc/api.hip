@@ -102,7 +102,7 @@ size_t ozaki25_planes_bytes(int64_t vecs, int64_t k, ozaki25_moduli_set set) {
 }
 
 ozaki25_status ozaki25_deconstruct(int side, int64_t vecs, int64_t k, const double* X, int64_t ldx,
-                                   ozaki25_moduli_set set, int8_t* planes, int32_t* exps,
+                                   ozaki25_moduli_set set, uint8_t* planes, int32_t* exps,
                                    void* stream) {
   if (!known_set(set) || (side != 0 && side != 1) || vecs < 0 || k < 0)
     return OZAKI25_ERR_INVALID_VALUE;
@@ -115,12 +115,13 @@ ozaki25_status ozaki25_deconstruct(int side, int64_t vecs, int64_t k, const doub
   hipStream_t s = (hipStream_t)stream;
   const int t = scale_bits(k);
   hipError_t e = oz::launch_scan(side, vecs, k, X, ldx, t, exps, s);
-  if (e == hipSuccess) e = oz::launch_deconstruct(side, vecs, k, k_pad(k), X, ldx, exps, planes, s);
+  if (e == hipSuccess)
+    e = oz::launch_deconstruct(side, vecs, k, k_pad(k), X, ldx, exps, (int8_t*)planes, s);
   return hip_status(e);
 }
 
-ozaki25_status ozaki25_residue_gemm(int64_t m, int64_t n, int64_t k, const int8_t* planesA,
-                                    const int8_t* planesB, ozaki25_moduli_set set, int32_t* Cres,
+ozaki25_status ozaki25_residue_gemm(int64_t m, int64_t n, int64_t k, const uint8_t* planesA,
+                                    const uint8_t* planesB, ozaki25_moduli_set set, int32_t* Cres,
                                     void* stream) {
   if (!known_set(set) || m < 0 || n < 0 || k < 0) return OZAKI25_ERR_INVALID_VALUE;
   if (k > OZAKI25_MAX_K || n > OZAKI25_MAX_N) return OZAKI25_ERR_UNSUPPORTED;
@@ -128,8 +129,8 @@ ozaki25_status ozaki25_residue_gemm(int64_t m, int64_t n, int64_t k, const int8_
   if (!Cres || (k > 0 && (!planesA || !planesB))) return OZAKI25_ERR_INVALID_VALUE;
   if (((uintptr_t)planesA & 15) || ((uintptr_t)planesB & 15) || ((uintptr_t)Cres & 3))
     return OZAKI25_ERR_INVALID_VALUE;
-  return hip_status(oz::launch_residue_gemm_i32(m, n, k_pad(k), planesA, planesB, Cres,
-                                                (hipStream_t)stream));
+  return hip_status(oz::launch_residue_gemm_i32(m, n, k_pad(k), (const int8_t*)planesA,
+                                                (const int8_t*)planesB, Cres, (hipStream_t)stream));
 }
 
 ozaki25_status ozaki25_reconstruct(int64_t m, int64_t n, const int32_t* Cres, const int32_t* expsA,

@@ -1,5 +1,6 @@
 // Deconstruction (Alg. 2): scale by 2^sigma, round to nearest even, twelve
-// centred residues, limb split, packed int8 plane stores.
+// centred residues, limb split, packed e4m3 plane stores (every limb is an
+// e4m3-exact integer, Lemma 1, so the conversion is exact).
 //
 // Each thread owns one vector (row of A / column of B) and 16 consecutive k,
 // so every plane store is one 16-byte write.  HBM-bound: 8 bytes read and 30
@@ -20,9 +21,10 @@ namespace {
 
 constexpr int kElems = 16;  // k values per thread
 
+// four limbs as e4m3 bytes (OCP E4M3FN), the first in the low byte
 __device__ __forceinline__ uint32_t pack4(int a, int b, int c, int d) {
-  return (uint32_t)(a & 0xFF) | ((uint32_t)(b & 0xFF) << 8) | ((uint32_t)(c & 0xFF) << 16) |
-         ((uint32_t)d << 24);
+  const int lo = __builtin_amdgcn_cvt_pk_fp8_f32((float)a, (float)b, 0, false);
+  return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32((float)c, (float)d, lo, true);
 }
 
 __device__ __forceinline__ void store16(int8_t* p, const int (&b)[kElems]) {

@@ -1,21 +1,30 @@
-// Per-modulus residue products (Eq. (residueprod)) on gfx950 int8 MFMA.
+// Per-modulus residue products (Eq. (residueprod)) on gfx950 FP8 MFMA.
 //
 // Each modulus needs three limb products of length k (square m = s^2: d0e1,
 // d1e0 with weight s and d0e0 with weight 1 -- the d1e1 term vanishes mod
 // s^2; nonsquare, Eq. (karcarry): d0e0, d1e1, (d0+d1)(e0+e1) with weights
-// -15, 240, 16).  A block owns one 256 x 256 output tile of one modulus and
-// runs the three products through ONE set of int32 MFMA accumulators: after
-// product p the accumulator is reduced mod m and multiplied by
-// w_p / w_{p+1} mod m (w_{p+1} is invertible whenever it differs from w_p),
-// so product p+1 accumulates on top of it and
-//     w_last * acc = sum_p w_p P_p   (mod m)
-// at the end.  Between reductions an accumulator holds at most m plus one
-// int8 dot product, |.| <= 22^2 k < 2^31 for k <= 4 194 304.
+// -15, 240, 16).  The planes hold the limbs as e4m3 bytes (every limb is
+// e4m3-exact, Lemma 1), and v_mfma_f32_32x32x64_f8f6f4 multiplies them with
+// FP32 accumulation, exact while every partial sum is an integer below 2^24.
 //
-// Layout: both plane operands are K-contiguous (rows of A, columns of B), the
-// form v_mfma_i32_32x32x32_i8 takes for both sides.  Its A and B register
-// layouts mirror each other, so loading both with lane = row/column +
-// 32 * (16-byte K half) pairs the same k on both sides.
+// A block owns one 256 x 256 output tile of one modulus and runs the three
+// products through ONE set of accumulators: after product p the accumulator
+// is reduced mod m and multiplied by w_p / w_{p+1} mod m (w_{p+1} is
+// invertible whenever it differs from w_p), so product p+1 accumulates on
+// top of it and
+//     w_last * acc = sum_p w_p P_p   (mod m)
+// at the end.  Products longer than kSeg stages (16384 k) are cut into
+// segments with a plain reduction between them, which keeps every sum
+// between two reductions below 2^24: at most 0.51 m + 22^2 * 16384, or
+// 0.51 m + 2 * 16^2 * 16384 for the two square products that share an
+// accumulator unreduced (only when each fits one segment).  This is the
+// paper's chunked FP32 accumulation (its depth limit 2^24 / 22^2 = 34663),
+// with the chunk at a power of two below it.
+//
+// Layout: both plane operands are K-contiguous (rows of A, columns of B).
+// The MFMA's A and B register layouts mirror each other: lane l holds
+// row/column l%32 and 32 of the 64 k bytes of the step, the same 32 on both
+// sides for equal l/32, so any fixed choice of those bytes pairs equal k.
 //
 // Tiling (4 wavefronts, 1 per SIMD): 256 x 256 block tile, 128 x 128 per
 // wavefront (4 x 4 MFMA blocks of 32 x 32), K stages of 128 bytes loaded
@@ -27,9 +36,10 @@
 // fragment reads of 8 (or 16) consecutive rows hit distinct banks.  Plane
 // rows are padded to a multiple of 128 bytes, so every stage is full.
 //
-// At this tile size the operand stream is 64 KiB per CU per 2048 MFMA
-// cycles (32 B/clk); the per-CU L2 read throughput that the counters show
-// (~20 B/clk at ~530 cycles average latency) is the bound, not the MFMAs.
+// At this tile size the operand stream is 64 KiB per CU per stage of 2048
+// MFMA cycles (32 B/clk at the FP8 peak); direct-to-LDS loads deliver about
+// 20 B/clk per CU here, and the MFMA rate itself drops with the switching
+// activity of dense data, so neither side runs at its nominal peak.
 #include "device_math.hpp"
 #include "kernels.hpp"
 #include "moduli.hpp"
@@ -38,7 +48,8 @@ namespace oz {
 namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
-typedef int v16i __attribute__((ext_vector_type(16)));
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
 
 constexpr int BM = 256;         // output rows per block
 constexpr int BN = 256;         // output columns per block
@@ -46,6 +57,7 @@ constexpr int BK = 128;         // k bytes per stage
 constexpr int kTile = BM * BK;  // bytes of one operand tile in LDS (BM == BN)
 static_assert(BK == kKAlign, "every K stage is full: planes are padded to BK");
 constexpr int kGroupM = 4;      // tile rows per group in the block order
+constexpr int kSeg = 128;       // K stages (16384 k) per accumulation segment
 
 // Per-modulus schedule, from the compile-time tables of moduli.hpp.
 struct ModSched {
@@ -99,15 +111,18 @@ __constant__ ModSched kSched[kR] = {make_sched(0), make_sched(1), make_sched(2),
                                     make_sched(4), make_sched(5), make_sched(6),  make_sched(7),
                                     make_sched(8), make_sched(9), make_sched(10), make_sched(11)};
 
-// acc * mult reduced mod m to a representative in [-m/2, m/2]: acc * mult is
-// exact in FP64 (|acc| < 2^31, mult < 2^11), its quotient by m is off from
-// the nearest integer by far less than 1/(2m) (odd m: never a tie; m = 1024:
-// exact), and the remainder is exact in one FMA.  Ties of the even modulus
-// may land on +m/2; the final reduction maps them to -m/2.
-__device__ __forceinline__ int mulmod_rt(int acc, double mult, double m, double mult_inv) {
-  const double a = (double)acc;
-  const double q = __builtin_rint(a * mult_inv);     // mult_inv = mult / m
-  return (int)__builtin_fma(a, mult, -q * m);         // a * mult exact, q * m exact
+// Modular reduction of an integer-valued fp32 accumulator, |x| < 2^24:
+// q = rint(x * (1/m)) is the nearest quotient or one off (the fp32 quotient
+// errs by far less than 1/100), x - q m is an integer below m in magnitude
+// and comes out of the FMA exactly, so the result is congruent to x with
+// |result| <= 0.51 m.
+__device__ __forceinline__ float reduce_f(float x, float m, float minv) {
+  const float q = __builtin_rintf(x * minv);
+  return __builtin_fmaf(-q, m, x);
+}
+// acc * mult mod m: reduce, multiply (|.| <= 0.51 m * mult < 2^24, exact), reduce
+__device__ __forceinline__ float mulmod_f(float x, float mult, float m, float minv) {
+  return reduce_f(reduce_f(x, m, minv) * mult, m, minv);
 }
 
 __device__ __forceinline__ int swz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
@@ -157,55 +172,85 @@ __device__ __forceinline__ void stage_load(__amdgpu_buffer_rsrc_t ra, __amdgpu_b
   }
 }
 
-__device__ __forceinline__ void load_frags(const int8_t* la, const int8_t* lb, int wr, int wc, int fr,
-                                           int fh, int ks, v4i (&af)[4], v4i (&bf)[4]) {
-#pragma unroll
-  for (int a = 0; a < 4; ++a) {
-    const int r = wr * 128 + a * 32 + fr;
-    af[a] = *reinterpret_cast<const v4i*>(la + r * BK + (((2 * ks + fh) ^ swz(r)) << 4));
-  }
-#pragma unroll
-  for (int b = 0; b < 4; ++b) {
-    const int r = wc * 128 + b * 32 + fr;
-    bf[b] = *reinterpret_cast<const v4i*>(lb + r * BK + (((2 * ks + fh) ^ swz(r)) << 4));
-  }
+__device__ __forceinline__ v8i cat(v4i lo, v4i hi) {
+  return v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
 }
 
-// One stage of MFMAs with the next stage's 16 DMA loads spread among them:
-// the fragments of step 0 first, then per K step [1 fragment read of the
-// next step, 1 DMA (steps 0-1 only), 2 MFMAs] x 8.
+// fp8 fragment of one 32-row block for one 64-byte K step: lane half fh
+// takes 16-byte chunks 4 ks + fh and 4 ks + 2 + fh of its row (the same on
+// both sides, so the MFMA pairs equal k)
+__device__ __forceinline__ v8i frag(const int8_t* base, int r, int ks, int fh) {
+  const int8_t* row = base + r * BK;
+  return cat(*reinterpret_cast<const v4i*>(row + (((4 * ks + fh) ^ swz(r)) << 4)),
+             *reinterpret_cast<const v4i*>(row + (((4 * ks + 2 + fh) ^ swz(r)) << 4)));
+}
+
+// One stage: two 64-byte K steps of 4 x 4 MFMAs in row-major order.  B's
+// four fragments of a step stay in registers; A's come one row block at a
+// time, the next one read while the current row's MFMAs run, and the next
+// step's B fragments are read during the last row.  The next stage's 16
+// DMA loads go among the first step's MFMAs.
 __device__ __forceinline__ void stage_mma_dma(const int8_t* la, const int8_t* lb, int wr, int wc,
-                                              int fr, int fh, v16i (&acc)[4][4],
+                                              int fr, int fh, v16f (&acc)[4][4],
                                               __amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rb,
                                               int8_t* na, int8_t* nb, const int (&voff)[8], int k0,
                                               int wave) {
-  v4i af[2][4], bf[2][4];
-  load_frags(la, lb, wr, wc, fr, fh, 0, af[0], bf[0]);
+  const int ra0 = wr * 128 + fr, rb0 = wc * 128 + fr;
+  v8i bcur[4], bnext[4], acur, anext;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int slab = (wave * 8 + i) * 1024;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr)(na + slab), 16, voff[i], k0, 0, 0);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr)(nb + slab), 16, voff[i], k0, 0, 0);
-  }
+  for (int b = 0; b < 4; ++b) bcur[b] = frag(lb, rb0 + 32 * b, 0, fh);
+  acur = frag(la, ra0, 0, fh);
 #pragma unroll
-  for (int ks = 0; ks < BK / 32; ++ks) {
-    const int cur = ks & 1;
-    if (ks + 1 < BK / 32) load_frags(la, lb, wr, wc, fr, fh, ks + 1, af[cur ^ 1], bf[cur ^ 1]);
+  for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
+    for (int a = 0; a < 4; ++a) {
+      if (a < 3) anext = frag(la, ra0 + 32 * (a + 1), ks, fh);
+      if (a == 3 && ks == 0) {
 #pragma unroll
-      for (int b = 0; b < 4; ++b)
-        acc[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[cur][a], bf[cur][b], acc[a][b], 0, 0, 0);
-  }
-  __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+        for (int b = 0; b < 4; ++b) bnext[b] = frag(lb, rb0 + 32 * b, 1, fh);
+        anext = frag(la, ra0, 1, fh);
+      }
 #pragma unroll
-  for (int ks = 0; ks < BK / 32; ++ks)
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      if (ks + 1 < BK / 32) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      if (ks < 2) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      for (int b = 0; b < 4; ++b) {
+        if (ks == 0) {
+          const int i = a * 4 + b;  // DMA i of 16: (slab i/2, side i%2)
+          const int slab = (wave * 8 + (i >> 1)) * 1024;
+          if (i & 1)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr)(nb + slab), 16, voff[i >> 1], k0, 0, 0);
+          else
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr)(na + slab), 16, voff[i >> 1], k0, 0, 0);
+        }
+        acc[a][b] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(acur, bcur[b], acc[a][b], 0, 0, 0,
+                                                                    0, 0, 0);
+      }
+      acur = anext;
     }
+    if (ks == 0) {
+#pragma unroll
+      for (int b = 0; b < 4; ++b) bcur[b] = bnext[b];
+    }
+  }
+  // issue order: 10 fragment reads; step 0: per row its fragment reads (the
+  // next row's A, or the next step's B and first A), then 4 x [DMA, MFMA];
+  // step 1: per row the next row's A reads, then 4 MFMAs
+  __builtin_amdgcn_sched_group_barrier(0x100, 10, 0);
+#pragma unroll
+  for (int a = 0; a < 4; ++a) {
+    if (a < 3)
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    else
+      __builtin_amdgcn_sched_group_barrier(0x100, 10, 0);
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    }
+  }
+#pragma unroll
+  for (int a = 0; a < 4; ++a) {
+    if (a < 3) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+  }
 }
 
 template <typename OT>
@@ -241,45 +286,55 @@ __global__ __launch_bounds__(256, 1) void residue_gemm_kernel(int64_t m, int64_t
   const int64_t rows_a = m - tm * BM < BM ? m - tm * BM : BM;
   const int64_t rows_b = n - tn * BN < BN ? n - tn * BN : BN;
 
-  v16i acc[4][4];
+  v16f acc[4][4];
 #pragma unroll
   for (int a = 0; a < 4; ++a)
 #pragma unroll
-    for (int b = 0; b < 4; ++b) acc[a][b] = v16i{};
+    for (int b = 0; b < 4; ++b) acc[a][b] = v16f{};
 
+  // The three products run as segments of at most kSeg stages: every fp32
+  // accumulator sum between two reductions stays below 2^24 (at most
+  // 545 + 484 * 128 * kSeg, or two square products of 16 x 16 terms when the
+  // whole product fits one segment).  A segment ends with the carry (the
+  // product's multiplier after its last segment, a plain reduction after the
+  // others; none mid-way between the two square products of weight s while
+  // they fit one segment each).
   const int nstage = (int)(kp / BK);
-  for (int p = 0; p < 3 && nstage > 0; ++p) {
-    const int8_t* A = uniform_ptr(pa + ((int64_t)sc.plane_a[p] * m + tm * BM) * kp);
-    const int8_t* B = uniform_ptr(pb + ((int64_t)sc.plane_b[p] * n + tn * BN) * kp);
+  const int nseg = nstage > 0 ? (nstage + kSeg - 1) / kSeg : 0;  // segments per product
+  for (int g = 0; g < 3 * nseg; ++g) {
+    const int p = g / nseg, c = g - p * nseg;
+    const int s0 = c * kSeg, s1 = s0 + kSeg < nstage ? s0 + kSeg : nstage;
+    const int8_t* A = uniform_ptr(pa + ((int64_t)kSched[mod].plane_a[p] * m + tm * BM) * kp);
+    const int8_t* B = uniform_ptr(pb + ((int64_t)kSched[mod].plane_b[p] * n + tn * BN) * kp);
     const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
         (void*)A, (short)0, __builtin_amdgcn_readfirstlane((int)(rows_a * kp)), 0x00020000);
     const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
         (void*)B, (short)0, __builtin_amdgcn_readfirstlane((int)(rows_b * kp)), 0x00020000);
 
-    stage_load(ra, rb, lds_a0, lds_b0, voff, 0, wave);
-    for (int s = 0; s < nstage; s += 2) {
+    stage_load(ra, rb, lds_a0, lds_b0, voff, s0 * BK, wave);
+    for (int s = s0; s < s1; s += 2) {
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
-      // the DMA of the stage after the last one reads past the panel: harmless,
-      // it lands in the idle buffer and is drained before the next product
+      // the DMA of the stage after the segment's last one lands in the idle
+      // buffer (zeros past the panel) and is drained before the next segment
       stage_mma_dma(lds_a0, lds_b0, wr, wc, fr, fh, acc, ra, rb, lds_a1, lds_b1, voff, (s + 1) * BK, wave);
-      if (s + 1 >= nstage) break;
+      if (s + 1 >= s1) break;
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
       stage_mma_dma(lds_a1, lds_b1, wr, wc, fr, fh, acc, ra, rb, lds_a0, lds_b0, voff, (s + 2) * BK, wave);
     }
     __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();  // every wave is done with the buffers before the next product loads
-    // carry: acc <- acc * mult_p mod m (a multiplier of 1 mid-way needs no reduction)
-    const int mult = sc.mult[p];
-    if (p == 2 || mult != 1) {
-      const double dm = (double)sc.m, dmult = (double)mult, dinv = (double)mult / (double)sc.m;
+    __syncthreads();  // every wave is done with the buffers before the next segment loads
+    const bool last = c == nseg - 1;
+    const int mult = last ? kSched[mod].mult[p] : 1;
+    if (p == 2 || mult != 1 || nseg > 1) {
+      const float fm = (float)sc.m, fmult = (float)mult, finv = 1.0f / (float)sc.m;
 #pragma unroll
       for (int a = 0; a < 4; ++a)
 #pragma unroll
         for (int b = 0; b < 4; ++b)
 #pragma unroll
-          for (int v = 0; v < 16; ++v) acc[a][b][v] = mulmod_rt(acc[a][b][v], dmult, dm, dinv);
+          for (int v = 0; v < 16; ++v) acc[a][b][v] = mulmod_f(acc[a][b][v], fmult, fm, finv);
     }
   }
 
@@ -298,9 +353,10 @@ __global__ __launch_bounds__(256, 1) void residue_gemm_kernel(int64_t m, int64_t
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int row = row0 + 8 * (v >> 2) + (v & 3);
-        // representatives lie in [-m/2, m/2]: only +m/2 (even m) needs wrapping
-        const int r = acc[a][b][v];
-        if (row < rows_left && col < cols_left) out[row * nn + col] = (OT)(r > sc.hi ? r - sc.m : r);
+        // the final carry leaves |r| <= 0.51 m: wrap into [-(m/2), (m-1)/2]
+        const int r = (int)acc[a][b][v];
+        const int c = r > sc.hi ? r - sc.m : (r < -(sc.m >> 1) ? r + sc.m : r);
+        if (row < rows_left && col < cols_left) out[row * nn + col] = (OT)c;
       }
     }
 }

@@ -73,6 +73,24 @@ def assert_int_equal(got: np.ndarray, want: np.ndarray, what: str):
         raise AssertionError(f"{what}: {len(bad)} entries differ; first at {idx}: got {got[idx]} want {want[idx]}")
 
 
+def e4m3_bytes(limbs: np.ndarray) -> np.ndarray:
+    """OCP FP8 E4M3FN encoding of integer limbs (the stored plane format),
+    written from the format: sign bit, 4-bit exponent of bias 7, 3-bit
+    mantissa; zero is 0x00.  Integers need no subnormals.  Raises if a value
+    is not exactly representable (Lemma 1 says every limb is)."""
+    v = np.asarray(limbs).astype(np.int64)
+    a = np.abs(v)
+    if np.any(a > 240):
+        raise ValueError("limb beyond the e4m3 integer range")
+    e = (a >= 2).astype(np.int64) + (a >= 4) + (a >= 8) + (a >= 16) + (a >= 32) + (a >= 64) + (a >= 128)
+    frac = (a - (np.int64(1) << e)) * 8  # mantissa * 2^e
+    if np.any((a > 0) & (frac % (np.int64(1) << e) != 0)):
+        raise ValueError("limb not exactly representable in e4m3")
+    mant = frac >> e
+    code = ((v < 0).astype(np.int64) << 7) | ((e + 7) << 3) | mant
+    return np.where(a == 0, 0, code).astype(np.uint8)
+
+
 def sample_indices(n: int, count: int, seed: int) -> np.ndarray:
     """Sorted sample of indices that always includes both ends (ragged tails)."""
     rng = np.random.default_rng(seed)

@@ -12,7 +12,7 @@ import pytest
 import oracle
 import paper_2609_09095_amd as oz
 import workloads
-from gpu_util import assert_bits_equal, assert_int_equal, log, require_gpu, sample_indices
+from gpu_util import assert_bits_equal, assert_int_equal, e4m3_bytes, log, require_gpu, sample_indices
 
 pytestmark = pytest.mark.gpu
 
@@ -61,8 +61,8 @@ def _run(name, nsample=96):
     assert_int_equal(eA, oracle.exponents(A, 0, t), "sigma (all rows)")
     assert_int_equal(eB, oracle.exponents(B, 1, t), "tau (all columns)")
     r = oracle.dgemm(A, B, C_in=C0, rows=rows, cols=cols)
-    assert_int_equal(pA_s, r.planesA, "planes of sampled rows of A")
-    assert_int_equal(pB_s, r.planesB, "planes of sampled columns of B")
+    assert_int_equal(pA_s, e4m3_bytes(r.planesA), "planes of sampled rows of A")
+    assert_int_equal(pB_s, e4m3_bytes(r.planesB), "planes of sampled columns of B")
     assert_int_equal(Cres_s, r.Cres, "per-modulus products (sampled)")
     assert_bits_equal(C_s, r.C, "C (sampled)")
     log(f"[large] {name}: ok")

@@ -12,8 +12,8 @@ import pytest
 import oracle
 import paper_2609_09095_amd as oz
 import workloads
-from gpu_util import (assert_bits_equal, assert_int_equal, gpu_deconstruct, gpu_dgemm, log,
-                      require_gpu, to_dev)
+from gpu_util import (assert_bits_equal, assert_int_equal, e4m3_bytes, gpu_deconstruct, gpu_dgemm,
+                      log, require_gpu, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -41,7 +41,7 @@ def test_deconstruct_matches_oracle(shape, s, seed, side):
     planes, exps = gpu_deconstruct(X, side)
     e, P = _oracle_side(X, side)
     assert_int_equal(exps.cpu().numpy(), e, "exponents")
-    assert_int_equal(planes.cpu().numpy(), P, "planes")
+    assert_int_equal(planes.cpu().numpy(), e4m3_bytes(P), "planes")
 
 
 def _edge_matrix(rows, k, seed):
@@ -75,7 +75,7 @@ def test_deconstruct_edge_values(side, k):
     planes, exps = gpu_deconstruct(X, side)
     e, P = _oracle_side(X, side)
     assert_int_equal(exps.cpu().numpy(), e, "exponents")
-    assert_int_equal(planes.cpu().numpy(), P, "planes")
+    assert_int_equal(planes.cpu().numpy(), e4m3_bytes(P), "planes")
     assert exps.cpu().numpy()[3] == oz.EXP_NONFINITE and exps.cpu().numpy()[4] == oz.EXP_NONFINITE
 
 
@@ -89,7 +89,7 @@ def test_deconstruct_leading_dimension():
     torch.cuda.synchronize()
     e, P = _oracle_side(X, 0)
     assert_int_equal(exps.cpu().numpy(), e, "exponents")
-    assert_int_equal(planes.cpu().numpy(), P, "planes")
+    assert_int_equal(planes.cpu().numpy(), e4m3_bytes(P), "planes")
 
 
 # ------------------------------------------------------------ residue products
@@ -104,7 +104,7 @@ def test_residue_gemm_matches_oracle(m, n, k, seed):
     ZA = oracle.quantise_vectors(A, 0, oracle.exponents(A, 0, t))
     ZB = oracle.quantise_vectors(B, 1, oracle.exponents(B, 1, t))
     PA, PB = oracle.planes(ZA), oracle.planes(ZB)
-    C = oz.ozaki25_residue_gemm(m, n, k, to_dev(PA), to_dev(PB))
+    C = oz.ozaki25_residue_gemm(m, n, k, to_dev(e4m3_bytes(PA)), to_dev(e4m3_bytes(PB)))
     torch.cuda.synchronize()
     want = oracle.residue_gemm(oracle.residues(ZA), oracle.residues(ZB))
     assert_int_equal(C.cpu().numpy(), want, "per-modulus products")
@@ -118,7 +118,28 @@ def test_residue_gemm_full_range_residues():
     m, n, k = 96, 160, 320
     ZA = rng.integers(-(1 << 62), 1 << 62, size=(m, k), dtype=np.int64)
     ZB = rng.integers(-(1 << 62), 1 << 62, size=(n, k), dtype=np.int64)
-    C = oz.ozaki25_residue_gemm(m, n, k, to_dev(oracle.planes(ZA)), to_dev(oracle.planes(ZB)))
+    C = oz.ozaki25_residue_gemm(m, n, k, to_dev(e4m3_bytes(oracle.planes(ZA))),
+                                to_dev(e4m3_bytes(oracle.planes(ZB))))
+    torch.cuda.synchronize()
+    want = oracle.residue_gemm(oracle.residues(ZA), oracle.residues(ZB))
+    assert_int_equal(C.cpu().numpy(), want, "per-modulus products")
+
+
+@pytest.mark.parametrize("k", [16384, 16512, 20000, 33000])
+def test_residue_gemm_long_constant_rows(k):
+    """Rows of A and columns of B that repeat one value: every term of a
+    limb product has the same sign and size, so the FP32 accumulator sums
+    grow linearly in k -- up to 22^2 * 16384 between reductions -- and the
+    products cross one, two or three accumulation segments."""
+    log(f"residue gemm, constant rows, k={k}")
+    import torch
+    rng = np.random.default_rng(k)
+    m, n = 40, 72
+    za = rng.integers(-(1 << 50), 1 << 50, size=(m, 1), dtype=np.int64)
+    zb = rng.integers(-(1 << 50), 1 << 50, size=(n, 1), dtype=np.int64)
+    ZA, ZB = np.repeat(za, k, axis=1), np.repeat(zb, k, axis=1)
+    C = oz.ozaki25_residue_gemm(m, n, k, to_dev(e4m3_bytes(oracle.planes(ZA))),
+                                to_dev(e4m3_bytes(oracle.planes(ZB))))
     torch.cuda.synchronize()
     want = oracle.residue_gemm(oracle.residues(ZA), oracle.residues(ZB))
     assert_int_equal(C.cpu().numpy(), want, "per-modulus products")
@@ -127,7 +148,7 @@ def test_residue_gemm_full_range_residues():
 def test_residue_gemm_k_zero_writes_zeros():
     import torch
     C = torch.full((12, 3, 4), 7, dtype=torch.int32, device="cuda")
-    dummy = torch.zeros(16, dtype=torch.int8, device="cuda")
+    dummy = torch.zeros(16, dtype=torch.uint8, device="cuda")
     oz.ozaki25_residue_gemm(3, 4, 0, dummy, dummy, C)
     torch.cuda.synchronize()
     assert not C.cpu().numpy().any()
@@ -219,8 +240,8 @@ def test_dgemm_tiny_workload():
     planesB, expsB = gpu_deconstruct(B, 1)
     assert_int_equal(expsA.cpu().numpy(), r.sigma, "sigma")
     assert_int_equal(expsB.cpu().numpy(), r.tau, "tau")
-    assert_int_equal(planesA.cpu().numpy(), r.planesA, "planes A")
-    assert_int_equal(planesB.cpu().numpy(), r.planesB, "planes B")
+    assert_int_equal(planesA.cpu().numpy(), e4m3_bytes(r.planesA), "planes A")
+    assert_int_equal(planesB.cpu().numpy(), e4m3_bytes(r.planesB), "planes B")
 
 
 def test_dgemm_reach_workload():
@@ -235,8 +256,8 @@ def test_dgemm_reach_workload():
     planesB, expsB = gpu_deconstruct(B, 1)
     assert_int_equal(expsA.cpu().numpy(), r.sigma, "sigma")
     assert_int_equal(expsB.cpu().numpy(), r.tau, "tau")
-    assert_int_equal(planesA.cpu().numpy(), r.planesA, "planes A")
-    assert_int_equal(planesB.cpu().numpy(), r.planesB, "planes B")
+    assert_int_equal(planesA.cpu().numpy(), e4m3_bytes(r.planesA), "planes A")
+    assert_int_equal(planesB.cpu().numpy(), e4m3_bytes(r.planesB), "planes B")
     Cres = oz.ozaki25_residue_gemm(256, 256, 8192, planesA, planesB)
     torch.cuda.synchronize()
     assert_int_equal(Cres.cpu().numpy(), r.Cres, "per-modulus products")
