@@ -116,7 +116,7 @@ ozaki25_status ozaki25_deconstruct(int side, int64_t vecs, int64_t k, const doub
   const int t = scale_bits(k);
   hipError_t e = oz::launch_scan(side, vecs, k, X, ldx, t, exps, s);
   if (e == hipSuccess)
-    e = oz::launch_deconstruct(side, vecs, k, k_pad(k), X, ldx, exps, (int8_t*)planes, s);
+    e = oz::launch_deconstruct(side, vecs, k, k_pad(k), t, X, ldx, exps, (int8_t*)planes, s);
   return hip_status(e);
 }
 
@@ -197,8 +197,8 @@ ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A
   if (e == hipSuccess) e = oz::launch_scan(0, m, k, A, lda, t, ea, s);
   if (e == hipSuccess) e = oz::launch_scan(1, n, k, B, ldb, t, eb, s);
   if (ev && e == hipSuccess) e = hipEventRecord(ev[1], s);
-  if (e == hipSuccess) e = oz::launch_deconstruct(0, m, k, kp, A, lda, ea, pa, s);
-  if (e == hipSuccess) e = oz::launch_deconstruct(1, n, k, kp, B, ldb, eb, pb, s);
+  if (e == hipSuccess) e = oz::launch_deconstruct(0, m, k, kp, t, A, lda, ea, pa, s);
+  if (e == hipSuccess) e = oz::launch_deconstruct(1, n, k, kp, t, B, ldb, eb, pb, s);
   if (ev && e == hipSuccess) e = hipEventRecord(ev[2], s);
   if (e == hipSuccess) e = oz::launch_residue_gemm_i16(m, n, kp, pa, pb, cres, s);
   if (ev && e == hipSuccess) e = hipEventRecord(ev[3], s);

@@ -3,13 +3,14 @@
 // e4m3-exact integer, Lemma 1, so the conversion is exact).
 //
 // Each thread owns one vector (row of A / column of B) and 16 consecutive k,
-// so every plane store is one 16-byte write.  HBM-bound: 8 bytes read and 30
-// bytes written per element.
+// so every plane store is one 16-byte write.  Bound by VALU work (about 300
+// instructions per element) with HBM close behind: 8 bytes read and 30 bytes
+// written per element.
 //  - A (side 0): a wavefront covers 1 row x 1024 k, so each plane store of the
 //    wavefront is 1 KiB contiguous.
-//  - B (side 1): a wavefront covers 32 columns x 32 k; every FP64 load of the
-//    wavefront reads 256 contiguous bytes of two rows of B; a block writes 128
-//    contiguous plane bytes per column.
+//  - B (side 1): a wavefront covers 8 columns x 128 k, so each plane store of
+//    the wavefront fills eight whole 128-byte lines; every FP64 load reads 64
+//    contiguous bytes of 8 rows of B.
 #include <utility>
 
 #include "device_math.hpp"
@@ -22,12 +23,12 @@ namespace {
 constexpr int kElems = 16;  // k values per thread
 
 // four limbs as e4m3 bytes (OCP E4M3FN), the first in the low byte
-__device__ __forceinline__ uint32_t pack4(int a, int b, int c, int d) {
-  const int lo = __builtin_amdgcn_cvt_pk_fp8_f32((float)a, (float)b, 0, false);
-  return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32((float)c, (float)d, lo, true);
+__device__ __forceinline__ uint32_t pack4(float a, float b, float c, float d) {
+  const int lo = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+  return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(c, d, lo, true);
 }
 
-__device__ __forceinline__ void store16(int8_t* p, const int (&b)[kElems]) {
+__device__ __forceinline__ void store16(int8_t* p, const float (&b)[kElems]) {
   uint4 w;
   w.x = pack4(b[0], b[1], b[2], b[3]);
   w.y = pack4(b[4], b[5], b[6], b[7]);
@@ -36,20 +37,44 @@ __device__ __forceinline__ void store16(int8_t* p, const int (&b)[kElems]) {
   *reinterpret_cast<uint4*>(p) = w;
 }
 
-// Square modulus s^2 (Eq. (pieces) with base s): d0 = centred d mod s (the
-// balanced digit, [-16, 15] for s = 32), d1 = (d - d0) / s.
-template <int S>
-__device__ __forceinline__ void split_square(int d, int& d0, int& d1) {
-  if constexpr (S == 32) {
-    d0 = ((d + 16) & 31) - 16;
-    d1 = (d - d0) >> 5;
+// Centred residue of the integer-valued y modulo M, in [-(M/2), (M-1)/2].
+// EXACT (|y| <= 2^50): the FP64 quotient y * RN(1/M) is within |y| 2^-52 / M
+// <= 1/(4M) of y / M, while for odd M y / M is at least 1/(2M) away from a
+// half integer, so rint gives the nearest quotient and y - qM is already
+// centred; for M = 1024 the quotient is exact and only the tie +512 needs
+// mapping to -512.  Otherwise the general form with its two corrections.
+template <int M, bool EXACT>
+__device__ __forceinline__ int centred_residue(double y) {
+  if constexpr (!EXACT) {
+    return cmod_f64<M>(y);
   } else {
-    // |d| <= 544 and s odd: d / s is never within 1/(2s) of a half integer,
-    // far above the FP32 error of d * (1/s), so rint gives the nearest digit.
-    constexpr float inv = 1.0f / S;
-    d1 = (int)__builtin_rintf((float)d * inv);
-    d0 = d - S * d1;
+    constexpr double inv = 1.0 / M;
+    const int r = (int)__builtin_fma(-__builtin_rint(y * inv), (double)M, y);
+    if constexpr ((M & 1) == 0)
+      return r == M / 2 ? -(M / 2) : r;
+    else
+      return r;
   }
+}
+
+// Square modulus s^2 (Eq. (pieces) with base s): d0 = centred d mod s (the
+// balanced digit, [-16, 15] for s = 32), d1 = (d - d0) / s.  |d| <= 544, so
+// every step is exact in FP32 and the digits come out as the floats the
+// e4m3 conversion takes.
+template <int S>
+__device__ __forceinline__ void split_square(int d, float& d0, float& d1) {
+  const float df = (float)d;
+  if constexpr (S % 2 == 0) {
+    // d1 = floor((d + s/2) / s): d0 lands in [-s/2, s/2)
+    d1 = __builtin_floorf(__builtin_fmaf(df, 1.0f / S, 0.5f));
+  } else {
+    // odd s: d / s is never within 1/(2s) of a half integer, far above the
+    // FP32 error of d * (1/s), so rint gives the nearest digit (+ 0 turns
+    // the -0 that rint returns for small negative quotients into +0, whose
+    // e4m3 code is 0x00)
+    d1 = __builtin_rintf(df * (1.0f / S)) + 0.0f;
+  }
+  d0 = __builtin_fmaf(-(float)S, d1, df);
 }
 
 // Nonsquare modulus (Lemma 1): canonical balanced base-16 split, then one
@@ -65,53 +90,54 @@ __device__ __forceinline__ void split_16(int d, int& d0, int& d1) {
   d1 = carry ? d1 + sg : d1;
 }
 
-template <int I>
+template <int I, bool EXACT>
 __device__ __forceinline__ void emit_modulus(const double (&y)[kElems], int8_t* planes,
                                              int64_t plane_stride, int64_t off) {
   constexpr int M = kModulus[I];
   constexpr int S = root_of(I);
   constexpr int Q = plane_base(I);
   int8_t* base = planes + (int64_t)Q * plane_stride + off;
-  int l0[kElems], l1[kElems];
+  float l0[kElems], l1[kElems], l2[kElems];
 #pragma unroll
   for (int c = 0; c < kElems; ++c) {
-    const int d = cmod_f64<M>(y[c]);
-    if constexpr (S != 0)
+    const int d = centred_residue<M, EXACT>(y[c]);
+    if constexpr (S != 0) {
       split_square<S>(d, l0[c], l1[c]);
-    else
-      split_16(d, l0[c], l1[c]);
+    } else {
+      int d0, d1;
+      split_16(d, d0, d1);
+      l0[c] = (float)d0;
+      l1[c] = (float)d1;
+      l2[c] = (float)(d0 + d1);
+    }
   }
   store16(base, l0);
   store16(base + plane_stride, l1);
-  if constexpr (S == 0) {
-    int l2[kElems];
-#pragma unroll
-    for (int c = 0; c < kElems; ++c) l2[c] = l0[c] + l1[c];
-    store16(base + 2 * plane_stride, l2);
-  }
+  if constexpr (S == 0) store16(base + 2 * plane_stride, l2);
 }
 
-template <int... I>
+template <bool EXACT, int... I>
 __device__ __forceinline__ void emit_all(std::integer_sequence<int, I...>, const double (&y)[kElems],
                                          int8_t* planes, int64_t plane_stride, int64_t off) {
-  (emit_modulus<I>(y, planes, plane_stride, off), ...);
+  (emit_modulus<I, EXACT>(y, planes, plane_stride, off), ...);
 }
 
-template <int SIDE>
+template <int SIDE, bool EXACT>
 __global__ __launch_bounds__(256) void deconstruct_kernel(int64_t vecs, int64_t k, int64_t kp,
                                                           const double* __restrict__ X, int64_t ldx,
                                                           const int32_t* __restrict__ exps,
                                                           int8_t* __restrict__ planes) {
   const int64_t ngroups = kp / kElems;
   int64_t v, g;
-  if constexpr (SIDE == 0) {  // block: 4 rows x 64 groups
+  if constexpr (SIDE == 0) {  // block: 4 rows x 64 groups, a wavefront per row
     const int64_t gb = (ngroups + 63) / 64;
     v = (int64_t)(blockIdx.x / gb) * 4 + (threadIdx.x >> 6);
     g = (int64_t)(blockIdx.x % gb) * 64 + (threadIdx.x & 63);
-  } else {  // block: 32 columns x 8 groups
+  } else {  // block: 32 columns x 8 groups, a wavefront per 8 columns
     const int64_t gb = (ngroups + 7) / 8;
-    v = (int64_t)(blockIdx.x / gb) * 32 + (threadIdx.x & 31);
-    g = (int64_t)(blockIdx.x % gb) * 8 + (threadIdx.x >> 5);
+    const int lane = threadIdx.x & 63;
+    v = (int64_t)(blockIdx.x / gb) * 32 + (threadIdx.x >> 6) * 8 + (lane & 7);
+    g = (int64_t)(blockIdx.x % gb) * 8 + (lane >> 3);
   }
   if (v >= vecs || g >= ngroups) return;
   int sigma = exps[v];
@@ -127,24 +153,34 @@ __global__ __launch_bounds__(256) void deconstruct_kernel(int64_t vecs, int64_t 
     // |x 2^sigma| < 2^t: the scaling is exact, rint is the one rounding.
     y[c] = __builtin_rint(__builtin_ldexp(x, sigma));
   }
-  emit_all(std::make_integer_sequence<int, kR>{}, y, planes, vecs * kp, v * kp + k0);
+  emit_all<EXACT>(std::make_integer_sequence<int, kR>{}, y, planes, vecs * kp, v * kp + k0);
+}
+
+template <int SIDE>
+void launch_side(int64_t blocks, bool exact, int64_t vecs, int64_t k, int64_t kp, const double* X,
+                 int64_t ldx, const int32_t* exps, int8_t* planes, hipStream_t stream) {
+  if (exact)
+    hipLaunchKernelGGL((deconstruct_kernel<SIDE, true>), dim3((unsigned)blocks), dim3(256), 0, stream,
+                       vecs, k, kp, X, ldx, exps, planes);
+  else
+    hipLaunchKernelGGL((deconstruct_kernel<SIDE, false>), dim3((unsigned)blocks), dim3(256), 0,
+                       stream, vecs, k, kp, X, ldx, exps, planes);
 }
 
 }  // namespace
 
-hipError_t launch_deconstruct(int side, int64_t vecs, int64_t k, int64_t kp, const double* X,
+hipError_t launch_deconstruct(int side, int64_t vecs, int64_t k, int64_t kp, int t, const double* X,
                               int64_t ldx, const int32_t* exps, int8_t* planes,
                               hipStream_t stream) {
   if (vecs <= 0 || kp <= 0) return hipSuccess;
   const int64_t ngroups = kp / kElems;
+  const bool exact = t <= 50;  // |y| <= 2^t: the quotient needs no correction
   if (side == 0) {
     const int64_t blocks = ((vecs + 3) / 4) * ((ngroups + 63) / 64);
-    hipLaunchKernelGGL(deconstruct_kernel<0>, dim3((unsigned)blocks), dim3(256), 0, stream, vecs, k,
-                       kp, X, ldx, exps, planes);
+    launch_side<0>(blocks, exact, vecs, k, kp, X, ldx, exps, planes, stream);
   } else {
     const int64_t blocks = ((vecs + 31) / 32) * ((ngroups + 7) / 8);
-    hipLaunchKernelGGL(deconstruct_kernel<1>, dim3((unsigned)blocks), dim3(256), 0, stream, vecs, k,
-                       kp, X, ldx, exps, planes);
+    launch_side<1>(blocks, exact, vecs, k, kp, X, ldx, exps, planes, stream);
   }
   return hipGetLastError();
 }

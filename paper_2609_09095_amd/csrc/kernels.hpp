@@ -13,8 +13,9 @@ namespace oz {
 hipError_t launch_scan(int side, int64_t vecs, int64_t k, const double* X, int64_t ldx, int t,
                        int32_t* exps, hipStream_t stream);
 
-// Alg. 2: scale, round, residues and limb planes of one operand, given exps.
-hipError_t launch_deconstruct(int side, int64_t vecs, int64_t k, int64_t kp, const double* X,
+// Alg. 2: scale, round, residues and e4m3 limb planes of one operand, given
+// exps and the scale bits t.
+hipError_t launch_deconstruct(int side, int64_t vecs, int64_t k, int64_t kp, int t, const double* X,
                               int64_t ldx, const int32_t* exps, int8_t* planes,
                               hipStream_t stream);
 
