@@ -1,19 +1,26 @@
 // Reconstruction (Alg. 3): Garner's mixed-radix digits of the twelve centred
-// residues (Eq. (garner)), Horner recombination (Eq. (horner)), the symmetric
-// lift to [-M/2, M/2), and one rounding of X 2^(-sigma_i - tau_j) to FP64.
+// residues (Eq. (garner)), Horner recombination (Eq. (horner)), the lift to
+// [-M/2, M/2), and one rounding of X 2^(-sigma_i - tau_j) to FP64.
 // One thread per output; the residue loads coalesce along the output row.
-// HBM-bound: 12 residues in, 8 bytes out.
+// 24 bytes in and 8 out per output, with VALU work of the same order.
 //
 // Integer work per output, all exact:
-//  - digit j in one reduction: v_j = (c_j w_j - sum_{l<j} v_l R_lj) mod m_j
-//    with R_lj = (m_0..m_{l-1}) w_j mod m_j folded at compile time; the
-//    argument stays below 2^24 in magnitude, so an FP32 quotient is exact up
-//    to one step that the corrections absorb.
-//  - Horner in two 64-bit halves, X = Xh P + Xl with P = m_0..m_5 < 2^59,
-//    Xl = v_0 + m_0 (v_1 + ... m_4 v_5) < P and Xh = v_6 + ... < M / P < 2^54.
-//  - the lift X >= M/2 compares the halves (M/2 = ((Q-1)/2) P + P/2 with
-//    Q = M / P odd); the magnitude is then H P + L with H < 2^54, L <= P,
-//    formed as a 128-bit integer and rounded once.
+//  - centred digits in one reduction each: v_j = (c_j w_j - sum_{l<j} v_l
+//    R_lj) mod m_j with w_j and R_lj = (m_0..m_{l-1}) w_j mod m_j centred
+//    compile-time constants.  Every term is below 545^2 in magnitude, the sum
+//    of at most twelve below 2^22, so for odd m_j the FP32 quotient
+//    rint(s / m_j) errs by less than 1/(2 m_j), the least distance of s / m_j
+//    from a half integer: one rint and one multiply-add give the centred
+//    digit.  m_j = 1024 takes the low ten bits.
+//  - centred digits make X = Xl + P Xh a balanced mixed-radix number with
+//    P = m_0..m_5 (even) and halves Xl = v_0 + m_0 (v_1 + ... m_4 v_5),
+//    |Xl| < P, and Xh likewise over m_6..m_11 with |Xh| <= (Q-1)/2, Q odd.
+//    Its range is [-M/2 - 544, M/2 - 545]; the few values below -M/2 are
+//    moved up by M (Xh += Q), which gives exactly the lift to [-M/2, M/2).
+//  - Horner pairs digits with 24-bit multiply-adds (|pair| < 2^20) and joins
+//    the three pairs of a half in 64-bit arithmetic.
+//  - |X| = H P + L with H = |Xh| < 2^53 and |L| < P, formed as a 128-bit
+//    integer and rounded once.
 #include <utility>
 
 #include "device_math.hpp"
@@ -36,16 +43,28 @@ constexpr uint64_t kP = prod_range(0, kSplit);   // m_0 ... m_5
 constexpr uint64_t kQ = prod_range(kSplit, kR);  // m_6 ... m_11
 static_assert(kP < (1ull << 59) && kQ < (1ull << 54), "halves fit 64 bits");
 static_assert(kQ % 2 == 1 && kP % 2 == 0, "lift rule assumes Q odd, P even");
+static_assert(kModulus[1] == 1024, "the power-of-two modulus sits at index 1");
 
-// Weight of digit l in the equation of digit j, times w_j, mod m_j; as
-// template variables so that they are compile-time immediates in the kernel.
-constexpr int garner_weight(int l, int j) {
-  return (int)((int64_t)radix_mod(l, j) * garner_w(j) % kModulus[j]);
-}
+constexpr int centred_const(int64_t x, int m) { return (int)(x > m / 2 ? x - m : x); }
+// centred weight of digit l in the equation of digit j (times w_j), and w_j;
+// as template variables so that they are compile-time immediates
 template <int L, int J>
-inline constexpr int kGarnerWeight = garner_weight(L, J);
+inline constexpr int kGarnerWeight =
+    centred_const((int64_t)radix_mod(L, J) * garner_w(J) % kModulus[J], kModulus[J]);
 template <int J>
-inline constexpr int kGarnerW = garner_w(J);
+inline constexpr int kGarnerW = centred_const(garner_w(J), kModulus[J]);
+
+constexpr bool garner_sums_fit() {
+  // |c_j w_j| + sum_{l<j} |v_l R_lj| < 2^22 with |c|, |v| <= m/2
+  for (int j = 0; j < kR; ++j) {
+    const int64_t mj = kModulus[j];
+    int64_t s = (mj / 2 + 1) * (mj / 2 + 1);
+    for (int l = 0; l < j; ++l) s += (kModulus[l] / 2 + 1) * (mj / 2 + 1);
+    if (s >= (int64_t)1 << 22) return false;
+  }
+  return true;
+}
+static_assert(garner_sums_fit(), "Garner sums stay below 2^22");
 
 template <int J>
 __device__ __forceinline__ void garner_digit(const int (&c)[kR], int (&v)[kR]) {
@@ -55,40 +74,52 @@ __device__ __forceinline__ void garner_digit(const int (&c)[kR], int (&v)[kR]) {
   [&]<int... L>(std::integer_sequence<int, L...>) {
     ((s -= __mul24(v[L], kGarnerWeight<L, J>)), ...);
   }(std::make_integer_sequence<int, J>{});
-  v[J] = pmod_small<M>(s);
+  if constexpr (M == 1024) {
+    v[J] = ((s + 512) & 1023) - 512;
+  } else {
+    const int q = (int)__builtin_rintf((float)s * (1.0f / M));
+    v[J] = s - q * M;
+  }
 }
 
-// X = sum_{j in [a, b)} v_j prod_{a <= l < j} m_l, Horner from the top.
-template <int A, int B>
-__device__ __forceinline__ uint64_t horner(const int (&v)[kR]) {
-  uint64_t x = (uint64_t)v[B - 1];
-#pragma unroll
-  for (int j = B - 2; j >= A; --j) x = x * (uint64_t)kModulus[j] + (uint64_t)v[j];
-  return x;
+// Balanced half sum_{j in [A, A+6)} v_j prod_{A <= l < j} m_l: digit pairs in
+// 24-bit arithmetic, then (g0 + b0 (g1 + b1 g2)) in 64 bits.
+template <int A>
+__device__ __forceinline__ int64_t half_value(const int (&v)[kR]) {
+  constexpr int m0 = kModulus[A], m1 = kModulus[A + 1], m2 = kModulus[A + 2];
+  constexpr int m3 = kModulus[A + 3], m4 = kModulus[A + 4];
+  const int g0 = v[A] + __mul24(v[A + 1], m0);
+  const int g1 = v[A + 2] + __mul24(v[A + 3], m2);
+  const int g2 = v[A + 4] + __mul24(v[A + 5], m4);
+  constexpr int64_t b0 = (int64_t)m0 * m1, b1 = (int64_t)m2 * m3;
+  const int64_t t = (int64_t)g1 + b1 * (int64_t)g2;  // |t| < 2^40
+  return (int64_t)g0 + b0 * t;
 }
 
-// RN_even(mag 2^e) for 0 < mag < 2^113: keep the top 53 bits (fewer in the
-// subnormal range, where the quantum is 2^-1074), round half to even on the
-// dropped bits, and scale the integer significand by ldexp, which is exact
-// here and overflows to infinity past the largest double.
+// RN_even(mag 2^e) for 0 < mag < 2^113.
+//  - normal (and overflowing) results: the top 64 bits of mag, with every
+//    lower bit ORed into bit 0 as a sticky bit, convert to FP64 with the one
+//    correct rounding (bit 0 lies ten places below the rounding point), and
+//    ldexp scales exactly or overflows to infinity as rounding would.
+//  - subnormal results (exponent below -1022): keep the bits down to 2^-1074
+//    and round half to even on the dropped ones by hand.
 __device__ __forceinline__ double round_scaled(u128 mag, int e) {
   const uint64_t hi = (uint64_t)(mag >> 64), lo = (uint64_t)mag;
-  const int p = hi ? 127 - __builtin_clzll(hi) : 63 - __builtin_clzll(lo);  // top bit
-  const int E = p + e;                                                     // exponent of the value
-  const int qe = E - 52 > -1074 ? E - 52 : -1074;                          // quantum exponent
-  const int sh = qe - e;                                                   // dropped bits
-  uint64_t mant;
-  if (sh <= 0) {
-    mant = lo << (-sh);  // at most 53 bits
-  } else if (sh > 113) {
-    mant = 0;  // below half the smallest subnormal
-  } else {
-    mant = (uint64_t)(mag >> sh);
-    const u128 rem = mag & (((u128)1 << sh) - 1);
-    const u128 half = (u128)1 << (sh - 1);
-    mant += (rem > half || (rem == half && (mant & 1))) ? 1 : 0;
+  const int c = hi ? __builtin_clzll(hi) : 64 + __builtin_clzll(lo);  // leading zeros of mag
+  const int E = 127 - c + e;  // the value lies in [2^E, 2^(E+1))
+  if (E >= -1022) {
+    const u128 norm = mag << c;
+    const uint64_t top = (uint64_t)(norm >> 64) | ((uint64_t)norm != 0 ? 1u : 0u);
+    return __builtin_ldexp((double)top, E - 63);
   }
-  return __builtin_ldexp((double)mant, qe);
+  const int sh = -1074 - e;  // dropped bits: the quantum is 2^-1074
+  if (sh <= 0) return __builtin_ldexp((double)(lo << -sh), -1074);  // exact, below 2^53
+  if (sh > 113) return 0.0;  // below half the smallest subnormal
+  uint64_t mant = (uint64_t)(mag >> sh);
+  const u128 rem = mag & (((u128)1 << sh) - 1);
+  const u128 half = (u128)1 << (sh - 1);
+  mant += (rem > half || (rem == half && (mant & 1))) ? 1 : 0;
+  return __builtin_ldexp((double)mant, -1074);
 }
 
 template <typename RT>
@@ -101,19 +132,16 @@ __device__ __forceinline__ double reconstruct_one(const RT* __restrict__ cres, i
   [&]<int... J>(std::integer_sequence<int, J...>) {
     (garner_digit<J>(c, v), ...);
   }(std::make_integer_sequence<int, kR>{});
-  const uint64_t xl = horner<0, kSplit>(v);   // < P
-  const uint64_t xh = horner<kSplit, kR>(v);  // < Q
-  constexpr uint64_t kHalfQ = (kQ - 1) / 2, kHalfP = kP / 2;
-  const bool neg = xh > kHalfQ || (xh == kHalfQ && xl >= kHalfP);
-  // |X| = H P + L: for X - M = (xh - Q) P + xl < 0, H = Q - xh - 1, L = P - xl
-  uint64_t H = neg ? kQ - xh - 1 : xh;
-  uint64_t L = neg ? kP - xl : xl;
-  if (L == kP) {  // only when xl == 0
-    H += 1;
-    L = 0;
-  }
-  const u128 mag = (u128)H * (u128)kP + (u128)L;
-  if (mag == 0) return 0.0;
+  const int64_t xl = half_value<0>(v);       // |xl| < P
+  int64_t xh = half_value<kSplit>(v);        // |xh| <= (Q - 1) / 2
+  constexpr int64_t kHalfQ = (int64_t)(kQ - 1) / 2, kHalfP = (int64_t)(kP / 2);
+  if (xh == -kHalfQ && xl < -kHalfP) xh += (int64_t)kQ;  // below -M/2: lift by M
+  if (xh == 0 && xl == 0) return 0.0;
+  const bool neg = xh < 0 || (xh == 0 && xl < 0);
+  // |X| = |xh| P + (+-xl), the sign of the second term following X
+  const uint64_t H = (uint64_t)(neg ? -xh : xh);
+  const int64_t L = neg ? -xl : xl;
+  const u128 mag = (u128)H * (u128)kP + (u128)(__int128)L;
   const double r = round_scaled(mag, -sa - sb);
   return neg ? -r : r;
 }

@@ -162,7 +162,12 @@ def _centred(x, m):
 
 def _random_X(rng, count):
     M = oracle.product_of_moduli()
-    xs = [0, 1, -1, -(M // 2), M // 2 - 1, (1 << 53) + 1, -(1 << 53) - 1, (1 << 54) + 2]
+    # both ends of [-M/2, M/2), including the 544 values at each end where a
+    # balanced mixed-radix form and the lift part ways
+    h = M // 2
+    xs = [0, 1, -1, -h, h - 1, (1 << 53) + 1, -(1 << 53) - 1, (1 << 54) + 2,
+          h - 2, h - 543, h - 544, h - 545, h - 546, h - 300,
+          -h + 1, -h + 543, -h + 544, -h + 545, -h + 300]
     while len(xs) < count:
         b = int(rng.integers(0, 112))
         x = int(rng.integers(0, 1 << 62)) * (1 << 50) + int(rng.integers(0, 1 << 50))
