@@ -26,15 +26,17 @@
 // row/column l%32 and 32 of the 64 k bytes of the step, the same 32 on both
 // sides for equal l/32, so any fixed choice of those bytes pairs equal k.
 //
-// Tiling (4 wavefronts, 1 per SIMD): 256 x 256 block tile, 128 x 128 per
-// wavefront (4 x 4 MFMA blocks of 32 x 32), K stages of 128 bytes loaded
-// straight from global memory into LDS (buffer loads with the lds bit; 2 x
-// 64 KiB, double buffered).  The 16 loads of stage s+1 are interleaved with
-// the first half of stage s's MFMAs, so the wave never stalls on a full
-// vector-memory queue with MFMAs waiting behind it.  LDS rows are 128 bytes
-// with the 16-byte chunk index XOR-swizzled by the row so that the b128
-// fragment reads of 8 (or 16) consecutive rows hit distinct banks.  Plane
-// rows are padded to a multiple of 128 bytes, so every stage is full.
+// Tiling: a block of 16 wavefronts (4 per SIMD) owns a 256 x 256 output
+// tile, 64 x 64 per wavefront (2 x 2 MFMA blocks of 32 x 32).  Four waves per
+// SIMD keep the matrix core fed while other waves wait at a barrier, on LDS
+// reads or on the operand stream; they cost twice the LDS reads of a 2 x 2
+// layout of 128 x 128 wavefronts (measured 5-6 % faster all the same).  K
+// stages of 128 bytes go straight from global memory into LDS (buffer loads
+// with the lds bit; 2 x 64 KiB, double buffered); the 4 loads of a wave for
+// stage s+1 are interleaved with stage s's first MFMAs.  LDS rows are 128
+// bytes with the 16-byte chunk index XOR-swizzled by the row so that the
+// b128 fragment reads of 8 (or 16) consecutive rows hit distinct banks.
+// Plane rows are padded to a multiple of 128 bytes, so every stage is full.
 //
 // At this tile size the operand stream is 64 KiB per CU per stage of 2048
 // MFMA cycles (32 B/clk at the FP8 peak); direct-to-LDS loads deliver about
@@ -56,7 +58,7 @@ constexpr int BN = 256;         // output columns per block
 constexpr int BK = 128;         // k bytes per stage
 constexpr int kTile = BM * BK;  // bytes of one operand tile in LDS (BM == BN)
 static_assert(BK == kKAlign, "every K stage is full: planes are padded to BK");
-constexpr int kGroupM = 4;      // tile rows per group in the block order
+constexpr int kGroupM = 2;      // tile rows per group in the block order
 constexpr int kSeg = 128;       // K stages (16384 k) per accumulation segment
 
 // Per-modulus schedule, from the compile-time tables of moduli.hpp.
@@ -128,10 +130,9 @@ __device__ __forceinline__ float mulmod_f(float x, float mult, float m, float mi
 __device__ __forceinline__ int swz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
 
 // Block order: moduli outermost; inside a modulus, tiles go in groups of
-// kGroupM tile rows, so that the ~256 blocks resident at a time cover a
-// compact patch of output tiles and share their A and B panels in the L2s
-// and the Infinity Cache.  (Giving each XCD a contiguous range of this order
-// measured slower: it spreads the XCDs over distant tiles and moduli.)
+// kGroupM = 2 tile rows.  Blocks are dealt round-robin over the 8 XCDs, so
+// the 32 blocks an XCD runs at a time cover 4 tile rows x 8 tile columns: 12
+// panels feed 32 tiles from its L2 (groups of 4 rows: 18 panels; 8 rows: 33).
 __device__ __forceinline__ void block_coords(int64_t tiles_m, int64_t tiles_n, int& mod,
                                              int64_t& tm, int64_t& tn) {
   const int64_t id = blockIdx.x;
@@ -157,16 +158,16 @@ __device__ __forceinline__ const int8_t* uniform_ptr(const int8_t* p) {
   return (const int8_t*)(((uint64_t)hi << 32) | lo);
 }
 
-// One K stage: the wave's share of the A and B tiles goes straight from
-// global memory into LDS.  A wave's load writes 1 KiB = 8 rows x 128 bytes,
-// lane l landing at row l/8, chunk l%8 of that slab; to realise the swizzled
-// layout the lane fetches the global chunk (l%8) ^ swz(row).
+// One K stage: the wave's share of the A and B tiles (32 rows of each) goes
+// straight from global memory into LDS.  A load writes 1 KiB = 8 rows x
+// 128 bytes, lane l landing at row l/8, chunk l%8 of that slab; to realise
+// the swizzled layout the lane fetches the global chunk (l%8) ^ swz(row).
 __device__ __forceinline__ void stage_load(__amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rb,
-                                           int8_t* la, int8_t* lb, const int (&voff)[8], int k0,
+                                           int8_t* la, int8_t* lb, const int (&voff)[2], int k0,
                                            int wave) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int slab = (wave * 8 + i) * 1024;
+  for (int i = 0; i < 2; ++i) {
+    const int slab = (wave * 2 + i) * 1024;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr)(la + slab), 16, voff[i], k0, 0, 0);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr)(lb + slab), 16, voff[i], k0, 0, 0);
   }
@@ -185,76 +186,52 @@ __device__ __forceinline__ v8i frag(const int8_t* base, int r, int ks, int fh) {
              *reinterpret_cast<const v4i*>(row + (((4 * ks + 2 + fh) ^ swz(r)) << 4)));
 }
 
-// One stage: two 64-byte K steps of 4 x 4 MFMAs in row-major order.  B's
-// four fragments of a step stay in registers; A's come one row block at a
-// time, the next one read while the current row's MFMAs run, and the next
-// step's B fragments are read during the last row.  The next stage's 16
-// DMA loads go among the first step's MFMAs.
-__device__ __forceinline__ void stage_mma_dma(const int8_t* la, const int8_t* lb, int wr, int wc,
-                                              int fr, int fh, v16f (&acc)[4][4],
+// One stage: two 64-byte K steps of 2 x 2 MFMAs (a wave owns 64 x 64;
+// four waves share each SIMD).  The next stage's 4 DMA loads go among step
+// 0's MFMAs.
+__device__ __forceinline__ void stage_mma_dma(const int8_t* la, const int8_t* lb, int ra0, int rb0,
+                                              int fh, v16f (&acc)[2][2],
                                               __amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rb,
-                                              int8_t* na, int8_t* nb, const int (&voff)[8], int k0,
+                                              int8_t* na, int8_t* nb, const int (&voff)[2], int k0,
                                               int wave) {
-  const int ra0 = wr * 128 + fr, rb0 = wc * 128 + fr;
-  v8i bcur[4], bnext[4], acur, anext;
+  v8i af[2][2], bf[2][2];
+  k0 = __builtin_amdgcn_readfirstlane(k0);
 #pragma unroll
-  for (int b = 0; b < 4; ++b) bcur[b] = frag(lb, rb0 + 32 * b, 0, fh);
-  acur = frag(la, ra0, 0, fh);
+  for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-  for (int ks = 0; ks < 2; ++ks) {
+    for (int x = 0; x < 2; ++x) {
+      af[ks][x] = frag(la, ra0 + 32 * x, ks, fh);
+      bf[ks][x] = frag(lb, rb0 + 32 * x, ks, fh);
+    }
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {
-      if (a < 3) anext = frag(la, ra0 + 32 * (a + 1), ks, fh);
-      if (a == 3 && ks == 0) {
+  for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-        for (int b = 0; b < 4; ++b) bnext[b] = frag(lb, rb0 + 32 * b, 1, fh);
-        anext = frag(la, ra0, 1, fh);
-      }
+    for (int a = 0; a < 2; ++a)
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
+      for (int b = 0; b < 2; ++b) {
         if (ks == 0) {
-          const int i = a * 4 + b;  // DMA i of 16: (slab i/2, side i%2)
-          const int slab = (wave * 8 + (i >> 1)) * 1024;
+          const int i = a * 2 + b;  // DMA i of 4: (slab i/2, side i%2)
+          const int slab = (wave * 2 + (i >> 1)) * 1024;
           if (i & 1)
             __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr)(nb + slab), 16, voff[i >> 1], k0, 0, 0);
           else
             __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr)(na + slab), 16, voff[i >> 1], k0, 0, 0);
         }
-        acc[a][b] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(acur, bcur[b], acc[a][b], 0, 0, 0,
-                                                                    0, 0, 0);
+        acc[a][b] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af[ks][a], bf[ks][b], acc[a][b], 0,
+                                                                    0, 0, 0, 0, 0);
       }
-      acur = anext;
-    }
-    if (ks == 0) {
+  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
-      for (int b = 0; b < 4; ++b) bcur[b] = bnext[b];
-    }
+  for (int i = 0; i < 4; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
   }
-  // issue order: 10 fragment reads; step 0: per row its fragment reads (the
-  // next row's A, or the next step's B and first A), then 4 x [DMA, MFMA];
-  // step 1: per row the next row's A reads, then 4 MFMAs
-  __builtin_amdgcn_sched_group_barrier(0x100, 10, 0);
-#pragma unroll
-  for (int a = 0; a < 4; ++a) {
-    if (a < 3)
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-    else
-      __builtin_amdgcn_sched_group_barrier(0x100, 10, 0);
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    }
-  }
-#pragma unroll
-  for (int a = 0; a < 4; ++a) {
-    if (a < 3) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-  }
+  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
 }
 
 template <typename OT>
-__global__ __launch_bounds__(256, 1) void residue_gemm_kernel(int64_t m, int64_t n, int64_t kp,
+__global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_t n, int64_t kp,
                                                               const int8_t* __restrict__ pa,
                                                               const int8_t* __restrict__ pb,
                                                               OT* __restrict__ cres) {
@@ -271,14 +248,15 @@ __global__ __launch_bounds__(256, 1) void residue_gemm_kernel(int64_t m, int64_t
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS-DMA base in M0
-  const int wr = wave >> 1, wc = wave & 1;
+  const int wr = wave >> 2, wc = wave & 3;  // 4 x 4 waves of 64 x 64
   const int fr = lane & 31, fh = lane >> 5;  // fragment row, 16-byte K half
+  const int ra0 = wr * 64 + fr, rb0 = wc * 64 + fr;
 
-  // byte offsets (within the block's 256-row panel) of the 8 slab loads
-  int voff[8];
+  // byte offsets (within the block's 256-row panel) of the 4 slab loads
+  int voff[2];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int r = wave * 64 + i * 8 + (lane >> 3);
+  for (int i = 0; i < 2; ++i) {
+    const int r = wave * 16 + i * 8 + (lane >> 3);
     voff[i] = r * (int)kp + (((lane & 7) ^ swz(r)) << 4);
   }
   // rows past the matrix edge read as zero (buffer range check); they only
@@ -286,11 +264,11 @@ __global__ __launch_bounds__(256, 1) void residue_gemm_kernel(int64_t m, int64_t
   const int64_t rows_a = m - tm * BM < BM ? m - tm * BM : BM;
   const int64_t rows_b = n - tn * BN < BN ? n - tn * BN : BN;
 
-  v16f acc[4][4];
+  v16f acc[2][2];
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int b = 0; b < 4; ++b) acc[a][b] = v16f{};
+    for (int b = 0; b < 2; ++b) acc[a][b] = v16f{};
 
   // The three products run as segments of at most kSeg stages: every fp32
   // accumulator sum between two reductions stays below 2^24 (at most
@@ -317,11 +295,11 @@ __global__ __launch_bounds__(256, 1) void residue_gemm_kernel(int64_t m, int64_t
       __syncthreads();
       // the DMA of the stage after the segment's last one lands in the idle
       // buffer (zeros past the panel) and is drained before the next segment
-      stage_mma_dma(lds_a0, lds_b0, wr, wc, fr, fh, acc, ra, rb, lds_a1, lds_b1, voff, (s + 1) * BK, wave);
+      stage_mma_dma(lds_a0, lds_b0, ra0, rb0, fh, acc, ra, rb, lds_a1, lds_b1, voff, (s + 1) * BK, wave);
       if (s + 1 >= s1) break;
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
-      stage_mma_dma(lds_a1, lds_b1, wr, wc, fr, fh, acc, ra, rb, lds_a0, lds_b0, voff, (s + 2) * BK, wave);
+      stage_mma_dma(lds_a1, lds_b1, ra0, rb0, fh, acc, ra, rb, lds_a0, lds_b0, voff, (s + 2) * BK, wave);
     }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();  // every wave is done with the buffers before the next segment loads
@@ -330,9 +308,9 @@ __global__ __launch_bounds__(256, 1) void residue_gemm_kernel(int64_t m, int64_t
     if (p == 2 || mult != 1 || nseg > 1) {
       const float fm = (float)sc.m, fmult = (float)mult, finv = 1.0f / (float)sc.m;
 #pragma unroll
-      for (int a = 0; a < 4; ++a)
+      for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int b = 0; b < 4; ++b)
+        for (int b = 0; b < 2; ++b)
 #pragma unroll
           for (int v = 0; v < 16; ++v) acc[a][b][v] = mulmod_f(acc[a][b][v], fmult, fm, finv);
     }
@@ -345,11 +323,11 @@ __global__ __launch_bounds__(256, 1) void residue_gemm_kernel(int64_t m, int64_t
   const int nn = (int)n;
   const int rows_left = (int)(m - tm * BM), cols_left = (int)(n - tn * BN);
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int col = wc * 128 + b * 32 + fr;
-      const int row0 = wr * 128 + a * 32 + 4 * fh;
+    for (int b = 0; b < 2; ++b) {
+      const int col = wc * 64 + b * 32 + fr;
+      const int row0 = wr * 64 + a * 32 + 4 * fh;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int row = row0 + 8 * (v >> 2) + (v & 3);
@@ -368,7 +346,7 @@ hipError_t launch_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* pa, const
   // the store epilogue uses 32-bit offsets within a 256-row tile
   if (n > kMaxResidueCols) return hipErrorInvalidValue;
   const int64_t blocks = (int64_t)kR * ((m + BM - 1) / BM) * ((n + BN - 1) / BN);
-  hipLaunchKernelGGL(residue_gemm_kernel<OT>, dim3((unsigned)blocks), dim3(256), 0, stream, m, n,
+  hipLaunchKernelGGL(residue_gemm_kernel<OT>, dim3((unsigned)blocks), dim3(1024), 0, stream, m, n,
                      kp, pa, pb, cres);
   return hipGetLastError();
 }
