@@ -37,21 +37,27 @@ __device__ __forceinline__ void store16(int8_t* p, const float (&b)[kElems]) {
   *reinterpret_cast<uint4*>(p) = w;
 }
 
-// Centred residue of the integer-valued y modulo M, in [-(M/2), (M-1)/2].
-// EXACT (|y| <= 2^50): the FP64 quotient y * RN(1/M) is within |y| 2^-52 / M
-// <= 1/(4M) of y / M, while for odd M y / M is at least 1/(2M) away from a
-// half integer, so rint gives the nearest quotient and y - qM is already
-// centred; for M = 1024 the quotient is exact and only the tie +512 needs
-// mapping to -512.  Otherwise the general form with its two corrections.
+// Centred residue of the integer-valued y modulo M, in [-(M/2), (M-1)/2],
+// as a float (exact: |residue| <= 544).  EXACT (|y| <= 2^50): the FP64
+// quotient y * RN(1/M) is within |y| 2^-52 / M <= 1/(4M) of y / M, while for
+// odd M y / M is at least 1/(2M) away from a half integer, so rint gives the
+// nearest quotient and y - qM is already centred; for M = 1024 the quotient
+// is exact and only the tie +512 needs mapping to -512.  Otherwise the
+// general form with its two corrections.
 template <int M, bool EXACT>
-__device__ __forceinline__ int centred_residue(double y) {
+__device__ __forceinline__ float centred_residue(double y) {
   if constexpr (!EXACT) {
-    return cmod_f64<M>(y);
+    return (float)cmod_f64<M>(y);
   } else {
     constexpr double inv = 1.0 / M;
-    const int r = (int)__builtin_fma(-__builtin_rint(y * inv), (double)M, y);
+    const double q = __builtin_rint(y * inv);
+    // y - q M in one three-operand FMA (the two-operand form would first copy
+    // y, which every modulus reuses)
+    double t;
+    asm("v_fma_f64 %0, %1, %2, %3" : "=v"(t) : "v"(q), "s"(-(double)M), "v"(y));
+    const float r = (float)t;
     if constexpr ((M & 1) == 0)
-      return r == M / 2 ? -(M / 2) : r;
+      return r == (float)(M / 2) ? -(float)(M / 2) : r;
     else
       return r;
   }
@@ -62,32 +68,31 @@ __device__ __forceinline__ int centred_residue(double y) {
 // every step is exact in FP32 and the digits come out as the floats the
 // e4m3 conversion takes.
 template <int S>
-__device__ __forceinline__ void split_square(int d, float& d0, float& d1) {
-  const float df = (float)d;
-  if constexpr (S % 2 == 0) {
-    // d1 = floor((d + s/2) / s): d0 lands in [-s/2, s/2)
-    d1 = __builtin_floorf(__builtin_fmaf(df, 1.0f / S, 0.5f));
-  } else {
-    // odd s: d / s is never within 1/(2s) of a half integer, far above the
-    // FP32 error of d * (1/s), so rint gives the nearest digit (+ 0 turns
-    // the -0 that rint returns for small negative quotients into +0, whose
-    // e4m3 code is 0x00)
-    d1 = __builtin_rintf(df * (1.0f / S)) + 0.0f;
-  }
-  d0 = __builtin_fmaf(-(float)S, d1, df);
+__device__ __forceinline__ void split_square(float d, float& d0, float& d1) {
+  // d1 = floor(d / s + 1/2): for even s exactly the balanced digit with d0 in
+  // [-s/2, s/2); for odd s, d / s is never within 1/(2s) of a half integer,
+  // far above the FP32 error of the FMA, so this is the nearest digit.  floor
+  // never returns -0 here, so a zero digit gets the e4m3 code 0x00.
+  d1 = __builtin_floorf(__builtin_fmaf(d, 1.0f / S, 0.5f));
+  d0 = __builtin_fmaf(-(float)S, d1, d);
 }
 
-// Nonsquare modulus (Lemma 1): canonical balanced base-16 split, then one
-// carry when d0 + d1 is odd with |d0 + d1| >= 17 -- exactly the sums
-// +-17, +-19, +-21, +-23 that e4m3 cannot hold.  d0 != 0 whenever it fires.
-__device__ __forceinline__ void split_16(int d, int& d0, int& d1) {
-  d0 = ((d + 8) & 15) - 8;
-  d1 = (d - d0) >> 4;
-  const int s = d0 + d1;
-  const bool carry = (s & 1) && ((unsigned)(s + 16) > 32u);
-  const int sg = d0 > 0 ? 1 : -1;
-  d0 = carry ? d0 - 16 * sg : d0;
-  d1 = carry ? d1 + sg : d1;
+// Nonsquare modulus (Lemma 1): canonical balanced base-16 split (d0 in
+// [-8, 7]), then one carry when d0 + d1 is odd with |d0 + d1| >= 17 --
+// exactly the sums +-17, +-19, +-21, +-23 that e4m3 cannot hold.  d0 != 0
+// whenever it fires.  All in FP32 on small integers, so exact; no -0 can
+// arise (x - x and x + (-x) give +0 under round to nearest).
+__device__ __forceinline__ void split_16(float d, float& d0, float& d1, float& d2) {
+  float h = __builtin_floorf(__builtin_fmaf(d, 1.0f / 16, 0.5f));
+  float l = __builtin_fmaf(-16.0f, h, d);
+  const float s = l + h;
+  const bool carry = __builtin_fabsf(s) > 16.0f && __builtin_amdgcn_fractf(s * 0.5f) != 0.0f;
+  const float sg = l > 0.0f ? 1.0f : -1.0f;
+  l = carry ? __builtin_fmaf(-16.0f, sg, l) : l;
+  h = carry ? h + sg : h;
+  d0 = l;
+  d1 = h;
+  d2 = l + h;
 }
 
 template <int I, bool EXACT>
@@ -100,16 +105,11 @@ __device__ __forceinline__ void emit_modulus(const double (&y)[kElems], int8_t* 
   float l0[kElems], l1[kElems], l2[kElems];
 #pragma unroll
   for (int c = 0; c < kElems; ++c) {
-    const int d = centred_residue<M, EXACT>(y[c]);
-    if constexpr (S != 0) {
+    const float d = centred_residue<M, EXACT>(y[c]);
+    if constexpr (S != 0)
       split_square<S>(d, l0[c], l1[c]);
-    } else {
-      int d0, d1;
-      split_16(d, d0, d1);
-      l0[c] = (float)d0;
-      l1[c] = (float)d1;
-      l2[c] = (float)(d0 + d1);
-    }
+    else
+      split_16(d, l0[c], l1[c], l2[c]);
   }
   store16(base, l0);
   store16(base + plane_stride, l1);
