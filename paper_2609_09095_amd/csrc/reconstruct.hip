@@ -122,13 +122,33 @@ __device__ __forceinline__ double round_scaled(u128 mag, int e) {
   return __builtin_ldexp((double)mant, -1074);
 }
 
+// Residue q of output (row, col): a buffer load with the row's scalar base
+// (row-uniform) and the column's 32-bit byte offset, shared by all twelve.
 template <typename RT>
-__device__ __forceinline__ double reconstruct_one(const RT* __restrict__ cres, int64_t mn, int64_t e,
-                                                  int sa, int sb) {
+__device__ __forceinline__ int load_residue(const RT* rowbase, int n, int col) {
+  // readfirstlane returns int: take both halves as uint32_t before widening
+  // (a sign-extended low half would corrupt the high one)
+  const uint64_t v = (uint64_t)rowbase;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  const void* base = (const void*)(((uint64_t)hi << 32) | lo);
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, n * (int)sizeof(RT), 0x00020000);
+  if constexpr (sizeof(RT) == 2)
+    return (int)(int16_t)__builtin_amdgcn_raw_buffer_load_b16(rs, col * 2, 0, 0);
+  else
+    return (int)__builtin_amdgcn_raw_buffer_load_b32(rs, col * 4, 0, 0);
+}
+
+// rowq: residues of this output row for modulus 0 (row-uniform); the
+// modulus-q row sits mn elements further per q.
+template <typename RT>
+__device__ __forceinline__ double reconstruct_one(const RT* rowq, int64_t mn, int n, int col, int sa,
+                                                  int sb) {
   if (sa == INT32_MIN || sb == INT32_MIN) return __builtin_nan("");
   int c[kR], v[kR];
 #pragma unroll
-  for (int q = 0; q < kR; ++q) c[q] = (int)cres[q * mn + e];
+  for (int q = 0; q < kR; ++q) c[q] = load_residue(rowq + q * mn, n, col);
   [&]<int... J>(std::integer_sequence<int, J...>) {
     (garner_digit<J>(c, v), ...);
   }(std::make_integer_sequence<int, kR>{});
@@ -159,7 +179,7 @@ __global__ __launch_bounds__(256) void reconstruct_kernel(int64_t m, int64_t n,
   const int64_t mn = m * n;
   const int sb = eb[col];
   for (int64_t row = blockIdx.y; row < m; row += gridDim.y) {
-    const double r = reconstruct_one(cres, mn, row * n + col, ea[row], sb);
+    const double r = reconstruct_one(cres + row * n, mn, (int)n, (int)col, ea[row], sb);
     double* out = C + row * ldc + col;
     *out = subtract ? *out - r : r;
   }
