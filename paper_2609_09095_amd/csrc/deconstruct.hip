@@ -3,9 +3,9 @@
 // e4m3-exact integer, Lemma 1, so the conversion is exact).
 //
 // Each thread owns one vector (row of A / column of B) and 16 consecutive k,
-// so every plane store is one 16-byte write.  Bound by VALU work (about 300
-// instructions per element) with HBM close behind: 8 bytes read and 30 bytes
-// written per element.
+// so every plane store is one 16-byte write.  VALU work and HBM traffic (8
+// bytes read and 30 bytes written per element) are close: the nonsquare
+// limb split comes from a small LDS table to keep the VALU side short.
 //  - A (side 0): a wavefront covers 1 row x 1024 k, so each plane store of the
 //    wavefront is 1 KiB contiguous.
 //  - B (side 1): a wavefront covers 8 columns x 128 k, so each plane store of
@@ -22,6 +22,13 @@ namespace {
 
 constexpr int kElems = 16;  // k values per thread
 
+// 16 plane bytes: a streaming store (the planes are read back by the
+// residue GEMM long after, from HBM)
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void put16(int8_t* p, uint4 w) {
+  __builtin_nontemporal_store(u32x4{w.x, w.y, w.z, w.w}, reinterpret_cast<u32x4*>(p));
+}
+
 // four limbs as e4m3 bytes (OCP E4M3FN), the first in the low byte
 __device__ __forceinline__ uint32_t pack4(float a, float b, float c, float d) {
   const int lo = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
@@ -34,7 +41,7 @@ __device__ __forceinline__ void store16(int8_t* p, const float (&b)[kElems]) {
   w.y = pack4(b[4], b[5], b[6], b[7]);
   w.z = pack4(b[8], b[9], b[10], b[11]);
   w.w = pack4(b[12], b[13], b[14], b[15]);
-  *reinterpret_cast<uint4*>(p) = w;
+  put16(p, w);
 }
 
 // Centred residue of the integer-valued y modulo M, in [-(M/2), (M-1)/2],
@@ -45,19 +52,18 @@ __device__ __forceinline__ void store16(int8_t* p, const float (&b)[kElems]) {
 // is exact and only the tie +512 needs mapping to -512.  Otherwise the
 // general form with its two corrections.
 template <int M, bool EXACT>
-__device__ __forceinline__ float centred_residue(double y) {
+__device__ __forceinline__ double centred_residue(double y) {
   if constexpr (!EXACT) {
-    return (float)cmod_f64<M>(y);
+    return (double)cmod_f64<M>(y);
   } else {
     constexpr double inv = 1.0 / M;
     const double q = __builtin_rint(y * inv);
     // y - q M in one three-operand FMA (the two-operand form would first copy
     // y, which every modulus reuses)
-    double t;
-    asm("v_fma_f64 %0, %1, %2, %3" : "=v"(t) : "v"(q), "s"(-(double)M), "v"(y));
-    const float r = (float)t;
+    double r;
+    asm("v_fma_f64 %0, %1, %2, %3" : "=v"(r) : "v"(q), "s"(-(double)M), "v"(y));
     if constexpr ((M & 1) == 0)
-      return r == (float)(M / 2) ? -(float)(M / 2) : r;
+      return r == (double)(M / 2) ? -(double)(M / 2) : r;
     else
       return r;
   }
@@ -95,31 +101,66 @@ __device__ __forceinline__ void split_16(float d, float& d0, float& d1, float& d
   d2 = l + h;
 }
 
+// The split depends on the residue alone, not on the modulus, and every
+// nonsquare residue lies in [-255, 255]: a block tabulates it once in LDS
+// as the three e4m3 codes (d0, d1, d0 + d1) in bytes 0-2 of entry d + 256.
+constexpr int kSplitTable = 512;
+
+__device__ __forceinline__ uint32_t split_16_codes(int d) {
+  float d0, d1, d2;
+  split_16((float)d, d0, d1, d2);
+  const int lo = __builtin_amdgcn_cvt_pk_fp8_f32(d0, d1, 0, false);
+  return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(d2, 0.0f, lo, true);
+}
+
+// Byte k of four table entries into one dword per plane (v_perm_b32 picks
+// bytes of {hi, lo}: 0-3 from lo, 4-7 from hi, 12 gives 0).
+__device__ __forceinline__ void gather_planes(uint32_t x0, uint32_t x1, uint32_t x2, uint32_t x3,
+                                              uint32_t& p0, uint32_t& p1, uint32_t& p2) {
+  const uint32_t t01 = __builtin_amdgcn_perm(x1, x0, 0x05010400u);  // x0.b0 x1.b0 x0.b1 x1.b1
+  const uint32_t t23 = __builtin_amdgcn_perm(x3, x2, 0x05010400u);
+  const uint32_t u01 = __builtin_amdgcn_perm(x1, x0, 0x0c0c0602u);  // x0.b2 x1.b2 0 0
+  const uint32_t u23 = __builtin_amdgcn_perm(x3, x2, 0x0c0c0602u);
+  p0 = __builtin_amdgcn_perm(t23, t01, 0x05040100u);
+  p1 = __builtin_amdgcn_perm(t23, t01, 0x07060302u);
+  p2 = __builtin_amdgcn_perm(u23, u01, 0x05040100u);
+}
+
 template <int I, bool EXACT>
 __device__ __forceinline__ void emit_modulus(const double (&y)[kElems], int8_t* planes,
-                                             int64_t plane_stride, int64_t off) {
+                                             int64_t plane_stride, int64_t off,
+                                             const uint32_t* lut) {
   constexpr int M = kModulus[I];
   constexpr int S = root_of(I);
   constexpr int Q = plane_base(I);
   int8_t* base = planes + (int64_t)Q * plane_stride + off;
-  float l0[kElems], l1[kElems], l2[kElems];
+  if constexpr (S != 0) {
+    float l0[kElems], l1[kElems];
 #pragma unroll
-  for (int c = 0; c < kElems; ++c) {
-    const float d = centred_residue<M, EXACT>(y[c]);
-    if constexpr (S != 0)
-      split_square<S>(d, l0[c], l1[c]);
-    else
-      split_16(d, l0[c], l1[c], l2[c]);
+    for (int c = 0; c < kElems; ++c)
+      split_square<S>((float)centred_residue<M, EXACT>(y[c]), l0[c], l1[c]);
+    store16(base, l0);
+    store16(base + plane_stride, l1);
+  } else {
+    uint32_t x[kElems];
+#pragma unroll
+    for (int c = 0; c < kElems; ++c) x[c] = lut[(int)centred_residue<M, EXACT>(y[c]) + 256];
+    uint4 w0, w1, w2;
+    gather_planes(x[0], x[1], x[2], x[3], w0.x, w1.x, w2.x);
+    gather_planes(x[4], x[5], x[6], x[7], w0.y, w1.y, w2.y);
+    gather_planes(x[8], x[9], x[10], x[11], w0.z, w1.z, w2.z);
+    gather_planes(x[12], x[13], x[14], x[15], w0.w, w1.w, w2.w);
+    put16(base, w0);
+    put16(base + plane_stride, w1);
+    put16(base + 2 * plane_stride, w2);
   }
-  store16(base, l0);
-  store16(base + plane_stride, l1);
-  if constexpr (S == 0) store16(base + 2 * plane_stride, l2);
 }
 
 template <bool EXACT, int... I>
 __device__ __forceinline__ void emit_all(std::integer_sequence<int, I...>, const double (&y)[kElems],
-                                         int8_t* planes, int64_t plane_stride, int64_t off) {
-  (emit_modulus<I, EXACT>(y, planes, plane_stride, off), ...);
+                                         int8_t* planes, int64_t plane_stride, int64_t off,
+                                         const uint32_t* lut) {
+  (emit_modulus<I, EXACT>(y, planes, plane_stride, off, lut), ...);
 }
 
 template <int SIDE, bool EXACT>
@@ -139,21 +180,37 @@ __global__ __launch_bounds__(256) void deconstruct_kernel(int64_t vecs, int64_t 
     v = (int64_t)(blockIdx.x / gb) * 32 + (threadIdx.x >> 6) * 8 + (lane & 7);
     g = (int64_t)(blockIdx.x % gb) * 8 + (lane >> 3);
   }
-  if (v >= vecs || g >= ngroups) return;
-  int sigma = exps[v];
+  const bool active = v < vecs && g < ngroups;
+  int sigma = active ? exps[v] : 0;
   const bool finite = sigma != INT32_MIN;
   sigma = finite ? sigma : 0;
   const int64_t k0 = g * kElems;
+  // unconditional loads from clamped (always valid) addresses, then the
+  // mask: no branches around the loads.  lim = last valid c of this group.
+  const int64_t vc = v < vecs ? v : vecs - 1;
+  const int64_t kc = k0 < k ? k0 : k - 1;
+  const int lim = k0 < k ? (int)(k - k0 < kElems ? k - k0 : kElems) - 1 : 0;
+  const double* first = SIDE == 0 ? X + vc * ldx + kc : X + kc * ldx + vc;
+  const bool live = active && finite;
+  double x[kElems];
+#pragma unroll
+  for (int c = 0; c < kElems; ++c) {
+    const int cc = c < lim ? c : lim;
+    const double xv = SIDE == 0 ? first[cc] : first[(int64_t)cc * ldx];
+    x[c] = (live && c <= lim && k0 + c < k) ? xv : 0.0;
+  }
+  // the split table, built while the loads are in flight
+  __shared__ uint32_t lut[kSplitTable];
+  for (int i = threadIdx.x; i < kSplitTable; i += 256) lut[i] = split_16_codes(i - 256);
+  __syncthreads();
+  if (!active) return;
   double y[kElems];
 #pragma unroll
   for (int c = 0; c < kElems; ++c) {
-    const int64_t l = k0 + c;
-    double x = 0.0;
-    if (finite && l < k) x = SIDE == 0 ? X[v * ldx + l] : X[l * ldx + v];
     // |x 2^sigma| < 2^t: the scaling is exact, rint is the one rounding.
-    y[c] = __builtin_rint(__builtin_ldexp(x, sigma));
+    y[c] = __builtin_rint(__builtin_ldexp(x[c], sigma));
   }
-  emit_all<EXACT>(std::make_integer_sequence<int, kR>{}, y, planes, vecs * kp, v * kp + k0);
+  emit_all<EXACT>(std::make_integer_sequence<int, kR>{}, y, planes, vecs * kp, v * kp + k0, lut);
 }
 
 template <int SIDE>
