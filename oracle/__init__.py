@@ -7,6 +7,10 @@ rounding), built with gcc into ``liboracle.so`` next to it; this module only
 marshals numpy arrays into it and chains its steps in the paper's order
 (Eq. (scale) -> Eq. (residueprod) -> Eq. (pieces)/Lemma 1 -> Eq. (garner),
 Eq. (horner) -> single rounding).
+
+``set`` selects the modulus set: 0 is the published twelve-modulus set, 1 the
+all-byte candidate set A of Sec. 5.1 on the INT8 route (its centred residues
+are the int8 planes, one per modulus).
 """
 from __future__ import annotations
 
@@ -22,7 +26,12 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 
 R = 12
 NPLANES = 30
+R_A = 15
 NONFINITE = -(2 ** 31)
+
+
+def num_moduli(set: int = 0) -> int:
+    return R_A if set == 1 else R
 
 
 def build(force: bool = True) -> str:
@@ -73,6 +82,17 @@ def lib():
         L.oracle_round_scaled.argtypes = [i64, ctypes.c_uint64, ctypes.c_int]
         L.oracle_round_scaled.restype = ctypes.c_double
         L.oracle_reconstruct.argtypes = [i64, i64, P, P, P, P, ctypes.c_int, P, i64]
+        ci = ctypes.c_int
+        L.oracle_set_num_moduli.argtypes = [ci]
+        L.oracle_set_modulus.argtypes = [ci, ci]
+        L.oracle_set_modulus.restype = i64
+        L.oracle_set_product_of_moduli.argtypes = [ci, P, P]
+        L.oracle_set_scale_bits.argtypes = [ci, i64]
+        L.oracle_set_residues.argtypes = [ci, i64, i64, P, P]
+        L.oracle_set_a_planes.argtypes = [i64, i64, i64, P, P]
+        L.oracle_set_residue_gemm.argtypes = [ci, i64, i64, i64, P, P, P]
+        L.oracle_set_garner_constants.argtypes = [ci, P]
+        L.oracle_set_garner.argtypes = [ci, i64, i64, P, P, P]
         _lib = L
     return _lib
 
@@ -82,8 +102,8 @@ def _p(a: np.ndarray):
 
 
 # ---------------------------------------------------------------- constants
-def moduli() -> list[int]:
-    return [int(lib().oracle_modulus(i)) for i in range(R)]
+def moduli(set: int = 0) -> list[int]:
+    return [int(lib().oracle_set_modulus(set, i)) for i in range(num_moduli(set))]
 
 
 def planes_of(i: int) -> int:
@@ -94,20 +114,20 @@ def plane_base(i: int) -> int:
     return int(lib().oracle_plane_base(i))
 
 
-def product_of_moduli() -> int:
+def product_of_moduli(set: int = 0) -> int:
     hi = np.zeros(1, np.uint64)
     lo = np.zeros(1, np.uint64)
-    lib().oracle_product_of_moduli(_p(hi), _p(lo))
+    lib().oracle_set_product_of_moduli(set, _p(hi), _p(lo))
     return (int(hi[0]) << 64) | int(lo[0])
 
 
-def scale_bits(k: int) -> int:
-    return int(lib().oracle_scale_bits(k))
+def scale_bits(k: int, set: int = 0) -> int:
+    return int(lib().oracle_set_scale_bits(set, k))
 
 
-def garner_constants() -> list[int]:
-    w = np.zeros(R, np.int64)
-    lib().oracle_garner_constants(_p(w))
+def garner_constants(set: int = 0) -> list[int]:
+    w = np.zeros(num_moduli(set), np.int64)
+    lib().oracle_set_garner_constants(set, _p(w))
     return [int(x) for x in w]
 
 
@@ -189,41 +209,47 @@ def quantise_vectors(X: np.ndarray, side: int, exps: np.ndarray) -> np.ndarray:
     return Z
 
 
-def residues(Z: np.ndarray) -> np.ndarray:
+def residues(Z: np.ndarray, set: int = 0) -> np.ndarray:
     Z = np.ascontiguousarray(Z, dtype=np.int64)
     nvec, k = Z.shape
-    out = np.zeros((R, nvec, k), np.int16)
-    lib().oracle_residues(nvec, k, _p(Z), _p(out))
+    out = np.zeros((num_moduli(set), nvec, k), np.int16)
+    lib().oracle_set_residues(set, nvec, k, _p(Z), _p(out))
     return out
 
 
-def planes(Z: np.ndarray, kp: int | None = None) -> np.ndarray:
+def planes(Z: np.ndarray, kp: int | None = None, set: int = 0) -> np.ndarray:
+    """Stored planes: the published set's limbs (30 planes), or set A's int8
+    residues (15 planes)."""
     Z = np.ascontiguousarray(Z, dtype=np.int64)
     nvec, k = Z.shape
     kp = k_pad(k) if kp is None else kp
+    if set == 1:
+        out = np.zeros((R_A, nvec, kp), np.int8)
+        lib().oracle_set_a_planes(nvec, k, kp, _p(Z), _p(out))
+        return out
     out = np.zeros((NPLANES, nvec, kp), np.int8)
     lib().oracle_planes(nvec, k, kp, _p(Z), _p(out))
     return out
 
 
-def residue_gemm(resA: np.ndarray, resB: np.ndarray) -> np.ndarray:
+def residue_gemm(resA: np.ndarray, resB: np.ndarray, set: int = 0) -> np.ndarray:
     resA = np.ascontiguousarray(resA, dtype=np.int16)
     resB = np.ascontiguousarray(resB, dtype=np.int16)
     _, m, k = resA.shape
     _, n, k2 = resB.shape
     assert k == k2
-    C = np.zeros((R, m, n), np.int32)
-    lib().oracle_residue_gemm(m, n, k, _p(resA), _p(resB), _p(C))
+    C = np.zeros((num_moduli(set), m, n), np.int32)
+    lib().oracle_set_residue_gemm(set, m, n, k, _p(resA), _p(resB), _p(C))
     return C
 
 
-def garner(Cres: np.ndarray):
+def garner(Cres: np.ndarray, set: int = 0):
     """Returns (Xhi int64, Xlo uint64) of the reconstructed integers."""
     Cres = np.ascontiguousarray(Cres, dtype=np.int32)
     _, m, n = Cres.shape
     hi = np.zeros((m, n), np.int64)
     lo = np.zeros((m, n), np.uint64)
-    lib().oracle_garner(m, n, _p(Cres), _p(hi), _p(lo))
+    lib().oracle_set_garner(set, m, n, _p(Cres), _p(hi), _p(lo))
     return hi, lo
 
 
@@ -273,7 +299,8 @@ class Result:
 
 
 def dgemm(A: np.ndarray, B: np.ndarray, C_in: np.ndarray | None = None,
-          rows=None, cols=None, want_planes: bool = True, check_exact: bool = True) -> Result:
+          rows=None, cols=None, want_planes: bool = True, check_exact: bool = True,
+          set: int = 0) -> Result:
     """Oracle emulated DGEMM on the full k, for all outputs or for the sampled
     rows of A and columns of B (each output depends only on its row and
     column).  Steps in the order of Alg. 1: exponent scan, quantise, residues
@@ -285,17 +312,17 @@ def dgemm(A: np.ndarray, B: np.ndarray, C_in: np.ndarray | None = None,
     assert k == k2
     rows = np.arange(m) if rows is None else np.asarray(rows)
     cols = np.arange(n) if cols is None else np.asarray(cols)
-    t = scale_bits(k)
+    t = scale_bits(k, set)
     As = np.ascontiguousarray(A[rows])
     Bs = np.ascontiguousarray(B[:, cols])
     sigma = exponents(As, 0, t)
     tau = exponents(Bs, 1, t)
     ZA = quantise_vectors(As, 0, sigma)
     ZB = quantise_vectors(Bs, 1, tau)
-    resA = residues(ZA)
-    resB = residues(ZB)
-    Cres = residue_gemm(resA, resB)
-    Xhi, Xlo = garner(Cres)
+    resA = residues(ZA, set)
+    resB = residues(ZB, set)
+    Cres = residue_gemm(resA, resB, set)
+    Xhi, Xlo = garner(Cres, set)
     if check_exact:
         Ehi, Elo = exact_product(ZA, ZB)
         if not (np.array_equal(Ehi, Xhi) and np.array_equal(Elo, Xlo)):
@@ -305,6 +332,6 @@ def dgemm(A: np.ndarray, B: np.ndarray, C_in: np.ndarray | None = None,
     r = Result(t=t, sigma=sigma, tau=tau, ZA=ZA, ZB=ZB, Cres=Cres, Xhi=Xhi, Xlo=Xlo, C=C,
                rows=rows, cols=cols)
     if want_planes:
-        r.planesA = planes(ZA)
-        r.planesB = planes(ZB)
+        r.planesA = planes(ZA, set=set)
+        r.planesB = planes(ZB, set=set)
     return r

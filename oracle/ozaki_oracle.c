@@ -1,6 +1,7 @@
 /*
  * CPU oracle for the Ozaki Scheme II emulated DGEMM (round-to-nearest variant,
- * published twelve-modulus set).  TEST INFRASTRUCTURE ONLY: the tests, the
+ * published twelve-modulus set, and the all-byte candidate set A of Sec. 5.1
+ * on the INT8 route).  TEST INFRASTRUCTURE ONLY: the tests, the
  * smoke check and the benchmark's CPU-baseline leg call it; the product path
  * never does.  It shares no code, header, table or constant generator with the
  * HIP library: every constant below is derived here from the moduli.
@@ -17,6 +18,10 @@
  *    carry-corrected three-plane layout for the nonsquare moduli).
  *  - Eq. (garner) and Eq. (horner): mixed-radix reconstruction, symmetric
  *    lift, single rounding.
+ *  - Sec. 5.1, candidate A: fifteen byte moduli whose centred residues fit an
+ *    int8 operand directly, so on the INT8 route each residue is its own
+ *    plane and each modulus needs one product (the oracle_set_* functions;
+ *    set 0 is the published set, set 1 is candidate A).
  *
  * Pin status: every function here is checked in the CPU tests against the
  * paper's worked values, closed forms or brute force with Python integers /
@@ -38,6 +43,18 @@ typedef unsigned __int128 u128;
 static const int64_t OR_MODULI[OR_R] = {1089, 1024, 961, 841, 625, 529,
                                         511,  509,  503, 499, 491, 487};
 
+/* Candidate set A of Sec. 5.1 (all-byte): fifteen coprime moduli <= 256. */
+#define OR_RA 15
+static const int64_t OR_MODULI_A[OR_RA] = {256, 255, 253, 251, 247, 241, 239, 233,
+                                           229, 227, 223, 217, 211, 199, 197};
+
+/* Set 0: the published set; set 1: candidate A.  r and the moduli. */
+static int or_set_r(int set) { return set == 1 ? OR_RA : OR_R; }
+static const int64_t* or_set_m(int set) { return set == 1 ? OR_MODULI_A : OR_MODULI; }
+
+int oracle_set_num_moduli(int set) { return or_set_r(set); }
+int64_t oracle_set_modulus(int set, int i) { return or_set_m(set)[i]; }
+
 /* Integer square root of m when m is a perfect square, else 0. */
 static int64_t or_square_root(int64_t m) {
   for (int64_t s = 1; s * s <= m; ++s)
@@ -51,25 +68,27 @@ int64_t oracle_modulus(int i) { return OR_MODULI[i]; }
 int oracle_planes_of(int i) { return or_square_root(OR_MODULI[i]) ? 2 : 3; }
 
 /* M = prod m_i (Eq. (moduli)), returned as two 64-bit halves. */
-void oracle_product_of_moduli(uint64_t* hi, uint64_t* lo) {
+void oracle_set_product_of_moduli(int set, uint64_t* hi, uint64_t* lo) {
   u128 M = 1;
-  for (int i = 0; i < OR_R; ++i) M *= (u128)OR_MODULI[i];
+  for (int i = 0; i < or_set_r(set); ++i) M *= (u128)or_set_m(set)[i];
   *hi = (uint64_t)(M >> 64);
   *lo = (uint64_t)M;
 }
+void oracle_product_of_moduli(uint64_t* hi, uint64_t* lo) { oracle_set_product_of_moduli(0, hi, lo); }
 
 /* t(k): the largest t with k * 2^{2t} <= M/2 - 1, so that every entry of
  * A'B' (bounded by k 2^{2t}, Eq. (moduli)) lies strictly inside the symmetric
  * range [-M/2, M/2).  Returns -1 for k < 1. */
-int oracle_scale_bits(int64_t k) {
+int oracle_set_scale_bits(int set, int64_t k) {
   if (k < 1) return -1;
   u128 M = 1;
-  for (int i = 0; i < OR_R; ++i) M *= (u128)OR_MODULI[i];
+  for (int i = 0; i < or_set_r(set); ++i) M *= (u128)or_set_m(set)[i];
   u128 q = (M / 2 - 1) / (u128)k; /* 2^{2t} <= q */
   int t = 0;
   while (((u128)1 << (2 * (t + 1))) <= q) ++t;
   return t;
 }
+int oracle_scale_bits(int64_t k) { return oracle_set_scale_bits(0, k); }
 
 /* a1 (Eq. (scale) and the exponent scan of Alg. 1): for each of nvec vectors
  * of length k, element l of vector v at X[v*sv + l*sk], the exponent e of the
@@ -122,11 +141,26 @@ int64_t oracle_centred_mod(int64_t z, int64_t x) {
 }
 
 /* a3 (Eq. (residueprod)): residues of quantised vectors, out[i][v][l]. */
-void oracle_residues(int64_t nvec, int64_t k, const int64_t* Z, int16_t* out) {
-  for (int i = 0; i < OR_R; ++i)
+void oracle_set_residues(int set, int64_t nvec, int64_t k, const int64_t* Z, int16_t* out) {
+  for (int i = 0; i < or_set_r(set); ++i)
     for (int64_t v = 0; v < nvec; ++v)
       for (int64_t l = 0; l < k; ++l)
-        out[(i * nvec + v) * k + l] = (int16_t)oracle_centred_mod(Z[v * k + l], OR_MODULI[i]);
+        out[(i * nvec + v) * k + l] = (int16_t)oracle_centred_mod(Z[v * k + l], or_set_m(set)[i]);
+}
+void oracle_residues(int64_t nvec, int64_t k, const int64_t* Z, int16_t* out) {
+  oracle_set_residues(0, nvec, k, Z, out);
+}
+
+/* Candidate A on the INT8 route (Sec. 5.1): the centred residue of a byte
+ * modulus lies in [-128, 127] and is itself the stored int8 plane, one per
+ * modulus: planes[i][v][kp], kp >= k, zero padded. */
+void oracle_set_a_planes(int64_t nvec, int64_t k, int64_t kp, const int64_t* Z, int8_t* planes) {
+  memset(planes, 0, (size_t)OR_RA * (size_t)nvec * (size_t)kp);
+  for (int i = 0; i < OR_RA; ++i)
+    for (int64_t v = 0; v < nvec; ++v)
+      for (int64_t l = 0; l < k; ++l)
+        planes[((int64_t)i * nvec + v) * kp + l] =
+            (int8_t)oracle_centred_mod(Z[v * k + l], OR_MODULI_A[i]);
 }
 
 /* Membership in the e4m3 integer set: integers M 2^e with |M| <= 15 and
@@ -239,17 +273,21 @@ void oracle_planes(int64_t nvec, int64_t k, int64_t kp, const int64_t* Z, int8_t
 /* a5 (Eq. (residueprod)): C^(i) = centred(sum_l d_il e_lj mod m_i) from the
  * residues themselves (not the limbs), in plain int64 loops.  resA is
  * [12][m][k] (rows of A), resB is [12][n][k] (columns of B), C is [12][m][n]. */
-void oracle_residue_gemm(int64_t m, int64_t n, int64_t k, const int16_t* resA,
-                         const int16_t* resB, int32_t* C) {
-  for (int i = 0; i < OR_R; ++i)
+void oracle_set_residue_gemm(int set, int64_t m, int64_t n, int64_t k, const int16_t* resA,
+                             const int16_t* resB, int32_t* C) {
+  for (int i = 0; i < or_set_r(set); ++i)
     for (int64_t r = 0; r < m; ++r)
       for (int64_t c = 0; c < n; ++c) {
         const int16_t* a = resA + (i * m + r) * k;
         const int16_t* b = resB + (i * n + c) * k;
         int64_t acc = 0;
         for (int64_t l = 0; l < k; ++l) acc += (int64_t)a[l] * b[l];
-        C[(i * m + r) * n + c] = (int32_t)oracle_centred_mod(acc, OR_MODULI[i]);
+        C[(i * m + r) * n + c] = (int32_t)oracle_centred_mod(acc, or_set_m(set)[i]);
       }
+}
+void oracle_residue_gemm(int64_t m, int64_t n, int64_t k, const int16_t* resA,
+                         const int16_t* resB, int32_t* C) {
+  oracle_set_residue_gemm(0, m, n, k, resA, resB, C);
 }
 
 /* Modular inverse by the extended Euclidean algorithm (a, m coprime). */
@@ -264,29 +302,34 @@ static int64_t or_inverse(int64_t a, int64_t m) {
 }
 
 /* Garner constants w_j = (m_1 ... m_{j-1})^{-1} mod m_j (Eq. (garner)). */
-void oracle_garner_constants(int64_t* w) {
+void oracle_set_garner_constants(int set, int64_t* w) {
+  const int r = or_set_r(set);
+  const int64_t* mod = or_set_m(set);
   w[0] = 1;
-  for (int j = 1; j < OR_R; ++j) {
+  for (int j = 1; j < r; ++j) {
     int64_t p = 1;
-    for (int l = 0; l < j; ++l) p = (p * (OR_MODULI[l] % OR_MODULI[j])) % OR_MODULI[j];
-    w[j] = or_inverse(p, OR_MODULI[j]);
+    for (int l = 0; l < j; ++l) p = (p * (mod[l] % mod[j])) % mod[j];
+    w[j] = or_inverse(p, mod[j]);
   }
 }
+void oracle_garner_constants(int64_t* w) { oracle_set_garner_constants(0, w); }
 
 /* a6 (Eq. (garner), Eq. (horner) and the symmetric lift): the integer X in
  * [-M/2, M/2) with X = c[i] (mod m_i) for all i.  Digits v_j in [0, m_j). */
-static i128 or_garner(const int64_t* c) {
-  int64_t w[OR_R], v[OR_R];
-  oracle_garner_constants(w);
+static i128 or_garner(int set, const int64_t* c) {
+  const int r = or_set_r(set);
+  const int64_t* mod = or_set_m(set);
+  int64_t w[OR_RA], v[OR_RA];
+  oracle_set_garner_constants(set, w);
   u128 M = 1;
-  for (int i = 0; i < OR_R; ++i) M *= (u128)OR_MODULI[i];
-  for (int j = 0; j < OR_R; ++j) {
-    int64_t mj = OR_MODULI[j];
+  for (int i = 0; i < r; ++i) M *= (u128)mod[i];
+  for (int j = 0; j < r; ++j) {
+    int64_t mj = mod[j];
     /* partial = v_1 + v_2 m_1 + ... + v_{j-1} m_1...m_{j-2} */
     u128 partial = 0, radix = 1;
     for (int l = 0; l < j; ++l) {
       partial += (u128)v[l] * radix;
-      radix *= (u128)OR_MODULI[l];
+      radix *= (u128)mod[l];
     }
     int64_t cj = ((c[j] % mj) + mj) % mj;
     int64_t pm = (int64_t)(partial % (u128)mj);
@@ -294,22 +337,26 @@ static i128 or_garner(const int64_t* c) {
     v[j] = (diff * w[j]) % mj;
   }
   /* Horner: v_1 + m_1 (v_2 + m_2 (v_3 + ... + m_{r-1} v_r)) */
-  u128 X = (u128)v[OR_R - 1];
-  for (int j = OR_R - 2; j >= 0; --j) X = X * (u128)OR_MODULI[j] + (u128)v[j];
+  u128 X = (u128)v[r - 1];
+  for (int j = r - 2; j >= 0; --j) X = X * (u128)mod[j] + (u128)v[j];
   if (X >= M / 2) return (i128)X - (i128)M;
   return (i128)X;
 }
 
-/* Garner over a block of outputs: Cres [12][m][n] -> X as (hi, lo) words of
+/* Garner over a block of outputs: Cres [r][m][n] -> X as (hi, lo) words of
  * the two's-complement 128-bit value, X = hi * 2^64 + lo. */
-void oracle_garner(int64_t m, int64_t n, const int32_t* Cres, int64_t* Xhi, uint64_t* Xlo) {
+void oracle_set_garner(int set, int64_t m, int64_t n, const int32_t* Cres, int64_t* Xhi,
+                       uint64_t* Xlo) {
   for (int64_t e = 0; e < m * n; ++e) {
-    int64_t c[OR_R];
-    for (int i = 0; i < OR_R; ++i) c[i] = Cres[(int64_t)i * m * n + e];
-    i128 X = or_garner(c);
+    int64_t c[OR_RA];
+    for (int i = 0; i < or_set_r(set); ++i) c[i] = Cres[(int64_t)i * m * n + e];
+    i128 X = or_garner(set, c);
     Xhi[e] = (int64_t)(X >> 64);
     Xlo[e] = (uint64_t)X;
   }
+}
+void oracle_garner(int64_t m, int64_t n, const int32_t* Cres, int64_t* Xhi, uint64_t* Xlo) {
+  oracle_set_garner(0, m, n, Cres, Xhi, Xlo);
 }
 
 /* The exact integer product X = sum_l a'_il b'_lj directly (the quantity CRT
@@ -326,14 +373,27 @@ void oracle_exact_product(int64_t m, int64_t n, int64_t k, const int64_t* ZA,
 }
 
 /* Single rounding (Alg. 3, last step): RN_even(X * 2^e) for a signed integer
- * X of at most 113 bits.  X converts exactly to binary128 (113-bit
- * significand), the power-of-two scaling is exact in binary128's exponent
- * range, and the conversion to double rounds once, to nearest even,
- * including the subnormal and overflow ranges.  X = 0 gives +0.0. */
+ * X (|X| < 2^127).  An X of at most 113 bits converts exactly to binary128
+ * (113-bit significand); a longer one is first shifted right by s bits with
+ * every dropped bit ORed into the lowest kept bit (exact for the rounding to
+ * 53 bits: that bit lies far below the rounding point) and e grows by s.
+ * The power-of-two scaling is exact in binary128's exponent range, and the
+ * conversion to double rounds once, to nearest even, including the
+ * subnormal and overflow ranges.  X = 0 gives +0.0. */
 double oracle_round_scaled(int64_t Xhi, uint64_t Xlo, int e) {
   i128 X = (i128)(((u128)(uint64_t)Xhi << 64) | (u128)Xlo);
   if (X == 0) return 0.0;
-  __float128 q = (__float128)X;
+  int neg = X < 0;
+  u128 a = neg ? (u128)(-X) : (u128)X;
+  int bits = 0;
+  for (u128 t = a; t; t >>= 1) ++bits;
+  if (bits > 113) {
+    int sh = bits - 113;
+    u128 dropped = a & (((u128)1 << sh) - 1);
+    a = (a >> sh) | (dropped ? 1 : 0);
+    e += sh;
+  }
+  __float128 q = neg ? -(__float128)a : (__float128)a;
   __float128 p = 1;
   for (int i = 0; i < e; ++i) p *= 2;
   for (int i = 0; i > e; --i) p /= 2;
