@@ -1,14 +1,15 @@
 /*
  * ozaki25.h -- emulated FP64 matrix multiplication by Ozaki Scheme II on the
- * FP8 matrix cores of an AMD Instinct MI355X (gfx950).
+ * FP8 (or, for the all-byte modulus set, int8) matrix cores of an AMD
+ * Instinct MI355X (gfx950).
  *
  * The method (Ozaki Scheme II, Sec. 2 of "Ozaki 2.5: Engineering the
  * Deconstruction Path of FP64-Emulated Dense Matrix Multiplication on FP8
  * Tensor Cores"):
  *   1. scale each row of A and each column of B by a power of two and round to
  *      integers, A' = RN(diag(2^sigma) A), B' = RN(B diag(2^tau))   Eq. (scale)
- *   2. reduce the integers to centred residues modulo the published twelve
- *      moduli and split each residue into low-precision limbs      Eq. (residueprod),
+ *   2. reduce the integers to centred residues modulo the moduli (the published
+ *      twelve, split into low-precision limbs; or fifteen byte moduli) Eq. (residueprod),
  *      Eq. (pieces), Lemma 1, Alg. 2
  *   3. form the per-modulus products C^(i) = A^(i) B^(i) mod m_i    Eq. (residueprod)
  *   4. recover A'B' by Garner's mixed-radix CRT, unscale and round once to
@@ -53,13 +54,23 @@ typedef enum {
   OZAKI25_ERR_HIP = 4            /* a HIP launch or runtime call failed */
 } ozaki25_status;
 
-/* The modulus sets.  OZAKI25_MODULI_S12 is the published set of Eq. (moduli),
- * in its published order: 1089, 1024, 961, 841, 625, 529 (squares of 33, 32,
- * 31, 29, 25, 23), then 511, 509, 503, 499, 491, 487.  log2(prod) = 111.84. */
-typedef enum { OZAKI25_MODULI_S12 = 0 } ozaki25_moduli_set;
+/* The modulus sets.
+ *  OZAKI25_MODULI_S12: the published set of Eq. (moduli), in its published
+ *    order: 1089, 1024, 961, 841, 625, 529 (squares of 33, 32, 31, 29, 25,
+ *    23), then 511, 509, 503, 499, 491, 487.  log2(prod) = 111.84.  FP8 route:
+ *    limb planes as e4m3 bytes, three FP8 products per modulus.
+ *  OZAKI25_MODULI_A15: the all-byte set of Sec. 5.1 (candidate A): 256, 255,
+ *    253, 251, 247, 241, 239, 233, 229, 227, 223, 217, 211, 199, 197.
+ *    log2(prod) = 117.8.  Int8 route: the centred residue of a byte modulus
+ *    lies in [-128, 127] and is itself the int8 plane, one int8 product per
+ *    modulus (the int8 substrate of Sec. 2: r + 1 = 16 products' worth of
+ *    matrix work against 3r + 1 = 37).  The same scale rule gives a few more
+ *    bits per operand (t(8192) = 51 against 48). */
+typedef enum { OZAKI25_MODULI_S12 = 0, OZAKI25_MODULI_A15 = 1 } ozaki25_moduli_set;
 
-#define OZAKI25_NUM_MODULI 12
-#define OZAKI25_NUM_PLANES 30          /* 2 per square modulus + 3 per nonsquare */
+#define OZAKI25_NUM_MODULI 12          /* S12 */
+#define OZAKI25_NUM_PLANES 30          /* S12: 2 per square modulus + 3 per nonsquare */
+#define OZAKI25_NUM_MODULI_A15 15      /* A15: also its number of planes */
 #define OZAKI25_K_ALIGN 128            /* planes are zero padded to a multiple of this */
 #define OZAKI25_MAX_K 4194304          /* 256-row plane panels: 32-bit byte offsets */
 #define OZAKI25_MAX_N 8388608          /* columns of B / C (32-bit offsets inside a tile) */
@@ -69,10 +80,10 @@ typedef enum { OZAKI25_MODULI_S12 = 0 } ozaki25_moduli_set;
 /* Text for a status code (static storage, never NULL). */
 const char* ozaki25_status_string(ozaki25_status status);
 
-/* Number of moduli r of a set (12 for S12), or -1 for an unknown set. */
+/* Number of moduli r of a set (12 for S12, 15 for A15), or -1 for an unknown set. */
 int ozaki25_num_moduli(ozaki25_moduli_set set);
 
-/* Number of stored limb planes of a set (30 for S12), or -1. */
+/* Number of stored planes of a set (30 for S12, 15 for A15), or -1. */
 int ozaki25_num_planes(ozaki25_moduli_set set);
 
 /* The i-th modulus of a set (0-based, published order), or -1. */
@@ -91,8 +102,8 @@ int64_t ozaki25_k_pad(int64_t k);
 size_t ozaki25_planes_bytes(int64_t vecs, int64_t k, ozaki25_moduli_set set);
 
 /* Deconstruction of one operand (Alg. 2 with the exponent scan of Alg. 1):
- * exponent scan, scale, round to nearest, twelve centred residues and the
- * limb split of Eq. (pieces) -- squares m = s^2: balanced base-s digits
+ * exponent scan, scale, round to nearest, the centred residues and, for S12,
+ * the limb split of Eq. (pieces) -- squares m = s^2: balanced base-s digits
  * (d0, d1) with d0 the centred residue of d mod s; nonsquares: Lemma 1's
  * carry-corrected base-16 layout (d0, d1, d0 + d1).
  *  side 0: X is A (vecs x k, row-major, ldx >= k); vector v is row v.
@@ -103,6 +114,8 @@ size_t ozaki25_planes_bytes(int64_t vecs, int64_t k, ozaki25_moduli_set set);
  *          (Lemma 1), zero is 0x00; plane q of modulus i is at
  *          q = (2 per earlier square + 3 per earlier nonsquare) + limb index;
  *          entries with l >= k are zero.
+ *          A15: int8 [15][vecs][k_pad], plane i the centred residue mod m_i
+ *          (two's complement byte, -128 included for m = 256).
  *  exps:   int32 [vecs], sigma (side 0) or tau (side 1), or
  *          OZAKI25_EXP_NONFINITE.
  * vecs == 0 or k == 0 is a no-op.  Errors: INVALID_VALUE (side, sizes, null
@@ -111,14 +124,16 @@ ozaki25_status ozaki25_deconstruct(int side, int64_t vecs, int64_t k, const doub
                                    int64_t ldx, ozaki25_moduli_set set, uint8_t* planes,
                                    int32_t* exps, void* stream);
 
-/* Per-modulus products (Eq. (residueprod)) from stored planes, on FP8 MFMA
- * with FP32 accumulation, reduced mod m_i at least every 16384 k so that every
- * partial sum is an integer below 2^24 and exact: for modulus i the limb
+/* Per-modulus products (Eq. (residueprod)) from stored planes.  S12: FP8
+ * MFMA with FP32 accumulation, reduced mod m_i at least every 16384 k so that
+ * every partial sum is an integer below 2^24 and exact: for modulus i the limb
  * products are combined with the square epilogue {1, s, s} (d1 e1 vanishes
  * mod s^2) or Eq. (karcarry)'s {-15, 16, 240}, and reduced to the centred
- * residue.
- *  planesA: uint8 e4m3 [num_planes][m][k_pad] (side 0 of ozaki25_deconstruct)
- *  planesB: uint8 e4m3 [num_planes][n][k_pad] (side 1)
+ * residue.  A15: one int8 MFMA product per modulus with int32 accumulation
+ * (exact: terms of at most 2^14, reduced every 65536 k).
+ *  planesA: uint8 [num_planes][m][k_pad] (side 0 of ozaki25_deconstruct):
+ *           e4m3 limbs for S12, int8 residues for A15
+ *  planesB: uint8 [num_planes][n][k_pad] (side 1)
  *  Cres:    int32 [r][m][n], centred C^(i) (written, caller-allocated)
  * m == 0 or n == 0 is a no-op; k == 0 writes zeros.  Errors as above. */
 ozaki25_status ozaki25_residue_gemm(int64_t m, int64_t n, int64_t k, const uint8_t* planesA,
@@ -126,7 +141,7 @@ ozaki25_status ozaki25_residue_gemm(int64_t m, int64_t n, int64_t k, const uint8
                                     int32_t* Cres, void* stream);
 
 /* Reconstruction (Alg. 3, Eq. (garner), Eq. (horner)): Garner's mixed-radix
- * digits of the r centred residues, the integer X in [-M/2, M/2), and
+ * digits of the r centred residues (12 or 15), the integer X in [-M/2, M/2), and
  * C_ij = RN(X 2^(-sigma_i - tau_j)) rounded once; NaN where expsA[i] or
  * expsB[j] is OZAKI25_EXP_NONFINITE.  With subtract != 0:
  * C_ij <- C_ij - RN(X 2^(-sigma_i - tau_j)) (the product rounded, then the

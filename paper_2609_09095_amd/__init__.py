@@ -1,4 +1,5 @@
-"""MI355X-native emulated FP64 GEMM by Ozaki Scheme II on FP8 MFMA.
+"""MI355X-native emulated FP64 GEMM by Ozaki Scheme II on FP8 MFMA (published
+moduli) or int8 MFMA (the all-byte moduli of Sec. 5.1, candidate A).
 
 Python binding of ``libozaki25.so`` (the C ABI declared in
 ``include/ozaki25.h``).  Argument marshalling only: every step of the
@@ -24,9 +25,11 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_PKG, "libozaki25.so")
 _HEADER = os.path.join(os.path.dirname(_PKG), "include", "ozaki25.h")
 
-S12 = 0
+S12 = 0           # published moduli, FP8 limb route
+A15 = 1           # all-byte moduli (Sec. 5.1 candidate A), int8 route
 NUM_MODULI = 12
 NUM_PLANES = 30
+NUM_MODULI_A15 = 15
 K_ALIGN = 128
 MAX_K = 4194304
 MAX_N = 8388608
@@ -151,16 +154,20 @@ def ozaki25_dgemm_workspace_size(m: int, n: int, k: int, set: int = S12) -> int:
 # ----------------------------------------------------------------- stages
 def ozaki25_deconstruct(side: int, X, planes=None, exps=None, set: int = S12, stream=None):
     """side 0: X is A (rows); side 1: X is B (columns).  Returns (planes, exps):
-    planes uint8 [30][vecs][k_pad] (limbs as OCP e4m3 bytes), exps int32 [vecs]."""
+    planes uint8 [num_planes][vecs][k_pad] (S12: limbs as OCP e4m3 bytes; A15:
+    int8 residues as two's complement bytes), exps int32 [vecs]."""
     import torch
     X, ldx = _matrix(X, "X")
     vecs, k = (X.shape[0], X.shape[1]) if side == 0 else (X.shape[1], X.shape[0])
     kp = ozaki25_k_pad(k)
+    npl = ozaki25_num_planes(set)
+    if npl < 0:
+        raise ValueError(f"unknown modulus set {set}")
     if planes is None:
-        planes = torch.empty((NUM_PLANES, vecs, kp), dtype=torch.uint8, device=X.device)
+        planes = torch.empty((npl, vecs, kp), dtype=torch.uint8, device=X.device)
     if exps is None:
         exps = torch.empty((vecs,), dtype=torch.int32, device=X.device)
-    if planes.numel() < NUM_PLANES * vecs * kp or exps.numel() < vecs:
+    if planes.numel() < npl * vecs * kp or exps.numel() < vecs:
         raise ValueError("output buffers too small")
     _check(lib().ozaki25_deconstruct(side, vecs, k, _ptr(X), ldx, set, _ptr(planes), _ptr(exps),
                                      _stream(stream)), "ozaki25_deconstruct")
@@ -169,12 +176,15 @@ def ozaki25_deconstruct(side: int, X, planes=None, exps=None, set: int = S12, st
 
 def ozaki25_residue_gemm(m: int, n: int, k: int, planesA, planesB, Cres=None, set: int = S12,
                          stream=None):
-    """Centred per-modulus products, int32 [12][m][n]."""
+    """Centred per-modulus products, int32 [r][m][n]."""
     import torch
     dev = planesA.device
+    r = ozaki25_num_moduli(set)
+    if r < 0:
+        raise ValueError(f"unknown modulus set {set}")
     if Cres is None:
-        Cres = torch.empty((NUM_MODULI, m, n), dtype=torch.int32, device=dev)
-    if Cres.numel() < NUM_MODULI * m * n:
+        Cres = torch.empty((r, m, n), dtype=torch.int32, device=dev)
+    if Cres.numel() < r * m * n:
         raise ValueError("Cres too small")
     _check(lib().ozaki25_residue_gemm(m, n, k, _ptr(planesA), _ptr(planesB), set, _ptr(Cres),
                                       _stream(stream)), "ozaki25_residue_gemm")
@@ -183,7 +193,7 @@ def ozaki25_residue_gemm(m: int, n: int, k: int, planesA, planesB, Cres=None, se
 
 def ozaki25_reconstruct(Cres, expsA, expsB, C=None, subtract: bool = False, set: int = S12,
                         stream=None):
-    """C (m x n float64) from int32 residues [12][m][n] and the exponents."""
+    """C (m x n float64) from int32 residues [r][m][n] and the exponents."""
     import torch
     m, n = expsA.numel(), expsB.numel()
     if C is None:

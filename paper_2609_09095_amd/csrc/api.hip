@@ -1,5 +1,6 @@
 // The C ABI of ozaki25.h: argument checks, the scale-bit rule, workspace
-// layout and the launch sequence of Alg. 1 on one stream.
+// layout and the launch sequence of Alg. 1 on one stream, for both modulus
+// sets.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -19,13 +20,28 @@ constexpr size_t kAlign = 256;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
-bool known_set(ozaki25_moduli_set set) { return set == OZAKI25_MODULI_S12; }
+static_assert(OZAKI25_MODULI_S12 == oz::kSetPublished && OZAKI25_MODULI_A15 == oz::kSetBytes,
+              "set numbering");
+static_assert(OZAKI25_NUM_MODULI == oz::kR && OZAKI25_NUM_PLANES == oz::kPlanes &&
+                  OZAKI25_NUM_MODULI_A15 == oz::kRA,
+              "set sizes");
+
+bool known_set(ozaki25_moduli_set set) {
+  return set == OZAKI25_MODULI_S12 || set == OZAKI25_MODULI_A15;
+}
+bool bytes_set(ozaki25_moduli_set set) { return set == OZAKI25_MODULI_A15; }
+int num_moduli(ozaki25_moduli_set set) { return bytes_set(set) ? oz::kRA : oz::kR; }
+// the all-byte set stores one int8 plane per modulus
+int num_planes(ozaki25_moduli_set set) { return bytes_set(set) ? oz::kRA : oz::kPlanes; }
+int64_t modulus(ozaki25_moduli_set set, int i) {
+  return bytes_set(set) ? oz::kModulusA[i] : oz::kModulus[i];
+}
 
 // t(k) = max{t : k 2^(2t) <= M/2 - 1} (Eq. (moduli) with mu = k 2^(2t)).
-int scale_bits(int64_t k) {
+int scale_bits(int64_t k, ozaki25_moduli_set set) {
   if (k < 1) return -1;
   u128 M = 1;
-  for (int i = 0; i < oz::kR; ++i) M *= (u128)oz::kModulus[i];
+  for (int i = 0; i < num_moduli(set); ++i) M *= (u128)modulus(set, i);
   const u128 q = (M / 2 - 1) / (u128)k;
   int t = 0;
   while (((u128)1 << (2 * (t + 1))) <= q) ++t;
@@ -51,20 +67,24 @@ struct Workspace {
   size_t planes_a, planes_b, exps_a, exps_b, cres, total;
 };
 
-Workspace layout(int64_t m, int64_t n, int64_t k) {
+// planes of A and B, exponents, and the residue products: int16 for the
+// published set (|c| <= 544), int8 for the all-byte set (|c| <= 128)
+Workspace layout(int64_t m, int64_t n, int64_t k, ozaki25_moduli_set set) {
   Workspace w;
   const int64_t kp = k_pad(k);
+  const size_t np = (size_t)num_planes(set);
+  const size_t cres_elem = bytes_set(set) ? sizeof(int8_t) : sizeof(int16_t);
   size_t off = 0;
   w.planes_a = off;
-  off = align_up(off + (size_t)oz::kPlanes * m * kp);
+  off = align_up(off + np * m * kp);
   w.planes_b = off;
-  off = align_up(off + (size_t)oz::kPlanes * n * kp);
+  off = align_up(off + np * n * kp);
   w.exps_a = off;
   off = align_up(off + (size_t)m * sizeof(int32_t));
   w.exps_b = off;
   off = align_up(off + (size_t)n * sizeof(int32_t));
   w.cres = off;
-  off = align_up(off + (size_t)oz::kR * m * n * sizeof(int16_t));
+  off = align_up(off + (size_t)num_moduli(set) * m * n * cres_elem);
   w.total = off;
   return w;
 }
@@ -84,21 +104,23 @@ const char* ozaki25_status_string(ozaki25_status s) {
   return "unknown status";
 }
 
-int ozaki25_num_moduli(ozaki25_moduli_set set) { return known_set(set) ? oz::kR : -1; }
+int ozaki25_num_moduli(ozaki25_moduli_set set) { return known_set(set) ? num_moduli(set) : -1; }
 
-int ozaki25_num_planes(ozaki25_moduli_set set) { return known_set(set) ? oz::kPlanes : -1; }
+int ozaki25_num_planes(ozaki25_moduli_set set) { return known_set(set) ? num_planes(set) : -1; }
 
 int64_t ozaki25_modulus(ozaki25_moduli_set set, int i) {
-  return known_set(set) && i >= 0 && i < oz::kR ? oz::kModulus[i] : -1;
+  return known_set(set) && i >= 0 && i < num_moduli(set) ? modulus(set, i) : -1;
 }
 
-int ozaki25_scale_bits(int64_t k, ozaki25_moduli_set set) { return known_set(set) ? scale_bits(k) : -1; }
+int ozaki25_scale_bits(int64_t k, ozaki25_moduli_set set) {
+  return known_set(set) ? scale_bits(k, set) : -1;
+}
 
 int64_t ozaki25_k_pad(int64_t k) { return k_pad(k); }
 
 size_t ozaki25_planes_bytes(int64_t vecs, int64_t k, ozaki25_moduli_set set) {
   if (!known_set(set) || vecs < 0 || k < 0) return 0;
-  return (size_t)oz::kPlanes * (size_t)vecs * (size_t)k_pad(k);
+  return (size_t)num_planes(set) * (size_t)vecs * (size_t)k_pad(k);
 }
 
 ozaki25_status ozaki25_deconstruct(int side, int64_t vecs, int64_t k, const double* X, int64_t ldx,
@@ -113,10 +135,10 @@ ozaki25_status ozaki25_deconstruct(int side, int64_t vecs, int64_t k, const doub
   if (((uintptr_t)planes & 15) || ((uintptr_t)exps & 3) || ((uintptr_t)X & 7))
     return OZAKI25_ERR_INVALID_VALUE;
   hipStream_t s = (hipStream_t)stream;
-  const int t = scale_bits(k);
+  const int t = scale_bits(k, set);
   hipError_t e = oz::launch_scan(side, vecs, k, X, ldx, t, exps, s);
   if (e == hipSuccess)
-    e = oz::launch_deconstruct(side, vecs, k, k_pad(k), t, X, ldx, exps, (int8_t*)planes, s);
+    e = oz::launch_deconstruct((int)set, side, vecs, k, k_pad(k), t, X, ldx, exps, (int8_t*)planes, s);
   return hip_status(e);
 }
 
@@ -129,8 +151,10 @@ ozaki25_status ozaki25_residue_gemm(int64_t m, int64_t n, int64_t k, const uint8
   if (!Cres || (k > 0 && (!planesA || !planesB))) return OZAKI25_ERR_INVALID_VALUE;
   if (((uintptr_t)planesA & 15) || ((uintptr_t)planesB & 15) || ((uintptr_t)Cres & 3))
     return OZAKI25_ERR_INVALID_VALUE;
-  return hip_status(oz::launch_residue_gemm_i32(m, n, k_pad(k), (const int8_t*)planesA,
-                                                (const int8_t*)planesB, Cres, (hipStream_t)stream));
+  const int8_t *pa = (const int8_t*)planesA, *pb = (const int8_t*)planesB;
+  hipStream_t s = (hipStream_t)stream;
+  return hip_status(bytes_set(set) ? oz::launch_residue_gemm_bytes_i32(m, n, k_pad(k), pa, pb, Cres, s)
+                                   : oz::launch_residue_gemm_i32(m, n, k_pad(k), pa, pb, Cres, s));
 }
 
 ozaki25_status ozaki25_reconstruct(int64_t m, int64_t n, const int32_t* Cres, const int32_t* expsA,
@@ -141,13 +165,16 @@ ozaki25_status ozaki25_reconstruct(int64_t m, int64_t n, const int32_t* Cres, co
   if (!Cres || !expsA || !expsB || !C || ldc < n) return OZAKI25_ERR_INVALID_VALUE;
   if (((uintptr_t)Cres & 3) || ((uintptr_t)expsA & 3) || ((uintptr_t)expsB & 3) || ((uintptr_t)C & 7))
     return OZAKI25_ERR_INVALID_VALUE;
-  return hip_status(oz::launch_reconstruct_i32(m, n, Cres, expsA, expsB, C, ldc, subtract ? 1 : 0,
-                                               (hipStream_t)stream));
+  hipStream_t s = (hipStream_t)stream;
+  const int sub = subtract ? 1 : 0;
+  return hip_status(bytes_set(set)
+                        ? oz::launch_reconstruct_bytes_i32(m, n, Cres, expsA, expsB, C, ldc, sub, s)
+                        : oz::launch_reconstruct_i32(m, n, Cres, expsA, expsB, C, ldc, sub, s));
 }
 
 size_t ozaki25_dgemm_workspace_size(int64_t m, int64_t n, int64_t k, ozaki25_moduli_set set) {
   if (!known_set(set) || m < 0 || n < 0 || k < 0) return 0;
-  return layout(m, n, k).total;
+  return layout(m, n, k, set).total;
 }
 
 ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
@@ -175,7 +202,7 @@ ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A
     return hip_status(e);
   }
 
-  const Workspace w = layout(m, n, k);
+  const Workspace w = layout(m, n, k, set);
   void* ws = workspace;
   bool owned = false;
   if (ws) {
@@ -189,20 +216,26 @@ ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A
   int8_t* pb = (int8_t*)(base + w.planes_b);
   int32_t* ea = (int32_t*)(base + w.exps_a);
   int32_t* eb = (int32_t*)(base + w.exps_b);
-  int16_t* cres = (int16_t*)(base + w.cres);
-  const int t = scale_bits(k);
+  void* cres = base + w.cres;
+  const bool bytes = bytes_set(set);
+  const int t = scale_bits(k, set);
   const int64_t kp = k_pad(k);
 
   if (ev) e = hipEventRecord(ev[0], s);
   if (e == hipSuccess) e = oz::launch_scan(0, m, k, A, lda, t, ea, s);
   if (e == hipSuccess) e = oz::launch_scan(1, n, k, B, ldb, t, eb, s);
   if (ev && e == hipSuccess) e = hipEventRecord(ev[1], s);
-  if (e == hipSuccess) e = oz::launch_deconstruct(0, m, k, kp, t, A, lda, ea, pa, s);
-  if (e == hipSuccess) e = oz::launch_deconstruct(1, n, k, kp, t, B, ldb, eb, pb, s);
+  if (e == hipSuccess) e = oz::launch_deconstruct((int)set, 0, m, k, kp, t, A, lda, ea, pa, s);
+  if (e == hipSuccess) e = oz::launch_deconstruct((int)set, 1, n, k, kp, t, B, ldb, eb, pb, s);
   if (ev && e == hipSuccess) e = hipEventRecord(ev[2], s);
-  if (e == hipSuccess) e = oz::launch_residue_gemm_i16(m, n, kp, pa, pb, cres, s);
+  if (e == hipSuccess)
+    e = bytes ? oz::launch_residue_gemm_bytes_i8(m, n, kp, pa, pb, (int8_t*)cres, s)
+              : oz::launch_residue_gemm_i16(m, n, kp, pa, pb, (int16_t*)cres, s);
   if (ev && e == hipSuccess) e = hipEventRecord(ev[3], s);
-  if (e == hipSuccess) e = oz::launch_reconstruct_i16(m, n, cres, ea, eb, C, ldc, subtract ? 1 : 0, s);
+  const int sub = subtract ? 1 : 0;
+  if (e == hipSuccess)
+    e = bytes ? oz::launch_reconstruct_bytes_i8(m, n, (const int8_t*)cres, ea, eb, C, ldc, sub, s)
+              : oz::launch_reconstruct_i16(m, n, (const int16_t*)cres, ea, eb, C, ldc, sub, s);
   if (ev && e == hipSuccess) e = hipEventRecord(ev[4], s);
   if (owned) {
     const hipError_t f = hipFreeAsync(ws, s);

@@ -1,6 +1,8 @@
 // Deconstruction (Alg. 2): scale by 2^sigma, round to nearest even, twelve
 // centred residues, limb split, packed e4m3 plane stores (every limb is an
-// e4m3-exact integer, Lemma 1, so the conversion is exact).
+// e4m3-exact integer, Lemma 1, so the conversion is exact).  For the
+// all-byte set (Sec. 5.1, candidate A) fifteen centred residues stored as
+// int8, one plane per modulus.
 //
 // Each thread owns one vector (row of A / column of B) and 16 consecutive k,
 // so every plane store is one 16-byte write.  VALU work and HBM traffic (8
@@ -45,12 +47,15 @@ __device__ __forceinline__ void store16(int8_t* p, const float (&b)[kElems]) {
 }
 
 // Centred residue of the integer-valued y modulo M, in [-(M/2), (M-1)/2],
-// as a float (exact: |residue| <= 544).  EXACT (|y| <= 2^50): the FP64
-// quotient y * RN(1/M) is within |y| 2^-52 / M <= 1/(4M) of y / M, while for
-// odd M y / M is at least 1/(2M) away from a half integer, so rint gives the
-// nearest quotient and y - qM is already centred; for M = 1024 the quotient
-// is exact and only the tie +512 needs mapping to -512.  Otherwise the
-// general form with its two corrections.
+// as a double (an integer, |residue| <= 544).  EXACT (|y| <= 2^51, M odd or
+// a power of two): for odd M, y / M is at least 1/(2M) away from a half
+// integer, and the FP64 quotient y * RN(1/M) is closer than that to y / M:
+// within |y| 2^-52 / M <= 1/(4M) for |y| <= 2^50, within
+// (2^51 - 1)(2^-52 + 2^-106) / M < 1/(2M) below 2^51, and within 1/(4M) at
+// |y| = 2^51 (a power of two scales RN(1/M) exactly).  So rint gives the
+// nearest quotient and y - qM is already centred; for a power of two the
+// quotient is exact and only the tie +M/2 needs mapping to -M/2.  Otherwise
+// the general form with its two corrections.
 template <int M, bool EXACT>
 __device__ __forceinline__ double centred_residue(double y) {
   if constexpr (!EXACT) {
@@ -163,13 +168,10 @@ __device__ __forceinline__ void emit_all(std::integer_sequence<int, I...>, const
   (emit_modulus<I, EXACT>(y, planes, plane_stride, off, lut), ...);
 }
 
-template <int SIDE, bool EXACT>
-__global__ __launch_bounds__(256) void deconstruct_kernel(int64_t vecs, int64_t k, int64_t kp,
-                                                          const double* __restrict__ X, int64_t ldx,
-                                                          const int32_t* __restrict__ exps,
-                                                          int8_t* __restrict__ planes) {
+// Thread -> (vector, 16-k group) map of both sides.
+template <int SIDE>
+__device__ __forceinline__ void group_of(int64_t kp, int64_t& v, int64_t& g) {
   const int64_t ngroups = kp / kElems;
-  int64_t v, g;
   if constexpr (SIDE == 0) {  // block: 4 rows x 64 groups, a wavefront per row
     const int64_t gb = (ngroups + 63) / 64;
     v = (int64_t)(blockIdx.x / gb) * 4 + (threadIdx.x >> 6);
@@ -180,64 +182,152 @@ __global__ __launch_bounds__(256) void deconstruct_kernel(int64_t vecs, int64_t 
     v = (int64_t)(blockIdx.x / gb) * 32 + (threadIdx.x >> 6) * 8 + (lane & 7);
     g = (int64_t)(blockIdx.x % gb) * 8 + (lane >> 3);
   }
-  const bool active = v < vecs && g < ngroups;
+}
+
+// The 16 inputs of a group: unconditional loads from clamped (always valid)
+// addresses, then the mask, so no branches sit around the loads; zeros past
+// k, for inactive threads and for a non-finite vector.  Returns sigma (0 for
+// a non-finite vector).
+template <int SIDE>
+__device__ __forceinline__ int load_group(int64_t vecs, int64_t k, const double* __restrict__ X,
+                                          int64_t ldx, const int32_t* __restrict__ exps, int64_t v,
+                                          int64_t k0, bool active, double (&x)[kElems]) {
   int sigma = active ? exps[v] : 0;
   const bool finite = sigma != INT32_MIN;
   sigma = finite ? sigma : 0;
-  const int64_t k0 = g * kElems;
-  // unconditional loads from clamped (always valid) addresses, then the
-  // mask: no branches around the loads.  lim = last valid c of this group.
+  // lim = last valid c of this group
   const int64_t vc = v < vecs ? v : vecs - 1;
   const int64_t kc = k0 < k ? k0 : k - 1;
   const int lim = k0 < k ? (int)(k - k0 < kElems ? k - k0 : kElems) - 1 : 0;
   const double* first = SIDE == 0 ? X + vc * ldx + kc : X + kc * ldx + vc;
   const bool live = active && finite;
-  double x[kElems];
 #pragma unroll
   for (int c = 0; c < kElems; ++c) {
     const int cc = c < lim ? c : lim;
     const double xv = SIDE == 0 ? first[cc] : first[(int64_t)cc * ldx];
     x[c] = (live && c <= lim && k0 + c < k) ? xv : 0.0;
   }
+  return sigma;
+}
+
+// |x 2^sigma| < 2^t: the scaling is exact, rint is the one rounding.
+__device__ __forceinline__ void scale_round(const double (&x)[kElems], int sigma,
+                                            double (&y)[kElems]) {
+#pragma unroll
+  for (int c = 0; c < kElems; ++c) y[c] = __builtin_rint(__builtin_ldexp(x[c], sigma));
+}
+
+template <int SIDE, bool EXACT>
+__global__ __launch_bounds__(256) void deconstruct_kernel(int64_t vecs, int64_t k, int64_t kp,
+                                                          const double* __restrict__ X, int64_t ldx,
+                                                          const int32_t* __restrict__ exps,
+                                                          int8_t* __restrict__ planes) {
+  int64_t v, g;
+  group_of<SIDE>(kp, v, g);
+  const bool active = v < vecs && g < kp / kElems;
+  const int64_t k0 = g * kElems;
+  double x[kElems];
+  const int sigma = load_group<SIDE>(vecs, k, X, ldx, exps, v, k0, active, x);
   // the split table, built while the loads are in flight
   __shared__ uint32_t lut[kSplitTable];
   for (int i = threadIdx.x; i < kSplitTable; i += 256) lut[i] = split_16_codes(i - 256);
   __syncthreads();
   if (!active) return;
   double y[kElems];
-#pragma unroll
-  for (int c = 0; c < kElems; ++c) {
-    // |x 2^sigma| < 2^t: the scaling is exact, rint is the one rounding.
-    y[c] = __builtin_rint(__builtin_ldexp(x[c], sigma));
-  }
+  scale_round(x, sigma, y);
   emit_all<EXACT>(std::make_integer_sequence<int, kR>{}, y, planes, vecs * kp, v * kp + k0, lut);
 }
 
+// ---- all-byte set (Sec. 5.1, candidate A) on the int8 route: the centred
+// residue of a byte modulus lies in [-128, 127] and is stored as it stands,
+// one int8 plane per modulus (8 bytes read, 15 written per element).
+
+// four residues in [-128, 127] as bytes, the first in the low byte
+// (v_perm_b32 selectors: 0-3 bytes of the second operand, 4-7 of the first,
+// 12 gives 0)
+__device__ __forceinline__ uint32_t pack_bytes(int a, int b, int c, int d) {
+  const uint32_t ab = __builtin_amdgcn_perm((uint32_t)b, (uint32_t)a, 0x0c0c0400u);
+  const uint32_t cd = __builtin_amdgcn_perm((uint32_t)d, (uint32_t)c, 0x0c0c0400u);
+  return __builtin_amdgcn_perm(cd, ab, 0x05040100u);
+}
+
+template <int I, bool EXACT>
+__device__ __forceinline__ void emit_byte_modulus(const double (&y)[kElems], int8_t* planes,
+                                                  int64_t plane_stride, int64_t off) {
+  constexpr int M = kModulusA[I];
+  int r[kElems];
+#pragma unroll
+  for (int c = 0; c < kElems; ++c) r[c] = (int)centred_residue<M, EXACT>(y[c]);
+  uint4 w;
+  w.x = pack_bytes(r[0], r[1], r[2], r[3]);
+  w.y = pack_bytes(r[4], r[5], r[6], r[7]);
+  w.z = pack_bytes(r[8], r[9], r[10], r[11]);
+  w.w = pack_bytes(r[12], r[13], r[14], r[15]);
+  put16(planes + (int64_t)I * plane_stride + off, w);
+}
+
+template <bool EXACT, int... I>
+__device__ __forceinline__ void emit_all_bytes(std::integer_sequence<int, I...>,
+                                               const double (&y)[kElems], int8_t* planes,
+                                               int64_t plane_stride, int64_t off) {
+  (emit_byte_modulus<I, EXACT>(y, planes, plane_stride, off), ...);
+}
+
+template <int SIDE, bool EXACT>
+__global__ __launch_bounds__(256) void deconstruct_bytes_kernel(int64_t vecs, int64_t k, int64_t kp,
+                                                                const double* __restrict__ X,
+                                                                int64_t ldx,
+                                                                const int32_t* __restrict__ exps,
+                                                                int8_t* __restrict__ planes) {
+  int64_t v, g;
+  group_of<SIDE>(kp, v, g);
+  const bool active = v < vecs && g < kp / kElems;
+  if (!active) return;
+  const int64_t k0 = g * kElems;
+  double x[kElems], y[kElems];
+  const int sigma = load_group<SIDE>(vecs, k, X, ldx, exps, v, k0, true, x);
+  scale_round(x, sigma, y);
+  emit_all_bytes<EXACT>(std::make_integer_sequence<int, kRA>{}, y, planes, vecs * kp, v * kp + k0);
+}
+
 template <int SIDE>
-void launch_side(int64_t blocks, bool exact, int64_t vecs, int64_t k, int64_t kp, const double* X,
-                 int64_t ldx, const int32_t* exps, int8_t* planes, hipStream_t stream) {
-  if (exact)
-    hipLaunchKernelGGL((deconstruct_kernel<SIDE, true>), dim3((unsigned)blocks), dim3(256), 0, stream,
-                       vecs, k, kp, X, ldx, exps, planes);
-  else
-    hipLaunchKernelGGL((deconstruct_kernel<SIDE, false>), dim3((unsigned)blocks), dim3(256), 0,
-                       stream, vecs, k, kp, X, ldx, exps, planes);
+void launch_side(int64_t blocks, bool bytes, bool exact, int64_t vecs, int64_t k, int64_t kp,
+                 const double* X, int64_t ldx, const int32_t* exps, int8_t* planes,
+                 hipStream_t stream) {
+  const dim3 grid((unsigned)blocks), block(256);
+  if (bytes) {
+    if (exact)
+      hipLaunchKernelGGL((deconstruct_bytes_kernel<SIDE, true>), grid, block, 0, stream, vecs, k, kp,
+                         X, ldx, exps, planes);
+    else
+      hipLaunchKernelGGL((deconstruct_bytes_kernel<SIDE, false>), grid, block, 0, stream, vecs, k,
+                         kp, X, ldx, exps, planes);
+  } else if (exact) {
+    hipLaunchKernelGGL((deconstruct_kernel<SIDE, true>), grid, block, 0, stream, vecs, k, kp, X, ldx,
+                       exps, planes);
+  } else {
+    hipLaunchKernelGGL((deconstruct_kernel<SIDE, false>), grid, block, 0, stream, vecs, k, kp, X,
+                       ldx, exps, planes);
+  }
 }
 
 }  // namespace
 
-hipError_t launch_deconstruct(int side, int64_t vecs, int64_t k, int64_t kp, int t, const double* X,
-                              int64_t ldx, const int32_t* exps, int8_t* planes,
+hipError_t launch_deconstruct(int set, int side, int64_t vecs, int64_t k, int64_t kp, int t,
+                              const double* X, int64_t ldx, const int32_t* exps, int8_t* planes,
                               hipStream_t stream) {
   if (vecs <= 0 || kp <= 0) return hipSuccess;
   const int64_t ngroups = kp / kElems;
-  const bool exact = t <= 50;  // |y| <= 2^t: the quotient needs no correction
+  const bool bytes = set == kSetBytes;
+  // |y| <= 2^t: the quotient needs no correction (the two bounds of
+  // centred_residue; the all-byte set takes the sharper one)
+  const bool exact = t <= (bytes ? 51 : 50);
   if (side == 0) {
     const int64_t blocks = ((vecs + 3) / 4) * ((ngroups + 63) / 64);
-    launch_side<0>(blocks, exact, vecs, k, kp, X, ldx, exps, planes, stream);
+    launch_side<0>(blocks, bytes, exact, vecs, k, kp, X, ldx, exps, planes, stream);
   } else {
     const int64_t blocks = ((vecs + 31) / 32) * ((ngroups + 7) / 8);
-    launch_side<1>(blocks, exact, vecs, k, kp, X, ldx, exps, planes, stream);
+    launch_side<1>(blocks, bytes, exact, vecs, k, kp, X, ldx, exps, planes, stream);
   }
   return hipGetLastError();
 }

@@ -6,13 +6,13 @@
 
 namespace oz {
 
-// Centred residue of an integer-valued double v (|v| < 2^56) modulo M, in
-// [-(M/2), (M-1)/2].  q = rint(v / M) is formed with one FP64 multiply by
-// the rounded reciprocal; the remainder v - q M is exact in one FMA; the
-// quotient can be one off only when v / M lies within 2^-6 of a half
-// integer, which puts the remainder just outside the centred range on the
-// other side, so one correction each way restores it.  The even modulus
-// 1024 also lands here: v 2^-10 is exact, and the tie +512 maps to -512.
+// Centred residue of an integer-valued double v (|v| <= 2^58) modulo M
+// (odd M >= 197, or a power of two), in [-(M/2), (M-1)/2].  q = rint(v / M)
+// is formed with one FP64 multiply by the rounded reciprocal, which errs by
+// at most |v| 2^-52 / M < 1/3; so q is the nearest quotient or one off, the
+// remainder v - q M (exact in one FMA) lies within 0.84 M of zero, and one
+// correction each way brings it into the centred range.  For a power of two
+// v / M is exact and the tie +M/2 maps to -M/2.
 template <int M>
 __device__ __forceinline__ int cmod_f64(double v) {
   constexpr double inv = 1.0 / M;

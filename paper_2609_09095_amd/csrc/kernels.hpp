@@ -8,24 +8,34 @@
 
 namespace oz {
 
+// Modulus sets, as numbered by ozaki25_moduli_set.
+constexpr int kSetPublished = 0;  // Eq. (moduli), FP8 limb route
+constexpr int kSetBytes = 1;      // Sec. 5.1 candidate A, int8 route
+
 // Exponent scan of A's rows (side 0) or B's columns (side 1), Alg. 1 setup:
 // exps[v] = t - e_v, or INT32_MIN for a vector holding a NaN or infinity.
 hipError_t launch_scan(int side, int64_t vecs, int64_t k, const double* X, int64_t ldx, int t,
                        int32_t* exps, hipStream_t stream);
 
-// Alg. 2: scale, round, residues and e4m3 limb planes of one operand, given
-// exps and the scale bits t.
-hipError_t launch_deconstruct(int side, int64_t vecs, int64_t k, int64_t kp, int t, const double* X,
-                              int64_t ldx, const int32_t* exps, int8_t* planes,
+// Alg. 2: scale, round, residues and the planes of one operand, given exps
+// and the scale bits t: e4m3 limb planes (published set) or int8 residue
+// planes (all-byte set).
+hipError_t launch_deconstruct(int set, int side, int64_t vecs, int64_t k, int64_t kp, int t,
+                              const double* X, int64_t ldx, const int32_t* exps, int8_t* planes,
                               hipStream_t stream);
 
-// Eq. (residueprod) on int8 MFMA: r centred per-modulus products [r][m][n].
-// n must not exceed kMaxResidueCols.
+// Eq. (residueprod): r centred per-modulus products [r][m][n], on FP8 MFMA
+// from limb planes (published set) or int8 MFMA from residue planes
+// (all-byte set).  n must not exceed kMaxResidueCols.
 constexpr int64_t kMaxResidueCols = (int64_t)1 << 23;
 hipError_t launch_residue_gemm_i32(int64_t m, int64_t n, int64_t kp, const int8_t* pa,
                                    const int8_t* pb, int32_t* cres, hipStream_t stream);
 hipError_t launch_residue_gemm_i16(int64_t m, int64_t n, int64_t kp, const int8_t* pa,
                                    const int8_t* pb, int16_t* cres, hipStream_t stream);
+hipError_t launch_residue_gemm_bytes_i32(int64_t m, int64_t n, int64_t kp, const int8_t* pa,
+                                         const int8_t* pb, int32_t* cres, hipStream_t stream);
+hipError_t launch_residue_gemm_bytes_i8(int64_t m, int64_t n, int64_t kp, const int8_t* pa,
+                                        const int8_t* pb, int8_t* cres, hipStream_t stream);
 
 // Alg. 3: Garner, Horner, lift, single rounding (C = or C -= ).
 hipError_t launch_reconstruct_i32(int64_t m, int64_t n, const int32_t* cres, const int32_t* ea,
@@ -34,6 +44,13 @@ hipError_t launch_reconstruct_i32(int64_t m, int64_t n, const int32_t* cres, con
 hipError_t launch_reconstruct_i16(int64_t m, int64_t n, const int16_t* cres, const int32_t* ea,
                                   const int32_t* eb, double* C, int64_t ldc, int subtract,
                                   hipStream_t stream);
+// the same for the fifteen residues of the all-byte set
+hipError_t launch_reconstruct_bytes_i32(int64_t m, int64_t n, const int32_t* cres,
+                                        const int32_t* ea, const int32_t* eb, double* C,
+                                        int64_t ldc, int subtract, hipStream_t stream);
+hipError_t launch_reconstruct_bytes_i8(int64_t m, int64_t n, const int8_t* cres, const int32_t* ea,
+                                       const int32_t* eb, double* C, int64_t ldc, int subtract,
+                                       hipStream_t stream);
 
 // C = +0.0 over an m x n block (the k == 0 product).
 hipError_t launch_zero_c(int64_t m, int64_t n, double* C, int64_t ldc, hipStream_t stream);

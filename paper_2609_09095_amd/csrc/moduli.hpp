@@ -1,7 +1,9 @@
-// Compile-time constants of the published modulus set (Eq. (moduli)) and the
-// tables derived from it: limb layout (Eq. (pieces), Lemma 1), epilogue
-// coefficients (square epilogue {1, s, s}, Eq. (karcarry)) and Garner
-// constants (Eq. (garner)).  Everything is constexpr, so kernels see the
+// Compile-time constants of the modulus sets and the tables derived from
+// them.  The published set (Eq. (moduli)): limb layout (Eq. (pieces),
+// Lemma 1), epilogue coefficients (square epilogue {1, s, s}, Eq. (karcarry))
+// and Garner constants (Eq. (garner)).  The all-byte set (Sec. 5.1,
+// candidate A): fifteen moduli <= 256 whose centred residues are int8
+// operands as they stand.  Everything is constexpr, so kernels see the
 // moduli as immediates and no table lives in memory.
 #pragma once
 
@@ -68,11 +70,48 @@ constexpr int product_plane_a(int i, int p) { return root_of(i) ? (p == 2 ? 1 : 
 constexpr int product_plane_b(int i, int p) { return root_of(i) ? (p == 1 ? 1 : 0) : p; }
 
 static_assert(plane_base(kR) == kPlanes, "30 stored planes for the published set");
+
+// ---- all-byte set (Sec. 5.1, candidate A): 256 first, then fourteen odd
+// moduli; log2 of the product 117.8
+constexpr int kRA = 15;
+constexpr int kModulusA[kRA] = {256, 255, 253, 251, 247, 241, 239, 233,
+                                229, 227, 223, 217, 211, 199, 197};
+
+// (m_0 ... m_{l-1}) mod m_j and the Garner constants of the all-byte set
+constexpr int radix_mod_a(int l, int j) {
+  int64_t p = 1;
+  for (int q = 0; q < l; ++q) p = (p * kModulusA[q]) % kModulusA[j];
+  return (int)p;
+}
+constexpr int garner_w_a(int j) { return (int)inverse_mod(radix_mod_a(j, j), kModulusA[j]); }
+
+constexpr bool set_a_is_coprime_bytes() {
+  for (int i = 0; i < kRA; ++i) {
+    if (kModulusA[i] > 256 || kModulusA[i] < 2) return false;
+    for (int j = i + 1; j < kRA; ++j) {
+      int64_t a = kModulusA[i], b = kModulusA[j];
+      while (b) {
+        const int64_t t = a % b;
+        a = b;
+        b = t;
+      }
+      if (a != 1) return false;
+    }
+  }
+  return true;
+}
+static_assert(set_a_is_coprime_bytes(), "pairwise coprime moduli of at most 256");
 constexpr bool garner_constants_invert() {
   for (int j = 1; j < kR; ++j)
     if ((int64_t)radix_mod(j, j) * garner_w(j) % kModulus[j] != 1) return false;
   return true;
 }
 static_assert(garner_constants_invert(), "w_j (m_0 ... m_{j-1}) = 1 mod m_j");
+constexpr bool garner_constants_invert_a() {
+  for (int j = 1; j < kRA; ++j)
+    if ((int64_t)radix_mod_a(j, j) * garner_w_a(j) % kModulusA[j] != 1) return false;
+  return true;
+}
+static_assert(garner_constants_invert_a(), "w_j (m_0 ... m_{j-1}) = 1 mod m_j, all-byte set");
 
 }  // namespace oz

@@ -1,5 +1,5 @@
-// Reconstruction (Alg. 3): Garner's mixed-radix digits of the twelve centred
-// residues (Eq. (garner)), Horner recombination (Eq. (horner)), the lift to
+// Reconstruction (Alg. 3): Garner's mixed-radix digits of the twelve (or,
+// for the all-byte set, fifteen) centred residues (Eq. (garner)), Horner recombination (Eq. (horner)), the lift to
 // [-M/2, M/2), and one rounding of X 2^(-sigma_i - tau_j) to FP64.
 // One thread per output; the residue loads coalesce along the output row.
 // 24 bytes in and 8 out per output, with VALU work of the same order.
@@ -96,14 +96,16 @@ __device__ __forceinline__ int64_t half_value(const int (&v)[kR]) {
   return (int64_t)g0 + b0 * t;
 }
 
-// RN_even(mag 2^e) for 0 < mag < 2^113.
+// RN_even(mag 2^e) for 0 < mag < 2^MAXBITS (MAXBITS <= 127).
 //  - normal (and overflowing) results: the top 64 bits of mag, with every
 //    lower bit ORed into bit 0 as a sticky bit, convert to FP64 with the one
 //    correct rounding (bit 0 lies ten places below the rounding point), and
 //    ldexp scales exactly or overflows to infinity as rounding would.
 //  - subnormal results (exponent below -1022): keep the bits down to 2^-1074
 //    and round half to even on the dropped ones by hand.
+template <int MAXBITS>
 __device__ __forceinline__ double round_scaled(u128 mag, int e) {
+  static_assert(MAXBITS <= 127, "shifts stay inside 128 bits");
   const uint64_t hi = (uint64_t)(mag >> 64), lo = (uint64_t)mag;
   const int c = hi ? __builtin_clzll(hi) : 64 + __builtin_clzll(lo);  // leading zeros of mag
   const int E = 127 - c + e;  // the value lies in [2^E, 2^(E+1))
@@ -114,7 +116,7 @@ __device__ __forceinline__ double round_scaled(u128 mag, int e) {
   }
   const int sh = -1074 - e;  // dropped bits: the quantum is 2^-1074
   if (sh <= 0) return __builtin_ldexp((double)(lo << -sh), -1074);  // exact, below 2^53
-  if (sh > 113) return 0.0;  // below half the smallest subnormal
+  if (sh > MAXBITS) return 0.0;  // below half the smallest subnormal
   uint64_t mant = (uint64_t)(mag >> sh);
   const u128 rem = mag & (((u128)1 << sh) - 1);
   const u128 half = (u128)1 << (sh - 1);
@@ -134,7 +136,9 @@ __device__ __forceinline__ int load_residue(const RT* rowbase, int n, int col) {
   const void* base = (const void*)(((uint64_t)hi << 32) | lo);
   const __amdgpu_buffer_rsrc_t rs =
       __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, n * (int)sizeof(RT), 0x00020000);
-  if constexpr (sizeof(RT) == 2)
+  if constexpr (sizeof(RT) == 1)
+    return (int)(int8_t)__builtin_amdgcn_raw_buffer_load_b8(rs, col, 0, 0);
+  else if constexpr (sizeof(RT) == 2)
     return (int)(int16_t)__builtin_amdgcn_raw_buffer_load_b16(rs, col * 2, 0, 0);
   else
     return (int)__builtin_amdgcn_raw_buffer_load_b32(rs, col * 4, 0, 0);
@@ -162,12 +166,92 @@ __device__ __forceinline__ double reconstruct_one(const RT* rowq, int64_t mn, in
   const uint64_t H = (uint64_t)(neg ? -xh : xh);
   const int64_t L = neg ? -xl : xl;
   const u128 mag = (u128)H * (u128)kP + (u128)(__int128)L;
-  const double r = round_scaled(mag, -sa - sb);
+  const double r = round_scaled<113>(mag, -sa - sb);
+  return neg ? -r : r;
+}
+
+// ---- all-byte set (Sec. 5.1, candidate A) ---------------------------------
+// Fifteen centred residues, |c| <= 128.  Garner sums stay below 15 * 2^14 <
+// 2^18, so the FP32 quotient of a digit errs by less than 2^-5 / m_j and
+// rint gives the centred digit for odd m_j; m_0 = 256 takes the low eight
+// bits.  With 256 first and every other modulus odd, the balanced halves
+// Xl (digits 0-6, |Xl| <= P/2) and Xh (digits 7-14, |Xh| <= (Q-1)/2, Q odd)
+// give X = Xl + P Xh in exactly [-M/2, M/2): no lift is needed.  |X| < 2^117.
+constexpr int kSplitA = 7;
+constexpr uint64_t prod_range_a(int a, int b) {
+  uint64_t p = 1;
+  for (int i = a; i < b; ++i) p *= (uint64_t)kModulusA[i];
+  return p;
+}
+constexpr uint64_t kPA = prod_range_a(0, kSplitA);
+constexpr uint64_t kQA = prod_range_a(kSplitA, kRA);
+static_assert(kPA < (1ull << 56) && kQA < (1ull << 63), "halves fit 64 bits");
+static_assert(kModulusA[0] == 256 && kQA % 2 == 1, "the one even modulus leads the low half");
+
+template <int L, int J>
+inline constexpr int kGarnerWeightA =
+    centred_const((int64_t)radix_mod_a(L, J) * garner_w_a(J) % kModulusA[J], kModulusA[J]);
+template <int J>
+inline constexpr int kGarnerWA = centred_const(garner_w_a(J), kModulusA[J]);
+
+template <int J>
+__device__ __forceinline__ void garner_digit_a(const int (&c)[kRA], int (&v)[kRA]) {
+  constexpr int M = kModulusA[J];
+  int s = __mul24(c[J], kGarnerWA<J>);
+  [&]<int... L>(std::integer_sequence<int, L...>) {
+    ((s -= __mul24(v[L], kGarnerWeightA<L, J>)), ...);
+  }(std::make_integer_sequence<int, J>{});
+  if constexpr (M == 256) {
+    v[J] = ((s + 128) & 255) - 128;
+  } else {
+    const int q = (int)__builtin_rintf((float)s * (1.0f / M));
+    v[J] = s - q * M;
+  }
+}
+
+// Balanced value of digits [A, B): digit pairs v_j + m_j v_{j+1} in 24-bit
+// arithmetic (|pair| < 2^16), then Horner over the pairs in 64 bits.
+template <int A, int B>
+__device__ __forceinline__ int64_t half_value_a(const int (&v)[kRA]) {
+  constexpr int np = (B - A + 1) / 2;
+  int g[np];
+#pragma unroll
+  for (int i = 0; i < np; ++i) {
+    const int j = A + 2 * i;
+    g[i] = j + 1 < B ? v[j] + __mul24(v[j + 1], kModulusA[j]) : v[j];
+  }
+  int64_t x = g[np - 1];
+#pragma unroll
+  for (int i = np - 2; i >= 0; --i) {
+    const int j = A + 2 * i;
+    x = (int64_t)g[i] + (int64_t)kModulusA[j] * kModulusA[j + 1] * x;
+  }
+  return x;
+}
+
+template <typename RT>
+__device__ __forceinline__ double reconstruct_one_a(const RT* rowq, int64_t mn, int n, int col,
+                                                    int sa, int sb) {
+  if (sa == INT32_MIN || sb == INT32_MIN) return __builtin_nan("");
+  int c[kRA], v[kRA];
+#pragma unroll
+  for (int q = 0; q < kRA; ++q) c[q] = load_residue(rowq + q * mn, n, col);
+  [&]<int... J>(std::integer_sequence<int, J...>) {
+    (garner_digit_a<J>(c, v), ...);
+  }(std::make_integer_sequence<int, kRA>{});
+  const int64_t xl = half_value_a<0, kSplitA>(v);   // |xl| <= P/2
+  const int64_t xh = half_value_a<kSplitA, kRA>(v);  // |xh| <= (Q - 1) / 2
+  if (xh == 0 && xl == 0) return 0.0;
+  const bool neg = xh < 0 || (xh == 0 && xl < 0);
+  const uint64_t H = (uint64_t)(neg ? -xh : xh);
+  const int64_t L = neg ? -xl : xl;
+  const u128 mag = (u128)H * (u128)kPA + (u128)(__int128)L;
+  const double r = round_scaled<117>(mag, -sa - sb);
   return neg ? -r : r;
 }
 
 // Grid: x over 256-column strips, y over rows (strided by gridDim.y).
-template <typename RT>
+template <bool BYTES, typename RT>
 __global__ __launch_bounds__(256) void reconstruct_kernel(int64_t m, int64_t n,
                                                           const RT* __restrict__ cres,
                                                           const int32_t* __restrict__ ea,
@@ -179,7 +263,8 @@ __global__ __launch_bounds__(256) void reconstruct_kernel(int64_t m, int64_t n,
   const int64_t mn = m * n;
   const int sb = eb[col];
   for (int64_t row = blockIdx.y; row < m; row += gridDim.y) {
-    const double r = reconstruct_one(cres + row * n, mn, (int)n, (int)col, ea[row], sb);
+    const double r = BYTES ? reconstruct_one_a(cres + row * n, mn, (int)n, (int)col, ea[row], sb)
+                           : reconstruct_one(cres + row * n, mn, (int)n, (int)col, ea[row], sb);
     double* out = C + row * ldc + col;
     *out = subtract ? *out - r : r;
   }
@@ -195,12 +280,12 @@ dim3 grid_for(int64_t m, int64_t n) {
   return dim3((unsigned)((n + 255) / 256), (unsigned)(m < 65535 ? m : 65535));
 }
 
-template <typename RT>
+template <bool BYTES, typename RT>
 hipError_t launch_rec(int64_t m, int64_t n, const RT* cres, const int32_t* ea, const int32_t* eb,
                       double* C, int64_t ldc, int subtract, hipStream_t stream) {
   if (m <= 0 || n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(reconstruct_kernel<RT>, grid_for(m, n), dim3(256), 0, stream, m, n, cres, ea,
-                     eb, C, ldc, subtract);
+  hipLaunchKernelGGL((reconstruct_kernel<BYTES, RT>), grid_for(m, n), dim3(256), 0, stream, m, n,
+                     cres, ea, eb, C, ldc, subtract);
   return hipGetLastError();
 }
 
@@ -209,13 +294,25 @@ hipError_t launch_rec(int64_t m, int64_t n, const RT* cres, const int32_t* ea, c
 hipError_t launch_reconstruct_i32(int64_t m, int64_t n, const int32_t* cres, const int32_t* ea,
                                   const int32_t* eb, double* C, int64_t ldc, int subtract,
                                   hipStream_t stream) {
-  return launch_rec<int32_t>(m, n, cres, ea, eb, C, ldc, subtract, stream);
+  return launch_rec<false, int32_t>(m, n, cres, ea, eb, C, ldc, subtract, stream);
 }
 
 hipError_t launch_reconstruct_i16(int64_t m, int64_t n, const int16_t* cres, const int32_t* ea,
                                   const int32_t* eb, double* C, int64_t ldc, int subtract,
                                   hipStream_t stream) {
-  return launch_rec<int16_t>(m, n, cres, ea, eb, C, ldc, subtract, stream);
+  return launch_rec<false, int16_t>(m, n, cres, ea, eb, C, ldc, subtract, stream);
+}
+
+hipError_t launch_reconstruct_bytes_i32(int64_t m, int64_t n, const int32_t* cres,
+                                        const int32_t* ea, const int32_t* eb, double* C,
+                                        int64_t ldc, int subtract, hipStream_t stream) {
+  return launch_rec<true, int32_t>(m, n, cres, ea, eb, C, ldc, subtract, stream);
+}
+
+hipError_t launch_reconstruct_bytes_i8(int64_t m, int64_t n, const int8_t* cres, const int32_t* ea,
+                                       const int32_t* eb, double* C, int64_t ldc, int subtract,
+                                       hipStream_t stream) {
+  return launch_rec<true, int8_t>(m, n, cres, ea, eb, C, ldc, subtract, stream);
 }
 
 hipError_t launch_zero_c(int64_t m, int64_t n, double* C, int64_t ldc, hipStream_t stream) {

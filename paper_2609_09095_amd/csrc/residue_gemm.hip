@@ -1,4 +1,6 @@
-// Per-modulus residue products (Eq. (residueprod)) on gfx950 FP8 MFMA.
+// Per-modulus residue products (Eq. (residueprod)) on gfx950 FP8 MFMA (the
+// published set's limb planes) and int8 MFMA (the all-byte set's residue
+// planes, further below).
 //
 // Each modulus needs three limb products of length k (square m = s^2: d0e1,
 // d1e0 with weight s and d0e0 with weight 1 -- the d1e1 term vanishes mod
@@ -51,6 +53,7 @@ namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v8i __attribute__((ext_vector_type(8)));
+typedef int v16i __attribute__((ext_vector_type(16)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 
 constexpr int BM = 256;         // output rows per block
@@ -294,12 +297,17 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
       // the DMA of the stage after the segment's last one lands in the idle
-      // buffer (zeros past the panel) and is drained before the next segment
-      stage_mma_dma(lds_a0, lds_b0, ra0, rb0, fh, acc, ra, rb, lds_a1, lds_b1, voff, (s + 1) * BK, wave);
+      // buffer and is drained before the next segment.  The stage offset
+      // rides in the scalar offset, which the buffer range check leaves out,
+      // so after the panel's last stage that stage is loaded again instead
+      // of the bytes past the panel.
+      stage_mma_dma(lds_a0, lds_b0, ra0, rb0, fh, acc, ra, rb, lds_a1, lds_b1, voff,
+                    (s + 1 < nstage ? s + 1 : s) * BK, wave);
       if (s + 1 >= s1) break;
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
-      stage_mma_dma(lds_a1, lds_b1, ra0, rb0, fh, acc, ra, rb, lds_a0, lds_b0, voff, (s + 2) * BK, wave);
+      stage_mma_dma(lds_a1, lds_b1, ra0, rb0, fh, acc, ra, rb, lds_a0, lds_b0, voff,
+                    (s + 2 < nstage ? s + 2 : s + 1) * BK, wave);
     }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();  // every wave is done with the buffers before the next segment loads
@@ -339,15 +347,193 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
     }
 }
 
+// ---- all-byte set (Sec. 5.1, candidate A) on int8 MFMA --------------------
+// The planes hold the centred residues themselves (|r| <= 128), so a modulus
+// is ONE int8 product, accumulated in int32 by v_mfma_i32_32x32x32_i8:
+// every term is at most 2^14 in magnitude, so partial sums are exact below
+// 2^31.  Products longer than kSegA stages (65536 k) reduce the accumulator
+// mod m between segments (|carry| <= m/2: every partial stays below
+// 2^30 + 2^7).  The int8 MFMA's operand layouts mirror each other like the
+// FP8 one's: lane l holds row/column l%32 and 16 of the 32 k bytes of the
+// step, the same 16 on both sides for equal l/32.  Same tiling, block
+// order and LDS pipeline as above; a stage is four 32-byte K steps.
+constexpr int kSegA = 512;
+
+__constant__ int kModA[kRA] = {kModulusA[0],  kModulusA[1],  kModulusA[2],  kModulusA[3],
+                               kModulusA[4],  kModulusA[5],  kModulusA[6],  kModulusA[7],
+                               kModulusA[8],  kModulusA[9],  kModulusA[10], kModulusA[11],
+                               kModulusA[12], kModulusA[13], kModulusA[14]};
+
+// int8 fragment of one 32-row block for one 32-byte K step: lane half fh
+// takes 16-byte chunk 2 ks + fh of its row
+__device__ __forceinline__ v4i frag_i8(const int8_t* base, int r, int ks, int fh) {
+  return *reinterpret_cast<const v4i*>(base + r * BK + (((2 * ks + fh) ^ swz(r)) << 4));
+}
+
+// Centred residue of an int32 modulo m (odd, or 256), in [-(m/2), (m-1)/2]:
+// |x| < 2^31, so the FP64 quotient x RN(1/m) is within 2^-21 / m of x / m,
+// far closer than the 1/(2m) that separates x / m from a half integer for
+// odd m; rint gives the nearest quotient and the FMA the exact remainder.
+// For m = 256 the quotient is exact and the tie +128 maps to -128.
+__device__ __forceinline__ int cmod_i32(int x, int m, double minv) {
+  const double xd = (double)x;
+  const double q = __builtin_rint(xd * minv);
+  const int r = (int)__builtin_fma(-q, (double)m, xd);
+  return 2 * r == m ? -r : r;
+}
+
+// One stage: four 32-byte K steps of 2 x 2 MFMAs; the next stage's 4 DMA
+// loads go among step 0's MFMAs, the fragment reads of step ks + 1 among
+// step ks's.
+__device__ __forceinline__ void stage_mma_dma_i8(const int8_t* la, const int8_t* lb, int ra0,
+                                                 int rb0, int fh, v16i (&acc)[2][2],
+                                                 __amdgpu_buffer_rsrc_t ra,
+                                                 __amdgpu_buffer_rsrc_t rb, int8_t* na, int8_t* nb,
+                                                 const int (&voff)[2], int k0, int wave) {
+  v4i af[4][2], bf[4][2];
+  k0 = __builtin_amdgcn_readfirstlane(k0);
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+    for (int x = 0; x < 2; ++x) {
+      af[ks][x] = frag_i8(la, ra0 + 32 * x, ks, fh);
+      bf[ks][x] = frag_i8(lb, rb0 + 32 * x, ks, fh);
+    }
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        if (ks == 0) {
+          const int i = a * 2 + b;  // DMA i of 4: (slab i/2, side i%2)
+          const int slab = (wave * 2 + (i >> 1)) * 1024;
+          if (i & 1)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr)(nb + slab), 16, voff[i >> 1], k0, 0, 0);
+          else
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr)(na + slab), 16, voff[i >> 1], k0, 0, 0);
+        }
+        acc[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[ks][a], bf[ks][b], acc[a][b], 0, 0, 0);
+      }
+  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+}
+
 template <typename OT>
+__global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, int64_t n,
+                                                                    int64_t kp,
+                                                                    const int8_t* __restrict__ pa,
+                                                                    const int8_t* __restrict__ pb,
+                                                                    OT* __restrict__ cres) {
+  __shared__ __attribute__((aligned(1024))) int8_t lds_a0[kTile];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_b0[kTile];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_a1[kTile];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_b1[kTile];
+  const int64_t tiles_m = (m + BM - 1) / BM, tiles_n = (n + BN - 1) / BN;
+  int mod;
+  int64_t tm, tn;
+  block_coords(tiles_m, tiles_n, mod, tm, tn);
+  const int mm = kModA[mod];
+  const double minv = 1.0 / (double)mm;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wr = wave >> 2, wc = wave & 3;
+  const int fr = lane & 31, fh = lane >> 5;
+  const int ra0 = wr * 64 + fr, rb0 = wc * 64 + fr;
+  int voff[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = wave * 16 + i * 8 + (lane >> 3);
+    voff[i] = r * (int)kp + (((lane & 7) ^ swz(r)) << 4);
+  }
+  const int64_t rows_a = m - tm * BM < BM ? m - tm * BM : BM;
+  const int64_t rows_b = n - tn * BN < BN ? n - tn * BN : BN;
+  const int8_t* A = uniform_ptr(pa + ((int64_t)mod * m + tm * BM) * kp);
+  const int8_t* B = uniform_ptr(pb + ((int64_t)mod * n + tn * BN) * kp);
+  const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)A, (short)0, __builtin_amdgcn_readfirstlane((int)(rows_a * kp)), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)B, (short)0, __builtin_amdgcn_readfirstlane((int)(rows_b * kp)), 0x00020000);
+
+  v16i acc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) acc[a][b] = v16i{};
+
+  const int nstage = (int)(kp / BK);
+  for (int s0 = 0; s0 < nstage; s0 += kSegA) {
+    const int s1 = s0 + kSegA < nstage ? s0 + kSegA : nstage;
+    stage_load(ra, rb, lds_a0, lds_b0, voff, s0 * BK, wave);
+    for (int s = s0; s < s1; s += 2) {
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      // the DMA after the segment's last stage lands in the idle buffer; past
+      // the panel's last stage it repeats that stage (as above)
+      stage_mma_dma_i8(lds_a0, lds_b0, ra0, rb0, fh, acc, ra, rb, lds_a1, lds_b1, voff,
+                       (s + 1 < nstage ? s + 1 : s) * BK, wave);
+      if (s + 1 >= s1) break;
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      stage_mma_dma_i8(lds_a1, lds_b1, ra0, rb0, fh, acc, ra, rb, lds_a0, lds_b0, voff,
+                       (s + 2 < nstage ? s + 2 : s + 1) * BK, wave);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();  // every wave is done with the buffers before the next segment loads
+    if (s1 < nstage) {
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) acc[a][b][v] = cmod_i32(acc[a][b][v], mm, minv);
+    }
+  }
+
+  // result layout as in the FP8 kernel
+  OT* out = (OT*)uniform_ptr((const int8_t*)(cres + (int64_t)mod * m * n + tm * BM * n + tn * BN));
+  const int nn = (int)n;
+  const int rows_left = (int)(m - tm * BM), cols_left = (int)(n - tn * BN);
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int col = wc * 64 + b * 32 + fr;
+      const int row0 = wr * 64 + a * 32 + 4 * fh;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = row0 + 8 * (v >> 2) + (v & 3);
+        const int c = cmod_i32(acc[a][b][v], mm, minv);
+        if (row < rows_left && col < cols_left) out[row * nn + col] = (OT)c;
+      }
+    }
+}
+
+template <bool BYTES, typename OT>
 hipError_t launch_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* pa, const int8_t* pb,
                        OT* cres, hipStream_t stream) {
   if (m <= 0 || n <= 0) return hipSuccess;
   // the store epilogue uses 32-bit offsets within a 256-row tile
   if (n > kMaxResidueCols) return hipErrorInvalidValue;
-  const int64_t blocks = (int64_t)kR * ((m + BM - 1) / BM) * ((n + BN - 1) / BN);
-  hipLaunchKernelGGL(residue_gemm_kernel<OT>, dim3((unsigned)blocks), dim3(1024), 0, stream, m, n,
-                     kp, pa, pb, cres);
+  const int64_t blocks = (int64_t)(BYTES ? kRA : kR) * ((m + BM - 1) / BM) * ((n + BN - 1) / BN);
+  if constexpr (BYTES)
+    hipLaunchKernelGGL(residue_gemm_bytes_kernel<OT>, dim3((unsigned)blocks), dim3(1024), 0, stream,
+                       m, n, kp, pa, pb, cres);
+  else
+    hipLaunchKernelGGL(residue_gemm_kernel<OT>, dim3((unsigned)blocks), dim3(1024), 0, stream, m, n,
+                       kp, pa, pb, cres);
   return hipGetLastError();
 }
 
@@ -355,12 +541,22 @@ hipError_t launch_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* pa, const
 
 hipError_t launch_residue_gemm_i32(int64_t m, int64_t n, int64_t kp, const int8_t* pa,
                                    const int8_t* pb, int32_t* cres, hipStream_t stream) {
-  return launch_gemm<int32_t>(m, n, kp, pa, pb, cres, stream);
+  return launch_gemm<false, int32_t>(m, n, kp, pa, pb, cres, stream);
 }
 
 hipError_t launch_residue_gemm_i16(int64_t m, int64_t n, int64_t kp, const int8_t* pa,
                                    const int8_t* pb, int16_t* cres, hipStream_t stream) {
-  return launch_gemm<int16_t>(m, n, kp, pa, pb, cres, stream);
+  return launch_gemm<false, int16_t>(m, n, kp, pa, pb, cres, stream);
+}
+
+hipError_t launch_residue_gemm_bytes_i32(int64_t m, int64_t n, int64_t kp, const int8_t* pa,
+                                         const int8_t* pb, int32_t* cres, hipStream_t stream) {
+  return launch_gemm<true, int32_t>(m, n, kp, pa, pb, cres, stream);
+}
+
+hipError_t launch_residue_gemm_bytes_i8(int64_t m, int64_t n, int64_t kp, const int8_t* pa,
+                                        const int8_t* pb, int8_t* cres, hipStream_t stream) {
+  return launch_gemm<true, int8_t>(m, n, kp, pa, pb, cres, stream);
 }
 
 }  // namespace oz

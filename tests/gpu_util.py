@@ -29,21 +29,21 @@ def to_dev(a: np.ndarray):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
-def gpu_deconstruct(X: np.ndarray, side: int):
+def gpu_deconstruct(X: np.ndarray, side: int, set: int = oz.S12):
     import torch
-    planes, exps = oz.ozaki25_deconstruct(side, to_dev(X))
+    planes, exps = oz.ozaki25_deconstruct(side, to_dev(X), set=set)
     torch.cuda.synchronize()
     return planes, exps
 
 
-def gpu_dgemm(A: np.ndarray, B: np.ndarray, C_in: np.ndarray | None = None):
+def gpu_dgemm(A: np.ndarray, B: np.ndarray, C_in: np.ndarray | None = None, set: int = oz.S12):
     import torch
     Ad, Bd = to_dev(A), to_dev(B)
     if C_in is None:
-        C = oz.ozaki25_dgemm(Ad, Bd)
+        C = oz.ozaki25_dgemm(Ad, Bd, set=set)
     else:
         C = to_dev(C_in)
-        oz.ozaki25_dgemm_sub(Ad, Bd, C)
+        oz.ozaki25_dgemm_sub(Ad, Bd, C, set=set)
     torch.cuda.synchronize()
     return C
 
@@ -71,6 +71,15 @@ def assert_int_equal(got: np.ndarray, want: np.ndarray, what: str):
     if bad.size:
         idx = tuple(bad[0])
         raise AssertionError(f"{what}: {len(bad)} entries differ; first at {idx}: got {got[idx]} want {want[idx]}")
+
+
+def int8_bytes(residues: np.ndarray) -> np.ndarray:
+    """The all-byte set's plane format: each centred residue as a two's
+    complement byte."""
+    v = np.asarray(residues).astype(np.int64)
+    if np.any(v < -128) or np.any(v > 127):
+        raise ValueError("residue beyond int8")
+    return (v & 0xFF).astype(np.uint8)
 
 
 def e4m3_bytes(limbs: np.ndarray) -> np.ndarray:

@@ -44,9 +44,18 @@ def test_constants():
     assert oz.ozaki25_status_string(99) == "unknown status"
 
 
+def test_constants_all_byte_set():
+    assert oz.ozaki25_num_moduli(oz.A15) == 15 == oz.NUM_MODULI_A15
+    assert oz.ozaki25_num_planes(oz.A15) == 15
+    assert [oz.ozaki25_modulus(i, oz.A15) for i in range(15)] == oracle.moduli(1)
+    assert oz.ozaki25_modulus(15, oz.A15) == -1
+    assert oz.ozaki25_num_moduli(2) == -1
+
+
 @pytest.mark.parametrize("k", [1, 2, 63, 64, 65, 100, 255, 256, 1024, 4096, 7937, 8192, 4194304])
 def test_scale_bits_matches_oracle(k):
     assert oz.ozaki25_scale_bits(k) == oracle.scale_bits(k)
+    assert oz.ozaki25_scale_bits(k, oz.A15) == oracle.scale_bits(k, 1)
 
 
 def test_scale_bits_invalid():
@@ -64,6 +73,10 @@ def test_size_helpers():
     ws = oz.ozaki25_dgemm_workspace_size(100, 50, 70)
     assert ws >= 30 * 100 * 128 + 30 * 50 * 128 + 4 * 150 + 12 * 100 * 50 * 2
     assert ws % 256 == 0
+    # all-byte set: 15 int8 planes per operand, int8 residue products
+    assert oz.ozaki25_planes_bytes(10, 70, oz.A15) == 15 * 10 * 128
+    wa = oz.ozaki25_dgemm_workspace_size(100, 50, 70, oz.A15)
+    assert 15 * 150 * 128 + 4 * 150 + 15 * 100 * 50 <= wa < ws and wa % 256 == 0
 
 
 def _v(x):
@@ -103,7 +116,7 @@ def test_argument_errors_are_synchronous():
     assert f(4, 4, 4, fake, 4, _v(0x300000), 4, _v(0x200000), 3, 0, 0, null, 0, null, null) == oz.ERR_INVALID_VALUE
     assert f(4, 4, 4, fake, 4, _v(0x300000), 4, fake, 4, 0, 0, null, 0, null, null) == oz.ERR_INVALID_VALUE
     assert f(4, 4, 4, null, 4, _v(0x300000), 4, _v(0x200000), 4, 0, 0, null, 0, null, null) == oz.ERR_INVALID_VALUE
-    assert f(4, 4, 4, fake, 4, _v(0x300000), 4, _v(0x200000), 4, 1, 0, null, 0, null, null) == oz.ERR_INVALID_VALUE
+    assert f(4, 4, 4, fake, 4, _v(0x300000), 4, _v(0x200000), 4, 2, 0, null, 0, null, null) == oz.ERR_INVALID_VALUE
     assert f(0, 4, 4, null, 4, null, 4, null, 4, 0, 0, null, 0, null, null) == oz.SUCCESS
     assert f(4, oz.MAX_N + 1, 4, fake, 4, _v(0x300000), oz.MAX_N + 1, _v(0x200000), oz.MAX_N + 1, 0, 0, null, 0, null, null) == oz.ERR_UNSUPPORTED
     # a caller workspace that is too small is refused before any launch

@@ -12,7 +12,8 @@ import pytest
 import oracle
 import paper_2609_09095_amd as oz
 import workloads
-from gpu_util import assert_bits_equal, assert_int_equal, e4m3_bytes, log, require_gpu, sample_indices
+from gpu_util import (assert_bits_equal, assert_int_equal, e4m3_bytes, int8_bytes, log, require_gpu,
+                      sample_indices)
 
 pytestmark = pytest.mark.gpu
 
@@ -22,19 +23,22 @@ def gpu():
     require_gpu()
 
 
-def _run(name, nsample=96):
+def _run(name, nsample=96, set=oz.S12):
+    """set: the library's modulus set (the oracle numbers them alike)."""
     import torch
     w = workloads.WORKLOADS[name]
-    log(f"[large] {name}: generating m={w.m} n={w.n} k={w.k}")
+    plane_bytes = int8_bytes if set == oz.A15 else e4m3_bytes
+    log(f"[large] {name} set={set}: generating m={w.m} n={w.n} k={w.k}")
     A, B, C0 = workloads.make_inputs(w)
     rows = sample_indices(w.m, nsample, 11)
     cols = sample_indices(w.n, nsample, 12)
     Ad = torch.from_numpy(A).cuda()
     Bd = torch.from_numpy(B).cuda()
     Cd = torch.from_numpy(C0).cuda() if C0 is not None else torch.empty((w.m, w.n), dtype=torch.float64, device="cuda")
-    ws = torch.empty(oz.ozaki25_dgemm_workspace_size(w.m, w.n, w.k), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(oz.ozaki25_dgemm_workspace_size(w.m, w.n, w.k, set), dtype=torch.uint8,
+                     device="cuda")
     log(f"[large] {name}: ozaki25_dgemm_ex")
-    oz.ozaki25_dgemm_ex(Ad, Bd, Cd, subtract=w.subtract, workspace=ws)
+    oz.ozaki25_dgemm_ex(Ad, Bd, Cd, subtract=w.subtract, workspace=ws, set=set)
     torch.cuda.synchronize()
     ri = torch.from_numpy(rows).cuda()
     ci = torch.from_numpy(cols).cuda()
@@ -43,13 +47,13 @@ def _run(name, nsample=96):
     torch.cuda.empty_cache()
 
     log(f"[large] {name}: stage API (exponents, planes, products)")
-    planesA, expsA = oz.ozaki25_deconstruct(0, Ad)
-    planesB, expsB = oz.ozaki25_deconstruct(1, Bd)
+    planesA, expsA = oz.ozaki25_deconstruct(0, Ad, set=set)
+    planesB, expsB = oz.ozaki25_deconstruct(1, Bd, set=set)
     torch.cuda.synchronize()
     del Ad, Bd
     pA_s = planesA.index_select(1, ri).cpu().numpy()
     pB_s = planesB.index_select(1, ci).cpu().numpy()
-    Cres = oz.ozaki25_residue_gemm(w.m, w.n, w.k, planesA, planesB)
+    Cres = oz.ozaki25_residue_gemm(w.m, w.n, w.k, planesA, planesB, set=set)
     torch.cuda.synchronize()
     Cres_s = Cres.index_select(1, ri).index_select(2, ci).cpu().numpy()
     eA, eB = expsA.cpu().numpy(), expsB.cpu().numpy()
@@ -57,12 +61,12 @@ def _run(name, nsample=96):
     torch.cuda.empty_cache()
 
     log(f"[large] {name}: oracle on {len(rows)} x {len(cols)} outputs")
-    t = oracle.scale_bits(w.k)
+    t = oracle.scale_bits(w.k, set)
     assert_int_equal(eA, oracle.exponents(A, 0, t), "sigma (all rows)")
     assert_int_equal(eB, oracle.exponents(B, 1, t), "tau (all columns)")
-    r = oracle.dgemm(A, B, C_in=C0, rows=rows, cols=cols)
-    assert_int_equal(pA_s, e4m3_bytes(r.planesA), "planes of sampled rows of A")
-    assert_int_equal(pB_s, e4m3_bytes(r.planesB), "planes of sampled columns of B")
+    r = oracle.dgemm(A, B, C_in=C0, rows=rows, cols=cols, set=set)
+    assert_int_equal(pA_s, plane_bytes(r.planesA), "planes of sampled rows of A")
+    assert_int_equal(pB_s, plane_bytes(r.planesB), "planes of sampled columns of B")
     assert_int_equal(Cres_s, r.Cres, "per-modulus products (sampled)")
     assert_bits_equal(C_s, r.C, "C (sampled)")
     log(f"[large] {name}: ok")
@@ -92,3 +96,11 @@ def test_long_k_single_output():
     C = oz.ozaki25_dgemm(torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda())
     torch.cuda.synchronize()
     assert_bits_equal(C.cpu().numpy(), oracle.dgemm(A, B, want_planes=False).C, "C")
+
+
+def test_square_8192_all_byte_set():
+    _run("square", set=oz.A15)
+
+
+def test_ragged_8191_8209_7937_all_byte_set():
+    _run("ragged", set=oz.A15)
