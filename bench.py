@@ -1,13 +1,18 @@
 #!/usr/bin/env python3
-"""Benchmark: emulated FP64 GEMM (Ozaki Scheme II, published 12-modulus set,
-round to nearest) on one MI355X, through the C ABI.
+"""Benchmark: emulated FP64 GEMM (Ozaki Scheme II, round to nearest) on one
+MI355X, through the C ABI.
 
 One step = one full ozaki25_dgemm_ex call: exponent scans, deconstruction of
-both operands into e4m3 planes, the 36 FP8-MFMA limb products (FP32
-accumulation) with the modular epilogue, and the CRT reconstruction, on synthetic seeded inputs that
-are already resident in HBM.  Prints one JSON line.
+both operands into planes, the per-modulus products and the CRT
+reconstruction, on synthetic seeded inputs that are already resident in HBM.
+The headline line is the published 12-modulus set (e4m3 planes, 36 FP8-MFMA
+limb products with FP32 accumulation and the modular epilogue); the same run
+also times the all-byte 15-modulus set of Sec. 5.1 (int8 planes, 15 int8-MFMA
+products) on the same inputs and reports it under "all_byte_set".
+``--moduli a15`` makes the all-byte set the headline instead.  Prints one
+JSON line.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload square]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload square] [--moduli s12|a15]
 """
 from __future__ import annotations
 
@@ -28,10 +33,25 @@ import workloads  # noqa: E402
 # MI355X published peaks
 HBM_PEAK_GBS = 8000.0
 FP8_PEAK_TOPS = 5000.0
+INT8_PEAK_TOPS = 5000.0
 FP64_PEAK_TFLOPS = 78.6
-PRODUCTS = 36               # 3 limb products for each of the 12 moduli
-PLANE_BYTES = 30            # stored e4m3 plane bytes per element
-COUNTER_FILE = os.path.join(ROOT, "profiles", "residue_gemm_square_counters.txt")
+
+# per modulus set: products per output, plane bytes per input element,
+# residue bytes per output (the fused path's internal products), peak
+SETS = {
+    "s12": dict(id=0, oracle_set=0, r=12, products=36, plane_bytes=30, cres_bytes=24,
+                peak=FP8_PEAK_TOPS, dtype="fp8", moduli="published 12-modulus set",
+                route="e4m3 MFMA, fp32 accumulate", gemm_kernel="residue_gemm_kernel<int16>",
+                dec_kernel="deconstruct_kernel<0>+<1>",
+                note="fp8 ops (1 MAC = 2 ops): 36 limb products x 2mnk per launch; peak is the dense fp8 rate"),
+    "a15": dict(id=1, oracle_set=1, r=15, products=15, plane_bytes=15, cres_bytes=15,
+                peak=INT8_PEAK_TOPS, dtype="int8", moduli="all-byte 15-modulus set (Sec. 5.1 candidate A)",
+                route="int8 MFMA, int32 accumulate", gemm_kernel="residue_gemm_bytes_kernel<int8>",
+                dec_kernel="deconstruct_bytes_kernel<0>+<1>",
+                note="int8 ops (1 MAC = 2 ops): 15 residue products x 2mnk per launch; peak is the dense int8 rate"),
+}
+COUNTER_FILES = {"s12": os.path.join(ROOT, "profiles", "residue_gemm_square_counters.txt"),
+                 "a15": os.path.join(ROOT, "profiles", "residue_gemm_bytes_square_counters.txt")}
 GEMM_SOURCE = os.path.join(ROOT, "paper_2609_09095_amd", "csrc", "residue_gemm.hip")
 
 
@@ -44,14 +64,15 @@ def source_hash(path):
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_traffic(w):
+def measured_traffic(w, moduli):
     """HBM bytes per residue-GEMM launch from the committed rocprofv3 counter
     summary, or None if it is absent, for another workload, or taken on an
     older version of the kernel source."""
-    if not os.path.exists(COUNTER_FILE):
+    path = COUNTER_FILES[moduli]
+    if not os.path.exists(path):
         return None
     kv = {}
-    with open(COUNTER_FILE) as f:
+    with open(path) as f:
         for line in f:
             if ":" in line and not line.startswith("#"):
                 key, val = line.split(":", 1)
@@ -64,19 +85,62 @@ def measured_traffic(w):
         return None
 
 
-def cpu_baseline(A, B, w, rows, cols):
+def cpu_baseline(A, B, w, rows, cols, cfg):
     import oracle
     oracle.build(force=False)
     ridx = np.arange(rows)
     cidx = np.arange(cols)
     t0 = time.perf_counter()
-    oracle.dgemm(A, B, rows=ridx, cols=cidx, want_planes=False)
+    oracle.dgemm(A, B, rows=ridx, cols=cidx, want_planes=False, set=cfg["oracle_set"])
     dt = time.perf_counter() - t0
     flops = 2.0 * rows * cols * w.k
     return {"value": flops / dt / 1e12, "unit": "TFLOPS", "cores": 1, "kind": "oracle",
             "sample": f"{rows} rows of A x {cols} columns of B of the {w.name} workload, full k={w.k} "
-                      f"(exponent scan, quantise, residues, 12 int64 residue GEMMs, Garner, rounding, "
-                      f"exact-product check), {dt:.1f} s single-threaded"}
+                      f"(exponent scan, quantise, residues, {cfg['r']} int64 residue GEMMs, Garner, "
+                      f"rounding, exact-product check), {dt:.1f} s single-threaded"}
+
+
+def time_set(oz, torch, w, Ad, Bd, Cd, cfg, steps, warmup):
+    """Mean ms per step and per stage of ozaki25_dgemm_ex for one modulus set."""
+    ws = torch.empty(oz.ozaki25_dgemm_workspace_size(w.m, w.n, w.k, cfg["id"]), dtype=torch.uint8,
+                     device=Ad.device)
+
+    def step(events=None):
+        oz.ozaki25_dgemm_ex(Ad, Bd, Cd, subtract=w.subtract, workspace=ws, stage_events=events,
+                            set=cfg["id"])
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(oz.NUM_STAGE_EVENTS)] for _ in range(steps)]
+    for row in ev:
+        for e in row:
+            e.record()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(steps):
+        step(ev[i])
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / steps
+    stage = np.array([[row[j].elapsed_time(row[j + 1]) for j in range(oz.NUM_STAGE_EVENTS - 1)] for row in ev])
+    del ws
+    return ms, stage.mean(axis=0).tolist()
+
+
+def rates(w, cfg, ms, stages):
+    scan_ms, dec_ms, gemm_ms, rec_ms = stages
+    elems = w.m * w.k + w.k * w.n
+    dec_bytes = elems * (8 + cfg["plane_bytes"])
+    rec_bytes = w.m * w.n * (cfg["cres_bytes"] + 8 + (8 if w.subtract else 0))
+    gemm_ops = 2.0 * cfg["products"] * w.m * w.n * w.k
+    return dict(tflops=w.flops / (ms * 1e-3) / 1e12, gemm_ops=gemm_ops,
+                gemm_tops=gemm_ops / (gemm_ms * 1e-3) / 1e12, dec_bytes=dec_bytes,
+                dec_gbs=dec_bytes / (dec_ms * 1e-3) / 1e9,
+                stage_gbs=(dec_bytes + elems * 8) / ((dec_ms + scan_ms) * 1e-3) / 1e9,
+                rec_gbs=rec_bytes / (rec_ms * 1e-3) / 1e9,
+                roof=cfg["peak"] / cfg["products"])
 
 
 def main():
@@ -91,6 +155,9 @@ def main():
     ap.add_argument("--calibration-copy", action="store_true",
                     help="copy 1 GiB device to device once before the run (a known-size kernel "
                          "for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE counters)")
+    ap.add_argument("--moduli", default="s12", choices=sorted(SETS),
+                    help="modulus set of the headline line (the other one is reported alongside)")
+    ap.add_argument("--only", action="store_true", help="time the headline modulus set only")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -112,12 +179,9 @@ def main():
     dev = torch.device("cuda:0")
     Ad = torch.from_numpy(A).to(dev)
     Bd = torch.from_numpy(B).to(dev)
-    Cd = torch.from_numpy(C0).to(dev) if C0 is not None else torch.empty((w.m, w.n), dtype=torch.float64, device=dev)
-    ws = torch.empty(oz.ozaki25_dgemm_workspace_size(w.m, w.n, w.k), dtype=torch.uint8, device=dev)
+    C0d = torch.from_numpy(C0).to(dev) if C0 is not None else None
+    Cd = C0d.clone() if C0d is not None else torch.empty((w.m, w.n), dtype=torch.float64, device=dev)
     torch.cuda.synchronize()
-
-    def step(events=None):
-        oz.ozaki25_dgemm_ex(Ad, Bd, Cd, subtract=w.subtract, workspace=ws, stage_events=events)
 
     if args.calibration_copy:
         src = torch.ones(1 << 27, dtype=torch.float64, device=dev)   # 1 GiB
@@ -127,41 +191,41 @@ def main():
         del src, dst
         log("[bench] calibration copy: 1 GiB read, 1 GiB written")
 
-    log(f"[bench] warmup {args.warmup}")
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(oz.NUM_STAGE_EVENTS)] for _ in range(args.steps)]
-    for row in ev:
-        for e in row:
-            e.record()
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    log(f"[bench] timing {args.steps} steps")
-    start.record()
-    for i in range(args.steps):
-        step(ev[i])
-    end.record()
-    torch.cuda.synchronize()
-    total_ms = start.elapsed_time(end)
-    ms = total_ms / args.steps
-    stage = np.array([[row[j].elapsed_time(row[j + 1]) for j in range(oz.NUM_STAGE_EVENTS - 1)] for row in ev])
-    scan_ms, dec_ms, gemm_ms, rec_ms = stage.mean(axis=0).tolist()
+    cfg = SETS[args.moduli]
+    log(f"[bench] {cfg['moduli']}: warmup {args.warmup}, timing {args.steps} steps")
+    ms, stages = time_set(oz, torch, w, Ad, Bd, Cd, cfg, args.steps, args.warmup)
+    scan_ms, dec_ms, gemm_ms, rec_ms = stages
+    rt = rates(w, cfg, ms, stages)
     log(f"[bench] {ms:.3f} ms/step; scan {scan_ms:.3f} deconstruct {dec_ms:.3f} gemm {gemm_ms:.3f} "
         f"reconstruct {rec_ms:.3f} ms")
 
-    tflops = w.flops / (ms * 1e-3) / 1e12
-    gemm_ops = 2.0 * PRODUCTS * w.m * w.n * w.k
-    gemm_tops = gemm_ops / (gemm_ms * 1e-3) / 1e12
-    elems = w.m * w.k + w.k * w.n
-    dec_bytes = elems * (8 + PLANE_BYTES)
-    scan_bytes = elems * 8
-    dec_gbs = dec_bytes / (dec_ms * 1e-3) / 1e9
-    stage_gbs = (dec_bytes + scan_bytes) / ((dec_ms + scan_ms) * 1e-3) / 1e9
-    rec_bytes = w.m * w.n * (12 * 2 + 8 + (8 if w.subtract else 0))
-    rec_gbs = rec_bytes / (rec_ms * 1e-3) / 1e9
-    roof = FP8_PEAK_TOPS / PRODUCTS
+    other = None
+    if not args.only:
+        name = "a15" if args.moduli == "s12" else "s12"
+        ocfg = SETS[name]
+        if C0d is not None:
+            Cd.copy_(C0d)
+        log(f"[bench] {ocfg['moduli']}: warmup {args.warmup}, timing {args.steps} steps")
+        oms, ostages = time_set(oz, torch, w, Ad, Bd, Cd, ocfg, args.steps, args.warmup)
+        ort = rates(w, ocfg, oms, ostages)
+        log(f"[bench] {oms:.3f} ms/step; stages {[round(x, 3) for x in ostages]}")
+        other = {
+            "moduli": ocfg["moduli"], "route": ocfg["route"], "dtype": ocfg["dtype"],
+            "value": round(ort["tflops"], 3), "unit": "TFLOPS", "ms_per_step": round(oms, 4),
+            "stage_ms": dict(zip(("scan", "deconstruct", "residue_gemm", "reconstruct"),
+                                 [round(x, 4) for x in ostages])),
+            "roofline": {"bound": "mfma", "kernel": ocfg["gemm_kernel"], "achieved": round(ort["gemm_tops"], 2),
+                         "peak": ocfg["peak"], "unit": "TFLOP/s" if ocfg["dtype"] == "fp8" else "TOP/s",
+                         "frac": round(ort["gemm_tops"] / ocfg["peak"], 4),
+                         "traffic": measured_traffic(w, name), "ops_per_launch": ort["gemm_ops"],
+                         "note": ocfg["note"]},
+            "roofline_deconstruct": {"bound": "hbm", "kernel": ocfg["dec_kernel"],
+                                     "achieved": round(ort["dec_gbs"], 1), "peak": HBM_PEAK_GBS,
+                                     "unit": "GB/s", "frac": round(ort["dec_gbs"] / HBM_PEAK_GBS, 4),
+                                     "bytes_per_call": ort["dec_bytes"]},
+            "emulation_roof_tflops": round(ort["roof"], 2),
+            "emulation_roof_frac": round(ort["tflops"] / ort["roof"], 4),
+        }
 
     native = None
     if not args.no_native and not w.subtract and w.m * w.n * w.k <= 8192 ** 3:
@@ -177,10 +241,10 @@ def main():
         native = w.flops / (s0.elapsed_time(s1) / 3 * 1e-3) / 1e12
         del Cn
 
-    traffic = measured_traffic(w)
+    peak_unit = "TFLOP/s" if cfg["dtype"] == "fp8" else "TOP/s"
     result = {
         "metric": "emulated FP64 TFLOPS (2mnk/s) + deconstruction GB/s vs HBM/MFMA roofs",
-        "value": round(tflops, 3),
+        "value": round(rt["tflops"], 3),
         "unit": "TFLOPS",
         "n_gpus": 1,
         "steps": args.steps,
@@ -189,40 +253,42 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "fp8",
+        "dtype": cfg["dtype"],
         "data": "synthetic",
         "config": {"workload": f"{w.name}: C {'-=' if w.subtract else '='} A.B, m={w.m} n={w.n} k={w.k}, "
                                f"entries (U-0.5)exp({w.s} N), seed {w.seed}",
-                   "m": w.m, "n": w.n, "k": w.k, "moduli": "published 12-modulus set", "quantiser": "RN",
-                   "route": "e4m3 MFMA, fp32 accumulate"},
-        "roofline": {"bound": "mfma", "kernel": "residue_gemm_kernel<int16>",
-                     "achieved": round(gemm_tops, 2), "peak": FP8_PEAK_TOPS, "unit": "TFLOP/s",
-                     "frac": round(gemm_tops / FP8_PEAK_TOPS, 4),
-                     "traffic": traffic,
-                     "ops_per_launch": gemm_ops,
-                     "note": "fp8 ops (1 MAC = 2 ops): 36 limb products x 2mnk per launch; peak is the dense fp8 rate"},
-        "roofline_deconstruct": {"bound": "hbm", "kernel": "deconstruct_kernel<0>+<1>",
-                                 "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                                 "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
-                                 "bytes_per_call": dec_bytes,
-                                 "stage_with_scan_gbs": round(stage_gbs, 1)},
-        "roofline_reconstruct": {"bound": "hbm", "achieved": round(rec_gbs, 1), "peak": HBM_PEAK_GBS,
-                                 "unit": "GB/s", "frac": round(rec_gbs / HBM_PEAK_GBS, 4)},
+                   "m": w.m, "n": w.n, "k": w.k, "moduli": cfg["moduli"], "quantiser": "RN",
+                   "route": cfg["route"]},
+        "roofline": {"bound": "mfma", "kernel": cfg["gemm_kernel"],
+                     "achieved": round(rt["gemm_tops"], 2), "peak": cfg["peak"], "unit": peak_unit,
+                     "frac": round(rt["gemm_tops"] / cfg["peak"], 4),
+                     "traffic": measured_traffic(w, args.moduli),
+                     "ops_per_launch": rt["gemm_ops"],
+                     "note": cfg["note"]},
+        "roofline_deconstruct": {"bound": "hbm", "kernel": cfg["dec_kernel"],
+                                 "achieved": round(rt["dec_gbs"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                 "frac": round(rt["dec_gbs"] / HBM_PEAK_GBS, 4),
+                                 "bytes_per_call": rt["dec_bytes"],
+                                 "stage_with_scan_gbs": round(rt["stage_gbs"], 1)},
+        "roofline_reconstruct": {"bound": "hbm", "achieved": round(rt["rec_gbs"], 1), "peak": HBM_PEAK_GBS,
+                                 "unit": "GB/s", "frac": round(rt["rec_gbs"] / HBM_PEAK_GBS, 4)},
         "stage_ms": {"scan": round(scan_ms, 4), "deconstruct": round(dec_ms, 4), "residue_gemm": round(gemm_ms, 4),
                      "reconstruct": round(rec_ms, 4)},
-        "emulation_roof_tflops": round(roof, 2),
-        "emulation_roof_frac": round(tflops / roof, 4),
+        "emulation_roof_tflops": round(rt["roof"], 2),
+        "emulation_roof_frac": round(rt["tflops"] / rt["roof"], 4),
         "native_fp64_tflops": round(native, 2) if native else None,
         "native_fp64_peak_tflops": FP64_PEAK_TFLOPS,
         "paper_context": "modelled Rubin projections (no measurement in the paper): 473 TFLOPS roof, 182-235 TFLOPS floors",
     }
-    del Ad, Bd, Cd, ws
+    if other is not None:
+        result["all_byte_set" if args.moduli == "s12" else "published_set"] = other
+    del Ad, Bd, Cd, C0d
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         rows = min(args.baseline_sample, w.m)
         cols = min(args.baseline_sample, w.n)
         log(f"[bench] cpu baseline: oracle on {rows}x{cols} outputs")
-        result["cpu_baseline"] = cpu_baseline(A, B, w, rows, cols)
+        result["cpu_baseline"] = cpu_baseline(A, B, w, rows, cols, cfg)
     else:
         result["cpu_baseline"] = None
     print(json.dumps(result), flush=True)

@@ -174,7 +174,7 @@ __device__ __forceinline__ double reconstruct_one(const RT* rowq, int64_t mn, in
 // Fifteen centred residues, |c| <= 128.  Garner sums stay below 15 * 2^14 <
 // 2^18, so the FP32 quotient of a digit errs by less than 2^-5 / m_j and
 // rint gives the centred digit for odd m_j; m_0 = 256 takes the low eight
-// bits.  With 256 first and every other modulus odd, the balanced halves
+// bits.  The sums run four terms at a time on the int8 dot product.  With 256 first and every other modulus odd, the balanced halves
 // Xl (digits 0-6, |Xl| <= P/2) and Xh (digits 7-14, |Xh| <= (Q-1)/2, Q odd)
 // give X = Xl + P Xh in exactly [-M/2, M/2): no lift is needed.  |X| < 2^117.
 constexpr int kSplitA = 7;
@@ -188,25 +188,54 @@ constexpr uint64_t kQA = prod_range_a(kSplitA, kRA);
 static_assert(kPA < (1ull << 56) && kQA < (1ull << 63), "halves fit 64 bits");
 static_assert(kModulusA[0] == 256 && kQA % 2 == 1, "the one even modulus leads the low half");
 
-template <int L, int J>
-inline constexpr int kGarnerWeightA =
-    centred_const((int64_t)radix_mod_a(L, J) * garner_w_a(J) % kModulusA[J], kModulusA[J]);
 template <int J>
 inline constexpr int kGarnerWA = centred_const(garner_w_a(J), kModulusA[J]);
 
+// Digits and Garner weights of the all-byte set are centred residues of
+// byte moduli, so they fit int8 and the sum over earlier digits runs on
+// v_dot4_i32_i8, four terms per instruction: word Q of the weights of digit
+// J holds -R_lJ for l = 4Q..4Q+3 (0 for l >= J; |R_lJ| <= 127 for the odd
+// m_J, so the negation fits).
+constexpr uint32_t garner_pack_a(int q, int j) {
+  uint32_t w = 0;
+  for (int i = 0; i < 4; ++i) {
+    const int l = 4 * q + i;
+    if (l < j) {
+      const int r = centred_const((int64_t)radix_mod_a(l, j) * garner_w_a(j) % kModulusA[j], kModulusA[j]);
+      w |= (uint32_t)(-r & 0xff) << (8 * i);
+    }
+  }
+  return w;
+}
+template <int Q, int J>
+inline constexpr int kGarnerPackA = (int)garner_pack_a(Q, J);
+constexpr bool garner_weights_fit_int8() {
+  for (int j = 1; j < kRA; ++j)
+    for (int l = 0; l < j; ++l) {
+      const int r = centred_const((int64_t)radix_mod_a(l, j) * garner_w_a(j) % kModulusA[j], kModulusA[j]);
+      if (r < -127 || r > 127) return false;
+    }
+  return true;
+}
+static_assert(garner_weights_fit_int8(), "negated weights fit int8");
+
+// digit J from the residue c_J and the packed earlier digits; appends v_J
 template <int J>
-__device__ __forceinline__ void garner_digit_a(const int (&c)[kRA], int (&v)[kRA]) {
+__device__ __forceinline__ int garner_digit_a(const int (&c)[kRA], uint32_t (&packed)[4]) {
   constexpr int M = kModulusA[J];
   int s = __mul24(c[J], kGarnerWA<J>);
-  [&]<int... L>(std::integer_sequence<int, L...>) {
-    ((s -= __mul24(v[L], kGarnerWeightA<L, J>)), ...);
-  }(std::make_integer_sequence<int, J>{});
+  [&]<int... Q>(std::integer_sequence<int, Q...>) {
+    ((s = __builtin_amdgcn_sdot4((int)packed[Q], kGarnerPackA<Q, J>, s, false)), ...);
+  }(std::make_integer_sequence<int, (J + 3) / 4>{});
+  int v;
   if constexpr (M == 256) {
-    v[J] = ((s + 128) & 255) - 128;
+    v = ((s + 128) & 255) - 128;
   } else {
     const int q = (int)__builtin_rintf((float)s * (1.0f / M));
-    v[J] = s - q * M;
+    v = s - q * M;
   }
+  packed[J / 4] |= (uint32_t)(v & 0xff) << (8 * (J % 4));
+  return v;
 }
 
 // Balanced value of digits [A, B): digit pairs v_j + m_j v_{j+1} in 24-bit
@@ -236,8 +265,9 @@ __device__ __forceinline__ double reconstruct_one_a(const RT* rowq, int64_t mn, 
   int c[kRA], v[kRA];
 #pragma unroll
   for (int q = 0; q < kRA; ++q) c[q] = load_residue(rowq + q * mn, n, col);
+  uint32_t packed[4] = {0, 0, 0, 0};
   [&]<int... J>(std::integer_sequence<int, J...>) {
-    (garner_digit_a<J>(c, v), ...);
+    ((v[J] = garner_digit_a<J>(c, packed)), ...);
   }(std::make_integer_sequence<int, kRA>{});
   const int64_t xl = half_value_a<0, kSplitA>(v);   // |xl| <= P/2
   const int64_t xh = half_value_a<kSplitA, kRA>(v);  // |xh| <= (Q - 1) / 2
