@@ -8,7 +8,9 @@ marshals numpy arrays into it and chains its steps in the paper's order
 (Eq. (scale) -> Eq. (residueprod) -> Eq. (pieces)/Lemma 1 -> Eq. (garner),
 Eq. (horner) -> single rounding).
 
-``set`` selects the modulus set: 0 is the published twelve-modulus set, 1 the
+``quant`` selects the quantiser of Eq. (scale): RN (round to nearest, ties
+to even; Ozaki-II-RN) or TZ (truncation toward zero; Ozaki-II-TZ of Table
+variants).  ``set`` selects the modulus set: 0 is the published twelve-modulus set, 1 the
 all-byte candidate set A of Sec. 5.1 on the INT8 route (its centred residues
 are the int8 planes, one per modulus).
 """
@@ -65,6 +67,9 @@ def lib():
         L.oracle_quantise.argtypes = [ctypes.c_double, i32]
         L.oracle_quantise.restype = i64
         L.oracle_quantise_vectors.argtypes = [i64, i64, P, i64, i64, P, P]
+        L.oracle_quantise_vectors_q.argtypes = [ctypes.c_int, i64, i64, P, i64, i64, P, P]
+        L.oracle_quantise_tz.argtypes = [ctypes.c_double, i32]
+        L.oracle_quantise_tz.restype = i64
         L.oracle_centred_mod.argtypes = [i64, i64]
         L.oracle_centred_mod.restype = i64
         L.oracle_residues.argtypes = [i64, i64, P, P]
@@ -171,7 +176,12 @@ def limb_product_table(i: int) -> np.ndarray:
     return out
 
 
-def quantise(x: float, sigma: int) -> int:
+RN, TZ = 0, 1   # quantisers of Eq. (scale): Ozaki-II-RN and Ozaki-II-TZ
+
+
+def quantise(x: float, sigma: int, quant: int = RN) -> int:
+    if quant == TZ:
+        return int(lib().oracle_quantise_tz(x, sigma))
     return int(lib().oracle_quantise(x, sigma))
 
 
@@ -200,12 +210,12 @@ def exponents(X: np.ndarray, side: int, t: int) -> np.ndarray:
     return out
 
 
-def quantise_vectors(X: np.ndarray, side: int, exps: np.ndarray) -> np.ndarray:
-    """Z[v][l]: the scaled, rounded integers of each row of A / column of B."""
+def quantise_vectors(X: np.ndarray, side: int, exps: np.ndarray, quant: int = RN) -> np.ndarray:
+    """Z[v][l]: the scaled, quantised integers of each row of A / column of B."""
     X, nvec, k, sv, sk = _vec_view(X, side)
     exps = np.ascontiguousarray(exps, dtype=np.int32)
     Z = np.zeros((nvec, k), np.int64)
-    lib().oracle_quantise_vectors(nvec, k, _p(X), sv, sk, _p(exps), _p(Z))
+    lib().oracle_quantise_vectors_q(quant, nvec, k, _p(X), sv, sk, _p(exps), _p(Z))
     return Z
 
 
@@ -300,7 +310,7 @@ class Result:
 
 def dgemm(A: np.ndarray, B: np.ndarray, C_in: np.ndarray | None = None,
           rows=None, cols=None, want_planes: bool = True, check_exact: bool = True,
-          set: int = 0) -> Result:
+          set: int = 0, quant: int = RN) -> Result:
     """Oracle emulated DGEMM on the full k, for all outputs or for the sampled
     rows of A and columns of B (each output depends only on its row and
     column).  Steps in the order of Alg. 1: exponent scan, quantise, residues
@@ -317,8 +327,8 @@ def dgemm(A: np.ndarray, B: np.ndarray, C_in: np.ndarray | None = None,
     Bs = np.ascontiguousarray(B[:, cols])
     sigma = exponents(As, 0, t)
     tau = exponents(Bs, 1, t)
-    ZA = quantise_vectors(As, 0, sigma)
-    ZB = quantise_vectors(Bs, 1, tau)
+    ZA = quantise_vectors(As, 0, sigma, quant)
+    ZB = quantise_vectors(Bs, 1, tau, quant)
     resA = residues(ZA, set)
     resB = residues(ZB, set)
     Cres = residue_gemm(resA, resB, set)

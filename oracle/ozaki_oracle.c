@@ -123,11 +123,26 @@ int64_t oracle_quantise(double x, int32_t sigma) {
   return (int64_t)rint(ldexp(x, sigma));
 }
 
-void oracle_quantise_vectors(int64_t nvec, int64_t k, const double* X, int64_t sv,
-                             int64_t sk, const int32_t* exps, int64_t* Z) {
+/* a2, truncation variant (Ozaki-II-TZ of Table variants, the quantiser of
+ * Eq. (scale) being truncation toward zero): z = trunc(x * 2^sigma), the
+ * scaling again exact. */
+int64_t oracle_quantise_tz(double x, int32_t sigma) {
+  if (sigma == OR_NONFINITE) return 0;
+  return (int64_t)trunc(ldexp(x, sigma));
+}
+
+/* quant 0: round to nearest (Ozaki-II-RN); 1: toward zero (Ozaki-II-TZ) */
+void oracle_quantise_vectors_q(int quant, int64_t nvec, int64_t k, const double* X, int64_t sv,
+                               int64_t sk, const int32_t* exps, int64_t* Z) {
   for (int64_t v = 0; v < nvec; ++v)
     for (int64_t l = 0; l < k; ++l)
-      Z[v * k + l] = oracle_quantise(X[v * sv + l * sk], exps[v]);
+      Z[v * k + l] = quant == 1 ? oracle_quantise_tz(X[v * sv + l * sk], exps[v])
+                                : oracle_quantise(X[v * sv + l * sk], exps[v]);
+}
+
+void oracle_quantise_vectors(int64_t nvec, int64_t k, const double* X, int64_t sv,
+                             int64_t sk, const int32_t* exps, int64_t* Z) {
+  oracle_quantise_vectors_q(0, nvec, k, X, sv, sk, exps, Z);
 }
 
 /* The centred residue convention: z mod x in [-x/2, x/2), for even x the
