@@ -32,8 +32,10 @@
  *    tau_j for the columns of B.  A row or column holding a NaN or an infinity
  *    gets OZAKI25_EXP_NONFINITE, its planes are zero and every output it
  *    touches is NaN (the non-finite contract of the validation plan, Sec. 7).
- *  - Rounding: the quantiser rounds to nearest, ties to even (the RN variant of
- *    Eq. (scale)); the final rescale rounds once to nearest even, subnormal and
+ *  - Rounding: the quantiser of Eq. (scale) rounds to nearest, ties to even
+ *    (Ozaki-II-RN), or, where an entry point takes an ozaki25_quantiser and
+ *    OZAKI25_QUANT_TZ is passed, truncates toward zero (Ozaki-II-TZ of Table
+ *    variants); the final rescale rounds once to nearest even, subnormal and
  *    overflow ranges included; an exact zero gives +0.0.
  */
 #ifndef OZAKI25_H
@@ -67,6 +69,14 @@ typedef enum {
  *    matrix work against 3r + 1 = 37).  The same scale rule gives a few more
  *    bits per operand (t(8192) = 51 against 48). */
 typedef enum { OZAKI25_MODULI_S12 = 0, OZAKI25_MODULI_A15 = 1 } ozaki25_moduli_set;
+
+/* The integer quantiser of Eq. (scale), by the variant names of Table
+ * variants: OZAKI25_QUANT_RN rounds x 2^sigma to nearest, ties to even
+ * (Ozaki-II-RN, the variant the error theorem covers); OZAKI25_QUANT_TZ
+ * truncates it toward zero (Ozaki-II-TZ, the shipping implementation's rule,
+ * whose accuracy the paper leaves as an open obligation).  Both keep the
+ * same scale bits t(k) and exponents, and |A'| never exceeds the RN bound. */
+typedef enum { OZAKI25_QUANT_RN = 0, OZAKI25_QUANT_TZ = 1 } ozaki25_quantiser;
 
 #define OZAKI25_NUM_MODULI 12          /* S12 */
 #define OZAKI25_NUM_PLANES 30          /* S12: 2 per square modulus + 3 per nonsquare */
@@ -118,11 +128,13 @@ size_t ozaki25_planes_bytes(int64_t vecs, int64_t k, ozaki25_moduli_set set);
  *          (two's complement byte, -128 included for m = 256).
  *  exps:   int32 [vecs], sigma (side 0) or tau (side 1), or
  *          OZAKI25_EXP_NONFINITE.
+ *  quant:  the quantiser (OZAKI25_QUANT_RN or OZAKI25_QUANT_TZ).
  * vecs == 0 or k == 0 is a no-op.  Errors: INVALID_VALUE (side, sizes, null
- * pointers with nonzero sizes, set), UNSUPPORTED (k > OZAKI25_MAX_K), HIP. */
+ * pointers with nonzero sizes, set, quantiser), UNSUPPORTED (k > OZAKI25_MAX_K),
+ * HIP. */
 ozaki25_status ozaki25_deconstruct(int side, int64_t vecs, int64_t k, const double* X,
-                                   int64_t ldx, ozaki25_moduli_set set, uint8_t* planes,
-                                   int32_t* exps, void* stream);
+                                   int64_t ldx, ozaki25_moduli_set set, ozaki25_quantiser quant,
+                                   uint8_t* planes, int32_t* exps, void* stream);
 
 /* Per-modulus products (Eq. (residueprod)) from stored planes.  S12: FP8
  * MFMA with FP32 accumulation, reduced mod m_i at least every 16384 k so that
@@ -171,7 +183,8 @@ ozaki25_status ozaki25_dgemm_sub(int64_t m, int64_t n, int64_t k, const double* 
                                  const double* B, int64_t ldb, double* C, int64_t ldc,
                                  ozaki25_moduli_set set, void* stream);
 
-/* Full form.  subtract: 0 for C = A B, 1 for C <- C - A B.
+/* Full form.  quant: the quantiser (ozaki25_dgemm and ozaki25_dgemm_sub use
+ * OZAKI25_QUANT_RN).  subtract: 0 for C = A B, 1 for C <- C - A B.
  * workspace: NULL to allocate stream-ordered, else a device buffer of at least
  *   ozaki25_dgemm_workspace_size() bytes (256-byte aligned), owned by the
  *   caller and not used by anything else until the stream has passed this call.
@@ -181,9 +194,32 @@ ozaki25_status ozaki25_dgemm_sub(int64_t m, int64_t n, int64_t k, const double* 
  *   reconstruction, for per-stage timing. */
 ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
                                 const double* B, int64_t ldb, double* C, int64_t ldc,
-                                ozaki25_moduli_set set, int subtract, void* workspace,
-                                size_t workspace_bytes, void* const* stage_events,
-                                void* stream);
+                                ozaki25_moduli_set set, ozaki25_quantiser quant, int subtract,
+                                void* workspace, size_t workspace_bytes,
+                                void* const* stage_events, void* stream);
+
+/* Device workspace that ozaki25_dgemm_planes needs for an m x n product (the
+ * per-modulus residue products: int16 for S12, int8 for A15). */
+size_t ozaki25_dgemm_planes_workspace_size(int64_t m, int64_t n, ozaki25_moduli_set set);
+
+/* Emulated DGEMM from stored planes -- storage mode P of Sec. 6.2, principle O1
+ * of Sec. 5 (planes converted once and kept across calls: a fixed A in
+ * block-Krylov or iterative refinement is deconstructed once, and each call
+ * pays only the residue products and the reconstruction).
+ *  planesA, expsA: ozaki25_deconstruct side 0 of an m x k A;
+ *  planesB, expsB: side 1 of a k x n B -- both with this k and set (either
+ *    quantiser; the result is that of ozaki25_dgemm_ex with the same
+ *    quantiser, bit for bit).
+ *  C, ldc, subtract: as in ozaki25_dgemm_ex.
+ *  workspace: NULL to allocate stream-ordered, else at least
+ *    ozaki25_dgemm_planes_workspace_size() bytes, 256-byte aligned.
+ * m == 0 or n == 0: no-op; k == 0: C = +0 (or unchanged with subtract).
+ * Errors: INVALID_VALUE, UNSUPPORTED, WORKSPACE, HIP. */
+ozaki25_status ozaki25_dgemm_planes(int64_t m, int64_t n, int64_t k, const uint8_t* planesA,
+                                    const int32_t* expsA, const uint8_t* planesB,
+                                    const int32_t* expsB, double* C, int64_t ldc,
+                                    ozaki25_moduli_set set, int subtract, void* workspace,
+                                    size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

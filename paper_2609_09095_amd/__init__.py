@@ -19,6 +19,7 @@ __all__ = [
     "ozaki25_scale_bits", "ozaki25_k_pad", "ozaki25_planes_bytes", "ozaki25_dgemm_workspace_size",
     "ozaki25_deconstruct", "ozaki25_residue_gemm", "ozaki25_reconstruct",
     "ozaki25_dgemm", "ozaki25_dgemm_sub", "ozaki25_dgemm_ex",
+    "ozaki25_dgemm_planes_workspace_size", "ozaki25_dgemm_planes",
 ]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -27,6 +28,8 @@ _HEADER = os.path.join(os.path.dirname(_PKG), "include", "ozaki25.h")
 
 S12 = 0           # published moduli, FP8 limb route
 A15 = 1           # all-byte moduli (Sec. 5.1 candidate A), int8 route
+RN = 0            # quantiser: round to nearest, ties to even (Ozaki-II-RN)
+TZ = 1            # quantiser: toward zero (Ozaki-II-TZ)
 NUM_MODULI = 12
 NUM_PLANES = 30
 NUM_MODULI_A15 = 15
@@ -68,13 +71,15 @@ def lib():
             "ozaki25_scale_bits": ([i64, i32], i32),
             "ozaki25_k_pad": ([i64], i64),
             "ozaki25_planes_bytes": ([i64, i64, i32], sz),
-            "ozaki25_deconstruct": ([i32, i64, i64, P, i64, i32, P, P, P], i32),
+            "ozaki25_deconstruct": ([i32, i64, i64, P, i64, i32, i32, P, P, P], i32),
             "ozaki25_residue_gemm": ([i64, i64, i64, P, P, i32, P, P], i32),
             "ozaki25_reconstruct": ([i64, i64, P, P, P, i32, P, i64, i32, P], i32),
             "ozaki25_dgemm_workspace_size": ([i64, i64, i64, i32], sz),
             "ozaki25_dgemm": ([i64, i64, i64, P, i64, P, i64, P, i64, i32, P], i32),
             "ozaki25_dgemm_sub": ([i64, i64, i64, P, i64, P, i64, P, i64, i32, P], i32),
-            "ozaki25_dgemm_ex": ([i64, i64, i64, P, i64, P, i64, P, i64, i32, i32, P, sz, P, P], i32),
+            "ozaki25_dgemm_ex": ([i64, i64, i64, P, i64, P, i64, P, i64, i32, i32, i32, P, sz, P, P], i32),
+            "ozaki25_dgemm_planes_workspace_size": ([i64, i64, i32], sz),
+            "ozaki25_dgemm_planes": ([i64, i64, i64, P, P, P, P, P, i64, i32, i32, P, sz, P], i32),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -152,7 +157,8 @@ def ozaki25_dgemm_workspace_size(m: int, n: int, k: int, set: int = S12) -> int:
 
 
 # ----------------------------------------------------------------- stages
-def ozaki25_deconstruct(side: int, X, planes=None, exps=None, set: int = S12, stream=None):
+def ozaki25_deconstruct(side: int, X, planes=None, exps=None, set: int = S12, quantiser: int = RN,
+                        stream=None):
     """side 0: X is A (rows); side 1: X is B (columns).  Returns (planes, exps):
     planes uint8 [num_planes][vecs][k_pad] (S12: limbs as OCP e4m3 bytes; A15:
     int8 residues as two's complement bytes), exps int32 [vecs]."""
@@ -169,8 +175,8 @@ def ozaki25_deconstruct(side: int, X, planes=None, exps=None, set: int = S12, st
         exps = torch.empty((vecs,), dtype=torch.int32, device=X.device)
     if planes.numel() < npl * vecs * kp or exps.numel() < vecs:
         raise ValueError("output buffers too small")
-    _check(lib().ozaki25_deconstruct(side, vecs, k, _ptr(X), ldx, set, _ptr(planes), _ptr(exps),
-                                     _stream(stream)), "ozaki25_deconstruct")
+    _check(lib().ozaki25_deconstruct(side, vecs, k, _ptr(X), ldx, set, quantiser, _ptr(planes),
+                                     _ptr(exps), _stream(stream)), "ozaki25_deconstruct")
     return planes, exps
 
 
@@ -206,7 +212,7 @@ def ozaki25_reconstruct(Cres, expsA, expsB, C=None, subtract: bool = False, set:
 
 # ----------------------------------------------------------------- GEMM
 def ozaki25_dgemm_ex(A, B, C, subtract: bool = False, workspace=None, stage_events=None,
-                     set: int = S12, stream=None):
+                     set: int = S12, quantiser: int = RN, stream=None):
     A, lda = _matrix(A, "A")
     B, ldb = _matrix(B, "B")
     C, ldc = _matrix(C, "C")
@@ -224,7 +230,7 @@ def ozaki25_dgemm_ex(A, B, C, subtract: bool = False, workspace=None, stage_even
         ev = (ctypes.c_void_p * NUM_STAGE_EVENTS)(*handles)
     ws_ptr = _ptr(workspace) if workspace is not None else ctypes.c_void_p(0)
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
-    _check(lib().ozaki25_dgemm_ex(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, set,
+    _check(lib().ozaki25_dgemm_ex(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, set, quantiser,
                                   1 if subtract else 0, ws_ptr, ws_bytes,
                                   ctypes.cast(ev, ctypes.c_void_p) if ev is not None else None,
                                   _stream(stream)), "ozaki25_dgemm_ex")
@@ -257,4 +263,34 @@ def ozaki25_dgemm_sub(A, B, C, set: int = S12, stream=None):
     _, n = B.shape
     _check(lib().ozaki25_dgemm_sub(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, set,
                                    _stream(stream)), "ozaki25_dgemm_sub")
+    return C
+
+
+def ozaki25_dgemm_planes_workspace_size(m: int, n: int, set: int = S12) -> int:
+    return lib().ozaki25_dgemm_planes_workspace_size(m, n, set)
+
+
+def ozaki25_dgemm_planes(k: int, planesA, expsA, planesB, expsB, C=None, subtract: bool = False,
+                         workspace=None, set: int = S12, stream=None):
+    """C = A B (or C -= A B) from stored planes (storage mode P): planes and
+    exponents from ozaki25_deconstruct of A (side 0) and B (side 1) with this
+    k and set.  m and n come from the exponent vectors."""
+    import torch
+    m, n = expsA.numel(), expsB.numel()
+    kp = ozaki25_k_pad(k)
+    npl = ozaki25_num_planes(set)
+    if npl < 0:
+        raise ValueError(f"unknown modulus set {set}")
+    if planesA.numel() < npl * m * kp or planesB.numel() < npl * n * kp:
+        raise ValueError("plane buffers too small for this k and set")
+    if C is None:
+        C = torch.empty((m, n), dtype=torch.float64, device=expsA.device)
+    C, ldc = _matrix(C, "C")
+    if tuple(C.shape) != (m, n):
+        raise ValueError("shape mismatch")
+    ws_ptr = _ptr(workspace) if workspace is not None else ctypes.c_void_p(0)
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().ozaki25_dgemm_planes(m, n, k, _ptr(planesA), _ptr(expsA), _ptr(planesB), _ptr(expsB),
+                                      _ptr(C), ldc, set, 1 if subtract else 0, ws_ptr, ws_bytes,
+                                      _stream(stream)), "ozaki25_dgemm_planes")
     return C

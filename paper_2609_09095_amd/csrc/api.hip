@@ -30,6 +30,8 @@ bool known_set(ozaki25_moduli_set set) {
   return set == OZAKI25_MODULI_S12 || set == OZAKI25_MODULI_A15;
 }
 bool bytes_set(ozaki25_moduli_set set) { return set == OZAKI25_MODULI_A15; }
+bool known_quantiser(ozaki25_quantiser q) { return q == OZAKI25_QUANT_RN || q == OZAKI25_QUANT_TZ; }
+static_assert(OZAKI25_QUANT_RN == oz::kQuantRN && OZAKI25_QUANT_TZ == oz::kQuantTZ, "quantiser numbering");
 int num_moduli(ozaki25_moduli_set set) { return bytes_set(set) ? oz::kRA : oz::kR; }
 // the all-byte set stores one int8 plane per modulus
 int num_planes(ozaki25_moduli_set set) { return bytes_set(set) ? oz::kRA : oz::kPlanes; }
@@ -124,9 +126,9 @@ size_t ozaki25_planes_bytes(int64_t vecs, int64_t k, ozaki25_moduli_set set) {
 }
 
 ozaki25_status ozaki25_deconstruct(int side, int64_t vecs, int64_t k, const double* X, int64_t ldx,
-                                   ozaki25_moduli_set set, uint8_t* planes, int32_t* exps,
-                                   void* stream) {
-  if (!known_set(set) || (side != 0 && side != 1) || vecs < 0 || k < 0)
+                                   ozaki25_moduli_set set, ozaki25_quantiser quant,
+                                   uint8_t* planes, int32_t* exps, void* stream) {
+  if (!known_set(set) || !known_quantiser(quant) || (side != 0 && side != 1) || vecs < 0 || k < 0)
     return OZAKI25_ERR_INVALID_VALUE;
   if (k > OZAKI25_MAX_K) return OZAKI25_ERR_UNSUPPORTED;
   if (vecs == 0 || k == 0) return OZAKI25_SUCCESS;
@@ -138,7 +140,8 @@ ozaki25_status ozaki25_deconstruct(int side, int64_t vecs, int64_t k, const doub
   const int t = scale_bits(k, set);
   hipError_t e = oz::launch_scan(side, vecs, k, X, ldx, t, exps, s);
   if (e == hipSuccess)
-    e = oz::launch_deconstruct((int)set, side, vecs, k, k_pad(k), t, X, ldx, exps, (int8_t*)planes, s);
+    e = oz::launch_deconstruct((int)set, (int)quant, side, vecs, k, k_pad(k), t, X, ldx, exps,
+                               (int8_t*)planes, s);
   return hip_status(e);
 }
 
@@ -179,9 +182,11 @@ size_t ozaki25_dgemm_workspace_size(int64_t m, int64_t n, int64_t k, ozaki25_mod
 
 ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
                                 const double* B, int64_t ldb, double* C, int64_t ldc,
-                                ozaki25_moduli_set set, int subtract, void* workspace,
-                                size_t workspace_bytes, void* const* stage_events, void* stream) {
-  if (!known_set(set) || m < 0 || n < 0 || k < 0) return OZAKI25_ERR_INVALID_VALUE;
+                                ozaki25_moduli_set set, ozaki25_quantiser quant, int subtract,
+                                void* workspace, size_t workspace_bytes,
+                                void* const* stage_events, void* stream) {
+  if (!known_set(set) || !known_quantiser(quant) || m < 0 || n < 0 || k < 0)
+    return OZAKI25_ERR_INVALID_VALUE;
   if (k > OZAKI25_MAX_K || n > OZAKI25_MAX_N) return OZAKI25_ERR_UNSUPPORTED;
   if (m == 0 || n == 0) return OZAKI25_SUCCESS;
   if (!C || ldc < n || ((uintptr_t)C & 7)) return OZAKI25_ERR_INVALID_VALUE;
@@ -225,8 +230,8 @@ ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A
   if (e == hipSuccess) e = oz::launch_scan(0, m, k, A, lda, t, ea, s);
   if (e == hipSuccess) e = oz::launch_scan(1, n, k, B, ldb, t, eb, s);
   if (ev && e == hipSuccess) e = hipEventRecord(ev[1], s);
-  if (e == hipSuccess) e = oz::launch_deconstruct((int)set, 0, m, k, kp, t, A, lda, ea, pa, s);
-  if (e == hipSuccess) e = oz::launch_deconstruct((int)set, 1, n, k, kp, t, B, ldb, eb, pb, s);
+  if (e == hipSuccess) e = oz::launch_deconstruct((int)set, (int)quant, 0, m, k, kp, t, A, lda, ea, pa, s);
+  if (e == hipSuccess) e = oz::launch_deconstruct((int)set, (int)quant, 1, n, k, kp, t, B, ldb, eb, pb, s);
   if (ev && e == hipSuccess) e = hipEventRecord(ev[2], s);
   if (e == hipSuccess)
     e = bytes ? oz::launch_residue_gemm_bytes_i8(m, n, kp, pa, pb, (int8_t*)cres, s)
@@ -244,16 +249,67 @@ ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A
   return hip_status(e);
 }
 
+size_t ozaki25_dgemm_planes_workspace_size(int64_t m, int64_t n, ozaki25_moduli_set set) {
+  if (!known_set(set) || m < 0 || n < 0) return 0;
+  return align_up((size_t)num_moduli(set) * m * n * (bytes_set(set) ? sizeof(int8_t) : sizeof(int16_t)));
+}
+
+ozaki25_status ozaki25_dgemm_planes(int64_t m, int64_t n, int64_t k, const uint8_t* planesA,
+                                    const int32_t* expsA, const uint8_t* planesB,
+                                    const int32_t* expsB, double* C, int64_t ldc,
+                                    ozaki25_moduli_set set, int subtract, void* workspace,
+                                    size_t workspace_bytes, void* stream) {
+  if (!known_set(set) || m < 0 || n < 0 || k < 0) return OZAKI25_ERR_INVALID_VALUE;
+  if (k > OZAKI25_MAX_K || n > OZAKI25_MAX_N) return OZAKI25_ERR_UNSUPPORTED;
+  if (m == 0 || n == 0) return OZAKI25_SUCCESS;
+  if (!C || ldc < n || ((uintptr_t)C & 7)) return OZAKI25_ERR_INVALID_VALUE;
+  hipStream_t s = (hipStream_t)stream;
+  if (k == 0) return hip_status(subtract ? hipSuccess : oz::launch_zero_c(m, n, C, ldc, s));
+  if (!planesA || !planesB || !expsA || !expsB) return OZAKI25_ERR_INVALID_VALUE;
+  if (((uintptr_t)planesA & 15) || ((uintptr_t)planesB & 15) || ((uintptr_t)expsA & 3) ||
+      ((uintptr_t)expsB & 3))
+    return OZAKI25_ERR_INVALID_VALUE;
+  const size_t need = ozaki25_dgemm_planes_workspace_size(m, n, set);
+  void* ws = workspace;
+  bool owned = false;
+  if (ws) {
+    if (workspace_bytes < need || ((uintptr_t)ws & (kAlign - 1))) return OZAKI25_ERR_WORKSPACE;
+  } else {
+    if (hipMallocAsync(&ws, need, s) != hipSuccess || !ws) return OZAKI25_ERR_WORKSPACE;
+    owned = true;
+  }
+  const int64_t kp = k_pad(k);
+  const int8_t *pa = (const int8_t*)planesA, *pb = (const int8_t*)planesB;
+  const int sub = subtract ? 1 : 0;
+  hipError_t e;
+  if (bytes_set(set)) {
+    int8_t* cres = (int8_t*)ws;
+    e = oz::launch_residue_gemm_bytes_i8(m, n, kp, pa, pb, cres, s);
+    if (e == hipSuccess) e = oz::launch_reconstruct_bytes_i8(m, n, cres, expsA, expsB, C, ldc, sub, s);
+  } else {
+    int16_t* cres = (int16_t*)ws;
+    e = oz::launch_residue_gemm_i16(m, n, kp, pa, pb, cres, s);
+    if (e == hipSuccess) e = oz::launch_reconstruct_i16(m, n, cres, expsA, expsB, C, ldc, sub, s);
+  }
+  if (owned) {
+    const hipError_t f = hipFreeAsync(ws, s);
+    if (e == hipSuccess) e = f;
+  }
+  return hip_status(e);
+}
+
 ozaki25_status ozaki25_dgemm(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
                              const double* B, int64_t ldb, double* C, int64_t ldc,
                              ozaki25_moduli_set set, void* stream) {
-  return ozaki25_dgemm_ex(m, n, k, A, lda, B, ldb, C, ldc, set, 0, nullptr, 0, nullptr, stream);
+  return ozaki25_dgemm_ex(m, n, k, A, lda, B, ldb, C, ldc, set, OZAKI25_QUANT_RN, 0, nullptr, 0,
+                          nullptr, stream);
 }
 
 ozaki25_status ozaki25_dgemm_sub(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
                                  const double* B, int64_t ldb, double* C, int64_t ldc,
                                  ozaki25_moduli_set set, void* stream) {
-  return ozaki25_dgemm_ex(m, n, k, A, lda, B, ldb, C, ldc, set, 1, nullptr, 0, nullptr, stream);
+  return ozaki25_dgemm_ex(m, n, k, A, lda, B, ldb, C, ldc, set, OZAKI25_QUANT_RN, 1, nullptr, 0,
+                          nullptr, stream);
 }
 
 }  // extern "C"

@@ -1,4 +1,5 @@
-// Deconstruction (Alg. 2): scale by 2^sigma, round to nearest even, twelve
+// Deconstruction (Alg. 2): scale by 2^sigma, quantise (round to nearest even,
+// or toward zero for the truncating variant), twelve
 // centred residues, limb split, packed e4m3 plane stores (every limb is an
 // e4m3-exact integer, Lemma 1, so the conversion is exact).  For the
 // all-byte set (Sec. 5.1, candidate A) fifteen centred residues stored as
@@ -210,14 +211,19 @@ __device__ __forceinline__ int load_group(int64_t vecs, int64_t k, const double*
   return sigma;
 }
 
-// |x 2^sigma| < 2^t: the scaling is exact, rint is the one rounding.
+// |x 2^sigma| < 2^t: the scaling is exact, and the quantiser of Eq. (scale)
+// is the one rounding: to nearest even (RN), or toward zero (TZ).
+template <bool TZ>
 __device__ __forceinline__ void scale_round(const double (&x)[kElems], int sigma,
                                             double (&y)[kElems]) {
 #pragma unroll
-  for (int c = 0; c < kElems; ++c) y[c] = __builtin_rint(__builtin_ldexp(x[c], sigma));
+  for (int c = 0; c < kElems; ++c) {
+    const double v = __builtin_ldexp(x[c], sigma);
+    y[c] = TZ ? __builtin_trunc(v) : __builtin_rint(v);
+  }
 }
 
-template <int SIDE, bool EXACT>
+template <int SIDE, bool EXACT, bool TZ>
 __global__ __launch_bounds__(256) void deconstruct_kernel(int64_t vecs, int64_t k, int64_t kp,
                                                           const double* __restrict__ X, int64_t ldx,
                                                           const int32_t* __restrict__ exps,
@@ -234,7 +240,7 @@ __global__ __launch_bounds__(256) void deconstruct_kernel(int64_t vecs, int64_t 
   __syncthreads();
   if (!active) return;
   double y[kElems];
-  scale_round(x, sigma, y);
+  scale_round<TZ>(x, sigma, y);
   emit_all<EXACT>(std::make_integer_sequence<int, kR>{}, y, planes, vecs * kp, v * kp + k0, lut);
 }
 
@@ -273,7 +279,7 @@ __device__ __forceinline__ void emit_all_bytes(std::integer_sequence<int, I...>,
   (emit_byte_modulus<I, EXACT>(y, planes, plane_stride, off), ...);
 }
 
-template <int SIDE, bool EXACT>
+template <int SIDE, bool EXACT, bool TZ>
 __global__ __launch_bounds__(256) void deconstruct_bytes_kernel(int64_t vecs, int64_t k, int64_t kp,
                                                                 const double* __restrict__ X,
                                                                 int64_t ldx,
@@ -286,48 +292,54 @@ __global__ __launch_bounds__(256) void deconstruct_bytes_kernel(int64_t vecs, in
   const int64_t k0 = g * kElems;
   double x[kElems], y[kElems];
   const int sigma = load_group<SIDE>(vecs, k, X, ldx, exps, v, k0, true, x);
-  scale_round(x, sigma, y);
+  scale_round<TZ>(x, sigma, y);
   emit_all_bytes<EXACT>(std::make_integer_sequence<int, kRA>{}, y, planes, vecs * kp, v * kp + k0);
 }
 
-template <int SIDE>
-void launch_side(int64_t blocks, bool bytes, bool exact, int64_t vecs, int64_t k, int64_t kp,
+template <int SIDE, bool BYTES, bool EXACT, bool TZ>
+void launch_one(int64_t blocks, int64_t vecs, int64_t k, int64_t kp, const double* X, int64_t ldx,
+                const int32_t* exps, int8_t* planes, hipStream_t stream) {
+  if constexpr (BYTES)
+    hipLaunchKernelGGL((deconstruct_bytes_kernel<SIDE, EXACT, TZ>), dim3((unsigned)blocks), dim3(256),
+                       0, stream, vecs, k, kp, X, ldx, exps, planes);
+  else
+    hipLaunchKernelGGL((deconstruct_kernel<SIDE, EXACT, TZ>), dim3((unsigned)blocks), dim3(256), 0,
+                       stream, vecs, k, kp, X, ldx, exps, planes);
+}
+
+template <int SIDE, bool BYTES>
+void launch_side(int64_t blocks, bool exact, bool tz, int64_t vecs, int64_t k, int64_t kp,
                  const double* X, int64_t ldx, const int32_t* exps, int8_t* planes,
                  hipStream_t stream) {
-  const dim3 grid((unsigned)blocks), block(256);
-  if (bytes) {
-    if (exact)
-      hipLaunchKernelGGL((deconstruct_bytes_kernel<SIDE, true>), grid, block, 0, stream, vecs, k, kp,
-                         X, ldx, exps, planes);
-    else
-      hipLaunchKernelGGL((deconstruct_bytes_kernel<SIDE, false>), grid, block, 0, stream, vecs, k,
-                         kp, X, ldx, exps, planes);
-  } else if (exact) {
-    hipLaunchKernelGGL((deconstruct_kernel<SIDE, true>), grid, block, 0, stream, vecs, k, kp, X, ldx,
-                       exps, planes);
+  if (exact) {
+    if (tz) launch_one<SIDE, BYTES, true, true>(blocks, vecs, k, kp, X, ldx, exps, planes, stream);
+    else launch_one<SIDE, BYTES, true, false>(blocks, vecs, k, kp, X, ldx, exps, planes, stream);
   } else {
-    hipLaunchKernelGGL((deconstruct_kernel<SIDE, false>), grid, block, 0, stream, vecs, k, kp, X,
-                       ldx, exps, planes);
+    if (tz) launch_one<SIDE, BYTES, false, true>(blocks, vecs, k, kp, X, ldx, exps, planes, stream);
+    else launch_one<SIDE, BYTES, false, false>(blocks, vecs, k, kp, X, ldx, exps, planes, stream);
   }
 }
 
 }  // namespace
 
-hipError_t launch_deconstruct(int set, int side, int64_t vecs, int64_t k, int64_t kp, int t,
-                              const double* X, int64_t ldx, const int32_t* exps, int8_t* planes,
-                              hipStream_t stream) {
+hipError_t launch_deconstruct(int set, int quant, int side, int64_t vecs, int64_t k, int64_t kp,
+                              int t, const double* X, int64_t ldx, const int32_t* exps,
+                              int8_t* planes, hipStream_t stream) {
   if (vecs <= 0 || kp <= 0) return hipSuccess;
   const int64_t ngroups = kp / kElems;
   const bool bytes = set == kSetBytes;
+  const bool tz = quant == kQuantTZ;
   // |y| <= 2^t: the quotient needs no correction (the two bounds of
   // centred_residue; the all-byte set takes the sharper one)
   const bool exact = t <= (bytes ? 51 : 50);
   if (side == 0) {
     const int64_t blocks = ((vecs + 3) / 4) * ((ngroups + 63) / 64);
-    launch_side<0>(blocks, bytes, exact, vecs, k, kp, X, ldx, exps, planes, stream);
+    if (bytes) launch_side<0, true>(blocks, exact, tz, vecs, k, kp, X, ldx, exps, planes, stream);
+    else launch_side<0, false>(blocks, exact, tz, vecs, k, kp, X, ldx, exps, planes, stream);
   } else {
     const int64_t blocks = ((vecs + 31) / 32) * ((ngroups + 7) / 8);
-    launch_side<1>(blocks, bytes, exact, vecs, k, kp, X, ldx, exps, planes, stream);
+    if (bytes) launch_side<1, true>(blocks, exact, tz, vecs, k, kp, X, ldx, exps, planes, stream);
+    else launch_side<1, false>(blocks, exact, tz, vecs, k, kp, X, ldx, exps, planes, stream);
   }
   return hipGetLastError();
 }

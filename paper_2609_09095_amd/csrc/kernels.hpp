@@ -11,18 +11,21 @@ namespace oz {
 // Modulus sets, as numbered by ozaki25_moduli_set.
 constexpr int kSetPublished = 0;  // Eq. (moduli), FP8 limb route
 constexpr int kSetBytes = 1;      // Sec. 5.1 candidate A, int8 route
+// Quantisers, as numbered by ozaki25_quantiser.
+constexpr int kQuantRN = 0;  // round to nearest, ties to even
+constexpr int kQuantTZ = 1;  // toward zero
 
 // Exponent scan of A's rows (side 0) or B's columns (side 1), Alg. 1 setup:
 // exps[v] = t - e_v, or INT32_MIN for a vector holding a NaN or infinity.
 hipError_t launch_scan(int side, int64_t vecs, int64_t k, const double* X, int64_t ldx, int t,
                        int32_t* exps, hipStream_t stream);
 
-// Alg. 2: scale, round, residues and the planes of one operand, given exps
+// Alg. 2: scale, quantise, residues and the planes of one operand, given exps
 // and the scale bits t: e4m3 limb planes (published set) or int8 residue
 // planes (all-byte set).
-hipError_t launch_deconstruct(int set, int side, int64_t vecs, int64_t k, int64_t kp, int t,
-                              const double* X, int64_t ldx, const int32_t* exps, int8_t* planes,
-                              hipStream_t stream);
+hipError_t launch_deconstruct(int set, int quant, int side, int64_t vecs, int64_t k, int64_t kp,
+                              int t, const double* X, int64_t ldx, const int32_t* exps,
+                              int8_t* planes, hipStream_t stream);
 
 // Eq. (residueprod): r centred per-modulus products [r][m][n], on FP8 MFMA
 // from limb planes (published set) or int8 MFMA from residue planes

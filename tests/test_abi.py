@@ -73,6 +73,9 @@ def test_size_helpers():
     ws = oz.ozaki25_dgemm_workspace_size(100, 50, 70)
     assert ws >= 30 * 100 * 128 + 30 * 50 * 128 + 4 * 150 + 12 * 100 * 50 * 2
     assert ws % 256 == 0
+    assert oz.ozaki25_dgemm_planes_workspace_size(100, 50) == 12 * 100 * 50 * 2 // 256 * 256 + 256 * (12 * 100 * 50 * 2 % 256 != 0)
+    assert oz.ozaki25_dgemm_planes_workspace_size(100, 50, oz.A15) >= 15 * 100 * 50
+    assert oz.ozaki25_dgemm_planes_workspace_size(100, 50, 3) == 0
     # all-byte set: 15 int8 planes per operand, int8 residue products
     assert oz.ozaki25_planes_bytes(10, 70, oz.A15) == 15 * 10 * 128
     wa = oz.ozaki25_dgemm_workspace_size(100, 50, 70, oz.A15)
@@ -88,17 +91,18 @@ def test_argument_errors_are_synchronous():
     fake = _v(0x100000)   # never dereferenced: every call below fails its checks first
     null = _v(0)
     # deconstruct: bad side, negative sizes, ldx too small, null pointers, bad set, k too large
-    assert L.ozaki25_deconstruct(2, 4, 4, fake, 4, 0, fake, fake, null) == oz.ERR_INVALID_VALUE
-    assert L.ozaki25_deconstruct(0, -1, 4, fake, 4, 0, fake, fake, null) == oz.ERR_INVALID_VALUE
-    assert L.ozaki25_deconstruct(0, 4, 8, fake, 4, 0, fake, fake, null) == oz.ERR_INVALID_VALUE
-    assert L.ozaki25_deconstruct(1, 8, 4, fake, 4, 0, fake, fake, null) == oz.ERR_INVALID_VALUE
-    assert L.ozaki25_deconstruct(0, 4, 4, null, 4, 0, fake, fake, null) == oz.ERR_INVALID_VALUE
-    assert L.ozaki25_deconstruct(0, 4, 4, fake, 4, 5, fake, fake, null) == oz.ERR_INVALID_VALUE
-    assert L.ozaki25_deconstruct(0, 4, oz.MAX_K + 1, fake, oz.MAX_K + 1, 0, fake, fake, null) == oz.ERR_UNSUPPORTED
-    assert L.ozaki25_deconstruct(0, 4, 4, fake, 4, 0, _v(0x100001), fake, null) == oz.ERR_INVALID_VALUE
+    assert L.ozaki25_deconstruct(2, 4, 4, fake, 4, 0, 0, fake, fake, null) == oz.ERR_INVALID_VALUE
+    assert L.ozaki25_deconstruct(0, -1, 4, fake, 4, 0, 0, fake, fake, null) == oz.ERR_INVALID_VALUE
+    assert L.ozaki25_deconstruct(0, 4, 8, fake, 4, 0, 0, fake, fake, null) == oz.ERR_INVALID_VALUE
+    assert L.ozaki25_deconstruct(1, 8, 4, fake, 4, 0, 0, fake, fake, null) == oz.ERR_INVALID_VALUE
+    assert L.ozaki25_deconstruct(0, 4, 4, null, 4, 0, 0, fake, fake, null) == oz.ERR_INVALID_VALUE
+    assert L.ozaki25_deconstruct(0, 4, 4, fake, 4, 5, 0, fake, fake, null) == oz.ERR_INVALID_VALUE
+    assert L.ozaki25_deconstruct(0, 4, 4, fake, 4, 0, 2, fake, fake, null) == oz.ERR_INVALID_VALUE
+    assert L.ozaki25_deconstruct(0, 4, oz.MAX_K + 1, fake, oz.MAX_K + 1, 0, 0, fake, fake, null) == oz.ERR_UNSUPPORTED
+    assert L.ozaki25_deconstruct(0, 4, 4, fake, 4, 0, 0, _v(0x100001), fake, null) == oz.ERR_INVALID_VALUE
     # empty work is a successful no-op
-    assert L.ozaki25_deconstruct(0, 0, 4, null, 4, 0, null, null, null) == oz.SUCCESS
-    assert L.ozaki25_deconstruct(0, 4, 0, null, 4, 0, null, null, null) == oz.SUCCESS
+    assert L.ozaki25_deconstruct(0, 0, 4, null, 4, 0, 0, null, null, null) == oz.SUCCESS
+    assert L.ozaki25_deconstruct(0, 4, 0, null, 4, 0, 0, null, null, null) == oz.SUCCESS
     # residue gemm
     assert L.ozaki25_residue_gemm(4, 4, 4, null, fake, 0, fake, null) == oz.ERR_INVALID_VALUE
     assert L.ozaki25_residue_gemm(4, 4, 4, fake, fake, 0, null, null) == oz.ERR_INVALID_VALUE
@@ -111,16 +115,28 @@ def test_argument_errors_are_synchronous():
     assert L.ozaki25_reconstruct(4, 0, null, null, null, 0, null, 0, 0, null) == oz.SUCCESS
     # dgemm: leading dimensions, aliasing, null pointers
     f = L.ozaki25_dgemm_ex
-    assert f(4, 4, 4, fake, 3, fake, 4, _v(0x200000), 4, 0, 0, null, 0, null, null) == oz.ERR_INVALID_VALUE
-    assert f(4, 4, 4, fake, 4, fake, 3, _v(0x200000), 4, 0, 0, null, 0, null, null) == oz.ERR_INVALID_VALUE
-    assert f(4, 4, 4, fake, 4, _v(0x300000), 4, _v(0x200000), 3, 0, 0, null, 0, null, null) == oz.ERR_INVALID_VALUE
-    assert f(4, 4, 4, fake, 4, _v(0x300000), 4, fake, 4, 0, 0, null, 0, null, null) == oz.ERR_INVALID_VALUE
-    assert f(4, 4, 4, null, 4, _v(0x300000), 4, _v(0x200000), 4, 0, 0, null, 0, null, null) == oz.ERR_INVALID_VALUE
-    assert f(4, 4, 4, fake, 4, _v(0x300000), 4, _v(0x200000), 4, 2, 0, null, 0, null, null) == oz.ERR_INVALID_VALUE
-    assert f(0, 4, 4, null, 4, null, 4, null, 4, 0, 0, null, 0, null, null) == oz.SUCCESS
-    assert f(4, oz.MAX_N + 1, 4, fake, 4, _v(0x300000), oz.MAX_N + 1, _v(0x200000), oz.MAX_N + 1, 0, 0, null, 0, null, null) == oz.ERR_UNSUPPORTED
+    assert f(4, 4, 4, fake, 3, fake, 4, _v(0x200000), 4, 0, 0, 0, null, 0, null, null) == oz.ERR_INVALID_VALUE
+    assert f(4, 4, 4, fake, 4, fake, 3, _v(0x200000), 4, 0, 0, 0, null, 0, null, null) == oz.ERR_INVALID_VALUE
+    assert f(4, 4, 4, fake, 4, _v(0x300000), 4, _v(0x200000), 3, 0, 0, 0, null, 0, null, null) == oz.ERR_INVALID_VALUE
+    assert f(4, 4, 4, fake, 4, _v(0x300000), 4, fake, 4, 0, 0, 0, null, 0, null, null) == oz.ERR_INVALID_VALUE
+    assert f(4, 4, 4, null, 4, _v(0x300000), 4, _v(0x200000), 4, 0, 0, 0, null, 0, null, null) == oz.ERR_INVALID_VALUE
+    assert f(4, 4, 4, fake, 4, _v(0x300000), 4, _v(0x200000), 4, 2, 0, 0, null, 0, null, null) == oz.ERR_INVALID_VALUE
+    assert f(4, 4, 4, fake, 4, _v(0x300000), 4, _v(0x200000), 4, 0, 2, 0, null, 0, null, null) == oz.ERR_INVALID_VALUE
+    assert f(0, 4, 4, null, 4, null, 4, null, 4, 0, 0, 0, null, 0, null, null) == oz.SUCCESS
+    assert f(4, oz.MAX_N + 1, 4, fake, 4, _v(0x300000), oz.MAX_N + 1, _v(0x200000), oz.MAX_N + 1, 0, 0, 0, null, 0, null, null) == oz.ERR_UNSUPPORTED
     # a caller workspace that is too small is refused before any launch
-    assert f(4, 4, 4, fake, 4, _v(0x300000), 4, _v(0x200000), 4, 0, 0, _v(0x400000), 16, null, null) == oz.ERR_WORKSPACE
+    assert f(4, 4, 4, fake, 4, _v(0x300000), 4, _v(0x200000), 4, 0, 0, 0, _v(0x400000), 16, null, null) == oz.ERR_WORKSPACE
+    # dgemm from stored planes
+    g = L.ozaki25_dgemm_planes
+    pa, ea, pb, eb, c = _v(0x100000), _v(0x200000), _v(0x300000), _v(0x400000), _v(0x500000)
+    assert g(4, 4, 4, pa, ea, pb, eb, c, 3, 0, 0, null, 0, null) == oz.ERR_INVALID_VALUE     # ldc < n
+    assert g(4, 4, 4, null, ea, pb, eb, c, 4, 0, 0, null, 0, null) == oz.ERR_INVALID_VALUE   # no planes
+    assert g(4, 4, 4, pa, null, pb, eb, c, 4, 0, 0, null, 0, null) == oz.ERR_INVALID_VALUE   # no exponents
+    assert g(4, 4, 4, pa, ea, pb, eb, c, 4, 2, 0, null, 0, null) == oz.ERR_INVALID_VALUE     # bad set
+    assert g(4, 4, 4, _v(0x100008), ea, pb, eb, c, 4, 0, 0, null, 0, null) == oz.ERR_INVALID_VALUE
+    assert g(4, 4, oz.MAX_K + 1, pa, ea, pb, eb, c, 4, 0, 0, null, 0, null) == oz.ERR_UNSUPPORTED
+    assert g(0, 4, 4, null, null, null, null, null, 4, 0, 0, null, 0, null) == oz.SUCCESS
+    assert g(4, 4, 4, pa, ea, pb, eb, c, 4, 0, 0, _v(0x600000), 8, null) == oz.ERR_WORKSPACE
 
 
 def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
