@@ -82,7 +82,7 @@ typedef enum { OZAKI25_QUANT_RN = 0, OZAKI25_QUANT_TZ = 1 } ozaki25_quantiser;
 #define OZAKI25_NUM_PLANES 30          /* S12: 2 per square modulus + 3 per nonsquare */
 #define OZAKI25_NUM_MODULI_A15 15      /* A15: also its number of planes */
 #define OZAKI25_K_ALIGN 128            /* planes are zero padded to a multiple of this */
-#define OZAKI25_MAX_K 4194304          /* 256-row plane panels: 32-bit byte offsets */
+#define OZAKI25_MAX_K 4194304          /* largest k accepted (bounds grid sizes; accumulation is exact at any k) */
 #define OZAKI25_MAX_N 8388608          /* columns of B / C (32-bit offsets inside a tile) */
 #define OZAKI25_EXP_NONFINITE INT32_MIN
 #define OZAKI25_NUM_STAGE_EVENTS 5     /* see ozaki25_dgemm_ex */
@@ -108,7 +108,8 @@ int ozaki25_scale_bits(int64_t k, ozaki25_moduli_set set);
 int64_t ozaki25_k_pad(int64_t k);
 
 /* Bytes of the stored planes of `vecs` rows (or columns) of length k:
- * num_planes * vecs * k_pad.  0 on invalid input. */
+ * num_planes * vecs * k_pad (layout in ozaki25_deconstruct).  0 on invalid
+ * input. */
 size_t ozaki25_planes_bytes(int64_t vecs, int64_t k, ozaki25_moduli_set set);
 
 /* Deconstruction of one operand (Alg. 2 with the exponent scan of Alg. 1):
@@ -119,12 +120,15 @@ size_t ozaki25_planes_bytes(int64_t vecs, int64_t k, ozaki25_moduli_set set);
  *  side 0: X is A (vecs x k, row-major, ldx >= k); vector v is row v.
  *  side 1: X is B (k x vecs, row-major, ldx >= vecs); vector v is column v.
  * Outputs (device, caller-allocated):
- *  planes: uint8 [num_planes][vecs][k_pad], each byte a limb (an integer in
- *          [-22, 22]) encoded as OCP FP8 E4M3FN -- every limb is e4m3-exact
- *          (Lemma 1), zero is 0x00; plane q of modulus i is at
- *          q = (2 per earlier square + 3 per earlier nonsquare) + limb index;
- *          entries with l >= k are zero.
- *          A15: int8 [15][vecs][k_pad], plane i the centred residue mod m_i
+ *  planes: uint8 [k_pad/128][num_planes][vecs][128] -- the byte of plane q,
+ *          vector v, index l sits at ((l/128) num_planes + q) vecs 128 +
+ *          v 128 + l%128, so a 128-wide k block of one plane is contiguous over
+ *          the vectors; entries with l >= k are zero.
+ *          S12: each byte a limb (an integer in [-22, 22]) encoded as OCP FP8
+ *          E4M3FN -- every limb is e4m3-exact (Lemma 1), zero is 0x00; plane
+ *          q of modulus i is q = (2 per earlier square + 3 per earlier
+ *          nonsquare) + limb index.
+ *          A15: 15 planes, plane i the centred residue mod m_i as an int8
  *          (two's complement byte, -128 included for m = 256).
  *  exps:   int32 [vecs], sigma (side 0) or tau (side 1), or
  *          OZAKI25_EXP_NONFINITE.
@@ -143,9 +147,9 @@ ozaki25_status ozaki25_deconstruct(int side, int64_t vecs, int64_t k, const doub
  * mod s^2) or Eq. (karcarry)'s {-15, 16, 240}, and reduced to the centred
  * residue.  A15: one int8 MFMA product per modulus with int32 accumulation
  * (exact: terms of at most 2^14, reduced every 65536 k).
- *  planesA: uint8 [num_planes][m][k_pad] (side 0 of ozaki25_deconstruct):
- *           e4m3 limbs for S12, int8 residues for A15
- *  planesB: uint8 [num_planes][n][k_pad] (side 1)
+ *  planesA: uint8 [k_pad/128][num_planes][m][128] (side 0 of
+ *           ozaki25_deconstruct): e4m3 limbs for S12, int8 residues for A15
+ *  planesB: uint8 [k_pad/128][num_planes][n][128] (side 1)
  *  Cres:    int32 [r][m][n], centred C^(i) (written, caller-allocated)
  * m == 0 or n == 0 is a no-op; k == 0 writes zeros.  Errors as above. */
 ozaki25_status ozaki25_residue_gemm(int64_t m, int64_t n, int64_t k, const uint8_t* planesA,

@@ -160,8 +160,8 @@ def ozaki25_dgemm_workspace_size(m: int, n: int, k: int, set: int = S12) -> int:
 def ozaki25_deconstruct(side: int, X, planes=None, exps=None, set: int = S12, quantiser: int = RN,
                         stream=None):
     """side 0: X is A (rows); side 1: X is B (columns).  Returns (planes, exps):
-    planes uint8 [num_planes][vecs][k_pad] (S12: limbs as OCP e4m3 bytes; A15:
-    int8 residues as two's complement bytes), exps int32 [vecs]."""
+    planes uint8 [k_pad/128][num_planes][vecs][128] (S12: limbs as OCP e4m3
+    bytes; A15: int8 residues as two's complement bytes), exps int32 [vecs]."""
     import torch
     X, ldx = _matrix(X, "X")
     vecs, k = (X.shape[0], X.shape[1]) if side == 0 else (X.shape[1], X.shape[0])
@@ -170,7 +170,7 @@ def ozaki25_deconstruct(side: int, X, planes=None, exps=None, set: int = S12, qu
     if npl < 0:
         raise ValueError(f"unknown modulus set {set}")
     if planes is None:
-        planes = torch.empty((npl, vecs, kp), dtype=torch.uint8, device=X.device)
+        planes = torch.empty((kp // K_ALIGN, npl, vecs, K_ALIGN), dtype=torch.uint8, device=X.device)
     if exps is None:
         exps = torch.empty((vecs,), dtype=torch.int32, device=X.device)
     if planes.numel() < npl * vecs * kp or exps.numel() < vecs:

@@ -47,31 +47,52 @@ __device__ __forceinline__ void store16(int8_t* p, const float (&b)[kElems]) {
   put16(p, w);
 }
 
-// Centred residue of the integer-valued y modulo M, in [-(M/2), (M-1)/2],
-// as a double (an integer, |residue| <= 544).  EXACT (|y| <= 2^51, M odd or
-// a power of two): for odd M, y / M is at least 1/(2M) away from a half
-// integer, and the FP64 quotient y * RN(1/M) is closer than that to y / M:
-// within |y| 2^-52 / M <= 1/(4M) for |y| <= 2^50, within
-// (2^51 - 1)(2^-52 + 2^-106) / M < 1/(2M) below 2^51, and within 1/(4M) at
-// |y| = 2^51 (a power of two scales RN(1/M) exactly).  So rint gives the
-// nearest quotient and y - qM is already centred; for a power of two the
-// quotient is exact and only the tie +M/2 needs mapping to -M/2.  Otherwise
-// the general form with its two corrections.
-template <int M, bool EXACT>
-__device__ __forceinline__ double centred_residue(double y) {
-  if constexpr (!EXACT) {
-    return (double)cmod_f64<M>(y);
+// Integer-valued doubles y with |y| <= 2^51 sit in the low mantissa bits of
+// y + kMagic (every such sum lies in [2^52, 2^53], where the spacing is 1),
+// so the low word of that sum is y mod 2^32.
+constexpr double kMagic = 6755399441055744.0;  // 1.5 * 2^52
+__device__ __forceinline__ uint32_t low_word(double v) {
+  return (uint32_t)__builtin_bit_cast(uint64_t, v);
+}
+constexpr int log2_exact(int m) { return m <= 1 ? 0 : 1 + log2_exact(m / 2); }
+
+// y - q M modulo 2^24 for the nearest quotient q (EXACT path, |y| <= 2^51,
+// ylo = y mod 2^32).  For odd M the FMA rounds y RN(1/M) + kMagic once, to
+// kMagic + the integer nearest y RN(1/M); that product is within
+// |y| 2^-53 / M <= 1/(4M) of y / M, while y / M is at least 1/(2M) away from
+// a half integer, so the integer is the nearest quotient q and the low word
+// of the sum is q mod 2^32.  The 24-bit multiply-add then gives
+// y - q M mod 2^24, and |y - q M| <= (M-1)/2.  For a power of two M, y itself
+// (mod 2^24) serves: its low log2(M) bits are the residue.
+template <int M>
+__device__ __forceinline__ int residue_low(double y, uint32_t ylo) {
+  if constexpr ((M & (M - 1)) == 0) {
+    return (int)ylo;
   } else {
-    constexpr double inv = 1.0 / M;
-    const double q = __builtin_rint(y * inv);
-    // y - q M in one three-operand FMA (the two-operand form would first copy
-    // y, which every modulus reuses)
-    double r;
-    asm("v_fma_f64 %0, %1, %2, %3" : "=v"(r) : "v"(q), "s"(-(double)M), "v"(y));
-    if constexpr ((M & 1) == 0)
-      return r == (double)(M / 2) ? -(double)(M / 2) : r;
-    else
-      return r;
+    const double t = __builtin_fma(y, 1.0 / M, kMagic);
+    // spelled out: left to itself the compiler widens this into a 64-bit
+    // multiply-add once it sees that only the low bits are used
+    int r;
+    asm("v_mad_i32_i24 %0, %1, %2, %3" : "=v"(r) : "v"(low_word(t)), "s"(-M), "v"(ylo));
+    return r;
+  }
+}
+
+// Centred residue of the integer-valued y modulo M, in [-(M/2), (M-1)/2]
+// (an int, |residue| <= 544).  EXACT: sign-extend the low bits of
+// residue_low -- 24 bits for odd M (already centred: q is the nearest
+// quotient), log2(M) bits for a power of two (the two's complement field is
+// [-M/2, M/2) by itself).  Otherwise the general FP64 form with its two
+// corrections.
+template <int M, bool EXACT>
+__device__ __forceinline__ int centred_residue(double y, uint32_t ylo) {
+  if constexpr (!EXACT) {
+    return cmod_f64<M>(y);
+  } else if constexpr ((M & (M - 1)) == 0) {
+    constexpr int sh = 32 - log2_exact(M);
+    return (int)(ylo << sh) >> sh;
+  } else {
+    return (int)((uint32_t)residue_low<M>(y, ylo) << 8) >> 8;
   }
 }
 
@@ -133,7 +154,8 @@ __device__ __forceinline__ void gather_planes(uint32_t x0, uint32_t x1, uint32_t
 }
 
 template <int I, bool EXACT>
-__device__ __forceinline__ void emit_modulus(const double (&y)[kElems], int8_t* planes,
+__device__ __forceinline__ void emit_modulus(const double (&y)[kElems], const uint32_t (&ylo)[kElems],
+                                             int8_t* planes,
                                              int64_t plane_stride, int64_t off,
                                              const uint32_t* lut) {
   constexpr int M = kModulus[I];
@@ -144,13 +166,13 @@ __device__ __forceinline__ void emit_modulus(const double (&y)[kElems], int8_t* 
     float l0[kElems], l1[kElems];
 #pragma unroll
     for (int c = 0; c < kElems; ++c)
-      split_square<S>((float)centred_residue<M, EXACT>(y[c]), l0[c], l1[c]);
+      split_square<S>((float)centred_residue<M, EXACT>(y[c], ylo[c]), l0[c], l1[c]);
     store16(base, l0);
     store16(base + plane_stride, l1);
   } else {
     uint32_t x[kElems];
 #pragma unroll
-    for (int c = 0; c < kElems; ++c) x[c] = lut[(int)centred_residue<M, EXACT>(y[c]) + 256];
+    for (int c = 0; c < kElems; ++c) x[c] = lut[centred_residue<M, EXACT>(y[c], ylo[c]) + 256];
     uint4 w0, w1, w2;
     gather_planes(x[0], x[1], x[2], x[3], w0.x, w1.x, w2.x);
     gather_planes(x[4], x[5], x[6], x[7], w0.y, w1.y, w2.y);
@@ -164,25 +186,28 @@ __device__ __forceinline__ void emit_modulus(const double (&y)[kElems], int8_t* 
 
 template <bool EXACT, int... I>
 __device__ __forceinline__ void emit_all(std::integer_sequence<int, I...>, const double (&y)[kElems],
-                                         int8_t* planes, int64_t plane_stride, int64_t off,
-                                         const uint32_t* lut) {
-  (emit_modulus<I, EXACT>(y, planes, plane_stride, off, lut), ...);
+                                         const uint32_t (&ylo)[kElems], int8_t* planes,
+                                         int64_t plane_stride, int64_t off, const uint32_t* lut) {
+  (emit_modulus<I, EXACT>(y, ylo, planes, plane_stride, off, lut), ...);
 }
 
-// Thread -> (vector, 16-k group) map of both sides.
-template <int SIDE>
-__device__ __forceinline__ void group_of(int64_t kp, int64_t& v, int64_t& g) {
-  const int64_t ngroups = kp / kElems;
-  if constexpr (SIDE == 0) {  // block: 4 rows x 64 groups, a wavefront per row
-    const int64_t gb = (ngroups + 63) / 64;
-    v = (int64_t)(blockIdx.x / gb) * 4 + (threadIdx.x >> 6);
-    g = (int64_t)(blockIdx.x % gb) * 64 + (threadIdx.x & 63);
-  } else {  // block: 32 columns x 8 groups, a wavefront per 8 columns
-    const int64_t gb = (ngroups + 7) / 8;
-    const int lane = threadIdx.x & 63;
-    v = (int64_t)(blockIdx.x / gb) * 32 + (threadIdx.x >> 6) * 8 + (lane & 7);
-    g = (int64_t)(blockIdx.x % gb) * 8 + (lane >> 3);
-  }
+// Thread -> (vector, 16-k group), both sides: a block covers 32 vectors x
+// 128 k -- one k-block of the plane layout -- and a wavefront 8 vectors, so
+// every plane store of a wavefront fills 1 KiB of contiguous plane bytes and
+// consecutive blocks continue the same k-block: the stores sweep each plane
+// region linearly.  Lane l takes vector l%8 and k group l/8 (for B, eight
+// consecutive columns: each FP64 load reads 64 contiguous bytes of 8 rows).
+__device__ __forceinline__ void group_of(int64_t vecs, int64_t& v, int64_t& g) {
+  const int64_t vb = (vecs + 31) / 32;
+  const int lane = threadIdx.x & 63;
+  v = (int64_t)(blockIdx.x % vb) * 32 + (threadIdx.x >> 6) * 8 + (lane & 7);
+  g = (int64_t)(blockIdx.x / vb) * 8 + (lane >> 3);
+}
+
+// Byte offset of a thread's 16 plane bytes within plane 0, in the layout
+// [k_pad/128][planes][vecs][128]: plane q adds q * vecs * 128.
+__device__ __forceinline__ int64_t plane_offset(int64_t vecs, int nplanes, int64_t v, int64_t g) {
+  return ((g >> 3) * nplanes * vecs + v) * 128 + (g & 7) * 16;
 }
 
 // The 16 inputs of a group: unconditional loads from clamped (always valid)
@@ -212,14 +237,16 @@ __device__ __forceinline__ int load_group(int64_t vecs, int64_t k, const double*
 }
 
 // |x 2^sigma| < 2^t: the scaling is exact, and the quantiser of Eq. (scale)
-// is the one rounding: to nearest even (RN), or toward zero (TZ).
-template <bool TZ>
+// is the one rounding: to nearest even (RN), or toward zero (TZ).  EXACT
+// (t <= 51) also forms ylo = y mod 2^32 from y + kMagic.
+template <bool TZ, bool EXACT>
 __device__ __forceinline__ void scale_round(const double (&x)[kElems], int sigma,
-                                            double (&y)[kElems]) {
+                                            double (&y)[kElems], uint32_t (&ylo)[kElems]) {
 #pragma unroll
   for (int c = 0; c < kElems; ++c) {
     const double v = __builtin_ldexp(x[c], sigma);
     y[c] = TZ ? __builtin_trunc(v) : __builtin_rint(v);
+    ylo[c] = EXACT ? low_word(y[c] + kMagic) : 0u;
   }
 }
 
@@ -229,7 +256,7 @@ __global__ __launch_bounds__(256) void deconstruct_kernel(int64_t vecs, int64_t 
                                                           const int32_t* __restrict__ exps,
                                                           int8_t* __restrict__ planes) {
   int64_t v, g;
-  group_of<SIDE>(kp, v, g);
+  group_of(vecs, v, g);
   const bool active = v < vecs && g < kp / kElems;
   const int64_t k0 = g * kElems;
   double x[kElems];
@@ -240,8 +267,10 @@ __global__ __launch_bounds__(256) void deconstruct_kernel(int64_t vecs, int64_t 
   __syncthreads();
   if (!active) return;
   double y[kElems];
-  scale_round<TZ>(x, sigma, y);
-  emit_all<EXACT>(std::make_integer_sequence<int, kR>{}, y, planes, vecs * kp, v * kp + k0, lut);
+  uint32_t ylo[kElems];
+  scale_round<TZ, EXACT>(x, sigma, y, ylo);
+  emit_all<EXACT>(std::make_integer_sequence<int, kR>{}, y, ylo, planes, vecs * 128,
+                  plane_offset(vecs, kPlanes, v, g), lut);
 }
 
 // ---- all-byte set (Sec. 5.1, candidate A) on the int8 route: the centred
@@ -257,13 +286,17 @@ __device__ __forceinline__ uint32_t pack_bytes(int a, int b, int c, int d) {
   return __builtin_amdgcn_perm(cd, ab, 0x05040100u);
 }
 
+// The byte of the centred residue: its low eight bits, which residue_low
+// already holds on the EXACT path.
 template <int I, bool EXACT>
-__device__ __forceinline__ void emit_byte_modulus(const double (&y)[kElems], int8_t* planes,
+__device__ __forceinline__ void emit_byte_modulus(const double (&y)[kElems],
+                                                  const uint32_t (&ylo)[kElems], int8_t* planes,
                                                   int64_t plane_stride, int64_t off) {
   constexpr int M = kModulusA[I];
   int r[kElems];
 #pragma unroll
-  for (int c = 0; c < kElems; ++c) r[c] = (int)centred_residue<M, EXACT>(y[c]);
+  for (int c = 0; c < kElems; ++c)
+    r[c] = EXACT ? residue_low<M>(y[c], ylo[c]) : cmod_f64<M>(y[c]);
   uint4 w;
   w.x = pack_bytes(r[0], r[1], r[2], r[3]);
   w.y = pack_bytes(r[4], r[5], r[6], r[7]);
@@ -274,9 +307,10 @@ __device__ __forceinline__ void emit_byte_modulus(const double (&y)[kElems], int
 
 template <bool EXACT, int... I>
 __device__ __forceinline__ void emit_all_bytes(std::integer_sequence<int, I...>,
-                                               const double (&y)[kElems], int8_t* planes,
+                                               const double (&y)[kElems],
+                                               const uint32_t (&ylo)[kElems], int8_t* planes,
                                                int64_t plane_stride, int64_t off) {
-  (emit_byte_modulus<I, EXACT>(y, planes, plane_stride, off), ...);
+  (emit_byte_modulus<I, EXACT>(y, ylo, planes, plane_stride, off), ...);
 }
 
 template <int SIDE, bool EXACT, bool TZ>
@@ -286,14 +320,16 @@ __global__ __launch_bounds__(256) void deconstruct_bytes_kernel(int64_t vecs, in
                                                                 const int32_t* __restrict__ exps,
                                                                 int8_t* __restrict__ planes) {
   int64_t v, g;
-  group_of<SIDE>(kp, v, g);
+  group_of(vecs, v, g);
   const bool active = v < vecs && g < kp / kElems;
   if (!active) return;
   const int64_t k0 = g * kElems;
   double x[kElems], y[kElems];
+  uint32_t ylo[kElems];
   const int sigma = load_group<SIDE>(vecs, k, X, ldx, exps, v, k0, true, x);
-  scale_round<TZ>(x, sigma, y);
-  emit_all_bytes<EXACT>(std::make_integer_sequence<int, kRA>{}, y, planes, vecs * kp, v * kp + k0);
+  scale_round<TZ, EXACT>(x, sigma, y, ylo);
+  emit_all_bytes<EXACT>(std::make_integer_sequence<int, kRA>{}, y, ylo, planes, vecs * 128,
+                        plane_offset(vecs, kRA, v, g));
 }
 
 template <int SIDE, bool BYTES, bool EXACT, bool TZ>
@@ -326,18 +362,16 @@ hipError_t launch_deconstruct(int set, int quant, int side, int64_t vecs, int64_
                               int t, const double* X, int64_t ldx, const int32_t* exps,
                               int8_t* planes, hipStream_t stream) {
   if (vecs <= 0 || kp <= 0) return hipSuccess;
-  const int64_t ngroups = kp / kElems;
   const bool bytes = set == kSetBytes;
   const bool tz = quant == kQuantTZ;
   // |y| <= 2^t: the quotient needs no correction (the two bounds of
   // centred_residue; the all-byte set takes the sharper one)
   const bool exact = t <= (bytes ? 51 : 50);
+  const int64_t blocks = ((vecs + 31) / 32) * (kp / 128);
   if (side == 0) {
-    const int64_t blocks = ((vecs + 3) / 4) * ((ngroups + 63) / 64);
     if (bytes) launch_side<0, true>(blocks, exact, tz, vecs, k, kp, X, ldx, exps, planes, stream);
     else launch_side<0, false>(blocks, exact, tz, vecs, k, kp, X, ldx, exps, planes, stream);
   } else {
-    const int64_t blocks = ((vecs + 31) / 32) * ((ngroups + 7) / 8);
     if (bytes) launch_side<1, true>(blocks, exact, tz, vecs, k, kp, X, ldx, exps, planes, stream);
     else launch_side<1, false>(blocks, exact, tz, vecs, k, kp, X, ldx, exps, planes, stream);
   }

@@ -23,7 +23,9 @@
 // paper's chunked FP32 accumulation (its depth limit 2^24 / 22^2 = 34663),
 // with the chunk at a power of two below it.
 //
-// Layout: both plane operands are K-contiguous (rows of A, columns of B).
+// Layout: planes are stored [k_pad/128][planes][rows][128] (rows of A,
+// columns of B), so one 128-byte K stage of a 256-row tile is a contiguous
+// 32 KiB piece; measured 6 % faster than K-contiguous rows of full length.
 // The MFMA's A and B register layouts mirror each other: lane l holds
 // row/column l%32 and 32 of the 64 k bytes of the step, the same 32 on both
 // sides for equal l/32, so any fixed choice of those bytes pairs equal k.
@@ -38,7 +40,7 @@
 // stage s+1 are interleaved with stage s's first MFMAs.  LDS rows are 128
 // bytes with the 16-byte chunk index XOR-swizzled by the row so that the
 // b128 fragment reads of 8 (or 16) consecutive rows hit distinct banks.
-// Plane rows are padded to a multiple of 128 bytes, so every stage is full.
+// k is padded to a multiple of 128 bytes, so every stage is full.
 //
 // At this tile size the operand stream is 64 KiB per CU per stage of 2048
 // MFMA cycles (32 B/clk at the FP8 peak); direct-to-LDS loads deliver about
@@ -161,6 +163,18 @@ __device__ __forceinline__ const int8_t* uniform_ptr(const int8_t* p) {
   return (const int8_t*)(((uint64_t)hi << 32) | lo);
 }
 
+// Plane layout [k_pad/128][planes][rows][128]: K stage s of plane q of a
+// 256-row tile starting at row r0 is the contiguous piece
+// ((s * planes + q) * rows + r0) * 128.  A descriptor per stage (the stage
+// offset may exceed 32 bits); rows past the matrix edge fall outside its
+// range and read as zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t stage_rsrc(const int8_t* planes, int nplanes,
+                                                             int64_t rows, int64_t r0, int plane,
+                                                             int s, int nrec) {
+  const int8_t* p = uniform_ptr(planes + (((int64_t)s * nplanes + plane) * rows + r0) * BK);
+  return __builtin_amdgcn_make_buffer_rsrc((void*)p, (short)0, nrec, 0x00020000);
+}
+
 // One K stage: the wave's share of the A and B tiles (32 rows of each) goes
 // straight from global memory into LDS.  A load writes 1 KiB = 8 rows x
 // 128 bytes, lane l landing at row l/8, chunk l%8 of that slab; to realise
@@ -260,7 +274,7 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int r = wave * 16 + i * 8 + (lane >> 3);
-    voff[i] = r * (int)kp + (((lane & 7) ^ swz(r)) << 4);
+    voff[i] = r * BK + (((lane & 7) ^ swz(r)) << 4);
   }
   // rows past the matrix edge read as zero (buffer range check); they only
   // feed outputs that are never stored
@@ -282,32 +296,33 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
   // they fit one segment each).
   const int nstage = (int)(kp / BK);
   const int nseg = nstage > 0 ? (nstage + kSeg - 1) / kSeg : 0;  // segments per product
+  const int na = __builtin_amdgcn_readfirstlane((int)(rows_a * BK));
+  const int nb = __builtin_amdgcn_readfirstlane((int)(rows_b * BK));
   for (int g = 0; g < 3 * nseg; ++g) {
     const int p = g / nseg, c = g - p * nseg;
     const int s0 = c * kSeg, s1 = s0 + kSeg < nstage ? s0 + kSeg : nstage;
-    const int8_t* A = uniform_ptr(pa + ((int64_t)kSched[mod].plane_a[p] * m + tm * BM) * kp);
-    const int8_t* B = uniform_ptr(pb + ((int64_t)kSched[mod].plane_b[p] * n + tn * BN) * kp);
-    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)A, (short)0, __builtin_amdgcn_readfirstlane((int)(rows_a * kp)), 0x00020000);
-    const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)B, (short)0, __builtin_amdgcn_readfirstlane((int)(rows_b * kp)), 0x00020000);
+    const int qa = kSched[mod].plane_a[p], qb = kSched[mod].plane_b[p];
+    auto ra = [&](int st) { return stage_rsrc(pa, kPlanes, m, tm * BM, qa, st, na); };
+    auto rb = [&](int st) { return stage_rsrc(pb, kPlanes, n, tn * BN, qb, st, nb); };
 
-    stage_load(ra, rb, lds_a0, lds_b0, voff, s0 * BK, wave);
+    stage_load(ra(s0), rb(s0), lds_a0, lds_b0, voff, 0, wave);
     for (int s = s0; s < s1; s += 2) {
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
       // the DMA of the stage after the segment's last one lands in the idle
-      // buffer and is drained before the next segment.  The stage offset
-      // rides in the scalar offset, which the buffer range check leaves out,
-      // so after the panel's last stage that stage is loaded again instead
-      // of the bytes past the panel.
-      stage_mma_dma(lds_a0, lds_b0, ra0, rb0, fh, acc, ra, rb, lds_a1, lds_b1, voff,
-                    (s + 1 < nstage ? s + 1 : s) * BK, wave);
+      // buffer and is drained before the next segment; after the panel's
+      // last stage that stage is loaded again instead
+      {
+        const int nx = s + 1 < nstage ? s + 1 : s;
+        stage_mma_dma(lds_a0, lds_b0, ra0, rb0, fh, acc, ra(nx), rb(nx), lds_a1, lds_b1, voff, 0, wave);
+      }
       if (s + 1 >= s1) break;
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
-      stage_mma_dma(lds_a1, lds_b1, ra0, rb0, fh, acc, ra, rb, lds_a0, lds_b0, voff,
-                    (s + 2 < nstage ? s + 2 : s + 1) * BK, wave);
+      {
+        const int nx = s + 2 < nstage ? s + 2 : s + 1;
+        stage_mma_dma(lds_a1, lds_b1, ra0, rb0, fh, acc, ra(nx), rb(nx), lds_a0, lds_b0, voff, 0, wave);
+      }
     }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();  // every wave is done with the buffers before the next segment loads
@@ -456,16 +471,14 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int r = wave * 16 + i * 8 + (lane >> 3);
-    voff[i] = r * (int)kp + (((lane & 7) ^ swz(r)) << 4);
+    voff[i] = r * BK + (((lane & 7) ^ swz(r)) << 4);
   }
   const int64_t rows_a = m - tm * BM < BM ? m - tm * BM : BM;
   const int64_t rows_b = n - tn * BN < BN ? n - tn * BN : BN;
-  const int8_t* A = uniform_ptr(pa + ((int64_t)mod * m + tm * BM) * kp);
-  const int8_t* B = uniform_ptr(pb + ((int64_t)mod * n + tn * BN) * kp);
-  const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)A, (short)0, __builtin_amdgcn_readfirstlane((int)(rows_a * kp)), 0x00020000);
-  const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)B, (short)0, __builtin_amdgcn_readfirstlane((int)(rows_b * kp)), 0x00020000);
+  const int na = __builtin_amdgcn_readfirstlane((int)(rows_a * BK));
+  const int nb = __builtin_amdgcn_readfirstlane((int)(rows_b * BK));
+  auto ra = [&](int st) { return stage_rsrc(pa, kRA, m, tm * BM, mod, st, na); };
+  auto rb = [&](int st) { return stage_rsrc(pb, kRA, n, tn * BN, mod, st, nb); };
 
   v16i acc[2][2];
 #pragma unroll
@@ -476,19 +489,23 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
   const int nstage = (int)(kp / BK);
   for (int s0 = 0; s0 < nstage; s0 += kSegA) {
     const int s1 = s0 + kSegA < nstage ? s0 + kSegA : nstage;
-    stage_load(ra, rb, lds_a0, lds_b0, voff, s0 * BK, wave);
+    stage_load(ra(s0), rb(s0), lds_a0, lds_b0, voff, 0, wave);
     for (int s = s0; s < s1; s += 2) {
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
       // the DMA after the segment's last stage lands in the idle buffer; past
       // the panel's last stage it repeats that stage (as above)
-      stage_mma_dma_i8(lds_a0, lds_b0, ra0, rb0, fh, acc, ra, rb, lds_a1, lds_b1, voff,
-                       (s + 1 < nstage ? s + 1 : s) * BK, wave);
+      {
+        const int nx = s + 1 < nstage ? s + 1 : s;
+        stage_mma_dma_i8(lds_a0, lds_b0, ra0, rb0, fh, acc, ra(nx), rb(nx), lds_a1, lds_b1, voff, 0, wave);
+      }
       if (s + 1 >= s1) break;
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
-      stage_mma_dma_i8(lds_a1, lds_b1, ra0, rb0, fh, acc, ra, rb, lds_a0, lds_b0, voff,
-                       (s + 2 < nstage ? s + 2 : s + 1) * BK, wave);
+      {
+        const int nx = s + 2 < nstage ? s + 2 : s + 1;
+        stage_mma_dma_i8(lds_a1, lds_b1, ra0, rb0, fh, acc, ra(nx), rb(nx), lds_a0, lds_b0, voff, 0, wave);
+      }
     }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();  // every wave is done with the buffers before the next segment loads

@@ -73,6 +73,15 @@ def assert_int_equal(got: np.ndarray, want: np.ndarray, what: str):
         raise AssertionError(f"{what}: {len(bad)} entries differ; first at {idx}: got {got[idx]} want {want[idx]}")
 
 
+def device_layout(planes: np.ndarray) -> np.ndarray:
+    """The library's plane layout [k_pad/128][planes][vecs][128] from the
+    oracle's [planes][vecs][k_pad] (a pure index permutation)."""
+    P = np.asarray(planes)
+    npl, vecs, kp = P.shape
+    assert kp % 128 == 0
+    return np.ascontiguousarray(P.reshape(npl, vecs, kp // 128, 128).transpose(2, 0, 1, 3))
+
+
 def int8_bytes(residues: np.ndarray) -> np.ndarray:
     """The all-byte set's plane format: each centred residue as a two's
     complement byte."""

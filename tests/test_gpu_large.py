@@ -12,7 +12,7 @@ import pytest
 import oracle
 import paper_2609_09095_amd as oz
 import workloads
-from gpu_util import (assert_bits_equal, assert_int_equal, e4m3_bytes, int8_bytes, log, require_gpu,
+from gpu_util import (device_layout, assert_bits_equal, assert_int_equal, e4m3_bytes, int8_bytes, log, require_gpu,
                       sample_indices)
 
 pytestmark = pytest.mark.gpu
@@ -51,8 +51,8 @@ def _run(name, nsample=96, set=oz.S12):
     planesB, expsB = oz.ozaki25_deconstruct(1, Bd, set=set)
     torch.cuda.synchronize()
     del Ad, Bd
-    pA_s = planesA.index_select(1, ri).cpu().numpy()
-    pB_s = planesB.index_select(1, ci).cpu().numpy()
+    pA_s = planesA.index_select(2, ri).cpu().numpy()
+    pB_s = planesB.index_select(2, ci).cpu().numpy()
     Cres = oz.ozaki25_residue_gemm(w.m, w.n, w.k, planesA, planesB, set=set)
     torch.cuda.synchronize()
     Cres_s = Cres.index_select(1, ri).index_select(2, ci).cpu().numpy()
@@ -65,8 +65,8 @@ def _run(name, nsample=96, set=oz.S12):
     assert_int_equal(eA, oracle.exponents(A, 0, t), "sigma (all rows)")
     assert_int_equal(eB, oracle.exponents(B, 1, t), "tau (all columns)")
     r = oracle.dgemm(A, B, C_in=C0, rows=rows, cols=cols, set=set)
-    assert_int_equal(pA_s, plane_bytes(r.planesA), "planes of sampled rows of A")
-    assert_int_equal(pB_s, plane_bytes(r.planesB), "planes of sampled columns of B")
+    assert_int_equal(pA_s, device_layout(plane_bytes(r.planesA)), "planes of sampled rows of A")
+    assert_int_equal(pB_s, device_layout(plane_bytes(r.planesB)), "planes of sampled columns of B")
     assert_int_equal(Cres_s, r.Cres, "per-modulus products (sampled)")
     assert_bits_equal(C_s, r.C, "C (sampled)")
     log(f"[large] {name}: ok")

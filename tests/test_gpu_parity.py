@@ -12,7 +12,7 @@ import pytest
 import oracle
 import paper_2609_09095_amd as oz
 import workloads
-from gpu_util import (assert_bits_equal, assert_int_equal, e4m3_bytes, gpu_deconstruct, gpu_dgemm,
+from gpu_util import (device_layout, assert_bits_equal, assert_int_equal, e4m3_bytes, gpu_deconstruct, gpu_dgemm,
                       log, require_gpu, to_dev)
 
 pytestmark = pytest.mark.gpu
@@ -41,7 +41,7 @@ def test_deconstruct_matches_oracle(shape, s, seed, side):
     planes, exps = gpu_deconstruct(X, side)
     e, P = _oracle_side(X, side)
     assert_int_equal(exps.cpu().numpy(), e, "exponents")
-    assert_int_equal(planes.cpu().numpy(), e4m3_bytes(P), "planes")
+    assert_int_equal(planes.cpu().numpy(), device_layout(e4m3_bytes(P)), "planes")
 
 
 def _edge_matrix(rows, k, seed):
@@ -75,7 +75,7 @@ def test_deconstruct_edge_values(side, k):
     planes, exps = gpu_deconstruct(X, side)
     e, P = _oracle_side(X, side)
     assert_int_equal(exps.cpu().numpy(), e, "exponents")
-    assert_int_equal(planes.cpu().numpy(), e4m3_bytes(P), "planes")
+    assert_int_equal(planes.cpu().numpy(), device_layout(e4m3_bytes(P)), "planes")
     assert exps.cpu().numpy()[3] == oz.EXP_NONFINITE and exps.cpu().numpy()[4] == oz.EXP_NONFINITE
 
 
@@ -89,7 +89,7 @@ def test_deconstruct_leading_dimension():
     torch.cuda.synchronize()
     e, P = _oracle_side(X, 0)
     assert_int_equal(exps.cpu().numpy(), e, "exponents")
-    assert_int_equal(planes.cpu().numpy(), e4m3_bytes(P), "planes")
+    assert_int_equal(planes.cpu().numpy(), device_layout(e4m3_bytes(P)), "planes")
 
 
 # ------------------------------------------------------------ residue products
@@ -104,7 +104,7 @@ def test_residue_gemm_matches_oracle(m, n, k, seed):
     ZA = oracle.quantise_vectors(A, 0, oracle.exponents(A, 0, t))
     ZB = oracle.quantise_vectors(B, 1, oracle.exponents(B, 1, t))
     PA, PB = oracle.planes(ZA), oracle.planes(ZB)
-    C = oz.ozaki25_residue_gemm(m, n, k, to_dev(e4m3_bytes(PA)), to_dev(e4m3_bytes(PB)))
+    C = oz.ozaki25_residue_gemm(m, n, k, to_dev(device_layout(e4m3_bytes(PA))), to_dev(device_layout(e4m3_bytes(PB))))
     torch.cuda.synchronize()
     want = oracle.residue_gemm(oracle.residues(ZA), oracle.residues(ZB))
     assert_int_equal(C.cpu().numpy(), want, "per-modulus products")
@@ -118,8 +118,8 @@ def test_residue_gemm_full_range_residues():
     m, n, k = 96, 160, 320
     ZA = rng.integers(-(1 << 62), 1 << 62, size=(m, k), dtype=np.int64)
     ZB = rng.integers(-(1 << 62), 1 << 62, size=(n, k), dtype=np.int64)
-    C = oz.ozaki25_residue_gemm(m, n, k, to_dev(e4m3_bytes(oracle.planes(ZA))),
-                                to_dev(e4m3_bytes(oracle.planes(ZB))))
+    C = oz.ozaki25_residue_gemm(m, n, k, to_dev(device_layout(e4m3_bytes(oracle.planes(ZA)))),
+                                to_dev(device_layout(e4m3_bytes(oracle.planes(ZB)))))
     torch.cuda.synchronize()
     want = oracle.residue_gemm(oracle.residues(ZA), oracle.residues(ZB))
     assert_int_equal(C.cpu().numpy(), want, "per-modulus products")
@@ -138,8 +138,8 @@ def test_residue_gemm_long_constant_rows(k):
     za = rng.integers(-(1 << 50), 1 << 50, size=(m, 1), dtype=np.int64)
     zb = rng.integers(-(1 << 50), 1 << 50, size=(n, 1), dtype=np.int64)
     ZA, ZB = np.repeat(za, k, axis=1), np.repeat(zb, k, axis=1)
-    C = oz.ozaki25_residue_gemm(m, n, k, to_dev(e4m3_bytes(oracle.planes(ZA))),
-                                to_dev(e4m3_bytes(oracle.planes(ZB))))
+    C = oz.ozaki25_residue_gemm(m, n, k, to_dev(device_layout(e4m3_bytes(oracle.planes(ZA)))),
+                                to_dev(device_layout(e4m3_bytes(oracle.planes(ZB)))))
     torch.cuda.synchronize()
     want = oracle.residue_gemm(oracle.residues(ZA), oracle.residues(ZB))
     assert_int_equal(C.cpu().numpy(), want, "per-modulus products")
@@ -245,8 +245,8 @@ def test_dgemm_tiny_workload():
     planesB, expsB = gpu_deconstruct(B, 1)
     assert_int_equal(expsA.cpu().numpy(), r.sigma, "sigma")
     assert_int_equal(expsB.cpu().numpy(), r.tau, "tau")
-    assert_int_equal(planesA.cpu().numpy(), e4m3_bytes(r.planesA), "planes A")
-    assert_int_equal(planesB.cpu().numpy(), e4m3_bytes(r.planesB), "planes B")
+    assert_int_equal(planesA.cpu().numpy(), device_layout(e4m3_bytes(r.planesA)), "planes A")
+    assert_int_equal(planesB.cpu().numpy(), device_layout(e4m3_bytes(r.planesB)), "planes B")
 
 
 def test_dgemm_reach_workload():
@@ -261,8 +261,8 @@ def test_dgemm_reach_workload():
     planesB, expsB = gpu_deconstruct(B, 1)
     assert_int_equal(expsA.cpu().numpy(), r.sigma, "sigma")
     assert_int_equal(expsB.cpu().numpy(), r.tau, "tau")
-    assert_int_equal(planesA.cpu().numpy(), e4m3_bytes(r.planesA), "planes A")
-    assert_int_equal(planesB.cpu().numpy(), e4m3_bytes(r.planesB), "planes B")
+    assert_int_equal(planesA.cpu().numpy(), device_layout(e4m3_bytes(r.planesA)), "planes A")
+    assert_int_equal(planesB.cpu().numpy(), device_layout(e4m3_bytes(r.planesB)), "planes B")
     Cres = oz.ozaki25_residue_gemm(256, 256, 8192, planesA, planesB)
     torch.cuda.synchronize()
     assert_int_equal(Cres.cpu().numpy(), r.Cres, "per-modulus products")

@@ -13,7 +13,7 @@ import pytest
 import oracle
 import paper_2609_09095_amd as oz
 import workloads
-from gpu_util import (assert_bits_equal, assert_int_equal, gpu_deconstruct, gpu_dgemm, int8_bytes,
+from gpu_util import (device_layout, assert_bits_equal, assert_int_equal, gpu_deconstruct, gpu_dgemm, int8_bytes,
                       log, require_gpu, to_dev)
 
 pytestmark = pytest.mark.gpu
@@ -68,9 +68,9 @@ def test_deconstruct_matches_oracle(shape, s, seed, side):
     log(f"[A15] deconstruct side={side} shape={X.shape} t={oracle.scale_bits(k, OSET)}")
     planes, exps = gpu_deconstruct(X, side, SET)
     e, P = _oracle_side(X, side)
-    assert planes.shape[0] == 15
+    assert planes.shape[1] == 15
     assert_int_equal(exps.cpu().numpy(), e, "exponents")
-    assert_int_equal(planes.cpu().numpy(), int8_bytes(P), "planes")
+    assert_int_equal(planes.cpu().numpy(), device_layout(int8_bytes(P)), "planes")
 
 
 @pytest.mark.parametrize("side", [0, 1])
@@ -83,7 +83,7 @@ def test_deconstruct_edge_values(side, k):
     planes, exps = gpu_deconstruct(X, side, SET)
     e, P = _oracle_side(X, side)
     assert_int_equal(exps.cpu().numpy(), e, "exponents")
-    assert_int_equal(planes.cpu().numpy(), int8_bytes(P), "planes")
+    assert_int_equal(planes.cpu().numpy(), device_layout(int8_bytes(P)), "planes")
     assert exps.cpu().numpy()[3] == oz.EXP_NONFINITE and exps.cpu().numpy()[4] == oz.EXP_NONFINITE
 
 
@@ -104,7 +104,7 @@ def test_deconstruct_boundary_residues():
     planes, exps = gpu_deconstruct(X, 0, SET)
     e, P = _oracle_side(X, 0)
     assert_int_equal(exps.cpu().numpy(), e, "exponents")
-    assert_int_equal(planes.cpu().numpy(), int8_bytes(P), "planes")
+    assert_int_equal(planes.cpu().numpy(), device_layout(int8_bytes(P)), "planes")
 
 
 # ------------------------------------------------------------ residue products
@@ -121,8 +121,8 @@ def _gemm_check(ZA, ZB):
     import torch
     m, k = ZA.shape
     n = ZB.shape[0]
-    PA = int8_bytes(oracle.planes(ZA, set=OSET))
-    PB = int8_bytes(oracle.planes(ZB, set=OSET))
+    PA = device_layout(int8_bytes(oracle.planes(ZA, set=OSET)))
+    PB = device_layout(int8_bytes(oracle.planes(ZB, set=OSET)))
     C = oz.ozaki25_residue_gemm(m, n, k, to_dev(PA), to_dev(PB), set=SET)
     torch.cuda.synchronize()
     want = oracle.residue_gemm(oracle.residues(ZA, OSET), oracle.residues(ZB, OSET), OSET)
