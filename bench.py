@@ -9,8 +9,10 @@ The headline line is the published 12-modulus set (e4m3 planes, 36 FP8-MFMA
 limb products with FP32 accumulation and the modular epilogue); the same run
 also times the all-byte 15-modulus set of Sec. 5.1 (int8 planes, 15 int8-MFMA
 products) on the same inputs and reports it under "all_byte_set".
-``--moduli a15`` makes the all-byte set the headline instead.  Prints one
-JSON line.
+``--moduli a15`` makes the all-byte set the headline instead; ``--quantiser
+tz`` times the truncating quantiser.  Each set also reports "stored_planes":
+the per-call time of ozaki25_dgemm_planes on planes made once (storage mode
+P).  Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload square] [--moduli s12|a15]
 """
@@ -100,14 +102,14 @@ def cpu_baseline(A, B, w, rows, cols, cfg):
                       f"rounding, exact-product check), {dt:.1f} s single-threaded"}
 
 
-def time_set(oz, torch, w, Ad, Bd, Cd, cfg, steps, warmup):
+def time_set(oz, torch, w, Ad, Bd, Cd, cfg, steps, warmup, quant):
     """Mean ms per step and per stage of ozaki25_dgemm_ex for one modulus set."""
     ws = torch.empty(oz.ozaki25_dgemm_workspace_size(w.m, w.n, w.k, cfg["id"]), dtype=torch.uint8,
                      device=Ad.device)
 
     def step(events=None):
         oz.ozaki25_dgemm_ex(Ad, Bd, Cd, subtract=w.subtract, workspace=ws, stage_events=events,
-                            set=cfg["id"])
+                            set=cfg["id"], quantiser=quant)
 
     for _ in range(warmup):
         step()
@@ -127,6 +129,30 @@ def time_set(oz, torch, w, Ad, Bd, Cd, cfg, steps, warmup):
     stage = np.array([[row[j].elapsed_time(row[j + 1]) for j in range(oz.NUM_STAGE_EVENTS - 1)] for row in ev])
     del ws
     return ms, stage.mean(axis=0).tolist()
+
+
+def time_planes(oz, torch, w, Ad, Bd, Cd, cfg, steps, quant):
+    """Storage mode P: ms per ozaki25_dgemm_planes call on planes made once."""
+    planesA, expsA = oz.ozaki25_deconstruct(0, Ad, set=cfg["id"], quantiser=quant)
+    planesB, expsB = oz.ozaki25_deconstruct(1, Bd, set=cfg["id"], quantiser=quant)
+    ws = torch.empty(oz.ozaki25_dgemm_planes_workspace_size(w.m, w.n, cfg["id"]), dtype=torch.uint8,
+                     device=Ad.device)
+
+    def step():
+        oz.ozaki25_dgemm_planes(w.k, planesA, expsA, planesB, expsB, Cd, subtract=w.subtract,
+                                workspace=ws, set=cfg["id"])
+
+    step()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        step()
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / steps
+    del planesA, planesB, ws
+    return ms
 
 
 def rates(w, cfg, ms, stages):
@@ -158,6 +184,8 @@ def main():
     ap.add_argument("--moduli", default="s12", choices=sorted(SETS),
                     help="modulus set of the headline line (the other one is reported alongside)")
     ap.add_argument("--only", action="store_true", help="time the headline modulus set only")
+    ap.add_argument("--quantiser", default="rn", choices=["rn", "tz"],
+                    help="quantiser of Eq. (scale): round to nearest (default) or toward zero")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -192,8 +220,9 @@ def main():
         log("[bench] calibration copy: 1 GiB read, 1 GiB written")
 
     cfg = SETS[args.moduli]
+    quant = oz.TZ if args.quantiser == "tz" else oz.RN
     log(f"[bench] {cfg['moduli']}: warmup {args.warmup}, timing {args.steps} steps")
-    ms, stages = time_set(oz, torch, w, Ad, Bd, Cd, cfg, args.steps, args.warmup)
+    ms, stages = time_set(oz, torch, w, Ad, Bd, Cd, cfg, args.steps, args.warmup, quant)
     scan_ms, dec_ms, gemm_ms, rec_ms = stages
     rt = rates(w, cfg, ms, stages)
     log(f"[bench] {ms:.3f} ms/step; scan {scan_ms:.3f} deconstruct {dec_ms:.3f} gemm {gemm_ms:.3f} "
@@ -206,7 +235,7 @@ def main():
         if C0d is not None:
             Cd.copy_(C0d)
         log(f"[bench] {ocfg['moduli']}: warmup {args.warmup}, timing {args.steps} steps")
-        oms, ostages = time_set(oz, torch, w, Ad, Bd, Cd, ocfg, args.steps, args.warmup)
+        oms, ostages = time_set(oz, torch, w, Ad, Bd, Cd, ocfg, args.steps, args.warmup, quant)
         ort = rates(w, ocfg, oms, ostages)
         log(f"[bench] {oms:.3f} ms/step; stages {[round(x, 3) for x in ostages]}")
         other = {
@@ -226,6 +255,16 @@ def main():
             "emulation_roof_tflops": round(ort["roof"], 2),
             "emulation_roof_frac": round(ort["tflops"] / ort["roof"], 4),
         }
+        if C0d is not None:
+            Cd.copy_(C0d)
+        pms = time_planes(oz, torch, w, Ad, Bd, Cd, ocfg, args.steps, quant)
+        other["stored_planes"] = {"ms_per_call": round(pms, 4), "value": round(w.flops / (pms * 1e-3) / 1e12, 3),
+                                  "unit": "TFLOPS"}
+
+    if C0d is not None:
+        Cd.copy_(C0d)
+    log("[bench] stored planes (mode P)")
+    pms = time_planes(oz, torch, w, Ad, Bd, Cd, cfg, args.steps, quant)
 
     native = None
     if not args.no_native and not w.subtract and w.m * w.n * w.k <= 8192 ** 3:
@@ -257,7 +296,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{w.name}: C {'-=' if w.subtract else '='} A.B, m={w.m} n={w.n} k={w.k}, "
                                f"entries (U-0.5)exp({w.s} N), seed {w.seed}",
-                   "m": w.m, "n": w.n, "k": w.k, "moduli": cfg["moduli"], "quantiser": "RN",
+                   "m": w.m, "n": w.n, "k": w.k, "moduli": cfg["moduli"], "quantiser": args.quantiser.upper(),
                    "route": cfg["route"]},
         "roofline": {"bound": "mfma", "kernel": cfg["gemm_kernel"],
                      "achieved": round(rt["gemm_tops"], 2), "peak": cfg["peak"], "unit": peak_unit,
@@ -276,6 +315,10 @@ def main():
                      "reconstruct": round(rec_ms, 4)},
         "emulation_roof_tflops": round(rt["roof"], 2),
         "emulation_roof_frac": round(rt["tflops"] / rt["roof"], 4),
+        "stored_planes": {"ms_per_call": round(pms, 4), "value": round(w.flops / (pms * 1e-3) / 1e12, 3),
+                          "unit": "TFLOPS",
+                          "note": "storage mode P: ozaki25_dgemm_planes on planes deconstructed once "
+                                  "(residue products + reconstruction per call)"},
         "native_fp64_tflops": round(native, 2) if native else None,
         "native_fp64_peak_tflops": FP64_PEAK_TFLOPS,
         "paper_context": "modelled Rubin projections (no measurement in the paper): 473 TFLOPS roof, 182-235 TFLOPS floors",
