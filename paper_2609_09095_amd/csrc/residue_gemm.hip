@@ -247,6 +247,28 @@ __device__ __forceinline__ void stage_mma_dma(const int8_t* la, const int8_t* lb
   __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
 }
 
+// After global stage G (product G / nstage, stage G % nstage): at the end of
+// a segment, a plain reduction (when the product spans several segments);
+// at the end of a product, its multiplier (squares skip it between their two
+// weight-s products while each fits one segment; the last product always
+// applies its weight).
+__device__ __forceinline__ void carry(v16f (&acc)[2][2], int G, int nstage, int nseg, int mod,
+                                      float fm, float finv) {
+  const int p = G / nstage, s = G - p * nstage;
+  const bool prod_end = s + 1 == nstage;
+  if (!prod_end && (s + 1) % kSeg != 0) return;
+  const int mult = prod_end ? kSched[mod].mult[p] : 1;
+  if (p == 2 || mult != 1 || nseg > 1) {
+    const float fmult = (float)mult;
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[a][b][v] = mulmod_f(acc[a][b][v], fmult, fm, finv);
+  }
+}
+
 template <typename OT>
 __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_t n, int64_t kp,
                                                               const int8_t* __restrict__ pa,
@@ -298,46 +320,36 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
   const int nseg = nstage > 0 ? (nstage + kSeg - 1) / kSeg : 0;  // segments per product
   const int na = __builtin_amdgcn_readfirstlane((int)(rows_a * BK));
   const int nb = __builtin_amdgcn_readfirstlane((int)(rows_b * BK));
-  for (int g = 0; g < 3 * nseg; ++g) {
-    const int p = g / nseg, c = g - p * nseg;
-    const int s0 = c * kSeg, s1 = s0 + kSeg < nstage ? s0 + kSeg : nstage;
-    const int qa = kSched[mod].plane_a[p], qb = kSched[mod].plane_b[p];
-    auto ra = [&](int st) { return stage_rsrc(pa, kPlanes, m, tm * BM, qa, st, na); };
-    auto rb = [&](int st) { return stage_rsrc(pb, kPlanes, n, tn * BN, qb, st, nb); };
-
-    stage_load(ra(s0), rb(s0), lds_a0, lds_b0, voff, 0, wave);
-    for (int s = s0; s < s1; s += 2) {
-      __builtin_amdgcn_s_waitcnt(0);
-      __syncthreads();
-      // the DMA of the stage after the segment's last one lands in the idle
-      // buffer and is drained before the next segment; after the panel's
-      // last stage that stage is loaded again instead
-      {
-        const int nx = s + 1 < nstage ? s + 1 : s;
-        stage_mma_dma(lds_a0, lds_b0, ra0, rb0, fh, acc, ra(nx), rb(nx), lds_a1, lds_b1, voff, 0, wave);
-      }
-      if (s + 1 >= s1) break;
-      __builtin_amdgcn_s_waitcnt(0);
-      __syncthreads();
-      {
-        const int nx = s + 2 < nstage ? s + 2 : s + 1;
-        stage_mma_dma(lds_a1, lds_b1, ra0, rb0, fh, acc, ra(nx), rb(nx), lds_a0, lds_b0, voff, 0, wave);
-      }
-    }
+  // One pipeline over the 3 * nstage stages of the three products: the load
+  // of the next stage -- the next product's first one at a product boundary
+  // -- is always in flight while a stage computes, and the carry runs on the
+  // registers after the last stage of a segment.
+  const int total = 3 * nstage;
+  auto ra = [&](int G) {
+    const int p = G / nstage;
+    return stage_rsrc(pa, kPlanes, m, tm * BM, kSched[mod].plane_a[p], G - p * nstage, na);
+  };
+  auto rb = [&](int G) {
+    const int p = G / nstage;
+    return stage_rsrc(pb, kPlanes, n, tn * BN, kSched[mod].plane_b[p], G - p * nstage, nb);
+  };
+  const float fm = (float)sc.m, finv = 1.0f / (float)sc.m;
+  if (total > 0) stage_load(ra(0), rb(0), lds_a0, lds_b0, voff, 0, wave);
+  for (int G = 0; G < total; G += 2) {
     __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();  // every wave is done with the buffers before the next segment loads
-    const bool last = c == nseg - 1;
-    const int mult = last ? kSched[mod].mult[p] : 1;
-    if (p == 2 || mult != 1 || nseg > 1) {
-      const float fm = (float)sc.m, fmult = (float)mult, finv = 1.0f / (float)sc.m;
-#pragma unroll
-      for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int b = 0; b < 2; ++b)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) acc[a][b][v] = mulmod_f(acc[a][b][v], fmult, fm, finv);
-    }
+    __syncthreads();
+    // after the very last stage the look-ahead load repeats it
+    stage_mma_dma(lds_a0, lds_b0, ra0, rb0, fh, acc, ra(G + 1 < total ? G + 1 : G),
+                  rb(G + 1 < total ? G + 1 : G), lds_a1, lds_b1, voff, 0, wave);
+    carry(acc, G, nstage, nseg, mod, fm, finv);
+    if (G + 1 >= total) break;
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    stage_mma_dma(lds_a1, lds_b1, ra0, rb0, fh, acc, ra(G + 2 < total ? G + 2 : G + 1),
+                  rb(G + 2 < total ? G + 2 : G + 1), lds_a0, lds_b0, voff, 0, wave);
+    carry(acc, G + 1, nstage, nseg, mod, fm, finv);
   }
+  __builtin_amdgcn_s_waitcnt(0);  // the repeated look-ahead load lands before the epilogue
 
   // 32x32 MFMA result layout: lane holds column lane%32 and rows
   // 8*(v/4) + 4*(lane/32) + v%4 of its 32x32 block.  Stores use the tile's
