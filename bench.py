@@ -135,7 +135,7 @@ def time_planes(oz, torch, w, Ad, Bd, Cd, cfg, steps, quant):
     """Storage mode P: ms per ozaki25_dgemm_planes call on planes made once."""
     planesA, expsA = oz.ozaki25_deconstruct(0, Ad, set=cfg["id"], quantiser=quant)
     planesB, expsB = oz.ozaki25_deconstruct(1, Bd, set=cfg["id"], quantiser=quant)
-    ws = torch.empty(oz.ozaki25_dgemm_planes_workspace_size(w.m, w.n, cfg["id"]), dtype=torch.uint8,
+    ws = torch.empty(oz.ozaki25_dgemm_planes_workspace_size(w.m, w.n, w.k, cfg["id"]), dtype=torch.uint8,
                      device=Ad.device)
 
     def step():

@@ -202,9 +202,11 @@ ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A
                                 void* workspace, size_t workspace_bytes,
                                 void* const* stage_events, void* stream);
 
-/* Device workspace that ozaki25_dgemm_planes needs for an m x n product (the
- * per-modulus residue products: int16 for S12, int8 for A15). */
-size_t ozaki25_dgemm_planes_workspace_size(int64_t m, int64_t n, ozaki25_moduli_set set);
+/* Device workspace that ozaki25_dgemm_planes needs for an m x n x k product
+ * (the per-modulus residue products -- int16 for S12, int8 for A15 -- and,
+ * when few output tiles would leave the chip idle, per-split partial
+ * products of a split k range). */
+size_t ozaki25_dgemm_planes_workspace_size(int64_t m, int64_t n, int64_t k, ozaki25_moduli_set set);
 
 /* Emulated DGEMM from stored planes -- storage mode P of Sec. 6.2, principle O1
  * of Sec. 5 (planes converted once and kept across calls: a fixed A in
@@ -216,7 +218,7 @@ size_t ozaki25_dgemm_planes_workspace_size(int64_t m, int64_t n, ozaki25_moduli_
  *    quantiser, bit for bit).
  *  C, ldc, subtract: as in ozaki25_dgemm_ex.
  *  workspace: NULL to allocate stream-ordered, else at least
- *    ozaki25_dgemm_planes_workspace_size() bytes, 256-byte aligned.
+ *    ozaki25_dgemm_planes_workspace_size(m, n, k, set) bytes, 256-byte aligned.
  * m == 0 or n == 0: no-op; k == 0: C = +0 (or unchanged with subtract).
  * Errors: INVALID_VALUE, UNSUPPORTED, WORKSPACE, HIP. */
 ozaki25_status ozaki25_dgemm_planes(int64_t m, int64_t n, int64_t k, const uint8_t* planesA,

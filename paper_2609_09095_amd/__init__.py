@@ -78,7 +78,7 @@ def lib():
             "ozaki25_dgemm": ([i64, i64, i64, P, i64, P, i64, P, i64, i32, P], i32),
             "ozaki25_dgemm_sub": ([i64, i64, i64, P, i64, P, i64, P, i64, i32, P], i32),
             "ozaki25_dgemm_ex": ([i64, i64, i64, P, i64, P, i64, P, i64, i32, i32, i32, P, sz, P, P], i32),
-            "ozaki25_dgemm_planes_workspace_size": ([i64, i64, i32], sz),
+            "ozaki25_dgemm_planes_workspace_size": ([i64, i64, i64, i32], sz),
             "ozaki25_dgemm_planes": ([i64, i64, i64, P, P, P, P, P, i64, i32, i32, P, sz, P], i32),
         }
         for name, (args, res) in sig.items():
@@ -266,8 +266,8 @@ def ozaki25_dgemm_sub(A, B, C, set: int = S12, stream=None):
     return C
 
 
-def ozaki25_dgemm_planes_workspace_size(m: int, n: int, set: int = S12) -> int:
-    return lib().ozaki25_dgemm_planes_workspace_size(m, n, set)
+def ozaki25_dgemm_planes_workspace_size(m: int, n: int, k: int, set: int = S12) -> int:
+    return lib().ozaki25_dgemm_planes_workspace_size(m, n, k, set)
 
 
 def ozaki25_dgemm_planes(k: int, planesA, expsA, planesB, expsB, C=None, subtract: bool = False,

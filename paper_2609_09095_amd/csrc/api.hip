@@ -66,8 +66,19 @@ size_t matrix_bytes(int64_t rows, int64_t cols, int64_t ld) {
 ozaki25_status hip_status(hipError_t e) { return e == hipSuccess ? OZAKI25_SUCCESS : OZAKI25_ERR_HIP; }
 
 struct Workspace {
-  size_t planes_a, planes_b, exps_a, exps_b, cres, total;
+  size_t planes_a, planes_b, exps_a, exps_b, cres, part, total;
+  int splits;
 };
+
+size_t cres_elem(ozaki25_moduli_set set) { return bytes_set(set) ? sizeof(int8_t) : sizeof(int16_t); }
+
+// the compact residue products and, with split-k, the per-split partials
+size_t products_bytes(int64_t m, int64_t n, int64_t k, ozaki25_moduli_set set, int* splits) {
+  const int sp = oz::residue_gemm_splits((int)set, m, n, k_pad(k));
+  if (splits) *splits = sp;
+  const size_t one = (size_t)num_moduli(set) * m * n * cres_elem(set);
+  return align_up(one) + (sp > 1 ? align_up(one * sp) : 0);
+}
 
 // planes of A and B, exponents, and the residue products: int16 for the
 // published set (|c| <= 544), int8 for the all-byte set (|c| <= 128)
@@ -75,7 +86,6 @@ Workspace layout(int64_t m, int64_t n, int64_t k, ozaki25_moduli_set set) {
   Workspace w;
   const int64_t kp = k_pad(k);
   const size_t np = (size_t)num_planes(set);
-  const size_t cres_elem = bytes_set(set) ? sizeof(int8_t) : sizeof(int16_t);
   size_t off = 0;
   w.planes_a = off;
   off = align_up(off + np * m * kp);
@@ -86,7 +96,10 @@ Workspace layout(int64_t m, int64_t n, int64_t k, ozaki25_moduli_set set) {
   w.exps_b = off;
   off = align_up(off + (size_t)n * sizeof(int32_t));
   w.cres = off;
-  off = align_up(off + (size_t)num_moduli(set) * m * n * cres_elem);
+  const size_t one = align_up((size_t)num_moduli(set) * m * n * cres_elem(set));
+  const size_t prod = products_bytes(m, n, k, set, &w.splits);
+  w.part = off + one;
+  off += prod;
   w.total = off;
   return w;
 }
@@ -222,6 +235,7 @@ ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A
   int32_t* ea = (int32_t*)(base + w.exps_a);
   int32_t* eb = (int32_t*)(base + w.exps_b);
   void* cres = base + w.cres;
+  void* part = w.splits > 1 ? base + w.part : nullptr;
   const bool bytes = bytes_set(set);
   const int t = scale_bits(k, set);
   const int64_t kp = k_pad(k);
@@ -234,8 +248,10 @@ ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A
   if (e == hipSuccess) e = oz::launch_deconstruct((int)set, (int)quant, 1, n, k, kp, t, B, ldb, eb, pb, s);
   if (ev && e == hipSuccess) e = hipEventRecord(ev[2], s);
   if (e == hipSuccess)
-    e = bytes ? oz::launch_residue_gemm_bytes_i8(m, n, kp, pa, pb, (int8_t*)cres, s)
-              : oz::launch_residue_gemm_i16(m, n, kp, pa, pb, (int16_t*)cres, s);
+    e = bytes ? oz::launch_residue_gemm_bytes_i8(m, n, kp, pa, pb, (int8_t*)cres, (int8_t*)part,
+                                                 w.splits, s)
+              : oz::launch_residue_gemm_i16(m, n, kp, pa, pb, (int16_t*)cres, (int16_t*)part,
+                                            w.splits, s);
   if (ev && e == hipSuccess) e = hipEventRecord(ev[3], s);
   const int sub = subtract ? 1 : 0;
   if (e == hipSuccess)
@@ -249,9 +265,9 @@ ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A
   return hip_status(e);
 }
 
-size_t ozaki25_dgemm_planes_workspace_size(int64_t m, int64_t n, ozaki25_moduli_set set) {
-  if (!known_set(set) || m < 0 || n < 0) return 0;
-  return align_up((size_t)num_moduli(set) * m * n * (bytes_set(set) ? sizeof(int8_t) : sizeof(int16_t)));
+size_t ozaki25_dgemm_planes_workspace_size(int64_t m, int64_t n, int64_t k, ozaki25_moduli_set set) {
+  if (!known_set(set) || m < 0 || n < 0 || k < 0) return 0;
+  return products_bytes(m, n, k, set, nullptr);
 }
 
 ozaki25_status ozaki25_dgemm_planes(int64_t m, int64_t n, int64_t k, const uint8_t* planesA,
@@ -269,7 +285,8 @@ ozaki25_status ozaki25_dgemm_planes(int64_t m, int64_t n, int64_t k, const uint8
   if (((uintptr_t)planesA & 15) || ((uintptr_t)planesB & 15) || ((uintptr_t)expsA & 3) ||
       ((uintptr_t)expsB & 3))
     return OZAKI25_ERR_INVALID_VALUE;
-  const size_t need = ozaki25_dgemm_planes_workspace_size(m, n, set);
+  int splits = 1;
+  const size_t need = products_bytes(m, n, k, set, &splits);
   void* ws = workspace;
   bool owned = false;
   if (ws) {
@@ -282,13 +299,15 @@ ozaki25_status ozaki25_dgemm_planes(int64_t m, int64_t n, int64_t k, const uint8
   const int8_t *pa = (const int8_t*)planesA, *pb = (const int8_t*)planesB;
   const int sub = subtract ? 1 : 0;
   hipError_t e;
+  const size_t one = align_up((size_t)num_moduli(set) * m * n * cres_elem(set));
+  char* part = splits > 1 ? (char*)ws + one : nullptr;
   if (bytes_set(set)) {
     int8_t* cres = (int8_t*)ws;
-    e = oz::launch_residue_gemm_bytes_i8(m, n, kp, pa, pb, cres, s);
+    e = oz::launch_residue_gemm_bytes_i8(m, n, kp, pa, pb, cres, (int8_t*)part, splits, s);
     if (e == hipSuccess) e = oz::launch_reconstruct_bytes_i8(m, n, cres, expsA, expsB, C, ldc, sub, s);
   } else {
     int16_t* cres = (int16_t*)ws;
-    e = oz::launch_residue_gemm_i16(m, n, kp, pa, pb, cres, s);
+    e = oz::launch_residue_gemm_i16(m, n, kp, pa, pb, cres, (int16_t*)part, splits, s);
     if (e == hipSuccess) e = oz::launch_reconstruct_i16(m, n, cres, expsA, expsB, C, ldc, sub, s);
   }
   if (owned) {

@@ -33,12 +33,19 @@ hipError_t launch_deconstruct(int set, int quant, int side, int64_t vecs, int64_
 constexpr int64_t kMaxResidueCols = (int64_t)1 << 23;
 hipError_t launch_residue_gemm_i32(int64_t m, int64_t n, int64_t kp, const int8_t* pa,
                                    const int8_t* pb, int32_t* cres, hipStream_t stream);
+// The fused path's compact products may split the k range (split-k) when
+// the output tiles are too few to fill the chip: `splits` from
+// residue_gemm_splits, and a partial buffer of splits * r * m * n elements.
+constexpr int kMaxSplits = 64;
+int residue_gemm_splits(int set, int64_t m, int64_t n, int64_t kp);
 hipError_t launch_residue_gemm_i16(int64_t m, int64_t n, int64_t kp, const int8_t* pa,
-                                   const int8_t* pb, int16_t* cres, hipStream_t stream);
+                                   const int8_t* pb, int16_t* cres, int16_t* part, int splits,
+                                   hipStream_t stream);
 hipError_t launch_residue_gemm_bytes_i32(int64_t m, int64_t n, int64_t kp, const int8_t* pa,
                                          const int8_t* pb, int32_t* cres, hipStream_t stream);
 hipError_t launch_residue_gemm_bytes_i8(int64_t m, int64_t n, int64_t kp, const int8_t* pa,
-                                        const int8_t* pb, int8_t* cres, hipStream_t stream);
+                                        const int8_t* pb, int8_t* cres, int8_t* part, int splits,
+                                        hipStream_t stream);
 
 // Alg. 3: Garner, Horner, lift, single rounding (C = or C -= ).
 hipError_t launch_reconstruct_i32(int64_t m, int64_t n, const int32_t* cres, const int32_t* ea,

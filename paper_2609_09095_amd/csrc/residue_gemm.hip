@@ -138,9 +138,8 @@ __device__ __forceinline__ int swz(int row) { return (row & 7) ^ ((row >> 3) & 1
 // kGroupM = 2 tile rows.  Blocks are dealt round-robin over the 8 XCDs, so
 // the 32 blocks an XCD runs at a time cover 4 tile rows x 8 tile columns: 12
 // panels feed 32 tiles from its L2 (groups of 4 rows: 18 panels; 8 rows: 33).
-__device__ __forceinline__ void block_coords(int64_t tiles_m, int64_t tiles_n, int& mod,
+__device__ __forceinline__ void block_coords(int64_t id, int64_t tiles_m, int64_t tiles_n, int& mod,
                                              int64_t& tm, int64_t& tn) {
-  const int64_t id = blockIdx.x;
   const int64_t per_mod = tiles_m * tiles_n;
   mod = (int)(id / per_mod);
   const int64_t t = id % per_mod;
@@ -269,21 +268,26 @@ __device__ __forceinline__ void carry(v16f (&acc)[2][2], int G, int nstage, int 
   }
 }
 
+// splits > 1 (split-k): consecutive blocks take the same tile's stage ranges,
+// and block (tile, split) writes its centred partial product to the split's
+// own [r][m][n] slice of cres; reduce_splits_kernel sums them mod m.
 template <typename OT>
 __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_t n, int64_t kp,
                                                               const int8_t* __restrict__ pa,
                                                               const int8_t* __restrict__ pb,
-                                                              OT* __restrict__ cres) {
+                                                              OT* __restrict__ cres, int splits) {
   // two LDS stages, each an A tile and a B tile of 256 rows x 128 bytes
   __shared__ __attribute__((aligned(1024))) int8_t lds_a0[kTile];
   __shared__ __attribute__((aligned(1024))) int8_t lds_b0[kTile];
   __shared__ __attribute__((aligned(1024))) int8_t lds_a1[kTile];
   __shared__ __attribute__((aligned(1024))) int8_t lds_b1[kTile];
   const int64_t tiles_m = (m + BM - 1) / BM, tiles_n = (n + BN - 1) / BN;
+  const int split = (int)(blockIdx.x % (unsigned)splits);
   int mod;
   int64_t tm, tn;
-  block_coords(tiles_m, tiles_n, mod, tm, tn);
+  block_coords(blockIdx.x / (unsigned)splits, tiles_m, tiles_n, mod, tm, tn);
   const ModSched sc = kSched[mod];
+  cres += (int64_t)split * kR * m * n;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS-DMA base in M0
@@ -316,7 +320,10 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
   // product's multiplier after its last segment, a plain reduction after the
   // others; none mid-way between the two square products of weight s while
   // they fit one segment each).
-  const int nstage = (int)(kp / BK);
+  // this block's stages [sbeg, sbeg + nstage) of each product
+  const int nstage_all = (int)(kp / BK);
+  const int sbeg = (int)((int64_t)nstage_all * split / splits);
+  const int nstage = (int)((int64_t)nstage_all * (split + 1) / splits) - sbeg;
   const int nseg = nstage > 0 ? (nstage + kSeg - 1) / kSeg : 0;  // segments per product
   const int na = __builtin_amdgcn_readfirstlane((int)(rows_a * BK));
   const int nb = __builtin_amdgcn_readfirstlane((int)(rows_b * BK));
@@ -327,11 +334,11 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
   const int total = 3 * nstage;
   auto ra = [&](int G) {
     const int p = G / nstage;
-    return stage_rsrc(pa, kPlanes, m, tm * BM, kSched[mod].plane_a[p], G - p * nstage, na);
+    return stage_rsrc(pa, kPlanes, m, tm * BM, kSched[mod].plane_a[p], sbeg + G - p * nstage, na);
   };
   auto rb = [&](int G) {
     const int p = G / nstage;
-    return stage_rsrc(pb, kPlanes, n, tn * BN, kSched[mod].plane_b[p], G - p * nstage, nb);
+    return stage_rsrc(pb, kPlanes, n, tn * BN, kSched[mod].plane_b[p], sbeg + G - p * nstage, nb);
   };
   const float fm = (float)sc.m, finv = 1.0f / (float)sc.m;
   if (total > 0) stage_load(ra(0), rb(0), lds_a0, lds_b0, voff, 0, wave);
@@ -462,16 +469,19 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
                                                                     int64_t kp,
                                                                     const int8_t* __restrict__ pa,
                                                                     const int8_t* __restrict__ pb,
-                                                                    OT* __restrict__ cres) {
+                                                                    OT* __restrict__ cres,
+                                                                    int splits) {
   __shared__ __attribute__((aligned(1024))) int8_t lds_a0[kTile];
   __shared__ __attribute__((aligned(1024))) int8_t lds_b0[kTile];
   __shared__ __attribute__((aligned(1024))) int8_t lds_a1[kTile];
   __shared__ __attribute__((aligned(1024))) int8_t lds_b1[kTile];
   const int64_t tiles_m = (m + BM - 1) / BM, tiles_n = (n + BN - 1) / BN;
+  const int split = (int)(blockIdx.x % (unsigned)splits);
   int mod;
   int64_t tm, tn;
-  block_coords(tiles_m, tiles_n, mod, tm, tn);
+  block_coords(blockIdx.x / (unsigned)splits, tiles_m, tiles_n, mod, tm, tn);
   const int mm = kModA[mod];
+  cres += (int64_t)split * kRA * m * n;
   const double minv = 1.0 / (double)mm;
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -498,8 +508,10 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
 #pragma unroll
     for (int b = 0; b < 2; ++b) acc[a][b] = v16i{};
 
-  const int nstage = (int)(kp / BK);
-  for (int s0 = 0; s0 < nstage; s0 += kSegA) {
+  const int nstage_all = (int)(kp / BK);
+  const int sbeg = (int)((int64_t)nstage_all * split / splits);
+  const int nstage = (int)((int64_t)nstage_all * (split + 1) / splits);  // one past the last
+  for (int s0 = sbeg; s0 < nstage; s0 += kSegA) {
     const int s1 = s0 + kSegA < nstage ? s0 + kSegA : nstage;
     stage_load(ra(s0), rb(s0), lds_a0, lds_b0, voff, 0, wave);
     for (int s = s0; s < s1; s += 2) {
@@ -550,42 +562,94 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
     }
 }
 
+// Sum of the splits' centred partial products, reduced to the centred
+// residue: |sum| <= splits * 545 < 2^16, exact in FP32, and the FP32
+// quotient of an integer below 2^16 by m errs far less than the 1/(2m)
+// that separates it from a half integer for odd m; for even m (1024, 256)
+// the tie +m/2 maps to -m/2.  Grid: x over m n, y over the moduli.
+template <bool BYTES, typename OT>
+__global__ __launch_bounds__(256) void reduce_splits_kernel(int64_t mn, int splits,
+                                                            const OT* __restrict__ part,
+                                                            OT* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= mn) return;
+  const int q = blockIdx.y;
+  const int mm = BYTES ? kModA[q] : kSched[q].m;
+  const int64_t stride = (int64_t)(BYTES ? kRA : kR) * mn;
+  const int64_t at = (int64_t)q * mn + i;
+  int sum = 0;
+  for (int sp = 0; sp < splits; ++sp) sum += (int)part[sp * stride + at];
+  const float qf = __builtin_rintf((float)sum * (1.0f / (float)mm));
+  int r = sum - (int)qf * mm;
+  r = 2 * r == mm ? -r : r;
+  out[at] = (OT)r;
+}
+
 template <bool BYTES, typename OT>
 hipError_t launch_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* pa, const int8_t* pb,
-                       OT* cres, hipStream_t stream) {
+                       OT* cres, OT* part, int splits, hipStream_t stream) {
   if (m <= 0 || n <= 0) return hipSuccess;
   // the store epilogue uses 32-bit offsets within a 256-row tile
   if (n > kMaxResidueCols) return hipErrorInvalidValue;
+  const int nstage = (int)(kp / BK);
+  if (splits < 1 || splits > (nstage > 1 ? nstage : 1) || (splits > 1 && !part))
+    return hipErrorInvalidValue;
   const int64_t blocks = (int64_t)(BYTES ? kRA : kR) * ((m + BM - 1) / BM) * ((n + BN - 1) / BN);
+  OT* dst = splits > 1 ? part : cres;
+  const dim3 grid((unsigned)(blocks * splits));
   if constexpr (BYTES)
-    hipLaunchKernelGGL(residue_gemm_bytes_kernel<OT>, dim3((unsigned)blocks), dim3(1024), 0, stream,
-                       m, n, kp, pa, pb, cres);
+    hipLaunchKernelGGL(residue_gemm_bytes_kernel<OT>, grid, dim3(1024), 0, stream, m, n, kp, pa, pb,
+                       dst, splits);
   else
-    hipLaunchKernelGGL(residue_gemm_kernel<OT>, dim3((unsigned)blocks), dim3(1024), 0, stream, m, n,
-                       kp, pa, pb, cres);
+    hipLaunchKernelGGL(residue_gemm_kernel<OT>, grid, dim3(1024), 0, stream, m, n, kp, pa, pb, dst,
+                       splits);
+  if (splits > 1) {
+    const int64_t mn = m * n;
+    hipLaunchKernelGGL((reduce_splits_kernel<BYTES, OT>),
+                       dim3((unsigned)((mn + 255) / 256), (unsigned)(BYTES ? kRA : kR)), dim3(256), 0,
+                       stream, mn, splits, part, cres);
+  }
   return hipGetLastError();
 }
 
 }  // namespace
 
+int residue_gemm_splits(int set, int64_t m, int64_t n, int64_t kp) {
+  // split the k range when the tiles of all moduli leave most of the chip
+  // idle: aim at about 1024 blocks, with at least 2 stages of each product
+  // per block (4 for the single-product int8 kernel)
+  if (m <= 0 || n <= 0) return 1;
+  const bool bytes = set == kSetBytes;
+  const int64_t blocks = (int64_t)(bytes ? kRA : kR) * ((m + BM - 1) / BM) * ((n + BN - 1) / BN);
+  const int64_t nstage = kp / BK;
+  if (blocks >= 512) return 1;
+  int64_t s = (1024 + blocks - 1) / blocks;
+  const int64_t cap = nstage / (bytes ? 4 : 2);
+  if (s > cap) s = cap;
+  if (s > kMaxSplits) s = kMaxSplits;
+  return s < 1 ? 1 : (int)s;
+}
+
 hipError_t launch_residue_gemm_i32(int64_t m, int64_t n, int64_t kp, const int8_t* pa,
                                    const int8_t* pb, int32_t* cres, hipStream_t stream) {
-  return launch_gemm<false, int32_t>(m, n, kp, pa, pb, cres, stream);
+  return launch_gemm<false, int32_t>(m, n, kp, pa, pb, cres, nullptr, 1, stream);
 }
 
 hipError_t launch_residue_gemm_i16(int64_t m, int64_t n, int64_t kp, const int8_t* pa,
-                                   const int8_t* pb, int16_t* cres, hipStream_t stream) {
-  return launch_gemm<false, int16_t>(m, n, kp, pa, pb, cres, stream);
+                                   const int8_t* pb, int16_t* cres, int16_t* part, int splits,
+                                   hipStream_t stream) {
+  return launch_gemm<false, int16_t>(m, n, kp, pa, pb, cres, part, splits, stream);
 }
 
 hipError_t launch_residue_gemm_bytes_i32(int64_t m, int64_t n, int64_t kp, const int8_t* pa,
                                          const int8_t* pb, int32_t* cres, hipStream_t stream) {
-  return launch_gemm<true, int32_t>(m, n, kp, pa, pb, cres, stream);
+  return launch_gemm<true, int32_t>(m, n, kp, pa, pb, cres, nullptr, 1, stream);
 }
 
 hipError_t launch_residue_gemm_bytes_i8(int64_t m, int64_t n, int64_t kp, const int8_t* pa,
-                                        const int8_t* pb, int8_t* cres, hipStream_t stream) {
-  return launch_gemm<true, int8_t>(m, n, kp, pa, pb, cres, stream);
+                                        const int8_t* pb, int8_t* cres, int8_t* part, int splits,
+                                        hipStream_t stream) {
+  return launch_gemm<true, int8_t>(m, n, kp, pa, pb, cres, part, splits, stream);
 }
 
 }  // namespace oz

@@ -73,9 +73,18 @@ def test_size_helpers():
     ws = oz.ozaki25_dgemm_workspace_size(100, 50, 70)
     assert ws >= 30 * 100 * 128 + 30 * 50 * 128 + 4 * 150 + 12 * 100 * 50 * 2
     assert ws % 256 == 0
-    assert oz.ozaki25_dgemm_planes_workspace_size(100, 50) == 12 * 100 * 50 * 2 // 256 * 256 + 256 * (12 * 100 * 50 * 2 % 256 != 0)
-    assert oz.ozaki25_dgemm_planes_workspace_size(100, 50, oz.A15) >= 15 * 100 * 50
-    assert oz.ozaki25_dgemm_planes_workspace_size(100, 50, 3) == 0
+    def up(x):
+        return (x + 255) // 256 * 256
+    # one tile per modulus, k = 70: a single k-split, just the residue products
+    assert oz.ozaki25_dgemm_planes_workspace_size(100, 50, 70) == up(12 * 100 * 50 * 2)
+    assert oz.ozaki25_dgemm_planes_workspace_size(100, 50, 70, oz.A15) == up(15 * 100 * 50)
+    # 256 x 256 x 8192: 12 tiles split 32 ways (at least 2 stages of 128 k each)
+    assert oz.ozaki25_dgemm_planes_workspace_size(256, 256, 8192) == up(12 * 256 * 256 * 2) * 33
+    # 15 tiles: 16 ways for the int8 kernel (at least 4 stages per split)
+    assert oz.ozaki25_dgemm_planes_workspace_size(256, 256, 8192, oz.A15) == up(15 * 256 * 256) * 17
+    # enough tiles: no split
+    assert oz.ozaki25_dgemm_planes_workspace_size(8192, 8192, 8192) == up(12 * 8192 * 8192 * 2)
+    assert oz.ozaki25_dgemm_planes_workspace_size(100, 50, 70, 3) == 0
     # all-byte set: 15 int8 planes per operand, int8 residue products
     assert oz.ozaki25_planes_bytes(10, 70, oz.A15) == 15 * 10 * 128
     wa = oz.ozaki25_dgemm_workspace_size(100, 50, 70, oz.A15)
@@ -137,6 +146,9 @@ def test_argument_errors_are_synchronous():
     assert g(4, 4, oz.MAX_K + 1, pa, ea, pb, eb, c, 4, 0, 0, null, 0, null) == oz.ERR_UNSUPPORTED
     assert g(0, 4, 4, null, null, null, null, null, 4, 0, 0, null, 0, null) == oz.SUCCESS
     assert g(4, 4, 4, pa, ea, pb, eb, c, 4, 0, 0, _v(0x600000), 8, null) == oz.ERR_WORKSPACE
+    # the dgemm workspace grows by the split-k partials for few output tiles
+    assert (oz.ozaki25_dgemm_workspace_size(256, 256, 8192)
+            >= oz.ozaki25_dgemm_planes_workspace_size(256, 256, 8192) + 2 * 30 * 256 * 8192)
 
 
 def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):

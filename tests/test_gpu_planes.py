@@ -35,7 +35,7 @@ def test_planes_gemm_matches_dgemm_ex_and_oracle(dset, oset, quant, m, n, k, see
         # subtract form with a caller workspace
         C0 = workloads.random_matrix(m, n, 1.0, seed + 5)
         Cs = to_dev(C0)
-        ws = torch.empty(oz.ozaki25_dgemm_planes_workspace_size(m, n, dset), dtype=torch.uint8, device="cuda")
+        ws = torch.empty(oz.ozaki25_dgemm_planes_workspace_size(m, n, k, dset), dtype=torch.uint8, device="cuda")
         oz.ozaki25_dgemm_planes(k, planesA, expsA, planesB, expsB, Cs, subtract=True, workspace=ws, set=dset)
         torch.cuda.synchronize()
         assert torch.equal(C.view(torch.int64), ref.view(torch.int64)), f"B #{i}"

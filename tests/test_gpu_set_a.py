@@ -305,3 +305,15 @@ def test_dgemm_strided_operands_and_workspace():
     r = oracle.dgemm(A, B, want_planes=False, set=OSET)
     assert_bits_equal(Cb[:, :n].cpu().numpy(), r.C, "C")
     assert np.all(Cb[:, n:].cpu().numpy() == 3.0)
+
+
+@pytest.mark.parametrize("m,n,k,seed", [(40, 300, 8576, 91), (24, 40, 70000, 92), (256, 256, 8192, 93)])
+def test_dgemm_split_k_matches_oracle(m, n, k, seed):
+    """Split k range for few output tiles (int8 kernel, partial residue
+    bytes summed mod m)."""
+    log(f"[A15] dgemm split-k m={m} n={n} k={k}")
+    A = workloads.random_matrix(m, k, 1.0, seed)
+    B = workloads.random_matrix(k, n, 1.0, seed + 1)
+    C = gpu_dgemm(A, B, set=SET)
+    r = oracle.dgemm(A, B, want_planes=False, set=OSET)
+    assert_bits_equal(C.cpu().numpy(), r.C, "C")
