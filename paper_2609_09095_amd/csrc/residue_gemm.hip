@@ -59,9 +59,13 @@ typedef int v16i __attribute__((ext_vector_type(16)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 
 constexpr int BM = 256;         // output rows per block
-constexpr int BN = 256;         // output columns per block
 constexpr int BK = 128;         // k bytes per stage
-constexpr int kTile = BM * BK;  // bytes of one operand tile in LDS (BM == BN)
+constexpr int kTile = BM * BK;  // bytes of the A tile of a stage in LDS
+// output columns per block: NB * 128 (NB = 2; NB = 1 for at most 128
+// columns, where a 256-wide tile would leave half of every MFMA idle); a
+// wave owns 64 rows x NB * 32 columns
+template <int NB>
+inline constexpr int kBN = 128 * NB;
 static_assert(BK == kKAlign, "every K stage is full: planes are padded to BK");
 constexpr int kGroupM = 2;      // tile rows per group in the block order
 constexpr int kSeg = 128;       // K stages (16384 k) per accumulation segment
@@ -178,15 +182,27 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t stage_rsrc(const int8_t* plane
 // straight from global memory into LDS.  A load writes 1 KiB = 8 rows x
 // 128 bytes, lane l landing at row l/8, chunk l%8 of that slab; to realise
 // the swizzled layout the lane fetches the global chunk (l%8) ^ swz(row).
+// DMA d of a stage (2 + NB per wave): d < 2 the A slab wave*2 + d; then the B
+// slab wave*NB + (d - 2).  voff[0..1]: rows wave*16 + 8 d + lane/8; voffb:
+// rows wave*8 + lane/8 (the B slab when NB = 1).
+template <int NB>
+__device__ __forceinline__ void stage_dma(int d, __amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rb,
+                                          int8_t* la, int8_t* lb, const int (&voff)[2], int voffb,
+                                          int wave) {
+  if (d < 2)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr)(la + (wave * 2 + d) * 1024), 16, voff[d], 0,
+                                             0, 0);
+  else
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr)(lb + (wave * NB + d - 2) * 1024), 16,
+                                             NB == 2 ? voff[d - 2] : voffb, 0, 0, 0);
+}
+
+template <int NB>
 __device__ __forceinline__ void stage_load(__amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rb,
-                                           int8_t* la, int8_t* lb, const int (&voff)[2], int k0,
+                                           int8_t* la, int8_t* lb, const int (&voff)[2], int voffb,
                                            int wave) {
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int slab = (wave * 2 + i) * 1024;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr)(la + slab), 16, voff[i], k0, 0, 0);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr)(lb + slab), 16, voff[i], k0, 0, 0);
-  }
+  for (int d = 0; d < 2 + NB; ++d) stage_dma<NB>(d, ra, rb, la, lb, voff, voffb, wave);
 }
 
 __device__ __forceinline__ v8i cat(v4i lo, v4i hi) {
@@ -202,48 +218,42 @@ __device__ __forceinline__ v8i frag(const int8_t* base, int r, int ks, int fh) {
              *reinterpret_cast<const v4i*>(row + (((4 * ks + 2 + fh) ^ swz(r)) << 4)));
 }
 
-// One stage: two 64-byte K steps of 2 x 2 MFMAs (a wave owns 64 x 64;
-// four waves share each SIMD).  The next stage's 4 DMA loads go among step
-// 0's MFMAs.
+// One stage: two 64-byte K steps of 2 x NB MFMAs (a wave owns 64 x 32 NB;
+// four waves share each SIMD).  The next stage's 2 + NB DMA loads go among
+// step 0's MFMAs.
+template <int NB>
 __device__ __forceinline__ void stage_mma_dma(const int8_t* la, const int8_t* lb, int ra0, int rb0,
-                                              int fh, v16f (&acc)[2][2],
+                                              int fh, v16f (&acc)[2][NB],
                                               __amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rb,
-                                              int8_t* na, int8_t* nb, const int (&voff)[2], int k0,
-                                              int wave) {
-  v8i af[2][2], bf[2][2];
-  k0 = __builtin_amdgcn_readfirstlane(k0);
+                                              int8_t* na, int8_t* nb, const int (&voff)[2],
+                                              int voffb, int wave) {
+  v8i af[2][2], bf[2][NB];
 #pragma unroll
-  for (int ks = 0; ks < 2; ++ks)
+  for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
-    for (int x = 0; x < 2; ++x) {
-      af[ks][x] = frag(la, ra0 + 32 * x, ks, fh);
-      bf[ks][x] = frag(lb, rb0 + 32 * x, ks, fh);
-    }
+    for (int x = 0; x < 2; ++x) af[ks][x] = frag(la, ra0 + 32 * x, ks, fh);
+#pragma unroll
+    for (int x = 0; x < NB; ++x) bf[ks][x] = frag(lb, rb0 + 32 * x, ks, fh);
+  }
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        if (ks == 0) {
-          const int i = a * 2 + b;  // DMA i of 4: (slab i/2, side i%2)
-          const int slab = (wave * 2 + (i >> 1)) * 1024;
-          if (i & 1)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr)(nb + slab), 16, voff[i >> 1], k0, 0, 0);
-          else
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr)(na + slab), 16, voff[i >> 1], k0, 0, 0);
-        }
+      for (int b = 0; b < NB; ++b) {
+        const int j = ks * 2 * NB + a * NB + b;  // MFMA number in issue order
+        if (j < 2 + NB) stage_dma<NB>(j, ra, rb, na, nb, voff, voffb, wave);
         acc[a][b] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af[ks][a], bf[ks][b], acc[a][b], 0,
                                                                     0, 0, 0, 0, 0);
       }
   __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < 2 + NB; ++i) {
     __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
   }
-  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+  __builtin_amdgcn_sched_group_barrier(0x008, 4 * NB - (2 + NB), 0);
 }
 
 // After global stage G (product G / nstage, stage G % nstage): at the end of
@@ -251,7 +261,8 @@ __device__ __forceinline__ void stage_mma_dma(const int8_t* la, const int8_t* lb
 // at the end of a product, its multiplier (squares skip it between their two
 // weight-s products while each fits one segment; the last product always
 // applies its weight).
-__device__ __forceinline__ void carry(v16f (&acc)[2][2], int G, int nstage, int nseg, int mod,
+template <int NB>
+__device__ __forceinline__ void carry(v16f (&acc)[2][NB], int G, int nstage, int nseg, int mod,
                                       float fm, float finv) {
   const int p = G / nstage, s = G - p * nstage;
   const bool prod_end = s + 1 == nstage;
@@ -262,7 +273,7 @@ __device__ __forceinline__ void carry(v16f (&acc)[2][2], int G, int nstage, int 
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
-      for (int b = 0; b < 2; ++b)
+      for (int b = 0; b < NB; ++b)
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[a][b][v] = mulmod_f(acc[a][b][v], fmult, fm, finv);
   }
@@ -271,16 +282,17 @@ __device__ __forceinline__ void carry(v16f (&acc)[2][2], int G, int nstage, int 
 // splits > 1 (split-k): consecutive blocks take the same tile's stage ranges,
 // and block (tile, split) writes its centred partial product to the split's
 // own [r][m][n] slice of cres; reduce_splits_kernel sums them mod m.
-template <typename OT>
+template <typename OT, int NB>
 __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_t n, int64_t kp,
                                                               const int8_t* __restrict__ pa,
                                                               const int8_t* __restrict__ pb,
                                                               OT* __restrict__ cres, int splits) {
   // two LDS stages, each an A tile and a B tile of 256 rows x 128 bytes
+  constexpr int BN = kBN<NB>;
   __shared__ __attribute__((aligned(1024))) int8_t lds_a0[kTile];
-  __shared__ __attribute__((aligned(1024))) int8_t lds_b0[kTile];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_b0[BN * BK];
   __shared__ __attribute__((aligned(1024))) int8_t lds_a1[kTile];
-  __shared__ __attribute__((aligned(1024))) int8_t lds_b1[kTile];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_b1[BN * BK];
   const int64_t tiles_m = (m + BM - 1) / BM, tiles_n = (n + BN - 1) / BN;
   const int split = (int)(blockIdx.x % (unsigned)splits);
   int mod;
@@ -293,7 +305,7 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS-DMA base in M0
   const int wr = wave >> 2, wc = wave & 3;  // 4 x 4 waves of 64 x 64
   const int fr = lane & 31, fh = lane >> 5;  // fragment row, 16-byte K half
-  const int ra0 = wr * 64 + fr, rb0 = wc * 64 + fr;
+  const int ra0 = wr * 64 + fr, rb0 = wc * 32 * NB + fr;
 
   // byte offsets (within the block's 256-row panel) of the 4 slab loads
   int voff[2];
@@ -302,16 +314,18 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
     const int r = wave * 16 + i * 8 + (lane >> 3);
     voff[i] = r * BK + (((lane & 7) ^ swz(r)) << 4);
   }
+  const int rbd = wave * 8 + (lane >> 3);  // B slab rows when NB = 1
+  const int voffb = rbd * BK + (((lane & 7) ^ swz(rbd)) << 4);
   // rows past the matrix edge read as zero (buffer range check); they only
   // feed outputs that are never stored
   const int64_t rows_a = m - tm * BM < BM ? m - tm * BM : BM;
   const int64_t rows_b = n - tn * BN < BN ? n - tn * BN : BN;
 
-  v16f acc[2][2];
+  v16f acc[2][NB];
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b) acc[a][b] = v16f{};
+    for (int b = 0; b < NB; ++b) acc[a][b] = v16f{};
 
   // The three products run as segments of at most kSeg stages: every fp32
   // accumulator sum between two reductions stays below 2^24 (at most
@@ -341,19 +355,19 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
     return stage_rsrc(pb, kPlanes, n, tn * BN, kSched[mod].plane_b[p], sbeg + G - p * nstage, nb);
   };
   const float fm = (float)sc.m, finv = 1.0f / (float)sc.m;
-  if (total > 0) stage_load(ra(0), rb(0), lds_a0, lds_b0, voff, 0, wave);
+  if (total > 0) stage_load<NB>(ra(0), rb(0), lds_a0, lds_b0, voff, voffb, wave);
   for (int G = 0; G < total; G += 2) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     // after the very last stage the look-ahead load repeats it
-    stage_mma_dma(lds_a0, lds_b0, ra0, rb0, fh, acc, ra(G + 1 < total ? G + 1 : G),
-                  rb(G + 1 < total ? G + 1 : G), lds_a1, lds_b1, voff, 0, wave);
+    stage_mma_dma<NB>(lds_a0, lds_b0, ra0, rb0, fh, acc, ra(G + 1 < total ? G + 1 : G),
+                      rb(G + 1 < total ? G + 1 : G), lds_a1, lds_b1, voff, voffb, wave);
     carry(acc, G, nstage, nseg, mod, fm, finv);
     if (G + 1 >= total) break;
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    stage_mma_dma(lds_a1, lds_b1, ra0, rb0, fh, acc, ra(G + 2 < total ? G + 2 : G + 1),
-                  rb(G + 2 < total ? G + 2 : G + 1), lds_a0, lds_b0, voff, 0, wave);
+    stage_mma_dma<NB>(lds_a1, lds_b1, ra0, rb0, fh, acc, ra(G + 2 < total ? G + 2 : G + 1),
+                      rb(G + 2 < total ? G + 2 : G + 1), lds_a0, lds_b0, voff, voffb, wave);
     carry(acc, G + 1, nstage, nseg, mod, fm, finv);
   }
   __builtin_amdgcn_s_waitcnt(0);  // the repeated look-ahead load lands before the epilogue
@@ -367,8 +381,8 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const int col = wc * 64 + b * 32 + fr;
+    for (int b = 0; b < NB; ++b) {
+      const int col = wc * 32 * NB + b * 32 + fr;
       const int row0 = wr * 64 + a * 32 + 4 * fh;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
@@ -416,65 +430,60 @@ __device__ __forceinline__ int cmod_i32(int x, int m, double minv) {
   return 2 * r == m ? -r : r;
 }
 
-// One stage: four 32-byte K steps of 2 x 2 MFMAs; the next stage's 4 DMA
-// loads go among step 0's MFMAs, the fragment reads of step ks + 1 among
+// One stage: four 32-byte K steps of 2 x NB MFMAs; the next stage's 2 + NB
+// DMA loads go among step 0's MFMAs, the fragment reads of step ks + 1 among
 // step ks's.
+template <int NB>
 __device__ __forceinline__ void stage_mma_dma_i8(const int8_t* la, const int8_t* lb, int ra0,
-                                                 int rb0, int fh, v16i (&acc)[2][2],
+                                                 int rb0, int fh, v16i (&acc)[2][NB],
                                                  __amdgpu_buffer_rsrc_t ra,
                                                  __amdgpu_buffer_rsrc_t rb, int8_t* na, int8_t* nb,
-                                                 const int (&voff)[2], int k0, int wave) {
-  v4i af[4][2], bf[4][2];
-  k0 = __builtin_amdgcn_readfirstlane(k0);
+                                                 const int (&voff)[2], int voffb, int wave) {
+  v4i af[4][2], bf[4][NB];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks)
+  for (int ks = 0; ks < 4; ++ks) {
 #pragma unroll
-    for (int x = 0; x < 2; ++x) {
-      af[ks][x] = frag_i8(la, ra0 + 32 * x, ks, fh);
-      bf[ks][x] = frag_i8(lb, rb0 + 32 * x, ks, fh);
-    }
+    for (int x = 0; x < 2; ++x) af[ks][x] = frag_i8(la, ra0 + 32 * x, ks, fh);
+#pragma unroll
+    for (int x = 0; x < NB; ++x) bf[ks][x] = frag_i8(lb, rb0 + 32 * x, ks, fh);
+  }
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        if (ks == 0) {
-          const int i = a * 2 + b;  // DMA i of 4: (slab i/2, side i%2)
-          const int slab = (wave * 2 + (i >> 1)) * 1024;
-          if (i & 1)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr)(nb + slab), 16, voff[i >> 1], k0, 0, 0);
-          else
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr)(na + slab), 16, voff[i >> 1], k0, 0, 0);
-        }
+      for (int b = 0; b < NB; ++b) {
+        const int j = ks * 2 * NB + a * NB + b;  // MFMA number in issue order
+        if (j < 2 + NB) stage_dma<NB>(j, ra, rb, na, nb, voff, voffb, wave);
         acc[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[ks][a], bf[ks][b], acc[a][b], 0, 0, 0);
       }
-  __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+  __builtin_amdgcn_sched_group_barrier(0x100, 2 + NB, 0);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < 2 + NB; ++i) {
     __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
   }
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
+  for (int i = 0; i < 2 * (2 + NB); ++i) {
     __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
   }
-  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+  __builtin_amdgcn_sched_group_barrier(0x008, 8 * NB - 3 * (2 + NB) > 0 ? 8 * NB - 3 * (2 + NB) : 0, 0);
 }
 
-template <typename OT>
+template <typename OT, int NB>
 __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, int64_t n,
                                                                     int64_t kp,
                                                                     const int8_t* __restrict__ pa,
                                                                     const int8_t* __restrict__ pb,
                                                                     OT* __restrict__ cres,
                                                                     int splits) {
+  constexpr int BN = kBN<NB>;
   __shared__ __attribute__((aligned(1024))) int8_t lds_a0[kTile];
-  __shared__ __attribute__((aligned(1024))) int8_t lds_b0[kTile];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_b0[BN * BK];
   __shared__ __attribute__((aligned(1024))) int8_t lds_a1[kTile];
-  __shared__ __attribute__((aligned(1024))) int8_t lds_b1[kTile];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_b1[BN * BK];
   const int64_t tiles_m = (m + BM - 1) / BM, tiles_n = (n + BN - 1) / BN;
   const int split = (int)(blockIdx.x % (unsigned)splits);
   int mod;
@@ -488,13 +497,15 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wr = wave >> 2, wc = wave & 3;
   const int fr = lane & 31, fh = lane >> 5;
-  const int ra0 = wr * 64 + fr, rb0 = wc * 64 + fr;
+  const int ra0 = wr * 64 + fr, rb0 = wc * 32 * NB + fr;
   int voff[2];
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int r = wave * 16 + i * 8 + (lane >> 3);
     voff[i] = r * BK + (((lane & 7) ^ swz(r)) << 4);
   }
+  const int rbd = wave * 8 + (lane >> 3);  // B slab rows when NB = 1
+  const int voffb = rbd * BK + (((lane & 7) ^ swz(rbd)) << 4);
   const int64_t rows_a = m - tm * BM < BM ? m - tm * BM : BM;
   const int64_t rows_b = n - tn * BN < BN ? n - tn * BN : BN;
   const int na = __builtin_amdgcn_readfirstlane((int)(rows_a * BK));
@@ -502,18 +513,18 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
   auto ra = [&](int st) { return stage_rsrc(pa, kRA, m, tm * BM, mod, st, na); };
   auto rb = [&](int st) { return stage_rsrc(pb, kRA, n, tn * BN, mod, st, nb); };
 
-  v16i acc[2][2];
+  v16i acc[2][NB];
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b) acc[a][b] = v16i{};
+    for (int b = 0; b < NB; ++b) acc[a][b] = v16i{};
 
   const int nstage_all = (int)(kp / BK);
   const int sbeg = (int)((int64_t)nstage_all * split / splits);
   const int nstage = (int)((int64_t)nstage_all * (split + 1) / splits);  // one past the last
   for (int s0 = sbeg; s0 < nstage; s0 += kSegA) {
     const int s1 = s0 + kSegA < nstage ? s0 + kSegA : nstage;
-    stage_load(ra(s0), rb(s0), lds_a0, lds_b0, voff, 0, wave);
+    stage_load<NB>(ra(s0), rb(s0), lds_a0, lds_b0, voff, voffb, wave);
     for (int s = s0; s < s1; s += 2) {
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
@@ -521,14 +532,16 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
       // the panel's last stage it repeats that stage (as above)
       {
         const int nx = s + 1 < nstage ? s + 1 : s;
-        stage_mma_dma_i8(lds_a0, lds_b0, ra0, rb0, fh, acc, ra(nx), rb(nx), lds_a1, lds_b1, voff, 0, wave);
+        stage_mma_dma_i8<NB>(lds_a0, lds_b0, ra0, rb0, fh, acc, ra(nx), rb(nx), lds_a1, lds_b1, voff, voffb,
+                             wave);
       }
       if (s + 1 >= s1) break;
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
       {
         const int nx = s + 2 < nstage ? s + 2 : s + 1;
-        stage_mma_dma_i8(lds_a1, lds_b1, ra0, rb0, fh, acc, ra(nx), rb(nx), lds_a0, lds_b0, voff, 0, wave);
+        stage_mma_dma_i8<NB>(lds_a1, lds_b1, ra0, rb0, fh, acc, ra(nx), rb(nx), lds_a0, lds_b0, voff, voffb,
+                             wave);
       }
     }
     __builtin_amdgcn_s_waitcnt(0);
@@ -537,7 +550,7 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
 #pragma unroll
       for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
+        for (int b = 0; b < NB; ++b)
 #pragma unroll
           for (int v = 0; v < 16; ++v) acc[a][b][v] = cmod_i32(acc[a][b][v], mm, minv);
     }
@@ -550,8 +563,8 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const int col = wc * 64 + b * 32 + fr;
+    for (int b = 0; b < NB; ++b) {
+      const int col = wc * 32 * NB + b * 32 + fr;
       const int row0 = wr * 64 + a * 32 + 4 * fh;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
@@ -594,15 +607,26 @@ hipError_t launch_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* pa, const
   const int nstage = (int)(kp / BK);
   if (splits < 1 || splits > (nstage > 1 ? nstage : 1) || (splits > 1 && !part))
     return hipErrorInvalidValue;
-  const int64_t blocks = (int64_t)(BYTES ? kRA : kR) * ((m + BM - 1) / BM) * ((n + BN - 1) / BN);
+  const bool narrow = n <= kBN<1>;
+  const int64_t bn = narrow ? kBN<1> : kBN<2>;
+  const int64_t blocks = (int64_t)(BYTES ? kRA : kR) * ((m + BM - 1) / BM) * ((n + bn - 1) / bn);
   OT* dst = splits > 1 ? part : cres;
   const dim3 grid((unsigned)(blocks * splits));
-  if constexpr (BYTES)
-    hipLaunchKernelGGL(residue_gemm_bytes_kernel<OT>, grid, dim3(1024), 0, stream, m, n, kp, pa, pb,
-                       dst, splits);
-  else
-    hipLaunchKernelGGL(residue_gemm_kernel<OT>, grid, dim3(1024), 0, stream, m, n, kp, pa, pb, dst,
-                       splits);
+  if constexpr (BYTES) {
+    if (narrow)
+      hipLaunchKernelGGL((residue_gemm_bytes_kernel<OT, 1>), grid, dim3(1024), 0, stream, m, n, kp, pa,
+                         pb, dst, splits);
+    else
+      hipLaunchKernelGGL((residue_gemm_bytes_kernel<OT, 2>), grid, dim3(1024), 0, stream, m, n, kp, pa,
+                         pb, dst, splits);
+  } else {
+    if (narrow)
+      hipLaunchKernelGGL((residue_gemm_kernel<OT, 1>), grid, dim3(1024), 0, stream, m, n, kp, pa, pb,
+                         dst, splits);
+    else
+      hipLaunchKernelGGL((residue_gemm_kernel<OT, 2>), grid, dim3(1024), 0, stream, m, n, kp, pa, pb,
+                         dst, splits);
+  }
   if (splits > 1) {
     const int64_t mn = m * n;
     hipLaunchKernelGGL((reduce_splits_kernel<BYTES, OT>),
@@ -620,7 +644,8 @@ int residue_gemm_splits(int set, int64_t m, int64_t n, int64_t kp) {
   // per block (4 for the single-product int8 kernel)
   if (m <= 0 || n <= 0) return 1;
   const bool bytes = set == kSetBytes;
-  const int64_t blocks = (int64_t)(bytes ? kRA : kR) * ((m + BM - 1) / BM) * ((n + BN - 1) / BN);
+  const int64_t bn = n <= kBN<1> ? kBN<1> : kBN<2>;
+  const int64_t blocks = (int64_t)(bytes ? kRA : kR) * ((m + BM - 1) / BM) * ((n + bn - 1) / bn);
   const int64_t nstage = kp / BK;
   if (blocks >= 512) return 1;
   int64_t s = (1024 + blocks - 1) / blocks;

@@ -370,3 +370,21 @@ def test_dgemm_split_k_matches_oracle(m, n, k, seed):
     C = gpu_dgemm(A, B)
     r = oracle.dgemm(A, B, want_planes=False)
     assert_bits_equal(C.cpu().numpy(), r.C, "C")
+
+
+@pytest.mark.parametrize("m,n,k,seed", [(300, 128, 700, 84), (300, 129, 700, 85), (513, 96, 2000, 86),
+                                        (260, 1, 129, 87)])
+def test_dgemm_narrow_tiles_match_oracle(m, n, k, seed):
+    """At most 128 columns use the 256 x 128 tile (n = 129 the 256 x 256 one)."""
+    log(f"dgemm narrow m={m} n={n} k={k}")
+    A = workloads.random_matrix(m, k, 1.0, seed)
+    B = workloads.random_matrix(k, n, 1.0, seed + 1)
+    C = gpu_dgemm(A, B)
+    r = oracle.dgemm(A, B, want_planes=False)
+    assert_bits_equal(C.cpu().numpy(), r.C, "C")
+    import torch
+    planesA, _ = gpu_deconstruct(A, 0)
+    planesB, _ = gpu_deconstruct(B, 1)
+    Cres = oz.ozaki25_residue_gemm(m, n, k, planesA, planesB)
+    torch.cuda.synchronize()
+    assert_int_equal(Cres.cpu().numpy(), r.Cres, "per-modulus products")

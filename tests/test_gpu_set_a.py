@@ -317,3 +317,13 @@ def test_dgemm_split_k_matches_oracle(m, n, k, seed):
     C = gpu_dgemm(A, B, set=SET)
     r = oracle.dgemm(A, B, want_planes=False, set=OSET)
     assert_bits_equal(C.cpu().numpy(), r.C, "C")
+
+
+@pytest.mark.parametrize("m,n,k,seed", [(300, 128, 700, 94), (300, 129, 700, 95), (513, 96, 2000, 96)])
+def test_dgemm_narrow_tiles_match_oracle(m, n, k, seed):
+    log(f"[A15] dgemm narrow m={m} n={n} k={k}")
+    A = workloads.random_matrix(m, k, 1.0, seed)
+    B = workloads.random_matrix(k, n, 1.0, seed + 1)
+    C = gpu_dgemm(A, B, set=SET)
+    r = oracle.dgemm(A, B, want_planes=False, set=OSET)
+    assert_bits_equal(C.cpu().numpy(), r.C, "C")
