@@ -12,7 +12,8 @@ products) on the same inputs and reports it under "all_byte_set".
 ``--moduli a15`` makes the all-byte set the headline instead; ``--quantiser
 tz`` times the truncating quantiser.  Each set also reports "stored_planes":
 the per-call time of ozaki25_dgemm_planes on planes made once (storage mode
-P).  Prints one JSON line.
+P); the headline set also "graph_replay": one call captured in a HIP graph
+and replayed.  Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload square] [--moduli s12|a15]
 """
@@ -155,6 +156,33 @@ def time_planes(oz, torch, w, Ad, Bd, Cd, cfg, steps, quant):
     return ms
 
 
+def time_graph(oz, torch, w, Ad, Bd, Cd, cfg, steps, quant):
+    """ms per replay of a HIP graph that captured one ozaki25_dgemm_ex call
+    (caller workspace: the call enqueues kernels only)."""
+    ws = torch.empty(oz.ozaki25_dgemm_workspace_size(w.m, w.n, w.k, cfg["id"]), dtype=torch.uint8,
+                     device=Ad.device)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        oz.ozaki25_dgemm_ex(Ad, Bd, Cd, subtract=w.subtract, workspace=ws, set=cfg["id"], quantiser=quant)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        oz.ozaki25_dgemm_ex(Ad, Bd, Cd, subtract=w.subtract, workspace=ws, set=cfg["id"], quantiser=quant)
+    g.replay()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        g.replay()
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / steps
+    del g, ws
+    return ms
+
+
 def rates(w, cfg, ms, stages):
     scan_ms, dec_ms, gemm_ms, rec_ms = stages
     elems = w.m * w.k + w.k * w.n
@@ -265,6 +293,10 @@ def main():
         Cd.copy_(C0d)
     log("[bench] stored planes (mode P)")
     pms = time_planes(oz, torch, w, Ad, Bd, Cd, cfg, args.steps, quant)
+    if C0d is not None:
+        Cd.copy_(C0d)
+    log("[bench] graph replay")
+    gms = time_graph(oz, torch, w, Ad, Bd, Cd, cfg, args.steps, quant)
 
     native = None
     if not args.no_native and not w.subtract and w.m * w.n * w.k <= 8192 ** 3:
@@ -319,6 +351,9 @@ def main():
                           "unit": "TFLOPS",
                           "note": "storage mode P: ozaki25_dgemm_planes on planes deconstructed once "
                                   "(residue products + reconstruction per call)"},
+        "graph_replay": {"ms_per_call": round(gms, 4), "value": round(w.flops / (gms * 1e-3) / 1e12, 3),
+                         "unit": "TFLOPS",
+                         "note": "one ozaki25_dgemm_ex call captured in a HIP graph, replayed"},
         "native_fp64_tflops": round(native, 2) if native else None,
         "native_fp64_peak_tflops": FP64_PEAK_TFLOPS,
         "paper_context": "modelled Rubin projections (no measurement in the paper): 473 TFLOPS roof, 182-235 TFLOPS floors",
