@@ -81,7 +81,7 @@ size_t products_bytes(int64_t m, int64_t n, int64_t k, ozaki25_moduli_set set, i
 }
 
 // planes of A and B, exponents, and the residue products: int16 for the
-// published set (|c| <= 544), int8 for the all-byte set (|c| <= 128)
+// published set (|c| <= 0.51 m <= 556), int8 for the all-byte set (|c| <= 128)
 Workspace layout(int64_t m, int64_t n, int64_t k, ozaki25_moduli_set set) {
   Workspace w;
   const int64_t kp = k_pad(k);

@@ -36,6 +36,9 @@ hipError_t launch_residue_gemm_i32(int64_t m, int64_t n, int64_t kp, const int8_
 // The fused path's compact products may split the k range (split-k) when
 // the output tiles are too few to fill the chip: `splits` from
 // residue_gemm_splits, and a partial buffer of splits * r * m * n elements.
+// Compact int16 products (published set) are the true residues divided by
+// compact_scale(i) mod m_i, reduced to |c| <= 0.51 m_i but not centred;
+// launch_reconstruct_i16 takes exactly these.
 constexpr int kMaxSplits = 64;
 int residue_gemm_splits(int set, int64_t m, int64_t n, int64_t kp);
 hipError_t launch_residue_gemm_i16(int64_t m, int64_t n, int64_t kp, const int8_t* pa,

@@ -69,6 +69,12 @@ constexpr int product_coef(int i, int p) {
 constexpr int product_plane_a(int i, int p) { return root_of(i) ? (p == 2 ? 1 : 0) : p; }
 constexpr int product_plane_b(int i, int p) { return root_of(i) ? (p == 1 ? 1 : 0) : p; }
 
+// The residue GEMM's compact (int16) outputs leave out the weight of the
+// last limb product it issues: a stored residue times compact_scale(i) is
+// the true one, mod m_i.  Squares end on the weight-1 product, nonsquares on
+// the weight-16 one.
+constexpr int compact_scale(int i) { return root_of(i) ? 1 : 16; }
+
 static_assert(plane_base(kR) == kPlanes, "30 stored planes for the published set");
 
 // ---- all-byte set (Sec. 5.1, candidate A): 256 first, then fourteen odd

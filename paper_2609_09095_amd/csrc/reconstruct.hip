@@ -7,8 +7,11 @@
 // Integer work per output, all exact:
 //  - centred digits in one reduction each: v_j = (c_j w_j - sum_{l<j} v_l
 //    R_lj) mod m_j with w_j and R_lj = (m_0..m_{l-1}) w_j mod m_j centred
-//    compile-time constants.  Every term is below 545^2 in magnitude, the sum
-//    of at most twelve below 2^22, so for odd m_j the FP32 quotient
+//    compile-time constants.  The residue GEMM's compact int16 residues c'_j
+//    are the true ones divided by a per-modulus factor f_j and reduced to
+//    |c'_j| <= 0.51 m_j: the term is then c'_j (f_j w_j mod m_j).  Every
+//    term is below 567 * 545 in magnitude, the sum of at most twelve below
+//    2^22, so for odd m_j the FP32 quotient
 //    rint(s / m_j) errs by less than 1/(2 m_j), the least distance of s / m_j
 //    from a half integer: one rint and one multiply-add give the centred
 //    digit.  m_j = 1024 takes the low ten bits.
@@ -53,12 +56,18 @@ inline constexpr int kGarnerWeight =
     centred_const((int64_t)radix_mod(L, J) * garner_w(J) % kModulus[J], kModulus[J]);
 template <int J>
 inline constexpr int kGarnerW = centred_const(garner_w(J), kModulus[J]);
+// the same for the residue GEMM's compact outputs, which leave out the
+// factor compact_scale(j): w_j times it
+template <int J>
+inline constexpr int kGarnerWCompact =
+    centred_const((int64_t)garner_w(J) * compact_scale(J) % kModulus[J], kModulus[J]);
 
 constexpr bool garner_sums_fit() {
-  // |c_j w_j| + sum_{l<j} |v_l R_lj| < 2^22 with |c|, |v| <= m/2
+  // |c_j w_j| + sum_{l<j} |v_l R_lj| < 2^22 with |v| <= m/2 and |c| <= 0.51 m
+  // (compact residues are reduced but not wrapped into the centred range)
   for (int j = 0; j < kR; ++j) {
     const int64_t mj = kModulus[j];
-    int64_t s = (mj / 2 + 1) * (mj / 2 + 1);
+    int64_t s = (mj / 2 + mj / 50 + 1) * (mj / 2 + 1);
     for (int l = 0; l < j; ++l) s += (kModulus[l] / 2 + 1) * (mj / 2 + 1);
     if (s >= (int64_t)1 << 22) return false;
   }
@@ -66,11 +75,11 @@ constexpr bool garner_sums_fit() {
 }
 static_assert(garner_sums_fit(), "Garner sums stay below 2^22");
 
-template <int J>
+template <int J, bool COMPACT>
 __device__ __forceinline__ void garner_digit(const int (&c)[kR], int (&v)[kR]) {
   constexpr int M = kModulus[J];
   // every factor is below 2^11 in magnitude: 24-bit multiplies are exact
-  int s = __mul24(c[J], kGarnerW<J>);
+  int s = __mul24(c[J], COMPACT ? kGarnerWCompact<J> : kGarnerW<J>);
   [&]<int... L>(std::integer_sequence<int, L...>) {
     ((s -= __mul24(v[L], kGarnerWeight<L, J>)), ...);
   }(std::make_integer_sequence<int, J>{});
@@ -154,7 +163,7 @@ __device__ __forceinline__ double reconstruct_one(const RT* rowq, int64_t mn, in
 #pragma unroll
   for (int q = 0; q < kR; ++q) c[q] = load_residue(rowq + q * mn, n, col);
   [&]<int... J>(std::integer_sequence<int, J...>) {
-    (garner_digit<J>(c, v), ...);
+    (garner_digit<J, sizeof(RT) == 2>(c, v), ...);
   }(std::make_integer_sequence<int, kR>{});
   const int64_t xl = half_value<0>(v);       // |xl| < P
   int64_t xh = half_value<kSplit>(v);        // |xh| <= (Q - 1) / 2

@@ -117,6 +117,12 @@ constexpr bool schedule_is_exact() {
   return true;
 }
 static_assert(schedule_is_exact(), "accumulator carry schedule reproduces the epilogue weights");
+constexpr bool compact_scale_matches() {
+  for (int i = 0; i < kR; ++i)
+    if (issue_weight(i, 2) != compact_scale(i)) return false;
+  return true;
+}
+static_assert(compact_scale_matches(), "compact outputs leave out the last product's weight");
 
 __constant__ ModSched kSched[kR] = {make_sched(0), make_sched(1), make_sched(2),  make_sched(3),
                                     make_sched(4), make_sched(5), make_sched(6),  make_sched(7),
@@ -256,28 +262,45 @@ __device__ __forceinline__ void stage_mma_dma(const int8_t* la, const int8_t* lb
   __builtin_amdgcn_sched_group_barrier(0x008, 4 * NB - (2 + NB), 0);
 }
 
-// After global stage G (product G / nstage, stage G % nstage): at the end of
-// a segment, a plain reduction (when the product spans several segments);
-// at the end of a product, its multiplier (squares skip it between their two
-// weight-s products while each fits one segment; the last product always
-// applies its weight).
-template <int NB>
+// After global stage G (product G / nstage, stage G % nstage):
+//  - end of a segment inside a product: a plain reduction;
+//  - end of product 0 or 1: reduce, then times the product's multiplier
+//    (no second reduction: |result| <= 0.51 m (m - 1) < 2^20 and the next
+//    segment adds at most 484 * 128 * kSeg, still below 2^24); squares skip
+//    it between their two weight-s products while each fits one segment;
+//  - end of product 2: reduce (|result| <= 0.51 m); with FINAL_W (true
+//    residues) times the last weight and reduce again.  Without FINAL_W the
+//    stored residue is the true one divided by that weight (compact outputs:
+//    reconstruction folds the weight into its Garner constants).
+// With FINAL_W every carry ends with a second reduction (harmless before the
+// last product); the compact form is one reduction and one multiply.
+template <int NB, bool FINAL_W>
 __device__ __forceinline__ void carry(v16f (&acc)[2][NB], int G, int nstage, int nseg, int mod,
                                       float fm, float finv) {
   const int p = G / nstage, s = G - p * nstage;
   const bool prod_end = s + 1 == nstage;
   if (!prod_end && (s + 1) % kSeg != 0) return;
-  const int mult = prod_end ? kSched[mod].mult[p] : 1;
-  if (p == 2 || mult != 1 || nseg > 1) {
-    const float fmult = (float)mult;
+  const int mult = prod_end && (p < 2 || FINAL_W) ? kSched[mod].mult[p] : 1;
+  if (mult == 1 && p < 2 && prod_end && nseg == 1) return;
+  const float fmult = (float)mult;
+  // one branch-free form for every carry (separate forms per case cost
+  // registers at their join inside the stage loop)
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < 2; ++a)
 #pragma unroll
-      for (int b = 0; b < NB; ++b)
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) acc[a][b][v] = mulmod_f(acc[a][b][v], fmult, fm, finv);
-  }
+      for (int v = 0; v < 16; ++v) {
+        float x = reduce_f(acc[a][b][v], fm, finv) * fmult;
+        if constexpr (FINAL_W) x = reduce_f(x, fm, finv);
+        acc[a][b][v] = x;
+      }
 }
+// the carried value times a multiplier plus one segment stays exact in fp32
+static_assert((int64_t)(kModulus[0] / 2 + kModulus[0] / 50 + 1) * (kModulus[0] - 1) + 484LL * BK * kSeg <
+                  (1LL << 24),
+              "carry bound");
+static_assert(kModulus[0] >= kModulus[kR - 1] && kModulus[0] >= kModulus[1], "largest modulus first");
 
 // splits > 1 (split-k): consecutive blocks take the same tile's stage ranges,
 // and block (tile, split) writes its centred partial product to the split's
@@ -362,13 +385,13 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
     // after the very last stage the look-ahead load repeats it
     stage_mma_dma<NB>(lds_a0, lds_b0, ra0, rb0, fh, acc, ra(G + 1 < total ? G + 1 : G),
                       rb(G + 1 < total ? G + 1 : G), lds_a1, lds_b1, voff, voffb, wave);
-    carry(acc, G, nstage, nseg, mod, fm, finv);
+    carry<NB, sizeof(OT) == 4>(acc, G, nstage, nseg, mod, fm, finv);
     if (G + 1 >= total) break;
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     stage_mma_dma<NB>(lds_a1, lds_b1, ra0, rb0, fh, acc, ra(G + 2 < total ? G + 2 : G + 1),
                       rb(G + 2 < total ? G + 2 : G + 1), lds_a0, lds_b0, voff, voffb, wave);
-    carry(acc, G + 1, nstage, nseg, mod, fm, finv);
+    carry<NB, sizeof(OT) == 4>(acc, G + 1, nstage, nseg, mod, fm, finv);
   }
   __builtin_amdgcn_s_waitcnt(0);  // the repeated look-ahead load lands before the epilogue
 
@@ -387,9 +410,10 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int row = row0 + 8 * (v >> 2) + (v & 3);
-        // the final carry leaves |r| <= 0.51 m: wrap into [-(m/2), (m-1)/2]
+        // the final carry leaves |r| <= 0.51 m: true residues are wrapped
+        // into [-(m/2), (m-1)/2]; compact ones are stored as they stand
         const int r = (int)acc[a][b][v];
-        const int c = r > sc.hi ? r - sc.m : (r < -(sc.m >> 1) ? r + sc.m : r);
+        const int c = sizeof(OT) == 4 ? (r > sc.hi ? r - sc.m : (r < -(sc.m >> 1) ? r + sc.m : r)) : r;
         if (row < rows_left && col < cols_left) out[row * nn + col] = (OT)c;
       }
     }
@@ -422,12 +446,15 @@ __device__ __forceinline__ v4i frag_i8(const int8_t* base, int r, int ks, int fh
 // |x| < 2^31, so the FP64 quotient x RN(1/m) is within 2^-21 / m of x / m,
 // far closer than the 1/(2m) that separates x / m from a half integer for
 // odd m; rint gives the nearest quotient and the FMA the exact remainder.
-// For m = 256 the quotient is exact and the tie +128 maps to -128.
+// For m = 256 the quotient is exact and the tie +128 maps to -128 (FOLD; an
+// int8 store of +128 gives -128 by itself, and a partial reduction needs
+// only |r| <= m/2).
+template <bool FOLD>
 __device__ __forceinline__ int cmod_i32(int x, int m, double minv) {
   const double xd = (double)x;
   const double q = __builtin_rint(xd * minv);
   const int r = (int)__builtin_fma(-q, (double)m, xd);
-  return 2 * r == m ? -r : r;
+  return FOLD && 2 * r == m ? -r : r;
 }
 
 // One stage: four 32-byte K steps of 2 x NB MFMAs; the next stage's 2 + NB
@@ -552,7 +579,7 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
 #pragma unroll
         for (int b = 0; b < NB; ++b)
 #pragma unroll
-          for (int v = 0; v < 16; ++v) acc[a][b][v] = cmod_i32(acc[a][b][v], mm, minv);
+          for (int v = 0; v < 16; ++v) acc[a][b][v] = cmod_i32<false>(acc[a][b][v], mm, minv);
     }
   }
 
@@ -569,7 +596,7 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int row = row0 + 8 * (v >> 2) + (v & 3);
-        const int c = cmod_i32(acc[a][b][v], mm, minv);
+        const int c = cmod_i32<sizeof(OT) == 4>(acc[a][b][v], mm, minv);
         if (row < rows_left && col < cols_left) out[row * nn + col] = (OT)c;
       }
     }

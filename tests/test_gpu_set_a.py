@@ -238,7 +238,8 @@ def test_reconstruct_exact_ties():
 @pytest.mark.parametrize("m,n,k,s,seed", [(64, 64, 64, 0.5, 1), (1, 1, 1, 1.0, 2), (3, 5, 7, 1.0, 3),
                                           (130, 129, 65, 2.0, 4), (257, 1, 300, 1.0, 5),
                                           (1, 300, 257, 1.0, 6), (200, 190, 1000, 4.0, 7),
-                                          (70, 260, 8192, 1.0, 8)])
+                                          (70, 260, 8192, 1.0, 8), (300, 272, 200, 1.0, 9),
+                                          (70, 528, 130, 2.0, 10), (300, 112, 150, 1.0, 11)])
 def test_dgemm_matches_oracle(m, n, k, s, seed):
     log(f"[A15] dgemm m={m} n={n} k={k} s={s}")
     A = workloads.random_matrix(m, k, s, seed)
