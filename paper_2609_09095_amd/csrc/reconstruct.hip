@@ -75,20 +75,52 @@ constexpr bool garner_sums_fit() {
 }
 static_assert(garner_sums_fit(), "Garner sums stay below 2^22");
 
+// The sum over earlier digits runs on v_dot2_i32_i16, two terms per
+// instruction: digits and weights are centred residues, |.| <= 544, so they
+// fit int16.  Word Q of the weights of digit J holds -R_lJ for l = 2Q, 2Q+1
+// (0 for l >= J); word Q of the digits holds v_2Q (low half) and v_2Q+1.
+constexpr uint32_t garner_pack(int q, int j) {
+  uint32_t w = 0;
+  for (int i = 0; i < 2; ++i) {
+    const int l = 2 * q + i;
+    if (l < j) {
+      const int r = centred_const((int64_t)radix_mod(l, j) * garner_w(j) % kModulus[j], kModulus[j]);
+      w |= (uint32_t)(-r & 0xffff) << (16 * i);
+    }
+  }
+  return w;
+}
+template <int Q, int J>
+inline constexpr int kGarnerPack = (int)garner_pack(Q, J);
+static_assert(kModulus[0] / 2 < 32767, "centred weights and digits fit int16");
+
+typedef short v2s __attribute__((ext_vector_type(2)));
+
+// digit J from the residue c_J and the packed earlier digits
 template <int J, bool COMPACT>
-__device__ __forceinline__ void garner_digit(const int (&c)[kR], int (&v)[kR]) {
+__device__ __forceinline__ void garner_digit(const int (&c)[kR], int (&v)[kR], uint32_t (&packed)[kR / 2]) {
   constexpr int M = kModulus[J];
   // every factor is below 2^11 in magnitude: 24-bit multiplies are exact
   int s = __mul24(c[J], COMPACT ? kGarnerWCompact<J> : kGarnerW<J>);
-  [&]<int... L>(std::integer_sequence<int, L...>) {
-    ((s -= __mul24(v[L], kGarnerWeight<L, J>)), ...);
-  }(std::make_integer_sequence<int, J>{});
+  [&]<int... Q>(std::integer_sequence<int, Q...>) {
+    ((s = __builtin_amdgcn_sdot2(__builtin_bit_cast(v2s, packed[Q]),
+                                 __builtin_bit_cast(v2s, kGarnerPack<Q, J>), s, false)),
+     ...);
+  }(std::make_integer_sequence<int, (J + 1) / 2>{});
+  int d;
   if constexpr (M == 1024) {
-    v[J] = ((s + 512) & 1023) - 512;
+    d = ((s + 512) & 1023) - 512;
   } else {
     const int q = (int)__builtin_rintf((float)s * (1.0f / M));
-    v[J] = s - q * M;
+    d = s - q * M;
   }
+  v[J] = d;
+  // an even digit opens its word (the high half's weight is 0 until the
+  // odd digit fills it); an odd one completes it
+  if constexpr (J % 2 == 0)
+    packed[J / 2] = (uint32_t)d;
+  else
+    packed[J / 2] = (packed[J / 2] & 0xffffu) | ((uint32_t)d << 16);
 }
 
 // Balanced half sum_{j in [A, A+6)} v_j prod_{A <= l < j} m_l: digit pairs in
@@ -160,10 +192,11 @@ __device__ __forceinline__ double reconstruct_one(const RT* rowq, int64_t mn, in
                                                   int sb) {
   if (sa == INT32_MIN || sb == INT32_MIN) return __builtin_nan("");
   int c[kR], v[kR];
+  uint32_t packed[kR / 2];
 #pragma unroll
   for (int q = 0; q < kR; ++q) c[q] = load_residue(rowq + q * mn, n, col);
   [&]<int... J>(std::integer_sequence<int, J...>) {
-    (garner_digit<J, sizeof(RT) == 2>(c, v), ...);
+    (garner_digit<J, sizeof(RT) == 2>(c, v, packed), ...);
   }(std::make_integer_sequence<int, kR>{});
   const int64_t xl = half_value<0>(v);       // |xl| < P
   int64_t xh = half_value<kSplit>(v);        // |xh| <= (Q - 1) / 2
