@@ -302,6 +302,61 @@ static_assert((int64_t)(kModulus[0] / 2 + kModulus[0] / 50 + 1) * (kModulus[0] -
               "carry bound");
 static_assert(kModulus[0] >= kModulus[kR - 1] && kModulus[0] >= kModulus[1], "largest modulus first");
 
+// Output stores through a global (not generic) pointer; NT marks them
+// streaming (measured: the FP8 kernel gains with it, the int8 one without).
+template <bool NT, typename OT>
+__device__ __forceinline__ void store_out(OT* p, OT v) {
+  auto* g = (__attribute__((address_space(1))) OT*)p;
+  if constexpr (NT)
+    __builtin_nontemporal_store(v, g);
+  else
+    *g = v;
+}
+
+// The wave's 2 x NB blocks of outputs (value(a, b, v) of accumulator v of
+// block (a, b)); 32x32 MFMA result layout: lane holds column lane%32 and
+// rows 8*(v/4) + 4*(lane/32) + v%4 of its block.  Whole tiles of the compact
+// outputs take 32-bit byte offsets from the tile's scalar base (row stride
+// times a constant per value: one add per store, no per-value bounds test;
+// offsets below 256 n size <= 2^32); edge tiles and int32 outputs test every
+// value and use 32-bit element offsets (256 n < 2^31).
+template <bool NT, typename OT, int NB, typename F>
+__device__ __forceinline__ void store_tile(OT* out, int nn, int rows_left, int cols_left, int wr,
+                                           int wc, int fr, int fh, F&& value) {
+  constexpr int BN = kBN<NB>;
+  if constexpr (sizeof(OT) <= 2) {
+    if (rows_left >= BM && cols_left >= BN) {
+      char* base = (char*)out;
+      const uint32_t stride = (uint32_t)nn * (uint32_t)sizeof(OT);
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+          const uint32_t off0 = (uint32_t)(wr * 64 + a * 32 + 4 * fh) * stride +
+                                (uint32_t)((wc * 32 * NB + b * 32 + fr) * (int)sizeof(OT));
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const uint32_t off = off0 + (uint32_t)(8 * (v >> 2) + (v & 3)) * stride;
+            store_out<NT>((OT*)(base + off), (OT)value(a, b, v));
+          }
+        }
+      return;
+    }
+  }
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const int col = wc * 32 * NB + b * 32 + fr;
+      const int row0 = wr * 64 + a * 32 + 4 * fh;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = row0 + 8 * (v >> 2) + (v & 3);
+        if (row < rows_left && col < cols_left) store_out<NT>(out + row * nn + col, (OT)value(a, b, v));
+      }
+    }
+}
+
 // splits > 1 (split-k): consecutive blocks take the same tile's stage ranges,
 // and block (tile, split) writes its centred partial product to the split's
 // own [r][m][n] slice of cres; reduce_splits_kernel sums them mod m.
@@ -395,28 +450,17 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
   }
   __builtin_amdgcn_s_waitcnt(0);  // the repeated look-ahead load lands before the epilogue
 
-  // 32x32 MFMA result layout: lane holds column lane%32 and rows
-  // 8*(v/4) + 4*(lane/32) + v%4 of its 32x32 block.  Stores use the tile's
-  // scalar base and 32-bit element offsets (256 n < 2^31).
   OT* out = (OT*)uniform_ptr((const int8_t*)(cres + (int64_t)mod * m * n + tm * BM * n + tn * BN));
-  const int nn = (int)n;
-  const int rows_left = (int)(m - tm * BM), cols_left = (int)(n - tn * BN);
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      const int col = wc * 32 * NB + b * 32 + fr;
-      const int row0 = wr * 64 + a * 32 + 4 * fh;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = row0 + 8 * (v >> 2) + (v & 3);
-        // the final carry leaves |r| <= 0.51 m: true residues are wrapped
-        // into [-(m/2), (m-1)/2]; compact ones are stored as they stand
-        const int r = (int)acc[a][b][v];
-        const int c = sizeof(OT) == 4 ? (r > sc.hi ? r - sc.m : (r < -(sc.m >> 1) ? r + sc.m : r)) : r;
-        if (row < rows_left && col < cols_left) out[row * nn + col] = (OT)c;
-      }
-    }
+  store_tile<true, OT, NB>(out, (int)n, (int)(m - tm * BM), (int)(n - tn * BN), wr, wc, fr, fh,
+                           [&](int a, int b, int v) {
+                             // the final carry leaves |r| <= 0.51 m: true residues
+                             // are wrapped into [-(m/2), (m-1)/2]; compact ones are
+                             // stored as they stand
+                             const int r = (int)acc[a][b][v];
+                             return sizeof(OT) == 4
+                                        ? (r > sc.hi ? r - sc.m : (r < -(sc.m >> 1) ? r + sc.m : r))
+                                        : r;
+                           });
 }
 
 // ---- all-byte set (Sec. 5.1, candidate A) on int8 MFMA --------------------
@@ -583,23 +627,11 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
     }
   }
 
-  // result layout as in the FP8 kernel
   OT* out = (OT*)uniform_ptr((const int8_t*)(cres + (int64_t)mod * m * n + tm * BM * n + tn * BN));
-  const int nn = (int)n;
-  const int rows_left = (int)(m - tm * BM), cols_left = (int)(n - tn * BN);
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      const int col = wc * 32 * NB + b * 32 + fr;
-      const int row0 = wr * 64 + a * 32 + 4 * fh;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = row0 + 8 * (v >> 2) + (v & 3);
-        const int c = cmod_i32<sizeof(OT) == 4>(acc[a][b][v], mm, minv);
-        if (row < rows_left && col < cols_left) out[row * nn + col] = (OT)c;
-      }
-    }
+  store_tile<false, OT, NB>(out, (int)n, (int)(m - tm * BM), (int)(n - tn * BN), wr, wc, fr, fh,
+                            [&](int a, int b, int v) {
+                              return cmod_i32<sizeof(OT) == 4>(acc[a][b][v], mm, minv);
+                            });
 }
 
 // Sum of the splits' centred partial products, reduced to the centred
