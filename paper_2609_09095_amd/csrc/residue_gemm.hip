@@ -137,10 +137,6 @@ __device__ __forceinline__ float reduce_f(float x, float m, float minv) {
   const float q = __builtin_rintf(x * minv);
   return __builtin_fmaf(-q, m, x);
 }
-// acc * mult mod m: reduce, multiply (|.| <= 0.51 m * mult < 2^24, exact), reduce
-__device__ __forceinline__ float mulmod_f(float x, float mult, float m, float minv) {
-  return reduce_f(reduce_f(x, m, minv) * mult, m, minv);
-}
 
 __device__ __forceinline__ int swz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
 
@@ -148,17 +144,25 @@ __device__ __forceinline__ int swz(int row) { return (row & 7) ^ ((row >> 3) & 1
 // kGroupM = 2 tile rows.  Blocks are dealt round-robin over the 8 XCDs, so
 // the 32 blocks an XCD runs at a time cover 4 tile rows x 8 tile columns: 12
 // panels feed 32 tiles from its L2 (groups of 4 rows: 18 panels; 8 rows: 33).
-__device__ __forceinline__ void block_coords(int64_t id, int64_t tiles_m, int64_t tiles_n, int& mod,
+// Unsigned 32-bit arithmetic throughout: the grid has fewer than 2^32 blocks
+// (checked at launch), so every count here fits, and 32-bit divisions cost a
+// small fraction of 64-bit ones.
+__device__ __forceinline__ void block_coords(uint32_t id, uint32_t tiles_m, uint32_t tiles_n, int& mod,
                                              int64_t& tm, int64_t& tn) {
-  const int64_t per_mod = tiles_m * tiles_n;
-  mod = (int)(id / per_mod);
-  const int64_t t = id % per_mod;
-  const int64_t group = t / (kGroupM * tiles_n);
-  const int64_t first = group * kGroupM;
-  const int64_t gsz = tiles_m - first < kGroupM ? tiles_m - first : kGroupM;
-  const int64_t in = t % (kGroupM * tiles_n);
-  tm = first + in % gsz;
-  tn = in / gsz;
+  const uint32_t per_mod = tiles_m * tiles_n;
+  const uint32_t q = id / per_mod;
+  mod = (int)q;
+  const uint32_t t = id - q * per_mod;
+  const uint32_t gw = kGroupM * tiles_n;
+  const uint32_t group = t / gw;
+  const uint32_t first = group * kGroupM;
+  const uint32_t in = t - group * gw;
+  static_assert(kGroupM == 2, "groups of at most two tile rows");
+  const bool pair = tiles_m - first >= 2;  // a full group: tile rows alternate
+  // uniform values: pinned to scalar registers
+  mod = __builtin_amdgcn_readfirstlane(mod);
+  tm = __builtin_amdgcn_readfirstlane((int)(first + (pair ? (in & 1u) : 0u)));
+  tn = __builtin_amdgcn_readfirstlane((int)(pair ? in >> 1 : in));
 }
 
 using lds_ptr = __attribute__((address_space(3))) void*;
@@ -174,15 +178,10 @@ __device__ __forceinline__ const int8_t* uniform_ptr(const int8_t* p) {
 
 // Plane layout [k_pad/128][planes][rows][128]: K stage s of plane q of a
 // 256-row tile starting at row r0 is the contiguous piece
-// ((s * planes + q) * rows + r0) * 128.  A descriptor per stage (the stage
+// ((s * planes + q) * rows + r0) * 128, and consecutive stages of a plane
+// are planes * rows * 128 bytes apart.  A descriptor per stage (the stage
 // offset may exceed 32 bits); rows past the matrix edge fall outside its
 // range and read as zero.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t stage_rsrc(const int8_t* planes, int nplanes,
-                                                             int64_t rows, int64_t r0, int plane,
-                                                             int s, int nrec) {
-  const int8_t* p = uniform_ptr(planes + (((int64_t)s * nplanes + plane) * rows + r0) * BK);
-  return __builtin_amdgcn_make_buffer_rsrc((void*)p, (short)0, nrec, 0x00020000);
-}
 
 // One K stage: the wave's share of the A and B tiles (32 rows of each) goes
 // straight from global memory into LDS.  A load writes 1 KiB = 8 rows x
@@ -262,7 +261,7 @@ __device__ __forceinline__ void stage_mma_dma(const int8_t* la, const int8_t* lb
   __builtin_amdgcn_sched_group_barrier(0x008, 4 * NB - (2 + NB), 0);
 }
 
-// After global stage G (product G / nstage, stage G % nstage):
+// After stage s of product p:
 //  - end of a segment inside a product: a plain reduction;
 //  - end of product 0 or 1: reduce, then times the product's multiplier
 //    (no second reduction: |result| <= 0.51 m (m - 1) < 2^20 and the next
@@ -275,11 +274,11 @@ __device__ __forceinline__ void stage_mma_dma(const int8_t* la, const int8_t* lb
 // With FINAL_W every carry ends with a second reduction (harmless before the
 // last product); the compact form is one reduction and one multiply.
 template <int NB, bool FINAL_W>
-__device__ __forceinline__ void carry(v16f (&acc)[2][NB], int G, int nstage, int nseg, int mod,
+__device__ __forceinline__ void carry(v16f (&acc)[2][NB], int p, int s, int nstage, int nseg, int mod,
                                       float fm, float finv) {
-  const int p = G / nstage, s = G - p * nstage;
+  static_assert((kSeg & (kSeg - 1)) == 0, "segment length is a power of two");
   const bool prod_end = s + 1 == nstage;
-  if (!prod_end && (s + 1) % kSeg != 0) return;
+  if (!prod_end && ((s + 1) & (kSeg - 1)) != 0) return;
   const int mult = prod_end && (p < 2 || FINAL_W) ? kSched[mod].mult[p] : 1;
   if (mult == 1 && p < 2 && prod_end && nseg == 1) return;
   const float fmult = (float)mult;
@@ -375,7 +374,7 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
   const int split = (int)(blockIdx.x % (unsigned)splits);
   int mod;
   int64_t tm, tn;
-  block_coords(blockIdx.x / (unsigned)splits, tiles_m, tiles_n, mod, tm, tn);
+  block_coords(blockIdx.x / (unsigned)splits, (uint32_t)tiles_m, (uint32_t)tiles_n, mod, tm, tn);
   const ModSched sc = kSched[mod];
   cres += (int64_t)split * kR * m * n;
 
@@ -424,29 +423,60 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
   // -- is always in flight while a stage computes, and the carry runs on the
   // registers after the last stage of a segment.
   const int total = 3 * nstage;
-  auto ra = [&](int G) {
-    const int p = G / nstage;
-    return stage_rsrc(pa, kPlanes, m, tm * BM, kSched[mod].plane_a[p], sbeg + G - p * nstage, na);
+  // Stage cursors, advanced without divisions: the look-ahead cursor (lp,
+  // ls) with the stage's A and B pieces, stepping by one K stage of the
+  // plane layout and jumping to the next product's first stage at a product
+  // boundary (it stays on the last stage, whose look-ahead load repeats
+  // it); the carry cursor (cp, cs) follows the stage just computed.
+  const int64_t step_a = (int64_t)kPlanes * m * BK, step_b = (int64_t)kPlanes * n * BK;
+  auto first_a = [&](int p) {
+    return pa + (((int64_t)sbeg * kPlanes + kSched[mod].plane_a[p]) * m + tm * BM) * BK;
   };
-  auto rb = [&](int G) {
-    const int p = G / nstage;
-    return stage_rsrc(pb, kPlanes, n, tn * BN, kSched[mod].plane_b[p], sbeg + G - p * nstage, nb);
+  auto first_b = [&](int p) {
+    return pb + (((int64_t)sbeg * kPlanes + kSched[mod].plane_b[p]) * n + tn * BN) * BK;
+  };
+  int lp = 0, ls = 0, cp = 0, cs = 0;
+  const int8_t* la = first_a(0);
+  const int8_t* lb = first_b(0);
+  auto advance = [&]() {
+    if (ls + 1 < nstage) {
+      ++ls;
+      la += step_a;
+      lb += step_b;
+    } else if (lp < 2) {
+      ++lp;
+      ls = 0;
+      la = first_a(lp);
+      lb = first_b(lp);
+    }
+  };
+  auto rsrc = [](const int8_t* p, int nrec) {
+    return __builtin_amdgcn_make_buffer_rsrc((void*)uniform_ptr(p), (short)0, nrec, 0x00020000);
   };
   const float fm = (float)sc.m, finv = 1.0f / (float)sc.m;
-  if (total > 0) stage_load<NB>(ra(0), rb(0), lds_a0, lds_b0, voff, voffb, wave);
+  auto carry_step = [&]() {
+    carry<NB, sizeof(OT) == 4>(acc, cp, cs, nstage, nseg, mod, fm, finv);
+    if (++cs == nstage) {
+      cs = 0;
+      ++cp;
+    }
+  };
+  if (total > 0) stage_load<NB>(rsrc(la, na), rsrc(lb, nb), lds_a0, lds_b0, voff, voffb, wave);
+  advance();
   for (int G = 0; G < total; G += 2) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    // after the very last stage the look-ahead load repeats it
-    stage_mma_dma<NB>(lds_a0, lds_b0, ra0, rb0, fh, acc, ra(G + 1 < total ? G + 1 : G),
-                      rb(G + 1 < total ? G + 1 : G), lds_a1, lds_b1, voff, voffb, wave);
-    carry<NB, sizeof(OT) == 4>(acc, G, nstage, nseg, mod, fm, finv);
+    stage_mma_dma<NB>(lds_a0, lds_b0, ra0, rb0, fh, acc, rsrc(la, na), rsrc(lb, nb), lds_a1, lds_b1,
+                      voff, voffb, wave);
+    advance();
+    carry_step();
     if (G + 1 >= total) break;
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    stage_mma_dma<NB>(lds_a1, lds_b1, ra0, rb0, fh, acc, ra(G + 2 < total ? G + 2 : G + 1),
-                      rb(G + 2 < total ? G + 2 : G + 1), lds_a0, lds_b0, voff, voffb, wave);
-    carry<NB, sizeof(OT) == 4>(acc, G + 1, nstage, nseg, mod, fm, finv);
+    stage_mma_dma<NB>(lds_a1, lds_b1, ra0, rb0, fh, acc, rsrc(la, na), rsrc(lb, nb), lds_a0, lds_b0,
+                      voff, voffb, wave);
+    advance();
+    carry_step();
   }
   __builtin_amdgcn_s_waitcnt(0);  // the repeated look-ahead load lands before the epilogue
 
@@ -559,7 +589,7 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
   const int split = (int)(blockIdx.x % (unsigned)splits);
   int mod;
   int64_t tm, tn;
-  block_coords(blockIdx.x / (unsigned)splits, tiles_m, tiles_n, mod, tm, tn);
+  block_coords(blockIdx.x / (unsigned)splits, (uint32_t)tiles_m, (uint32_t)tiles_n, mod, tm, tn);
   const int mm = kModA[mod];
   cres += (int64_t)split * kRA * m * n;
   const double minv = 1.0 / (double)mm;
@@ -581,8 +611,9 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
   const int64_t rows_b = n - tn * BN < BN ? n - tn * BN : BN;
   const int na = __builtin_amdgcn_readfirstlane((int)(rows_a * BK));
   const int nb = __builtin_amdgcn_readfirstlane((int)(rows_b * BK));
-  auto ra = [&](int st) { return stage_rsrc(pa, kRA, m, tm * BM, mod, st, na); };
-  auto rb = [&](int st) { return stage_rsrc(pb, kRA, n, tn * BN, mod, st, nb); };
+  auto rsrc = [](const int8_t* p, int nrec) {
+    return __builtin_amdgcn_make_buffer_rsrc((void*)uniform_ptr(p), (short)0, nrec, 0x00020000);
+  };
 
   v16i acc[2][NB];
 #pragma unroll
@@ -593,27 +624,42 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
   const int nstage_all = (int)(kp / BK);
   const int sbeg = (int)((int64_t)nstage_all * split / splits);
   const int nstage = (int)((int64_t)nstage_all * (split + 1) / splits);  // one past the last
+  // look-ahead cursor: stage ls and its A and B pieces, one K stage of the
+  // plane layout apart (it stays on the panel's last stage)
+  const int64_t step_a = (int64_t)kRA * m * BK, step_b = (int64_t)kRA * n * BK;
+  const int8_t* const first_a = pa + (((int64_t)sbeg * kRA + mod) * m + tm * BM) * BK;
+  const int8_t* const first_b = pb + (((int64_t)sbeg * kRA + mod) * n + tn * BN) * BK;
+  int ls = sbeg;
+  const int8_t* la = first_a;
+  const int8_t* lb = first_b;
+  auto advance = [&]() {
+    if (ls + 1 < nstage) {
+      ++ls;
+      la += step_a;
+      lb += step_b;
+    }
+  };
   for (int s0 = sbeg; s0 < nstage; s0 += kSegA) {
     const int s1 = s0 + kSegA < nstage ? s0 + kSegA : nstage;
-    stage_load<NB>(ra(s0), rb(s0), lds_a0, lds_b0, voff, voffb, wave);
+    ls = s0;
+    la = first_a + (int64_t)(s0 - sbeg) * step_a;
+    lb = first_b + (int64_t)(s0 - sbeg) * step_b;
+    stage_load<NB>(rsrc(la, na), rsrc(lb, nb), lds_a0, lds_b0, voff, voffb, wave);
+    advance();
     for (int s = s0; s < s1; s += 2) {
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
       // the DMA after the segment's last stage lands in the idle buffer; past
       // the panel's last stage it repeats that stage (as above)
-      {
-        const int nx = s + 1 < nstage ? s + 1 : s;
-        stage_mma_dma_i8<NB>(lds_a0, lds_b0, ra0, rb0, fh, acc, ra(nx), rb(nx), lds_a1, lds_b1, voff, voffb,
-                             wave);
-      }
+      stage_mma_dma_i8<NB>(lds_a0, lds_b0, ra0, rb0, fh, acc, rsrc(la, na), rsrc(lb, nb), lds_a1, lds_b1,
+                           voff, voffb, wave);
+      advance();
       if (s + 1 >= s1) break;
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
-      {
-        const int nx = s + 2 < nstage ? s + 2 : s + 1;
-        stage_mma_dma_i8<NB>(lds_a1, lds_b1, ra0, rb0, fh, acc, ra(nx), rb(nx), lds_a0, lds_b0, voff, voffb,
-                             wave);
-      }
+      stage_mma_dma_i8<NB>(lds_a1, lds_b1, ra0, rb0, fh, acc, rsrc(la, na), rsrc(lb, nb), lds_a0, lds_b0,
+                           voff, voffb, wave);
+      advance();
     }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();  // every wave is done with the buffers before the next segment loads
@@ -670,6 +716,8 @@ hipError_t launch_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* pa, const
   const int64_t bn = narrow ? kBN<1> : kBN<2>;
   const int64_t blocks = (int64_t)(BYTES ? kRA : kR) * ((m + BM - 1) / BM) * ((n + bn - 1) / bn);
   OT* dst = splits > 1 ? part : cres;
+  // block indices (and block_coords' arithmetic) are 32-bit
+  if (blocks * splits > (int64_t)UINT32_MAX) return hipErrorInvalidValue;
   const dim3 grid((unsigned)(blocks * splits));
   if constexpr (BYTES) {
     if (narrow)
