@@ -77,6 +77,7 @@ struct ModSched {
   int plane_a[3];  // A plane of each product, in issue order
   int plane_b[3];  // B plane of each product
   int mult[3];     // multiplier after product p (p = 2: the final weight)
+  float inv;       // RN(1/m)
 };
 
 // Issue order: squares put the two weight-s products first so they share the
@@ -102,7 +103,8 @@ constexpr ModSched make_sched(int i) {
                   (kModulus[i] - 1) / 2,
                   {issue_plane_a(i, 0), issue_plane_a(i, 1), issue_plane_a(i, 2)},
                   {issue_plane_b(i, 0), issue_plane_b(i, 1), issue_plane_b(i, 2)},
-                  {issue_mult(i, 0), issue_mult(i, 1), issue_mult(i, 2)}};
+                  {issue_mult(i, 0), issue_mult(i, 1), issue_mult(i, 2)},
+                  1.0f / (float)kModulus[i]};
 }
 constexpr bool schedule_is_exact() {
   // the later multipliers applied to P_p give back its weight w_p, mod m
@@ -413,8 +415,9 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
   // they fit one segment each).
   // this block's stages [sbeg, sbeg + nstage) of each product
   const int nstage_all = (int)(kp / BK);
-  const int sbeg = (int)((int64_t)nstage_all * split / splits);
-  const int nstage = (int)((int64_t)nstage_all * (split + 1) / splits) - sbeg;
+  // 32-bit: at most 2^15 stages times 64 splits
+  const int sbeg = (int)((uint32_t)nstage_all * (uint32_t)split / (uint32_t)splits);
+  const int nstage = (int)((uint32_t)nstage_all * (uint32_t)(split + 1) / (uint32_t)splits) - sbeg;
   const int nseg = nstage > 0 ? (nstage + kSeg - 1) / kSeg : 0;  // segments per product
   const int na = __builtin_amdgcn_readfirstlane((int)(rows_a * BK));
   const int nb = __builtin_amdgcn_readfirstlane((int)(rows_b * BK));
@@ -453,7 +456,7 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
   auto rsrc = [](const int8_t* p, int nrec) {
     return __builtin_amdgcn_make_buffer_rsrc((void*)uniform_ptr(p), (short)0, nrec, 0x00020000);
   };
-  const float fm = (float)sc.m, finv = 1.0f / (float)sc.m;
+  const float fm = (float)sc.m, finv = sc.inv;
   auto carry_step = [&]() {
     carry<NB, sizeof(OT) == 4>(acc, cp, cs, nstage, nseg, mod, fm, finv);
     if (++cs == nstage) {
@@ -509,6 +512,12 @@ __constant__ int kModA[kRA] = {kModulusA[0],  kModulusA[1],  kModulusA[2],  kMod
                                kModulusA[4],  kModulusA[5],  kModulusA[6],  kModulusA[7],
                                kModulusA[8],  kModulusA[9],  kModulusA[10], kModulusA[11],
                                kModulusA[12], kModulusA[13], kModulusA[14]};
+// RN(1/m) of each modulus
+__constant__ double kInvA[kRA] = {
+    1.0 / kModulusA[0],  1.0 / kModulusA[1],  1.0 / kModulusA[2],  1.0 / kModulusA[3],
+    1.0 / kModulusA[4],  1.0 / kModulusA[5],  1.0 / kModulusA[6],  1.0 / kModulusA[7],
+    1.0 / kModulusA[8],  1.0 / kModulusA[9],  1.0 / kModulusA[10], 1.0 / kModulusA[11],
+    1.0 / kModulusA[12], 1.0 / kModulusA[13], 1.0 / kModulusA[14]};
 
 // int8 fragment of one 32-row block for one 32-byte K step: lane half fh
 // takes 16-byte chunk 2 ks + fh of its row
@@ -592,7 +601,7 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
   block_coords(blockIdx.x / (unsigned)splits, (uint32_t)tiles_m, (uint32_t)tiles_n, mod, tm, tn);
   const int mm = kModA[mod];
   cres += (int64_t)split * kRA * m * n;
-  const double minv = 1.0 / (double)mm;
+  const double minv = kInvA[mod];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -622,8 +631,9 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
     for (int b = 0; b < NB; ++b) acc[a][b] = v16i{};
 
   const int nstage_all = (int)(kp / BK);
-  const int sbeg = (int)((int64_t)nstage_all * split / splits);
-  const int nstage = (int)((int64_t)nstage_all * (split + 1) / splits);  // one past the last
+  // 32-bit: at most 2^15 stages times 64 splits
+  const int sbeg = (int)((uint32_t)nstage_all * (uint32_t)split / (uint32_t)splits);
+  const int nstage = (int)((uint32_t)nstage_all * (uint32_t)(split + 1) / (uint32_t)splits);  // one past the last
   // look-ahead cursor: stage ls and its A and B pieces, one K stage of the
   // plane layout apart (it stays on the panel's last stage)
   const int64_t step_a = (int64_t)kRA * m * BK, step_b = (int64_t)kRA * n * BK;
