@@ -756,20 +756,32 @@ hipError_t launch_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* pa, const
 }  // namespace
 
 int residue_gemm_splits(int set, int64_t m, int64_t n, int64_t kp) {
-  // split the k range when the tiles of all moduli leave most of the chip
-  // idle: aim at about 1024 blocks, with at least 2 stages of each product
-  // per block (4 for the single-product int8 kernel)
+  // Split the k range when the tiles of all moduli leave most of the chip
+  // idle.  A block holds a whole CU, so blocks run in rounds of kCUs; the
+  // split count minimises rounds x (fixed cost of a block + its stages),
+  // the fixed cost (prologue, carries, epilogue) measured at about seven
+  // stage times, with at least 2 stages of each product per block (4 for
+  // the single-product int8 kernel).
+  constexpr int64_t kCUs = 256, kFixedStages = 7;
   if (m <= 0 || n <= 0) return 1;
   const bool bytes = set == kSetBytes;
   const int64_t bn = n <= kBN<1> ? kBN<1> : kBN<2>;
   const int64_t blocks = (int64_t)(bytes ? kRA : kR) * ((m + BM - 1) / BM) * ((n + bn - 1) / bn);
   const int64_t nstage = kp / BK;
   if (blocks >= 512) return 1;
-  int64_t s = (1024 + blocks - 1) / blocks;
-  const int64_t cap = nstage / (bytes ? 4 : 2);
-  if (s > cap) s = cap;
-  if (s > kMaxSplits) s = kMaxSplits;
-  return s < 1 ? 1 : (int)s;
+  int64_t cap = nstage / (bytes ? 4 : 2);
+  if (cap > kMaxSplits) cap = kMaxSplits;
+  const int64_t prods = bytes ? 1 : 3;
+  int64_t best = -1, best_s = 1;
+  for (int64_t s = 1; s <= cap; ++s) {
+    const int64_t rounds = (blocks * s + kCUs - 1) / kCUs;
+    const int64_t t = rounds * (kFixedStages + prods * ((nstage + s - 1) / s));
+    if (best < 0 || t < best) {
+      best = t;
+      best_s = s;
+    }
+  }
+  return (int)best_s;
 }
 
 hipError_t launch_residue_gemm_i32(int64_t m, int64_t n, int64_t kp, const int8_t* pa,

@@ -78,10 +78,12 @@ def test_size_helpers():
     # one tile per modulus, k = 70: a single k-split, just the residue products
     assert oz.ozaki25_dgemm_planes_workspace_size(100, 50, 70) == up(12 * 100 * 50 * 2)
     assert oz.ozaki25_dgemm_planes_workspace_size(100, 50, 70, oz.A15) == up(15 * 100 * 50)
-    # 256 x 256 x 8192: 12 tiles split 32 ways (at least 2 stages of 128 k each)
-    assert oz.ozaki25_dgemm_planes_workspace_size(256, 256, 8192) == up(12 * 256 * 256 * 2) * 33
+    # 256 x 256 x 8192: 12 tiles split 16 ways (192 blocks: one round on 256 CUs)
+    assert oz.ozaki25_dgemm_planes_workspace_size(256, 256, 8192) == up(12 * 256 * 256 * 2) * 17
     # 15 tiles: 16 ways for the int8 kernel (at least 4 stages per split)
     assert oz.ozaki25_dgemm_planes_workspace_size(256, 256, 8192, oz.A15) == up(15 * 256 * 256) * 17
+    # 1024 x 1024 x 8192, int8: 240 tiles already fill one round
+    assert oz.ozaki25_dgemm_planes_workspace_size(1024, 1024, 8192, oz.A15) == up(15 * 1024 * 1024)
     # enough tiles: no split
     assert oz.ozaki25_dgemm_planes_workspace_size(8192, 8192, 8192) == up(12 * 8192 * 8192 * 2)
     assert oz.ozaki25_dgemm_planes_workspace_size(100, 50, 70, 3) == 0

@@ -364,8 +364,7 @@ def test_dgemm_stage_events():
 @pytest.mark.parametrize("m,n,k,seed", [(40, 300, 8576, 81), (24, 40, 70000, 82), (256, 256, 1024, 83)])
 def test_dgemm_split_k_matches_oracle(m, n, k, seed):
     """Few output tiles: the fused path splits the k range across blocks
-    (uneven stage ranges; ranges crossing FP32 segments for long k) and sums
-    the centred partial products mod m."""
+    (uneven stage ranges) and sums the partial products mod m."""
     log(f"dgemm split-k m={m} n={n} k={k}")
     A = workloads.random_matrix(m, k, 1.0, seed)
     B = workloads.random_matrix(k, n, 1.0, seed + 1)
