@@ -106,8 +106,8 @@ def test_ragged_8191_8209_7937_all_byte_set():
     _run("ragged", set=oz.A15)
 
 
-def test_krylov_262144_128_4096():
-    _run("krylov", nsample=64)
+def test_hpl_trailing_update_32768_1024_all_byte_set():
+    _run("hpl", nsample=64, set=oz.A15)
 
 
 def test_krylov_262144_128_4096_all_byte_set():
