@@ -56,6 +56,8 @@ SETS = {
 COUNTER_FILES = {"s12": os.path.join(ROOT, "profiles", "residue_gemm_square_counters.txt"),
                  "a15": os.path.join(ROOT, "profiles", "residue_gemm_bytes_square_counters.txt")}
 GEMM_SOURCE = os.path.join(ROOT, "paper_2609_09095_amd", "csrc", "residue_gemm.hip")
+DEC_COUNTERS = os.path.join(ROOT, "profiles", "deconstruct_square_counters.txt")
+DEC_SOURCES = [os.path.join(ROOT, "paper_2609_09095_amd", "csrc", f) for f in ("scan.hip", "deconstruct.hip")]
 
 
 def log(msg):
@@ -67,25 +69,48 @@ def source_hash(path):
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_traffic(w, moduli):
-    """HBM bytes per residue-GEMM launch from the committed rocprofv3 counter
-    summary, or None if it is absent, for another workload, or taken on an
-    older version of the kernel source."""
-    path = COUNTER_FILES[moduli]
+def sources_hash(paths):
+    h = hashlib.sha256()
+    for path in paths:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def counter_value(path, w, digest, key):
+    """A value from a committed rocprofv3 counter summary, or None if it is
+    absent, for another workload, or taken on another version of the kernel
+    sources (digest)."""
     if not os.path.exists(path):
         return None
     kv = {}
     with open(path) as f:
         for line in f:
             if ":" in line and not line.startswith("#"):
-                key, val = line.split(":", 1)
-                kv[key.strip()] = val.strip()
+                k, val = line.split(":", 1)
+                kv[k.strip()] = val.strip()
     try:
-        if kv.get("workload") != w.name or kv.get("source_sha256_16") != source_hash(GEMM_SOURCE):
+        if kv.get("workload") != w.name or kv.get("source_sha256_16") != digest:
             return None
-        return float(kv["hbm_bytes_per_launch"])
+        return float(kv[key])
     except (KeyError, ValueError):
         return None
+
+
+def measured_traffic(w, moduli):
+    """HBM bytes per residue-GEMM launch (FETCH_SIZE and WRITE_SIZE, scaled)."""
+    return counter_value(COUNTER_FILES[moduli], w, source_hash(GEMM_SOURCE), "hbm_bytes_per_launch")
+
+
+def measured_deconstruction(w, moduli, scan_ms, dec_ms):
+    """HBM bytes the exponent scans and the deconstruction of both operands
+    move per call, as counted, and their fraction of the HBM peak over the
+    two stages' time."""
+    b = counter_value(DEC_COUNTERS, w, sources_hash(DEC_SOURCES), f"hbm_bytes_per_call_{moduli}")
+    if b is None:
+        return {"measured_bytes": None, "measured_frac": None}
+    return {"measured_bytes": b,
+            "measured_frac": round(b / ((scan_ms + dec_ms) * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
 
 
 def cpu_baseline(A, B, w, rows, cols, cfg):
@@ -279,7 +304,8 @@ def main():
             "roofline_deconstruct": {"bound": "hbm", "kernel": ocfg["dec_kernel"],
                                      "achieved": round(ort["dec_gbs"], 1), "peak": HBM_PEAK_GBS,
                                      "unit": "GB/s", "frac": round(ort["dec_gbs"] / HBM_PEAK_GBS, 4),
-                                     "bytes_per_call": ort["dec_bytes"]},
+                                     "bytes_per_call": ort["dec_bytes"],
+                                     **measured_deconstruction(w, name, ostages[0], ostages[1])},
             "emulation_roof_tflops": round(ort["roof"], 2),
             "emulation_roof_frac": round(ort["tflops"] / ort["roof"], 4),
         }
@@ -340,7 +366,8 @@ def main():
                                  "achieved": round(rt["dec_gbs"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                  "frac": round(rt["dec_gbs"] / HBM_PEAK_GBS, 4),
                                  "bytes_per_call": rt["dec_bytes"],
-                                 "stage_with_scan_gbs": round(rt["stage_gbs"], 1)},
+                                 "stage_with_scan_gbs": round(rt["stage_gbs"], 1),
+                                 **measured_deconstruction(w, args.moduli, scan_ms, dec_ms)},
         "roofline_reconstruct": {"bound": "hbm", "achieved": round(rt["rec_gbs"], 1), "peak": HBM_PEAK_GBS,
                                  "unit": "GB/s", "frac": round(rt["rec_gbs"] / HBM_PEAK_GBS, 4)},
         "stage_ms": {"scan": round(scan_ms, 4), "deconstruct": round(dec_ms, 4), "residue_gemm": round(gemm_ms, 4),

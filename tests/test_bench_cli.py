@@ -22,3 +22,35 @@ def test_set_constants():
     assert (s12["r"], s12["products"], s12["plane_bytes"]) == (12, 36, 30)
     assert (a15["r"], a15["products"], a15["plane_bytes"]) == (15, 15, 15)
     assert s12["cres_bytes"] == 12 * 2 and a15["cres_bytes"] == 15
+
+
+def test_committed_counters_are_plausible():
+    """The rocprofv3 counter summaries bench.py reads for roofline.traffic and
+    roofline_deconstruct.measured_*: square workload, byte counts at least the
+    algorithmic ones (planes read once per GEMM launch; FP64 read, planes
+    written and one exponent-scan read per call), and taken on the current
+    kernel sources (else skipped: the bench then reports null)."""
+    sys.path.insert(0, ROOT)
+    import bench
+    import workloads
+    w = workloads.WORKLOADS["square"]
+    stale = []
+    for name, cfg in bench.SETS.items():
+        path = bench.COUNTER_FILES[name]
+        kv = dict(line.split(":", 1) for line in open(path) if ":" in line and not line.startswith("#"))
+        kv = {k.strip(): v.strip() for k, v in kv.items()}
+        assert kv["workload"] == "square"
+        planes = cfg["plane_bytes"] * (w.m * w.k + w.k * w.n)
+        assert float(kv["hbm_bytes_per_launch"]) >= planes
+        if bench.measured_traffic(w, name) is None:
+            stale.append(path)
+    kv = dict(line.split(":", 1) for line in open(bench.DEC_COUNTERS) if ":" in line and not line.startswith("#"))
+    kv = {k.strip(): v.strip() for k, v in kv.items()}
+    for name, cfg in bench.SETS.items():
+        alg = (8 + cfg["plane_bytes"] + 8) * (w.m * w.k + w.k * w.n)
+        assert 0.95 * alg <= float(kv[f"hbm_bytes_per_call_{name}"]) <= 1.5 * alg
+    if bench.measured_deconstruction(w, "s12", 0.2, 1.0)["measured_bytes"] is None:
+        stale.append(bench.DEC_COUNTERS)
+    if stale:
+        import pytest
+        pytest.skip(f"counter summaries taken on older kernel sources: {stale}")
