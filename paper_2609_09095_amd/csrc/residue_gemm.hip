@@ -58,14 +58,26 @@ typedef int v8i __attribute__((ext_vector_type(8)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 
-constexpr int BM = 256;         // output rows per block
-constexpr int BK = 128;         // k bytes per stage
-constexpr int kTile = BM * BK;  // bytes of the A tile of a stage in LDS
-// output columns per block: NB * 128 (NB = 2; NB = 1 for at most 128
-// columns, where a 256-wide tile would leave half of every MFMA idle); a
-// wave owns 64 rows x NB * 32 columns
-template <int NB>
-inline constexpr int kBN = 128 * NB;
+constexpr int BK = 128;  // k bytes per stage
+// Block tile shapes, the kernels' template parameter S (16 waves; a wave owns
+// 64 rows x 32 BB columns):
+//  1: 256 x 128, for at most 128 columns (a 256-wide tile would leave half
+//     of every MFMA idle);
+//  2: 256 x 256;
+//  3: 512 x 128 (tall), for at most 128 columns and many rows: a stage
+//     moves 80 KiB for twice the MACs of shape 1's 48 KiB (17 % fewer
+//     operand bytes per MAC), and its two stages fill the 160 KiB of LDS.
+template <int S>
+struct Tile {
+  static constexpr int BM = S == 3 ? 512 : 256;  // output rows per block
+  static constexpr int BN = S == 2 ? 256 : 128;  // output columns per block
+  static constexpr int BB = S == 1 ? 1 : 2;      // 32-column blocks per wave
+  static constexpr int WC = BN / (32 * BB);      // waves across the tile
+  static constexpr int ADMA = BM / 128;          // A slabs (8 rows x 128 B) per wave and stage
+  static constexpr int BDMA = BN / 128;          // B slabs per wave and stage
+  static constexpr int DMA = ADMA + BDMA;
+  static_assert(BM / 64 * WC == 16, "16 waves");
+};
 static_assert(BK == kKAlign, "every K stage is full: planes are padded to BK");
 constexpr int kGroupM = 2;      // tile rows per group in the block order
 constexpr int kSeg = 128;       // K stages (16384 k) per accumulation segment
@@ -189,27 +201,39 @@ __device__ __forceinline__ const int8_t* uniform_ptr(const int8_t* p) {
 // straight from global memory into LDS.  A load writes 1 KiB = 8 rows x
 // 128 bytes, lane l landing at row l/8, chunk l%8 of that slab; to realise
 // the swizzled layout the lane fetches the global chunk (l%8) ^ swz(row).
-// DMA d of a stage (2 + NB per wave): d < 2 the A slab wave*2 + d; then the B
-// slab wave*NB + (d - 2).  voff[0..1]: rows wave*16 + 8 d + lane/8; voffb:
-// rows wave*8 + lane/8 (the B slab when NB = 1).
-template <int NB>
+// DMA d of a stage (Tile<S>::DMA per wave): d < ADMA the A slab
+// wave * ADMA + d, then the B slab wave * BDMA + (d - ADMA).  voffa[i]: rows
+// (wave * ADMA + i) * 8 + lane/8 of the A tile; voffb[i] likewise for B.
+template <int S>
 __device__ __forceinline__ void stage_dma(int d, __amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rb,
-                                          int8_t* la, int8_t* lb, const int (&voff)[2], int voffb,
-                                          int wave) {
-  if (d < 2)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr)(la + (wave * 2 + d) * 1024), 16, voff[d], 0,
+                                          int8_t* la, int8_t* lb, const int* voffa,
+                                          const int* voffb, int wave) {
+  constexpr int AD = Tile<S>::ADMA, BD = Tile<S>::BDMA;
+  if (d < AD)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr)(la + (wave * AD + d) * 1024), 16, voffa[d], 0,
                                              0, 0);
   else
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr)(lb + (wave * NB + d - 2) * 1024), 16,
-                                             NB == 2 ? voff[d - 2] : voffb, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr)(lb + (wave * BD + d - AD) * 1024), 16,
+                                             voffb[d - AD], 0, 0, 0);
 }
 
-template <int NB>
+template <int S>
 __device__ __forceinline__ void stage_load(__amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rb,
-                                           int8_t* la, int8_t* lb, const int (&voff)[2], int voffb,
-                                           int wave) {
+                                           int8_t* la, int8_t* lb, const int* voffa,
+                                           const int* voffb, int wave) {
 #pragma unroll
-  for (int d = 0; d < 2 + NB; ++d) stage_dma<NB>(d, ra, rb, la, lb, voff, voffb, wave);
+  for (int d = 0; d < Tile<S>::DMA; ++d) stage_dma<S>(d, ra, rb, la, lb, voffa, voffb, wave);
+}
+
+// Byte offsets within a tile's 128-byte rows of the slab loads of a wave:
+// row (wave * D + i) * 8 + lane/8, chunk (lane % 8) ^ swz(row).
+template <int D>
+__device__ __forceinline__ void slab_offsets(int wave, int lane, int (&voff)[D]) {
+#pragma unroll
+  for (int i = 0; i < D; ++i) {
+    const int r = (wave * D + i) * 8 + (lane >> 3);
+    voff[i] = r * BK + (((lane & 7) ^ swz(r)) << 4);
+  }
 }
 
 __device__ __forceinline__ v8i cat(v4i lo, v4i hi) {
@@ -225,15 +249,16 @@ __device__ __forceinline__ v8i frag(const int8_t* base, int r, int ks, int fh) {
              *reinterpret_cast<const v4i*>(row + (((4 * ks + 2 + fh) ^ swz(r)) << 4)));
 }
 
-// One stage: two 64-byte K steps of 2 x NB MFMAs (a wave owns 64 x 32 NB;
-// four waves share each SIMD).  The next stage's 2 + NB DMA loads go among
-// step 0's MFMAs.
-template <int NB>
+// One stage: two 64-byte K steps of 2 x BB MFMAs (a wave owns 64 x 32 BB;
+// four waves share each SIMD).  The next stage's DMA loads go among the
+// first MFMAs.
+template <int S, int NB = Tile<S>::BB>
 __device__ __forceinline__ void stage_mma_dma(const int8_t* la, const int8_t* lb, int ra0, int rb0,
                                               int fh, v16f (&acc)[2][NB],
                                               __amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rb,
-                                              int8_t* na, int8_t* nb, const int (&voff)[2],
-                                              int voffb, int wave) {
+                                              int8_t* na, int8_t* nb, const int* voffa,
+                                              const int* voffb, int wave) {
+  constexpr int ND = Tile<S>::DMA;
   v8i af[2][2], bf[2][NB];
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) {
@@ -249,18 +274,18 @@ __device__ __forceinline__ void stage_mma_dma(const int8_t* la, const int8_t* lb
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
         const int j = ks * 2 * NB + a * NB + b;  // MFMA number in issue order
-        if (j < 2 + NB) stage_dma<NB>(j, ra, rb, na, nb, voff, voffb, wave);
+        if (j < ND) stage_dma<S>(j, ra, rb, na, nb, voffa, voffb, wave);
         acc[a][b] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af[ks][a], bf[ks][b], acc[a][b], 0,
                                                                     0, 0, 0, 0, 0);
       }
   __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
-  for (int i = 0; i < 2 + NB; ++i) {
+  for (int i = 0; i < ND; ++i) {
     __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
   }
-  __builtin_amdgcn_sched_group_barrier(0x008, 4 * NB - (2 + NB), 0);
+  __builtin_amdgcn_sched_group_barrier(0x008, 4 * NB - ND, 0);
 }
 
 // After stage s of product p:
@@ -321,10 +346,10 @@ __device__ __forceinline__ void store_out(OT* p, OT v) {
 // times a constant per value: one add per store, no per-value bounds test;
 // offsets below 256 n size <= 2^32); edge tiles and int32 outputs test every
 // value and use 32-bit element offsets (256 n < 2^31).
-template <bool NT, typename OT, int NB, typename F>
+template <bool NT, typename OT, int S, typename F>
 __device__ __forceinline__ void store_tile(OT* out, int nn, int rows_left, int cols_left, int wr,
                                            int wc, int fr, int fh, F&& value) {
-  constexpr int BN = kBN<NB>;
+  constexpr int BM = Tile<S>::BM, BN = Tile<S>::BN, NB = Tile<S>::BB;
   if constexpr (sizeof(OT) <= 2) {
     if (rows_left >= BM && cols_left >= BN) {
       char* base = (char*)out;
@@ -361,16 +386,16 @@ __device__ __forceinline__ void store_tile(OT* out, int nn, int rows_left, int c
 // splits > 1 (split-k): consecutive blocks take the same tile's stage ranges,
 // and block (tile, split) writes its centred partial product to the split's
 // own [r][m][n] slice of cres; reduce_splits_kernel sums them mod m.
-template <typename OT, int NB>
+template <typename OT, int S>
 __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_t n, int64_t kp,
                                                               const int8_t* __restrict__ pa,
                                                               const int8_t* __restrict__ pb,
                                                               OT* __restrict__ cres, int splits) {
-  // two LDS stages, each an A tile and a B tile of 256 rows x 128 bytes
-  constexpr int BN = kBN<NB>;
-  __shared__ __attribute__((aligned(1024))) int8_t lds_a0[kTile];
+  // two LDS stages, each an A tile (BM rows x 128 bytes) and a B tile
+  constexpr int BM = Tile<S>::BM, BN = Tile<S>::BN, NB = Tile<S>::BB, WC = Tile<S>::WC;
+  __shared__ __attribute__((aligned(1024))) int8_t lds_a0[BM * BK];
   __shared__ __attribute__((aligned(1024))) int8_t lds_b0[BN * BK];
-  __shared__ __attribute__((aligned(1024))) int8_t lds_a1[kTile];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_a1[BM * BK];
   __shared__ __attribute__((aligned(1024))) int8_t lds_b1[BN * BK];
   const int64_t tiles_m = (m + BM - 1) / BM, tiles_n = (n + BN - 1) / BN;
   const int split = (int)(blockIdx.x % (unsigned)splits);
@@ -382,19 +407,14 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS-DMA base in M0
-  const int wr = wave >> 2, wc = wave & 3;  // 4 x 4 waves of 64 x 64
+  const int wr = wave / WC, wc = wave % WC;  // (16 / WC) x WC waves of 64 x 32 NB
   const int fr = lane & 31, fh = lane >> 5;  // fragment row, 16-byte K half
   const int ra0 = wr * 64 + fr, rb0 = wc * 32 * NB + fr;
 
-  // byte offsets (within the block's 256-row panel) of the 4 slab loads
-  int voff[2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int r = wave * 16 + i * 8 + (lane >> 3);
-    voff[i] = r * BK + (((lane & 7) ^ swz(r)) << 4);
-  }
-  const int rbd = wave * 8 + (lane >> 3);  // B slab rows when NB = 1
-  const int voffb = rbd * BK + (((lane & 7) ^ swz(rbd)) << 4);
+  // byte offsets (within the block's panels) of the slab loads
+  int voffa[Tile<S>::ADMA], voffb[Tile<S>::BDMA];
+  slab_offsets(wave, lane, voffa);
+  slab_offsets(wave, lane, voffb);
   // rows past the matrix edge read as zero (buffer range check); they only
   // feed outputs that are never stored
   const int64_t rows_a = m - tm * BM < BM ? m - tm * BM : BM;
@@ -464,27 +484,27 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
       ++cp;
     }
   };
-  if (total > 0) stage_load<NB>(rsrc(la, na), rsrc(lb, nb), lds_a0, lds_b0, voff, voffb, wave);
+  if (total > 0) stage_load<S>(rsrc(la, na), rsrc(lb, nb), lds_a0, lds_b0, voffa, voffb, wave);
   advance();
   for (int G = 0; G < total; G += 2) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    stage_mma_dma<NB>(lds_a0, lds_b0, ra0, rb0, fh, acc, rsrc(la, na), rsrc(lb, nb), lds_a1, lds_b1,
-                      voff, voffb, wave);
+    stage_mma_dma<S>(lds_a0, lds_b0, ra0, rb0, fh, acc, rsrc(la, na), rsrc(lb, nb), lds_a1, lds_b1,
+                      voffa, voffb, wave);
     advance();
     carry_step();
     if (G + 1 >= total) break;
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    stage_mma_dma<NB>(lds_a1, lds_b1, ra0, rb0, fh, acc, rsrc(la, na), rsrc(lb, nb), lds_a0, lds_b0,
-                      voff, voffb, wave);
+    stage_mma_dma<S>(lds_a1, lds_b1, ra0, rb0, fh, acc, rsrc(la, na), rsrc(lb, nb), lds_a0, lds_b0,
+                      voffa, voffb, wave);
     advance();
     carry_step();
   }
   __builtin_amdgcn_s_waitcnt(0);  // the repeated look-ahead load lands before the epilogue
 
   OT* out = (OT*)uniform_ptr((const int8_t*)(cres + (int64_t)mod * m * n + tm * BM * n + tn * BN));
-  store_tile<true, OT, NB>(out, (int)n, (int)(m - tm * BM), (int)(n - tn * BN), wr, wc, fr, fh,
+  store_tile<true, OT, S>(out, (int)n, (int)(m - tm * BM), (int)(n - tn * BN), wr, wc, fr, fh,
                            [&](int a, int b, int v) {
                              // the final carry leaves |r| <= 0.51 m: true residues
                              // are wrapped into [-(m/2), (m-1)/2]; compact ones are
@@ -540,15 +560,17 @@ __device__ __forceinline__ int cmod_i32(int x, int m, double minv) {
   return FOLD && 2 * r == m ? -r : r;
 }
 
-// One stage: four 32-byte K steps of 2 x NB MFMAs; the next stage's 2 + NB
-// DMA loads go among step 0's MFMAs, the fragment reads of step ks + 1 among
+// One stage: four 32-byte K steps of 2 x BB MFMAs; the next stage's DMA
+// loads go among step 0's MFMAs, the fragment reads of step ks + 1 among
 // step ks's.
-template <int NB>
+template <int S, int NB = Tile<S>::BB>
 __device__ __forceinline__ void stage_mma_dma_i8(const int8_t* la, const int8_t* lb, int ra0,
                                                  int rb0, int fh, v16i (&acc)[2][NB],
                                                  __amdgpu_buffer_rsrc_t ra,
                                                  __amdgpu_buffer_rsrc_t rb, int8_t* na, int8_t* nb,
-                                                 const int (&voff)[2], int voffb, int wave) {
+                                                 const int* voffa,
+                                                 const int* voffb, int wave) {
+  constexpr int ND = Tile<S>::DMA;
   v4i af[4][2], bf[4][NB];
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) {
@@ -564,35 +586,35 @@ __device__ __forceinline__ void stage_mma_dma_i8(const int8_t* la, const int8_t*
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
         const int j = ks * 2 * NB + a * NB + b;  // MFMA number in issue order
-        if (j < 2 + NB) stage_dma<NB>(j, ra, rb, na, nb, voff, voffb, wave);
+        if (j < ND) stage_dma<S>(j, ra, rb, na, nb, voffa, voffb, wave);
         acc[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[ks][a], bf[ks][b], acc[a][b], 0, 0, 0);
       }
-  __builtin_amdgcn_sched_group_barrier(0x100, 2 + NB, 0);
+  __builtin_amdgcn_sched_group_barrier(0x100, ND, 0);
 #pragma unroll
-  for (int i = 0; i < 2 + NB; ++i) {
+  for (int i = 0; i < ND; ++i) {
     __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
   }
 #pragma unroll
-  for (int i = 0; i < 2 * (2 + NB); ++i) {
+  for (int i = 0; i < 2 * ND; ++i) {
     __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
   }
-  __builtin_amdgcn_sched_group_barrier(0x008, 8 * NB - 3 * (2 + NB) > 0 ? 8 * NB - 3 * (2 + NB) : 0, 0);
+  __builtin_amdgcn_sched_group_barrier(0x008, 8 * NB - 3 * ND > 0 ? 8 * NB - 3 * ND : 0, 0);
 }
 
-template <typename OT, int NB>
+template <typename OT, int S>
 __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, int64_t n,
                                                                     int64_t kp,
                                                                     const int8_t* __restrict__ pa,
                                                                     const int8_t* __restrict__ pb,
                                                                     OT* __restrict__ cres,
                                                                     int splits) {
-  constexpr int BN = kBN<NB>;
-  __shared__ __attribute__((aligned(1024))) int8_t lds_a0[kTile];
+  constexpr int BM = Tile<S>::BM, BN = Tile<S>::BN, NB = Tile<S>::BB, WC = Tile<S>::WC;
+  __shared__ __attribute__((aligned(1024))) int8_t lds_a0[BM * BK];
   __shared__ __attribute__((aligned(1024))) int8_t lds_b0[BN * BK];
-  __shared__ __attribute__((aligned(1024))) int8_t lds_a1[kTile];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_a1[BM * BK];
   __shared__ __attribute__((aligned(1024))) int8_t lds_b1[BN * BK];
   const int64_t tiles_m = (m + BM - 1) / BM, tiles_n = (n + BN - 1) / BN;
   const int split = (int)(blockIdx.x % (unsigned)splits);
@@ -605,17 +627,12 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wr = wave >> 2, wc = wave & 3;
+  const int wr = wave / WC, wc = wave % WC;
   const int fr = lane & 31, fh = lane >> 5;
   const int ra0 = wr * 64 + fr, rb0 = wc * 32 * NB + fr;
-  int voff[2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int r = wave * 16 + i * 8 + (lane >> 3);
-    voff[i] = r * BK + (((lane & 7) ^ swz(r)) << 4);
-  }
-  const int rbd = wave * 8 + (lane >> 3);  // B slab rows when NB = 1
-  const int voffb = rbd * BK + (((lane & 7) ^ swz(rbd)) << 4);
+  int voffa[Tile<S>::ADMA], voffb[Tile<S>::BDMA];
+  slab_offsets(wave, lane, voffa);
+  slab_offsets(wave, lane, voffb);
   const int64_t rows_a = m - tm * BM < BM ? m - tm * BM : BM;
   const int64_t rows_b = n - tn * BN < BN ? n - tn * BN : BN;
   const int na = __builtin_amdgcn_readfirstlane((int)(rows_a * BK));
@@ -654,21 +671,21 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
     ls = s0;
     la = first_a + (int64_t)(s0 - sbeg) * step_a;
     lb = first_b + (int64_t)(s0 - sbeg) * step_b;
-    stage_load<NB>(rsrc(la, na), rsrc(lb, nb), lds_a0, lds_b0, voff, voffb, wave);
+    stage_load<S>(rsrc(la, na), rsrc(lb, nb), lds_a0, lds_b0, voffa, voffb, wave);
     advance();
     for (int s = s0; s < s1; s += 2) {
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
       // the DMA after the segment's last stage lands in the idle buffer; past
       // the panel's last stage it repeats that stage (as above)
-      stage_mma_dma_i8<NB>(lds_a0, lds_b0, ra0, rb0, fh, acc, rsrc(la, na), rsrc(lb, nb), lds_a1, lds_b1,
-                           voff, voffb, wave);
+      stage_mma_dma_i8<S>(lds_a0, lds_b0, ra0, rb0, fh, acc, rsrc(la, na), rsrc(lb, nb), lds_a1, lds_b1,
+                           voffa, voffb, wave);
       advance();
       if (s + 1 >= s1) break;
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
-      stage_mma_dma_i8<NB>(lds_a1, lds_b1, ra0, rb0, fh, acc, rsrc(la, na), rsrc(lb, nb), lds_a0, lds_b0,
-                           voff, voffb, wave);
+      stage_mma_dma_i8<S>(lds_a1, lds_b1, ra0, rb0, fh, acc, rsrc(la, na), rsrc(lb, nb), lds_a0, lds_b0,
+                           voffa, voffb, wave);
       advance();
     }
     __builtin_amdgcn_s_waitcnt(0);
@@ -684,7 +701,7 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
   }
 
   OT* out = (OT*)uniform_ptr((const int8_t*)(cres + (int64_t)mod * m * n + tm * BM * n + tn * BN));
-  store_tile<false, OT, NB>(out, (int)n, (int)(m - tm * BM), (int)(n - tn * BN), wr, wc, fr, fh,
+  store_tile<false, OT, S>(out, (int)n, (int)(m - tm * BM), (int)(n - tn * BN), wr, wc, fr, fh,
                             [&](int a, int b, int v) {
                               return cmod_i32<sizeof(OT) == 4>(acc[a][b][v], mm, minv);
                             });
@@ -713,32 +730,42 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(int64_t mn, int spli
   out[at] = (OT)r;
 }
 
+// Tile shape for n columns: at most 128 columns take a 128-wide tile (512
+// rows on the FP8 route, 256 on the int8 one), more columns 256 x 256.
+constexpr int gemm_shape(bool bytes, int64_t n) { return n <= 128 ? 3 : 2; }
+constexpr int64_t gemm_blocks(bool bytes, int64_t m, int64_t n) {
+  const int s = gemm_shape(bytes, n);
+  const int64_t bm = s == 3 ? Tile<3>::BM : Tile<1>::BM, bn = s == 2 ? Tile<2>::BN : Tile<1>::BN;
+  return (int64_t)(bytes ? kRA : kR) * ((m + bm - 1) / bm) * ((n + bn - 1) / bn);
+}
+static_assert(Tile<1>::BM == Tile<2>::BM && Tile<1>::BN == Tile<3>::BN, "tile shapes");
+
 template <bool BYTES, typename OT>
 hipError_t launch_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* pa, const int8_t* pb,
                        OT* cres, OT* part, int splits, hipStream_t stream) {
   if (m <= 0 || n <= 0) return hipSuccess;
-  // the store epilogue uses 32-bit offsets within a 256-row tile
+  // the store epilogue uses 32-bit offsets within a tile (at most 256 rows
+  // when n > 128)
   if (n > kMaxResidueCols) return hipErrorInvalidValue;
   const int nstage = (int)(kp / BK);
   if (splits < 1 || splits > (nstage > 1 ? nstage : 1) || (splits > 1 && !part))
     return hipErrorInvalidValue;
-  const bool narrow = n <= kBN<1>;
-  const int64_t bn = narrow ? kBN<1> : kBN<2>;
-  const int64_t blocks = (int64_t)(BYTES ? kRA : kR) * ((m + BM - 1) / BM) * ((n + bn - 1) / bn);
+  const int shape = gemm_shape(BYTES, n);
+  const int64_t blocks = gemm_blocks(BYTES, m, n);
   OT* dst = splits > 1 ? part : cres;
   // block indices (and block_coords' arithmetic) are 32-bit
   if (blocks * splits > (int64_t)UINT32_MAX) return hipErrorInvalidValue;
   const dim3 grid((unsigned)(blocks * splits));
   if constexpr (BYTES) {
-    if (narrow)
-      hipLaunchKernelGGL((residue_gemm_bytes_kernel<OT, 1>), grid, dim3(1024), 0, stream, m, n, kp, pa,
+    if (shape == 3)
+      hipLaunchKernelGGL((residue_gemm_bytes_kernel<OT, 3>), grid, dim3(1024), 0, stream, m, n, kp, pa,
                          pb, dst, splits);
     else
       hipLaunchKernelGGL((residue_gemm_bytes_kernel<OT, 2>), grid, dim3(1024), 0, stream, m, n, kp, pa,
                          pb, dst, splits);
   } else {
-    if (narrow)
-      hipLaunchKernelGGL((residue_gemm_kernel<OT, 1>), grid, dim3(1024), 0, stream, m, n, kp, pa, pb,
+    if (shape == 3)
+      hipLaunchKernelGGL((residue_gemm_kernel<OT, 3>), grid, dim3(1024), 0, stream, m, n, kp, pa, pb,
                          dst, splits);
     else
       hipLaunchKernelGGL((residue_gemm_kernel<OT, 2>), grid, dim3(1024), 0, stream, m, n, kp, pa, pb,
@@ -765,8 +792,7 @@ int residue_gemm_splits(int set, int64_t m, int64_t n, int64_t kp) {
   constexpr int64_t kCUs = 256, kFixedStages = 7;
   if (m <= 0 || n <= 0) return 1;
   const bool bytes = set == kSetBytes;
-  const int64_t bn = n <= kBN<1> ? kBN<1> : kBN<2>;
-  const int64_t blocks = (int64_t)(bytes ? kRA : kR) * ((m + BM - 1) / BM) * ((n + bn - 1) / bn);
+  const int64_t blocks = gemm_blocks(bytes, m, n);
   const int64_t nstage = kp / BK;
   if (blocks >= 512) return 1;
   int64_t cap = nstage / (bytes ? 4 : 2);
