@@ -60,13 +60,13 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 
 constexpr int BK = 128;  // k bytes per stage
 // Block tile shapes, the kernels' template parameter S (16 waves; a wave owns
-// 64 rows x 32 BB columns):
-//  1: 256 x 128, for at most 128 columns (a 256-wide tile would leave half
-//     of every MFMA idle);
+// 64 rows x 32 BB columns).  The library launches 2 and 3:
+//  1: 256 x 128 (the 128-column tile that 3 replaced);
 //  2: 256 x 256;
-//  3: 512 x 128 (tall), for at most 128 columns and many rows: a stage
-//     moves 80 KiB for twice the MACs of shape 1's 48 KiB (17 % fewer
-//     operand bytes per MAC), and its two stages fill the 160 KiB of LDS.
+//  3: 512 x 128, for at most 128 columns (a 256-wide tile would leave half
+//     of every MFMA idle): a stage moves 80 KiB for twice the MACs of shape
+//     1's 48 KiB (17 % fewer operand bytes per MAC), and its two stages fill
+//     the 160 KiB of LDS.
 template <int S>
 struct Tile {
   static constexpr int BM = S == 3 ? 512 : 256;  // output rows per block
