@@ -39,17 +39,19 @@ __device__ __forceinline__ uint32_t wave_max(uint32_t v) {
   return v;
 }
 
-// One wavefront per row of A; rows are contiguous, so loads coalesce.
+// One block of four wavefronts per row of A; rows are contiguous, so loads
+// coalesce, and short matrices (few rows, long k) still spread over the
+// chip.  The waves' maxima meet in LDS.
 __global__ __launch_bounds__(256) void scan_rows_kernel(int64_t vecs, int64_t k, const double* X,
                                                         int64_t ldx, int t, int32_t* exps) {
-  const int lane = threadIdx.x & 63;
-  const int64_t v = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (v >= vecs) return;
+  __shared__ uint32_t part[4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t v = blockIdx.x;
   const uint64_t* row = reinterpret_cast<const uint64_t*>(X + v * ldx);
   uint64_t mx0 = 0, mx1 = 0;
-  int64_t l = lane;
-  for (; l + 64 < k; l += 128) {
-    const uint64_t a = row[l] & kAbsMask, b = row[l + 64] & kAbsMask;
+  int64_t l = threadIdx.x;
+  for (; l + 256 < k; l += 512) {
+    const uint64_t a = row[l] & kAbsMask, b = row[l + 256] & kAbsMask;
     mx0 = a > mx0 ? a : mx0;
     mx1 = b > mx1 ? b : mx1;
   }
@@ -57,9 +59,14 @@ __global__ __launch_bounds__(256) void scan_rows_kernel(int64_t vecs, int64_t k,
     const uint64_t a = row[l] & kAbsMask;
     mx0 = a > mx0 ? a : mx0;
   }
-  const uint64_t mx = mx0 > mx1 ? mx0 : mx1;
-  const uint32_t key = wave_max(exponent_key(mx));
-  if (lane == 0) exps[v] = key_to_sigma(key, t);
+  const uint32_t key = wave_max(exponent_key(mx0 > mx1 ? mx0 : mx1));
+  if (lane == 0) part[wave] = key;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t m = part[0];
+    for (int w = 1; w < 4; ++w) m = part[w] > m ? part[w] : m;
+    exps[v] = key_to_sigma(m, t);
+  }
 }
 
 __global__ __launch_bounds__(256) void clear_keys_kernel(int64_t vecs, int32_t* keys) {
@@ -107,8 +114,9 @@ hipError_t launch_scan(int side, int64_t vecs, int64_t k, const double* X, int64
                        int32_t* exps, hipStream_t stream) {
   if (vecs <= 0) return hipSuccess;
   if (side == 0) {
-    hipLaunchKernelGGL(scan_rows_kernel, dim3((unsigned)((vecs + 3) / 4)), dim3(256), 0, stream,
-                       vecs, k, X, ldx, t, exps);
+    if (vecs > (int64_t)UINT32_MAX) return hipErrorInvalidValue;  // one block per row
+    hipLaunchKernelGGL(scan_rows_kernel, dim3((unsigned)vecs), dim3(256), 0, stream, vecs, k, X, ldx,
+                       t, exps);
     return hipGetLastError();
   }
   const unsigned vb = (unsigned)((vecs + 255) / 256);
