@@ -121,9 +121,10 @@ hipError_t launch_scan(int side, int64_t vecs, int64_t k, const double* X, int64
   }
   const unsigned vb = (unsigned)((vecs + 255) / 256);
   hipLaunchKernelGGL(clear_keys_kernel, dim3(vb), dim3(256), 0, stream, vecs, exps);
-  const int64_t rows_per_block = 256;
-  const int64_t kblocks = (k + rows_per_block - 1) / rows_per_block;
+  // k blocks of 256 rows, or of 64 when that leaves fewer than 1024 blocks
   const int64_t strips = (vecs + 63) / 64;
+  const int64_t rows_per_block = strips * ((k + 255) / 256) < 1024 ? 64 : 256;
+  const int64_t kblocks = (k + rows_per_block - 1) / rows_per_block;
   if (kblocks > 0)
     hipLaunchKernelGGL(scan_cols_kernel, dim3((unsigned)(strips * kblocks)), dim3(256), 0, stream,
                        vecs, k, X, ldx, rows_per_block, exps);
