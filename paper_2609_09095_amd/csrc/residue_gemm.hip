@@ -79,7 +79,6 @@ struct Tile {
   static_assert(BM / 64 * WC == 16, "16 waves");
 };
 static_assert(BK == kKAlign, "every K stage is full: planes are padded to BK");
-constexpr int kGroupM = 2;      // tile rows per group in the block order
 constexpr int kSeg = 128;       // K stages (16384 k) per accumulation segment
 
 // Per-modulus schedule, from the compile-time tables of moduli.hpp.
@@ -154,29 +153,30 @@ __device__ __forceinline__ float reduce_f(float x, float m, float minv) {
 
 __device__ __forceinline__ int swz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
 
-// Block order: moduli outermost; inside a modulus, tiles go in groups of
-// kGroupM = 2 tile rows.  Blocks are dealt round-robin over the 8 XCDs, so
-// the 32 blocks an XCD runs at a time cover 4 tile rows x 8 tile columns: 12
-// panels feed 32 tiles from its L2 (groups of 4 rows: 18 panels; 8 rows: 33).
+// Block order: moduli outermost; inside a modulus, tiles go in groups of G
+// tile rows, column by column.  Blocks are dealt round-robin over the 8
+// XCDs; with G = 2 and 32 tile columns the 32 blocks an XCD runs at a time
+// cover 4 tile rows x 8 tile columns: 12 panels feed 32 tiles from its L2
+// (G = 4: 18 panels; 8: 33).  Short k (small panels) prefers G = 1 on the
+// FP8 route and G = 4 on the int8 one (gemm_group).
 // Unsigned 32-bit arithmetic throughout: the grid has fewer than 2^32 blocks
 // (checked at launch), so every count here fits, and 32-bit divisions cost a
 // small fraction of 64-bit ones.
-__device__ __forceinline__ void block_coords(uint32_t id, uint32_t tiles_m, uint32_t tiles_n, int& mod,
-                                             int64_t& tm, int64_t& tn) {
+__device__ __forceinline__ void block_coords(uint32_t id, uint32_t tiles_m, uint32_t tiles_n,
+                                             uint32_t group, int& mod, int64_t& tm, int64_t& tn) {
   const uint32_t per_mod = tiles_m * tiles_n;
   const uint32_t q = id / per_mod;
-  mod = (int)q;
   const uint32_t t = id - q * per_mod;
-  const uint32_t gw = kGroupM * tiles_n;
-  const uint32_t group = t / gw;
-  const uint32_t first = group * kGroupM;
-  const uint32_t in = t - group * gw;
-  static_assert(kGroupM == 2, "groups of at most two tile rows");
-  const bool pair = tiles_m - first >= 2;  // a full group: tile rows alternate
+  const uint32_t gw = group * tiles_n;
+  const uint32_t g = t / gw;
+  const uint32_t first = g * group;
+  const uint32_t in = t - g * gw;
+  const uint32_t gsz = tiles_m - first < group ? tiles_m - first : group;
+  const uint32_t c = in / gsz;
   // uniform values: pinned to scalar registers
-  mod = __builtin_amdgcn_readfirstlane(mod);
-  tm = __builtin_amdgcn_readfirstlane((int)(first + (pair ? (in & 1u) : 0u)));
-  tn = __builtin_amdgcn_readfirstlane((int)(pair ? in >> 1 : in));
+  mod = __builtin_amdgcn_readfirstlane((int)q);
+  tm = __builtin_amdgcn_readfirstlane((int)(first + (in - c * gsz)));
+  tn = __builtin_amdgcn_readfirstlane((int)c);
 }
 
 using lds_ptr = __attribute__((address_space(3))) void*;
@@ -390,7 +390,8 @@ template <typename OT, int S>
 __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_t n, int64_t kp,
                                                               const int8_t* __restrict__ pa,
                                                               const int8_t* __restrict__ pb,
-                                                              OT* __restrict__ cres, int splits) {
+                                                              OT* __restrict__ cres, int splits,
+                                                              int group) {
   // two LDS stages, each an A tile (BM rows x 128 bytes) and a B tile
   constexpr int BM = Tile<S>::BM, BN = Tile<S>::BN, NB = Tile<S>::BB, WC = Tile<S>::WC;
   __shared__ __attribute__((aligned(1024))) int8_t lds_a0[BM * BK];
@@ -401,7 +402,8 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
   const int split = (int)(blockIdx.x % (unsigned)splits);
   int mod;
   int64_t tm, tn;
-  block_coords(blockIdx.x / (unsigned)splits, (uint32_t)tiles_m, (uint32_t)tiles_n, mod, tm, tn);
+  block_coords(blockIdx.x / (unsigned)splits, (uint32_t)tiles_m, (uint32_t)tiles_n, (uint32_t)group, mod,
+               tm, tn);
   const ModSched sc = kSched[mod];
   cres += (int64_t)split * kR * m * n;
 
@@ -610,7 +612,7 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
                                                                     const int8_t* __restrict__ pa,
                                                                     const int8_t* __restrict__ pb,
                                                                     OT* __restrict__ cres,
-                                                                    int splits) {
+                                                                    int splits, int group) {
   constexpr int BM = Tile<S>::BM, BN = Tile<S>::BN, NB = Tile<S>::BB, WC = Tile<S>::WC;
   __shared__ __attribute__((aligned(1024))) int8_t lds_a0[BM * BK];
   __shared__ __attribute__((aligned(1024))) int8_t lds_b0[BN * BK];
@@ -620,7 +622,8 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
   const int split = (int)(blockIdx.x % (unsigned)splits);
   int mod;
   int64_t tm, tn;
-  block_coords(blockIdx.x / (unsigned)splits, (uint32_t)tiles_m, (uint32_t)tiles_n, mod, tm, tn);
+  block_coords(blockIdx.x / (unsigned)splits, (uint32_t)tiles_m, (uint32_t)tiles_n, (uint32_t)group, mod,
+               tm, tn);
   const int mm = kModA[mod];
   cres += (int64_t)split * kRA * m * n;
   const double minv = kInvA[mod];
@@ -751,6 +754,11 @@ hipError_t launch_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* pa, const
   if (splits < 1 || splits > (nstage > 1 ? nstage : 1) || (splits > 1 && !part))
     return hipErrorInvalidValue;
   const int shape = gemm_shape(BYTES, n);
+  // tile rows per group of the block order: 2; short k (at most 16 stages,
+  // panels of at most 512 KiB per plane) 1 on the FP8 route, 4 on the int8
+  // one (measured on the 32768^2 x 1024 update: 33.7 -> 32.7 ms and 20.6 ->
+  // 19.4 ms; 8192^3 and ragged 8191 x 8209 x 7937 are fastest with 2)
+  const int group = kp <= 16 * BK ? (BYTES ? 4 : 1) : 2;
   const int64_t blocks = gemm_blocks(BYTES, m, n);
   OT* dst = splits > 1 ? part : cres;
   // block indices (and block_coords' arithmetic) are 32-bit
@@ -759,17 +767,17 @@ hipError_t launch_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* pa, const
   if constexpr (BYTES) {
     if (shape == 3)
       hipLaunchKernelGGL((residue_gemm_bytes_kernel<OT, 3>), grid, dim3(1024), 0, stream, m, n, kp, pa,
-                         pb, dst, splits);
+                         pb, dst, splits, group);
     else
       hipLaunchKernelGGL((residue_gemm_bytes_kernel<OT, 2>), grid, dim3(1024), 0, stream, m, n, kp, pa,
-                         pb, dst, splits);
+                         pb, dst, splits, group);
   } else {
     if (shape == 3)
       hipLaunchKernelGGL((residue_gemm_kernel<OT, 3>), grid, dim3(1024), 0, stream, m, n, kp, pa, pb,
-                         dst, splits);
+                         dst, splits, group);
     else
       hipLaunchKernelGGL((residue_gemm_kernel<OT, 2>), grid, dim3(1024), 0, stream, m, n, kp, pa, pb,
-                         dst, splits);
+                         dst, splits, group);
   }
   if (splits > 1) {
     const int64_t mn = m * n;
