@@ -9,17 +9,17 @@
 // e4m3-exact, Lemma 1), and v_mfma_f32_32x32x64_f8f6f4 multiplies them with
 // FP32 accumulation, exact while every partial sum is an integer below 2^24.
 //
-// A block owns one 256 x 256 output tile of one modulus and runs the three
-// products through ONE set of accumulators: after product p the accumulator
-// is reduced mod m and multiplied by w_p / w_{p+1} mod m (w_{p+1} is
-// invertible whenever it differs from w_p), so product p+1 accumulates on
-// top of it and
+// A block owns one output tile of one modulus and runs the three products
+// through ONE set of accumulators: after product p the accumulator is
+// reduced mod m and multiplied by w_p / w_{p+1} mod m (w_{p+1} is invertible
+// whenever it differs from w_p), so product p+1 accumulates on top of it and
 //     w_last * acc = sum_p w_p P_p   (mod m)
-// at the end.  Products longer than kSeg stages (16384 k) are cut into
-// segments with a plain reduction between them, which keeps every sum
-// between two reductions below 2^24: at most 0.51 m + 22^2 * 16384, or
-// 0.51 m + 2 * 16^2 * 16384 for the two square products that share an
-// accumulator unreduced (only when each fits one segment).  This is the
+// at the end (the compact outputs store acc itself, reduced; the
+// reconstruction applies w_last).  Products longer than kSeg stages (16384
+// k) are cut into segments with a plain reduction between them, which keeps
+// every sum between two reductions below 2^24: at most 0.51 m (m - 1) +
+// 22^2 * 16384, or 2 * 16^2 * 16384 for the two square products that share
+// an accumulator unreduced (only when each fits one segment).  This is the
 // paper's chunked FP32 accumulation (its depth limit 2^24 / 22^2 = 34663),
 // with the chunk at a power of two below it.
 //
@@ -31,21 +31,23 @@
 // sides for equal l/32, so any fixed choice of those bytes pairs equal k.
 //
 // Tiling: a block of 16 wavefronts (4 per SIMD) owns a 256 x 256 output
-// tile, 64 x 64 per wavefront (2 x 2 MFMA blocks of 32 x 32).  Four waves per
+// tile (512 x 128 for at most 128 columns), 64 x 64 per wavefront (2 x 2
+// MFMA blocks of 32 x 32).  Four waves per
 // SIMD keep the matrix core fed while other waves wait at a barrier, on LDS
 // reads or on the operand stream; they cost twice the LDS reads of a 2 x 2
 // layout of 128 x 128 wavefronts (measured 5-6 % faster all the same).  K
 // stages of 128 bytes go straight from global memory into LDS (buffer loads
-// with the lds bit; 2 x 64 KiB, double buffered); the 4 loads of a wave for
-// stage s+1 are interleaved with stage s's first MFMAs.  LDS rows are 128
+// with the lds bit; two stages, double buffered); a wave's loads for stage
+// s+1 are interleaved with stage s's first MFMAs.  LDS rows are 128
 // bytes with the 16-byte chunk index XOR-swizzled by the row so that the
 // b128 fragment reads of 8 (or 16) consecutive rows hit distinct banks.
 // k is padded to a multiple of 128 bytes, so every stage is full.
 //
 // At this tile size the operand stream is 64 KiB per CU per stage of 2048
 // MFMA cycles (32 B/clk at the FP8 peak); direct-to-LDS loads deliver about
-// 20 B/clk per CU here, and the MFMA rate itself drops with the switching
-// activity of dense data, so neither side runs at its nominal peak.
+// 20-25 B/clk per CU, which bounds a stage (halving the stream cuts the time
+// by a quarter, halving the LDS fragment reads by 2 %), and the MFMA clock
+// itself drops with the switching activity of dense data.
 #include "device_math.hpp"
 #include "kernels.hpp"
 #include "moduli.hpp"
@@ -60,18 +62,18 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 
 constexpr int BK = 128;  // k bytes per stage
 // Block tile shapes, the kernels' template parameter S (16 waves; a wave owns
-// 64 rows x 32 BB columns).  The library launches 2 and 3:
-//  1: 256 x 128 (the 128-column tile that 3 replaced);
+// 64 rows x 64 columns):
 //  2: 256 x 256;
 //  3: 512 x 128, for at most 128 columns (a 256-wide tile would leave half
-//     of every MFMA idle): a stage moves 80 KiB for twice the MACs of shape
-//     1's 48 KiB (17 % fewer operand bytes per MAC), and its two stages fill
-//     the 160 KiB of LDS.
+//     of every MFMA idle): a stage moves 80 KiB for twice the MACs of a
+//     256 x 128 tile's 48 KiB (17 % fewer operand bytes per MAC), and its two
+//     stages fill the 160 KiB of LDS.
 template <int S>
 struct Tile {
+  static_assert(S == 2 || S == 3, "tile shape");
   static constexpr int BM = S == 3 ? 512 : 256;  // output rows per block
   static constexpr int BN = S == 2 ? 256 : 128;  // output columns per block
-  static constexpr int BB = S == 1 ? 1 : 2;      // 32-column blocks per wave
+  static constexpr int BB = 2;                   // 32-column blocks per wave
   static constexpr int WC = BN / (32 * BB);      // waves across the tile
   static constexpr int ADMA = BM / 128;          // A slabs (8 rows x 128 B) per wave and stage
   static constexpr int BDMA = BN / 128;          // B slabs per wave and stage
@@ -733,15 +735,14 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(int64_t mn, int spli
   out[at] = (OT)r;
 }
 
-// Tile shape for n columns: at most 128 columns take a 128-wide tile (512
-// rows on the FP8 route, 256 on the int8 one), more columns 256 x 256.
+// Tile shape for n columns, on both routes: at most 128 columns take the
+// 512 x 128 tile, more columns 256 x 256.
 constexpr int gemm_shape(bool bytes, int64_t n) { return n <= 128 ? 3 : 2; }
 constexpr int64_t gemm_blocks(bool bytes, int64_t m, int64_t n) {
-  const int s = gemm_shape(bytes, n);
-  const int64_t bm = s == 3 ? Tile<3>::BM : Tile<1>::BM, bn = s == 2 ? Tile<2>::BN : Tile<1>::BN;
+  const bool tall = gemm_shape(bytes, n) == 3;
+  const int64_t bm = tall ? Tile<3>::BM : Tile<2>::BM, bn = tall ? Tile<3>::BN : Tile<2>::BN;
   return (int64_t)(bytes ? kRA : kR) * ((m + bm - 1) / bm) * ((n + bn - 1) / bn);
 }
-static_assert(Tile<1>::BM == Tile<2>::BM && Tile<1>::BN == Tile<3>::BN, "tile shapes");
 
 template <bool BYTES, typename OT>
 hipError_t launch_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* pa, const int8_t* pb,

@@ -222,6 +222,40 @@ def test_reconstruct_exact_ties():
     assert_bits_equal(Cd.cpu().numpy()[0], np.array([float(x) for x in Xs]), "ties vs CPython")
 
 
+def test_reconstruct_near_rounding_boundaries():
+    """Values at and next to rounding boundaries at every magnitude, near
+    small multiples of the high half's weight and at the range ends, unscaled
+    and scaled to land on the subnormal and overflow thresholds: bit for bit
+    with the oracle, and unscaled with CPython's correctly rounded int to
+    float conversion."""
+    log("reconstruct near rounding boundaries")
+    import torch
+    mods = oracle.moduli()
+    M = oracle.product_of_moduli()
+    Xs = workloads.boundary_values(M, _high_weight(mods))
+    n = len(Xs)
+    Cres = np.array([[_centred(x, mm) for x in Xs] for mm in mods], dtype=np.int32).reshape(12, 1, n)
+    hi, lo = oracle.garner(Cres)
+    ea = np.zeros(1, np.int32)
+    eb = np.zeros(n, np.int32)
+    Cd = oz.ozaki25_reconstruct(to_dev(Cres), to_dev(ea), to_dev(eb))
+    torch.cuda.synchronize()
+    assert_bits_equal(Cd.cpu().numpy(), oracle.reconstruct(hi, lo, ea, eb), "unscaled")
+    assert_bits_equal(Cd.cpu().numpy()[0], np.array([float(x) for x in Xs]), "unscaled vs CPython")
+    # sigma_i + tau_j = -e puts each result at exponent bitlen(X) - 1 + e
+    for target in (-1022, -1023, -1030, -1075, 1023, 1024):
+        eb = np.array([-(target - (abs(x).bit_length() - 1)) for x in Xs], dtype=np.int32)
+        Cd = oz.ozaki25_reconstruct(to_dev(Cres), to_dev(ea), to_dev(eb))
+        torch.cuda.synchronize()
+        assert_bits_equal(Cd.cpu().numpy(), oracle.reconstruct(hi, lo, ea, eb), f"result exponent {target}")
+
+
+def _high_weight(mods):
+    """Product of the moduli below the reconstruction's high half."""
+    split = 6 if len(mods) == 12 else 7
+    return math.prod(int(m) for m in mods[:split])
+
+
 # ------------------------------------------------------------ end to end
 @pytest.mark.parametrize("m,n,k,s,seed", [(64, 64, 64, 0.5, 1), (1, 1, 1, 1.0, 2), (3, 5, 7, 1.0, 3),
                                           (130, 129, 65, 2.0, 4), (257, 1, 300, 1.0, 5),
@@ -376,7 +410,7 @@ def test_dgemm_split_k_matches_oracle(m, n, k, seed):
 @pytest.mark.parametrize("m,n,k,seed", [(300, 128, 700, 84), (300, 129, 700, 85), (513, 96, 2000, 86),
                                         (260, 1, 129, 87)])
 def test_dgemm_narrow_tiles_match_oracle(m, n, k, seed):
-    """At most 128 columns use the 256 x 128 tile (n = 129 the 256 x 256 one)."""
+    """At most 128 columns use the 512 x 128 tile (n = 129 the 256 x 256 one)."""
     log(f"dgemm narrow m={m} n={n} k={k}")
     A = workloads.random_matrix(m, k, 1.0, seed)
     B = workloads.random_matrix(k, n, 1.0, seed + 1)

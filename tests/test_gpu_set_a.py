@@ -3,10 +3,12 @@
 
 Planes (int8 residues), per-modulus products and exponents must match bit
 for bit, the FP64 output to 0 ulp (any NaN matches any NaN).  Shapes span
-several 256 x 256 output tiles, several 128-byte k stages and ragged tails;
+several output tiles of both shapes, several 128-byte k stages and ragged tails;
 k values reach both residue paths of the deconstruction (scale bits above
 and at most 51) and the int32 segment reduction of the product (k beyond
 65536)."""
+import math
+
 import numpy as np
 import pytest
 
@@ -232,6 +234,40 @@ def test_reconstruct_exact_ties():
     hi, lo = oracle.garner(Cres, OSET)
     assert_bits_equal(Cd.cpu().numpy(), oracle.reconstruct(hi, lo, ea, eb), "ties")
     assert_bits_equal(Cd.cpu().numpy()[0], np.array([float(x) for x in Xs]), "ties vs CPython")
+
+
+def test_reconstruct_near_rounding_boundaries():
+    """Values at and next to rounding boundaries at every magnitude, near
+    small multiples of the high half's weight and at the range ends, unscaled
+    and scaled to land on the subnormal and overflow thresholds: bit for bit
+    with the oracle, and unscaled with CPython's correctly rounded int to
+    float conversion."""
+    log("[A15] reconstruct near rounding boundaries")
+    import torch
+    mods = oracle.moduli(OSET)
+    M = oracle.product_of_moduli(OSET)
+    Xs = workloads.boundary_values(M, _high_weight(mods))
+    n = len(Xs)
+    Cres = np.array([[_centred(x, mm) for x in Xs] for mm in mods], dtype=np.int32).reshape(15, 1, n)
+    hi, lo = oracle.garner(Cres, OSET)
+    ea = np.zeros(1, np.int32)
+    eb = np.zeros(n, np.int32)
+    Cd = oz.ozaki25_reconstruct(to_dev(Cres), to_dev(ea), to_dev(eb), set=SET)
+    torch.cuda.synchronize()
+    assert_bits_equal(Cd.cpu().numpy(), oracle.reconstruct(hi, lo, ea, eb), "unscaled")
+    assert_bits_equal(Cd.cpu().numpy()[0], np.array([float(x) for x in Xs]), "unscaled vs CPython")
+    # sigma_i + tau_j = -e puts each result at exponent bitlen(X) - 1 + e
+    for target in (-1022, -1023, -1030, -1075, 1023, 1024):
+        eb = np.array([-(target - (abs(x).bit_length() - 1)) for x in Xs], dtype=np.int32)
+        Cd = oz.ozaki25_reconstruct(to_dev(Cres), to_dev(ea), to_dev(eb), set=SET)
+        torch.cuda.synchronize()
+        assert_bits_equal(Cd.cpu().numpy(), oracle.reconstruct(hi, lo, ea, eb), f"result exponent {target}")
+
+
+def _high_weight(mods):
+    """Product of the moduli below the reconstruction's high half."""
+    split = 6 if len(mods) == 12 else 7
+    return math.prod(int(m) for m in mods[:split])
 
 
 # ------------------------------------------------------------ end to end

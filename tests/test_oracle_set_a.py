@@ -242,3 +242,20 @@ def test_set_a_is_at_least_as_accurate_as_published_set():
             ea += abs(Fraction(float(ra[i, j])) - exact)
             es += abs(Fraction(float(rs[i, j])) - exact)
     assert ea <= es
+
+
+def test_rounding_at_boundaries_matches_python():
+    """Values at and next to FP64 rounding boundaries at every magnitude,
+    unscaled and scaled onto the subnormal and overflow thresholds, round as
+    CPython's correctly rounded conversions do."""
+    mods = oracle.moduli(1)
+    Xs = workloads.boundary_values(oracle.product_of_moduli(1), math.prod(int(m) for m in mods[:7]))
+    C = np.array([[[_centred(x, m) for x in Xs]] for m in mods], dtype=np.int32)
+    hi, lo = oracle.garner(C, 1)
+    ea = np.zeros(1, np.int32)
+    for target in (None, -1022, -1023, -1030, -1075, 1023, 1024):
+        es = [0 if target is None else target - (abs(x).bit_length() - 1) for x in Xs]
+        eb = np.array([-e for e in es], dtype=np.int32)
+        got = oracle.reconstruct(hi, lo, ea, eb)[0]
+        want = np.array([_py_round(x, e) for x, e in zip(Xs, es)])
+        assert np.array_equal(got.view(np.uint64), want.view(np.uint64)), target

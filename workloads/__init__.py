@@ -76,3 +76,30 @@ def make_inputs(w: Workload | str, seed: int | None = None):
 def random_matrix(rows: int, cols: int, s: float, seed: int) -> np.ndarray:
     """A single seeded matrix of the same distribution (for ad-hoc shapes)."""
     return draw(np.random.default_rng(seed), rows, cols, s)
+
+
+def boundary_values(M: int, P: int) -> list:
+    """Integers in [-M/2, M/2) at or next to FP64 rounding boundaries at
+    every magnitude from 2^54 up: powers of two and midpoints between
+    neighbouring doubles, each with small offsets on both sides; values near
+    small multiples of P (the weight of the reconstruction's high half) and
+    the two ends of the range."""
+    h = M // 2
+    xs = []
+    top = h.bit_length() - 1
+    for b in range(54, top + 1):
+        pw = 1 << b
+        mid = pw + (5 << (b - 53)) + (1 << (b - 54))   # a midpoint with an odd neighbour below
+        for base in (pw, mid):
+            for d in (0, 1, -1, 2, -2, 17, -17, 33, -33, 64, -64, 1 << 12, -(1 << 12)):
+                xs.append(base + d)
+    for q in (1, 2, 3, 5):
+        for d in (0, 1, -1, P // 2, -(P // 2), P // 2 - 1, 1 << 40):
+            xs.append(q * P + d)
+    xs += [h - 1, h - 2, -h, -h + 1]
+    out = []
+    for x in xs:
+        for s in (x, -x):
+            if -h <= s < h:
+                out.append(s)
+    return out
