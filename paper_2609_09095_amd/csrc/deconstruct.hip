@@ -9,11 +9,10 @@
 // so every plane store is one 16-byte write.  VALU work and HBM traffic (8
 // bytes read and 30 bytes written per element) are close: the nonsquare
 // limb split comes from a small LDS table to keep the VALU side short.
-//  - A (side 0): a wavefront covers 1 row x 1024 k, so each plane store of the
-//    wavefront is 1 KiB contiguous.
-//  - B (side 1): a wavefront covers 8 columns x 128 k, so each plane store of
-//    the wavefront fills eight whole 128-byte lines; every FP64 load reads 64
-//    contiguous bytes of 8 rows of B.
+// A wavefront covers 8 vectors x 128 k on both sides (group_of), so each of
+// its plane stores is one contiguous KiB of the k-block-major layout:
+//  - A (side 0): eight lanes read 1 KiB of one row;
+//  - B (side 1): every FP64 load reads 64 contiguous bytes of 8 rows of B.
 #include <utility>
 
 #include "device_math.hpp"

@@ -2,7 +2,9 @@
 // for the all-byte set, fifteen) centred residues (Eq. (garner)), Horner recombination (Eq. (horner)), the lift to
 // [-M/2, M/2), and one rounding of X 2^(-sigma_i - tau_j) to FP64.
 // One thread per output; the residue loads coalesce along the output row.
-// 24 bytes in and 8 out per output, with VALU work of the same order.
+// 24 bytes in and 8 out per output (8 more in for C -= ...): the mix of
+// reads and writes bounds it at the rate of a plain copy, with the VALU work
+// (about 140 instructions per output) hidden under it.
 //
 // Integer work per output, all exact:
 //  - centred digits in one reduction each: v_j = (c_j w_j - sum_{l<j} v_l
