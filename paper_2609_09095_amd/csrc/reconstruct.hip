@@ -1,6 +1,7 @@
 // Reconstruction (Alg. 3): Garner's mixed-radix digits of the twelve (or,
-// for the all-byte set, fifteen) centred residues (Eq. (garner)), Horner recombination (Eq. (horner)), the lift to
-// [-M/2, M/2), and one rounding of X 2^(-sigma_i - tau_j) to FP64.
+// for the all-byte set, fifteen) centred residues (Eq. (garner)), Horner
+// recombination (Eq. (horner)), the lift to [-M/2, M/2), and one rounding
+// of X 2^(-sigma_i - tau_j) to FP64.
 // One thread per output; the residue loads coalesce along the output row.
 // 24 bytes in and 8 out per output (8 more in for C -= ...): the mix of
 // reads and writes bounds it at the rate of a plain copy, with the VALU work
@@ -274,7 +275,8 @@ __device__ __forceinline__ double reconstruct_one(const RT* rowq, int64_t mn, in
 // Fifteen centred residues, |c| <= 128.  Garner sums stay below 15 * 2^14 <
 // 2^18, so the FP32 quotient of a digit errs by less than 2^-5 / m_j and
 // rint gives the centred digit for odd m_j; m_0 = 256 takes the low eight
-// bits.  The sums run four terms at a time on the int8 dot product.  With 256 first and every other modulus odd, the balanced halves
+// bits.  The sums run four terms at a time on the int8 dot product.  With
+// 256 first and every other modulus odd, the balanced halves
 // Xl (digits 0-6, |Xl| <= P/2) and Xh (digits 7-14, |Xh| <= (Q-1)/2, Q odd)
 // give X = Xl + P Xh in exactly [-M/2, M/2): no lift is needed.  |X| < 2^117.
 constexpr int kSplitA = 7;
