@@ -178,14 +178,29 @@ __device__ __forceinline__ double round_exact_a(int64_t xl, int64_t xh, int e) {
   return neg ? -r : r;
 }
 
-// x = hi + lo exactly with hi = RN(x): the two 32-bit halves convert
-// exactly and Fast2Sum splits their one rounded sum (the high term has the
-// larger exponent unless it is 0, and then lo = 0).
-__device__ __forceinline__ double split_i64(int64_t x, double& lo) {
-  const double a = (double)(int32_t)(x >> 32) * 0x1p32, b = (double)(uint32_t)x;
-  const double hi = a + b;
-  lo = b - (hi - a);
-  return hi;
+// The halves of the all-byte set in FP64 from digit pairs g = v_j + m_j
+// v_{j+1} (|g| < 2^16).  Low half (digits 0-6): two exact fmas (below 2^40)
+// and one that rounds, so lh = RN(xl).  High half (digits 7-14): exact
+// fmas up to 2^47, then the last weight's product split exactly by fma
+// (ph + pl), pl + g exact (integers below 2^16), and Fast2Sum of ph and that
+// sum (|ph| is larger unless ph = 0, and then hl = 0), so hh = RN(xh) and
+// hl = xh - hh exactly, |hl| <= 2^8.
+__device__ __forceinline__ int digit_pair_a(const int (&v)[kRA], int j) {
+  return v[j] + __mul24(v[j + 1], kModulusA[j]);
+}
+__device__ __forceinline__ double weight_a(int j) { return (double)kModulusA[j] * kModulusA[j + 1]; }
+static_assert(kSplitA == 7 && kRA == 15, "three pairs and a digit low, four pairs high");
+__device__ __forceinline__ void halves_fp64_a(const int (&v)[kRA], double& lh, double& hh, double& hl) {
+  const double tl = __builtin_fma(weight_a(4), (double)v[6], (double)digit_pair_a(v, 4));
+  const double tm = __builtin_fma(weight_a(2), tl, (double)digit_pair_a(v, 2));
+  lh = __builtin_fma(weight_a(0), tm, (double)digit_pair_a(v, 0));
+  const double u = __builtin_fma(weight_a(11), (double)digit_pair_a(v, 13), (double)digit_pair_a(v, 11));
+  const double w = __builtin_fma(weight_a(9), u, (double)digit_pair_a(v, 9));
+  const double ph = weight_a(7) * w;
+  const double pl = __builtin_fma(weight_a(7), w, -ph);
+  const double ee = pl + (double)digit_pair_a(v, 7);
+  hh = ph + ee;
+  hl = ee - (hh - ph);
 }
 
 // The same rounding in FP64 with a proof, as round_fast for the published
@@ -201,9 +216,9 @@ __device__ __forceinline__ double split_i64(int64_t x, double& lo) {
 // r, a subnormal result); those outputs take round_exact_a.
 constexpr double kPAd = (double)kPA;
 static_assert((uint64_t)kPAd == kPA, "P is exact in FP64");
-__device__ __forceinline__ bool round_fast_a(int64_t xl, int64_t xh, int e, double& out) {
-  double hl, ll;
-  const double hh = split_i64(xh, hl), lh = split_i64(xl, ll);
+__device__ __forceinline__ bool round_fast_a(const int (&v)[kRA], int e, double& out) {
+  double lh, hh, hl;
+  halves_fp64_a(v, lh, hh, hl);
   const double p = hh * kPAd;
   const double ep = __builtin_fma(hh, kPAd, -p);
   const double q = __builtin_fma(hl, kPAd, lh);
@@ -214,7 +229,7 @@ __device__ __forceinline__ bool round_fast_a(int64_t xl, int64_t xh, int e, doub
   const int eb = (int)(rb >> 52) & 0x7FF;  // biased exponent of r (r >= 2^55 when xh != 0)
   const double halfu = __builtin_bit_cast(double, (uint64_t)(eb - 53) << 52);
   const double bound = __builtin_fma(__builtin_fabs(t), 0x1p-51, 0x1p13) + __builtin_fabs(res);
-  const bool rounded = xh == 0 || (bound < halfu && (rb << 12) != 0);
+  const bool rounded = hh == 0.0 || (bound < halfu && (rb << 12) != 0);
   out = __builtin_ldexp(r, e);
   return rounded && (eb + e >= 1 || eb == 0);
 }

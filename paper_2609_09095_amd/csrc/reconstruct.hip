@@ -220,11 +220,10 @@ __device__ __forceinline__ double reconstruct_one_a(const RT* rowq, int64_t mn, 
   [&]<int... J>(std::integer_sequence<int, J...>) {
     ((v[J] = garner_digit_a<J>(c, packed)), ...);
   }(std::make_integer_sequence<int, kRA>{});
-  const int64_t xl = half_value_a<0, kSplitA>(v);   // |xl| <= P/2
-  const int64_t xh = half_value_a<kSplitA, kRA>(v);  // |xh| <= (Q - 1) / 2
   const int e = -sa - sb;
   double out;
-  if (!round_fast_a(xl, xh, e, out)) out = round_exact_a(xl, xh, e);
+  if (!round_fast_a(v, e, out))  // |xl| <= P/2, |xh| <= (Q - 1) / 2
+    out = round_exact_a(half_value_a<0, kSplitA>(v), half_value_a<kSplitA, kRA>(v), e);
   return out;
 }
 

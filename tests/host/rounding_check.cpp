@@ -69,8 +69,15 @@ static bool run_s12(Set<kR>& S, const int (&v)[kR], int e) {
 }
 static bool run_a15(Set<kRA>& S, const int (&v)[kRA], int e) {
   const int64_t xl = half_value_a<0, kSplitA>(v), xh = half_value_a<kSplitA, kRA>(v);
+  // the FP64 halves: lh = RN(xl), hh = RN(xh), hh + hl = xh exactly (the
+  // host's int64 -> double conversion rounds to nearest even)
+  double lh, hh, hl;
+  halves_fp64_a(v, lh, hh, hl);
+  if (!same(lh, (double)xl) || !same(hh, (double)xh) || (i128)(int64_t)hh + (i128)(int64_t)hl != (i128)xh) {
+    if (++S.bad < 5) printf("A15 halves differ: xl=%lld xh=%lld\n", (long long)xl, (long long)xh);
+  }
   double f;
-  const bool ok = round_fast_a(xl, xh, e, f);
+  const bool ok = round_fast_a(v, e, f);
   const double x = round_exact_a(xl, xh, e);
   if (ok) {
     ++S.fast;
