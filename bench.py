@@ -103,14 +103,18 @@ def measured_traffic(w, moduli):
 
 
 def measured_deconstruction(w, moduli, scan_ms, dec_ms):
-    """HBM bytes the exponent scans and the deconstruction of both operands
-    move per call, as counted, and their fraction of the HBM peak over the
-    two stages' time."""
+    """Bytes the exponent scans and the deconstruction of both operands move
+    between L2 and the memory side per call (FETCH_SIZE + WRITE_SIZE, scaled),
+    and that rate over the two stages' time as a fraction of the HBM peak.
+    The deconstruction of a run re-reads what its scan just read, mostly from
+    the last-level cache, which these counters do not tell apart from HBM:
+    the fraction is an upper bound on HBM use."""
     b = counter_value(DEC_COUNTERS, w, sources_hash(DEC_SOURCES), f"hbm_bytes_per_call_{moduli}")
     if b is None:
         return {"measured_bytes": None, "measured_frac": None}
     return {"measured_bytes": b,
-            "measured_frac": round(b / ((scan_ms + dec_ms) * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+            "measured_frac": round(b / ((scan_ms + dec_ms) * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "measured_note": "bytes beyond L2 (HBM or the last-level cache); an upper bound on HBM use"}
 
 
 def cpu_baseline(A, B, w, rows, cols, cfg):

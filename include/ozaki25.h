@@ -193,9 +193,12 @@ ozaki25_status ozaki25_dgemm_sub(int64_t m, int64_t n, int64_t k, const double* 
  *   ozaki25_dgemm_workspace_size() bytes (256-byte aligned), owned by the
  *   caller and not used by anything else until the stream has passed this call.
  * stage_events: NULL, or OZAKI25_NUM_STAGE_EVENTS hipEvent_t handles (passed as
- *   void*) that are recorded on `stream` before the first kernel and after the
- *   exponent scans, the deconstruction, the residue products and the
- *   reconstruction, for per-stage timing. */
+ *   void*) that are recorded on `stream` before the first kernel, after the
+ *   exponent scans, after the deconstruction, after the residue products and
+ *   after the reconstruction, for per-stage timing.  The scans run
+ *   interleaved with the deconstruction (runs of about 256 MiB of each
+ *   operand, each deconstructed right after its scan), so the first two
+ *   events are recorded together and the deconstruct stage holds the scans. */
 ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
                                 const double* B, int64_t ldb, double* C, int64_t ldc,
                                 ozaki25_moduli_set set, ozaki25_quantiser quant, int subtract,

@@ -104,6 +104,31 @@ Workspace layout(int64_t m, int64_t n, int64_t k, ozaki25_moduli_set set) {
   return w;
 }
 
+// Exponent scan and deconstruction of one operand, in runs of whole
+// 256-vector tiles holding about 256 MiB of FP64 each (the size of the
+// MI355X last-level cache): each run's deconstruction reads the run right
+// after its scan, from that cache rather than HBM (8192 x 8192: 1.21 ->
+// 0.94 ms for both operands).  Each run writes its part of the full plane
+// layout.
+hipError_t scan_and_deconstruct(ozaki25_moduli_set set, ozaki25_quantiser quant, int side, int64_t vecs,
+                                int64_t k, const double* X, int64_t ldx, int t, int32_t* exps,
+                                int8_t* planes, hipStream_t s) {
+  const int64_t kp = k_pad(k);
+  constexpr int64_t kRunBytes = (int64_t)256 << 20, kTile = 256;
+  const int64_t per_run = kRunBytes / (kp * (int64_t)sizeof(double)) / kTile * kTile;
+  const int64_t run = per_run > kTile ? per_run : kTile;
+  hipError_t e = hipSuccess;
+  for (int64_t v0 = 0; v0 < vecs && e == hipSuccess; v0 += run) {
+    const int64_t nv = vecs - v0 < run ? vecs - v0 : run;
+    const double* Xr = side == 0 ? X + v0 * ldx : X + v0;
+    e = oz::launch_scan(side, nv, k, Xr, ldx, t, exps + v0, s);
+    if (e == hipSuccess)
+      e = oz::launch_deconstruct((int)set, (int)quant, side, nv, vecs, k, kp, t, Xr, ldx, exps + v0,
+                                 planes + v0 * oz::kKAlign, s);
+  }
+  return e;
+}
+
 }  // namespace
 
 extern "C" {
@@ -149,13 +174,8 @@ ozaki25_status ozaki25_deconstruct(int side, int64_t vecs, int64_t k, const doub
   if (!X || !planes || !exps) return OZAKI25_ERR_INVALID_VALUE;
   if (((uintptr_t)planes & 15) || ((uintptr_t)exps & 3) || ((uintptr_t)X & 7))
     return OZAKI25_ERR_INVALID_VALUE;
-  hipStream_t s = (hipStream_t)stream;
-  const int t = scale_bits(k, set);
-  hipError_t e = oz::launch_scan(side, vecs, k, X, ldx, t, exps, s);
-  if (e == hipSuccess)
-    e = oz::launch_deconstruct((int)set, (int)quant, side, vecs, k, k_pad(k), t, X, ldx, exps,
-                               (int8_t*)planes, s);
-  return hip_status(e);
+  return hip_status(scan_and_deconstruct(set, quant, side, vecs, k, X, ldx, scale_bits(k, set), exps,
+                                          (int8_t*)planes, (hipStream_t)stream));
 }
 
 ozaki25_status ozaki25_residue_gemm(int64_t m, int64_t n, int64_t k, const uint8_t* planesA,
@@ -241,11 +261,11 @@ ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A
   const int64_t kp = k_pad(k);
 
   if (ev) e = hipEventRecord(ev[0], s);
-  if (e == hipSuccess) e = oz::launch_scan(0, m, k, A, lda, t, ea, s);
-  if (e == hipSuccess) e = oz::launch_scan(1, n, k, B, ldb, t, eb, s);
+  // the scans run interleaved with the deconstruction (scan_and_deconstruct),
+  // so the scan stage is empty and the deconstruct stage holds both
   if (ev && e == hipSuccess) e = hipEventRecord(ev[1], s);
-  if (e == hipSuccess) e = oz::launch_deconstruct((int)set, (int)quant, 0, m, k, kp, t, A, lda, ea, pa, s);
-  if (e == hipSuccess) e = oz::launch_deconstruct((int)set, (int)quant, 1, n, k, kp, t, B, ldb, eb, pb, s);
+  if (e == hipSuccess) e = scan_and_deconstruct(set, quant, 0, m, k, A, lda, t, ea, pa, s);
+  if (e == hipSuccess) e = scan_and_deconstruct(set, quant, 1, n, k, B, ldb, t, eb, pb, s);
   if (ev && e == hipSuccess) e = hipEventRecord(ev[2], s);
   if (e == hipSuccess)
     e = bytes ? oz::launch_residue_gemm_bytes_i8(m, n, kp, pa, pb, (int8_t*)cres, (int8_t*)part,

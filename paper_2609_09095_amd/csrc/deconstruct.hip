@@ -250,9 +250,9 @@ __device__ __forceinline__ void scale_round(const double (&x)[kElems], int sigma
 }
 
 template <int SIDE, bool EXACT, bool TZ>
-__global__ __launch_bounds__(256) void deconstruct_kernel(int64_t vecs, int64_t k, int64_t kp,
-                                                          const double* __restrict__ X, int64_t ldx,
-                                                          const int32_t* __restrict__ exps,
+__global__ __launch_bounds__(256) void deconstruct_kernel(int64_t vecs, int64_t vstride, int64_t k,
+                                                          int64_t kp, const double* __restrict__ X,
+                                                          int64_t ldx, const int32_t* __restrict__ exps,
                                                           int8_t* __restrict__ planes) {
   int64_t v, g;
   group_of(vecs, v, g);
@@ -268,8 +268,8 @@ __global__ __launch_bounds__(256) void deconstruct_kernel(int64_t vecs, int64_t 
   double y[kElems];
   uint32_t ylo[kElems];
   scale_round<TZ, EXACT>(x, sigma, y, ylo);
-  emit_all<EXACT>(std::make_integer_sequence<int, kR>{}, y, ylo, planes, vecs * 128,
-                  plane_offset(vecs, kPlanes, v, g), lut);
+  emit_all<EXACT>(std::make_integer_sequence<int, kR>{}, y, ylo, planes, vstride * 128,
+                  plane_offset(vstride, kPlanes, v, g), lut);
 }
 
 // ---- all-byte set (Sec. 5.1, candidate A) on the int8 route: the centred
@@ -313,8 +313,8 @@ __device__ __forceinline__ void emit_all_bytes(std::integer_sequence<int, I...>,
 }
 
 template <int SIDE, bool EXACT, bool TZ>
-__global__ __launch_bounds__(256) void deconstruct_bytes_kernel(int64_t vecs, int64_t k, int64_t kp,
-                                                                const double* __restrict__ X,
+__global__ __launch_bounds__(256) void deconstruct_bytes_kernel(int64_t vecs, int64_t vstride, int64_t k,
+                                                                int64_t kp, const double* __restrict__ X,
                                                                 int64_t ldx,
                                                                 const int32_t* __restrict__ exps,
                                                                 int8_t* __restrict__ planes) {
@@ -327,39 +327,41 @@ __global__ __launch_bounds__(256) void deconstruct_bytes_kernel(int64_t vecs, in
   uint32_t ylo[kElems];
   const int sigma = load_group<SIDE>(vecs, k, X, ldx, exps, v, k0, true, x);
   scale_round<TZ, EXACT>(x, sigma, y, ylo);
-  emit_all_bytes<EXACT>(std::make_integer_sequence<int, kRA>{}, y, ylo, planes, vecs * 128,
-                        plane_offset(vecs, kRA, v, g));
+  emit_all_bytes<EXACT>(std::make_integer_sequence<int, kRA>{}, y, ylo, planes, vstride * 128,
+                        plane_offset(vstride, kRA, v, g));
 }
 
 template <int SIDE, bool BYTES, bool EXACT, bool TZ>
-void launch_one(int64_t blocks, int64_t vecs, int64_t k, int64_t kp, const double* X, int64_t ldx,
+void launch_one(int64_t blocks, int64_t vecs, int64_t vstride, int64_t k, int64_t kp, const double* X,
+                int64_t ldx,
                 const int32_t* exps, int8_t* planes, hipStream_t stream) {
   if constexpr (BYTES)
     hipLaunchKernelGGL((deconstruct_bytes_kernel<SIDE, EXACT, TZ>), dim3((unsigned)blocks), dim3(256),
-                       0, stream, vecs, k, kp, X, ldx, exps, planes);
+                       0, stream, vecs, vstride, k, kp, X, ldx, exps, planes);
   else
     hipLaunchKernelGGL((deconstruct_kernel<SIDE, EXACT, TZ>), dim3((unsigned)blocks), dim3(256), 0,
-                       stream, vecs, k, kp, X, ldx, exps, planes);
+                       stream, vecs, vstride, k, kp, X, ldx, exps, planes);
 }
 
 template <int SIDE, bool BYTES>
-void launch_side(int64_t blocks, bool exact, bool tz, int64_t vecs, int64_t k, int64_t kp,
+void launch_side(int64_t blocks, bool exact, bool tz, int64_t vecs, int64_t vstride, int64_t k, int64_t kp,
                  const double* X, int64_t ldx, const int32_t* exps, int8_t* planes,
                  hipStream_t stream) {
   if (exact) {
-    if (tz) launch_one<SIDE, BYTES, true, true>(blocks, vecs, k, kp, X, ldx, exps, planes, stream);
-    else launch_one<SIDE, BYTES, true, false>(blocks, vecs, k, kp, X, ldx, exps, planes, stream);
+    if (tz) launch_one<SIDE, BYTES, true, true>(blocks, vecs, vstride, k, kp, X, ldx, exps, planes, stream);
+    else launch_one<SIDE, BYTES, true, false>(blocks, vecs, vstride, k, kp, X, ldx, exps, planes, stream);
   } else {
-    if (tz) launch_one<SIDE, BYTES, false, true>(blocks, vecs, k, kp, X, ldx, exps, planes, stream);
-    else launch_one<SIDE, BYTES, false, false>(blocks, vecs, k, kp, X, ldx, exps, planes, stream);
+    if (tz) launch_one<SIDE, BYTES, false, true>(blocks, vecs, vstride, k, kp, X, ldx, exps, planes, stream);
+    else launch_one<SIDE, BYTES, false, false>(blocks, vecs, vstride, k, kp, X, ldx, exps, planes, stream);
   }
 }
 
 }  // namespace
 
-hipError_t launch_deconstruct(int set, int quant, int side, int64_t vecs, int64_t k, int64_t kp,
-                              int t, const double* X, int64_t ldx, const int32_t* exps,
+hipError_t launch_deconstruct(int set, int quant, int side, int64_t vecs, int64_t vstride, int64_t k,
+                              int64_t kp, int t, const double* X, int64_t ldx, const int32_t* exps,
                               int8_t* planes, hipStream_t stream) {
+  if (vstride < vecs) return hipErrorInvalidValue;
   if (vecs <= 0 || kp <= 0) return hipSuccess;
   const bool bytes = set == kSetBytes;
   const bool tz = quant == kQuantTZ;
@@ -368,11 +370,11 @@ hipError_t launch_deconstruct(int set, int quant, int side, int64_t vecs, int64_
   const bool exact = t <= (bytes ? 51 : 50);
   const int64_t blocks = ((vecs + 31) / 32) * (kp / 128);
   if (side == 0) {
-    if (bytes) launch_side<0, true>(blocks, exact, tz, vecs, k, kp, X, ldx, exps, planes, stream);
-    else launch_side<0, false>(blocks, exact, tz, vecs, k, kp, X, ldx, exps, planes, stream);
+    if (bytes) launch_side<0, true>(blocks, exact, tz, vecs, vstride, k, kp, X, ldx, exps, planes, stream);
+    else launch_side<0, false>(blocks, exact, tz, vecs, vstride, k, kp, X, ldx, exps, planes, stream);
   } else {
-    if (bytes) launch_side<1, true>(blocks, exact, tz, vecs, k, kp, X, ldx, exps, planes, stream);
-    else launch_side<1, false>(blocks, exact, tz, vecs, k, kp, X, ldx, exps, planes, stream);
+    if (bytes) launch_side<1, true>(blocks, exact, tz, vecs, vstride, k, kp, X, ldx, exps, planes, stream);
+    else launch_side<1, false>(blocks, exact, tz, vecs, vstride, k, kp, X, ldx, exps, planes, stream);
   }
   return hipGetLastError();
 }

@@ -22,9 +22,11 @@ hipError_t launch_scan(int side, int64_t vecs, int64_t k, const double* X, int64
 
 // Alg. 2: scale, quantise, residues and the planes of one operand, given exps
 // and the scale bits t: e4m3 limb planes (published set) or int8 residue
-// planes (all-byte set).
-hipError_t launch_deconstruct(int set, int quant, int side, int64_t vecs, int64_t k, int64_t kp,
-                              int t, const double* X, int64_t ldx, const int32_t* exps,
+// planes (all-byte set).  vecs vectors of X, written into a plane layout of
+// vstride >= vecs vectors (planes points at the first one's bytes), so that
+// a run of vectors can fill its part of a larger operand's planes.
+hipError_t launch_deconstruct(int set, int quant, int side, int64_t vecs, int64_t vstride, int64_t k,
+                              int64_t kp, int t, const double* X, int64_t ldx, const int32_t* exps,
                               int8_t* planes, hipStream_t stream);
 
 // Eq. (residueprod): r centred per-modulus products [r][m][n], on FP8 MFMA
