@@ -118,18 +118,64 @@ def measured_deconstruction(w, moduli, scan_ms, dec_ms):
 
 
 def cpu_baseline(A, B, w, rows, cols, cfg):
+    """The oracle as it stands on `rows` x `cols` outputs of the workload at
+    full k, its output rows dealt over host threads (one oracle call per
+    block of rows; the oracle's C calls release the GIL)."""
+    import concurrent.futures as cf
     import oracle
     oracle.build(force=False)
-    ridx = np.arange(rows)
+    threads = max(1, min(16, os.cpu_count() or 1, rows))
     cidx = np.arange(cols)
+    blocks = np.array_split(np.arange(rows), threads)
     t0 = time.perf_counter()
-    oracle.dgemm(A, B, rows=ridx, cols=cidx, want_planes=False, set=cfg["oracle_set"])
+    with cf.ThreadPoolExecutor(max_workers=threads) as ex:
+        for f in [ex.submit(oracle.dgemm, A, B, rows=b, cols=cidx, want_planes=False, set=cfg["oracle_set"])
+                  for b in blocks]:
+            f.result()
     dt = time.perf_counter() - t0
     flops = 2.0 * rows * cols * w.k
-    return {"value": flops / dt / 1e12, "unit": "TFLOPS", "cores": 1, "kind": "oracle",
+    return {"value": flops / dt / 1e12, "unit": "TFLOPS", "cores": threads, "kind": "oracle",
             "sample": f"{rows} rows of A x {cols} columns of B of the {w.name} workload, full k={w.k} "
                       f"(exponent scan, quantise, residues, {cfg['r']} int64 residue GEMMs, Garner, "
-                      f"rounding, exact-product check), {dt:.1f} s single-threaded"}
+                      f"rounding, exact-product check), {dt:.1f} s on {threads} threads"}
+
+
+def vendor_lowp_gemm(torch, w, cfg, steps):
+    """The vendor library's dense low-precision GEMM on one residue product's
+    shape (m x k times k x n, limb-sized integer data): hipBLASLt e4m3 through
+    torch._scaled_mm for the published set, int8 through torch._int_mm for the
+    all-byte set.  A practical reference for the residue GEMM's rate, not part
+    of the emulated path."""
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    A = torch.randint(-22, 23, (w.m, w.k), dtype=torch.int8, device=dev, generator=g)
+    Bt = torch.randint(-22, 23, (w.n, w.k), dtype=torch.int8, device=dev, generator=g)
+    if cfg["dtype"] == "fp8":
+        Af = A.to(torch.float32).to(torch.float8_e4m3fn)
+        Bf = Bt.to(torch.float32).to(torch.float8_e4m3fn)
+        one = torch.tensor(1.0, device=dev)
+        fn = lambda: torch._scaled_mm(Af, Bf.t(), scale_a=one, scale_b=one, out_dtype=torch.bfloat16)  # noqa: E731
+        lib_name = "hipBLASLt e4m3 x e4m3 -> bf16 (torch._scaled_mm)"
+    else:
+        fn = lambda: torch._int_mm(A, Bt.t())  # noqa: E731
+        lib_name = "int8 x int8 -> int32 (torch._int_mm)"
+    try:
+        fn()
+        torch.cuda.synchronize()
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s0.record()
+        for _ in range(steps):
+            fn()
+        s1.record()
+        torch.cuda.synchronize()
+        ms = s0.elapsed_time(s1) / steps
+    except Exception as e:  # the library may lack a solution for the shape
+        return {"library": lib_name, "error": str(e)[:200]}
+    tops = 2.0 * w.m * w.n * w.k / (ms * 1e-3) / 1e12
+    return {"library": lib_name, "ms_per_call": round(ms, 4), "achieved": round(tops, 1),
+            "peak": cfg["peak"], "frac": round(tops / cfg["peak"], 4),
+            "unit": "TFLOP/s" if cfg["dtype"] == "fp8" else "TOP/s"}
 
 
 def time_set(oz, torch, w, Ad, Bd, Cd, cfg, steps, warmup, quant):
@@ -157,8 +203,9 @@ def time_set(oz, torch, w, Ad, Bd, Cd, cfg, steps, warmup, quant):
     torch.cuda.synchronize()
     ms = start.elapsed_time(end) / steps
     stage = np.array([[row[j].elapsed_time(row[j + 1]) for j in range(oz.NUM_STAGE_EVENTS - 1)] for row in ev])
+    median = float(np.median([row[0].elapsed_time(row[-1]) for row in ev]))
     del ws
-    return ms, stage.mean(axis=0).tolist()
+    return ms, stage.mean(axis=0).tolist(), median
 
 
 def time_planes(oz, torch, w, Ad, Bd, Cd, cfg, steps, quant):
@@ -234,7 +281,10 @@ def main():
     ap.add_argument("--workload", default="square", choices=sorted(workloads.WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-native", action="store_true")
-    ap.add_argument("--baseline-sample", type=int, default=512)
+    ap.add_argument("--baseline-rows", type=int, default=4096,
+                    help="rows of A in the oracle's timed sample (all of them when fewer)")
+    ap.add_argument("--baseline-cols", type=int, default=1024,
+                    help="columns of B in the oracle's timed sample (all of them when fewer)")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="copy 1 GiB device to device once before the run (a known-size kernel "
                          "for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE counters)")
@@ -279,7 +329,7 @@ def main():
     cfg = SETS[args.moduli]
     quant = oz.TZ if args.quantiser == "tz" else oz.RN
     log(f"[bench] {cfg['moduli']}: warmup {args.warmup}, timing {args.steps} steps")
-    ms, stages = time_set(oz, torch, w, Ad, Bd, Cd, cfg, args.steps, args.warmup, quant)
+    ms, stages, ms_median = time_set(oz, torch, w, Ad, Bd, Cd, cfg, args.steps, args.warmup, quant)
     scan_ms, dec_ms, gemm_ms, rec_ms = stages
     rt = rates(w, cfg, ms, stages)
     log(f"[bench] {ms:.3f} ms/step; scan {scan_ms:.3f} deconstruct {dec_ms:.3f} gemm {gemm_ms:.3f} "
@@ -292,7 +342,7 @@ def main():
         if C0d is not None:
             Cd.copy_(C0d)
         log(f"[bench] {ocfg['moduli']}: warmup {args.warmup}, timing {args.steps} steps")
-        oms, ostages = time_set(oz, torch, w, Ad, Bd, Cd, ocfg, args.steps, args.warmup, quant)
+        oms, ostages, _ = time_set(oz, torch, w, Ad, Bd, Cd, ocfg, args.steps, args.warmup, quant)
         ort = rates(w, ocfg, oms, ostages)
         log(f"[bench] {oms:.3f} ms/step; stages {[round(x, 3) for x in ostages]}")
         other = {
@@ -329,18 +379,30 @@ def main():
     gms = time_graph(oz, torch, w, Ad, Bd, Cd, cfg, args.steps, quant)
 
     native = None
-    if not args.no_native and not w.subtract and w.m * w.n * w.k <= 8192 ** 3:
-        log("[bench] native FP64 matmul")
-        Cn = torch.matmul(Ad, Bd)
+    vendor = None
+    if not args.no_native:
+        log("[bench] native FP64 " + ("addmm (C - A.B)" if w.subtract else "matmul"))
+        if w.subtract:
+            Cn = C0d.clone()
+            fn = lambda: torch.addmm(C0d, Ad, Bd, beta=1.0, alpha=-1.0, out=Cn)  # noqa: E731
+        else:
+            Cn = torch.empty((w.m, w.n), dtype=torch.float64, device=dev)
+            fn = lambda: torch.matmul(Ad, Bd, out=Cn)  # noqa: E731
+        fn()
         torch.cuda.synchronize()
         s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         s0.record()
         for _ in range(3):
-            torch.matmul(Ad, Bd, out=Cn)
+            fn()
         s1.record()
         torch.cuda.synchronize()
         native = w.flops / (s0.elapsed_time(s1) / 3 * 1e-3) / 1e12
         del Cn
+        log("[bench] vendor low-precision GEMM on one residue product's shape")
+        vendor = vendor_lowp_gemm(torch, w, cfg, args.steps)
+        if "achieved" in vendor:
+            per_product = rt["gemm_tops"]
+            vendor["residue_gemm_over_vendor"] = round(per_product / vendor["achieved"], 4)
 
     peak_unit = "TFLOP/s" if cfg["dtype"] == "fp8" else "TOP/s"
     result = {
@@ -351,6 +413,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
+        "ms_per_step_median": round(ms_median, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -386,6 +449,7 @@ def main():
                          "unit": "TFLOPS",
                          "note": "one ozaki25_dgemm_ex call captured in a HIP graph, replayed"},
         "native_fp64_tflops": round(native, 2) if native else None,
+        "vendor_lowp_gemm": vendor,
         "native_fp64_peak_tflops": FP64_PEAK_TFLOPS,
         "paper_context": "modelled Rubin projections (no measurement in the paper): 473 TFLOPS roof, 182-235 TFLOPS floors",
     }
@@ -394,8 +458,8 @@ def main():
     del Ad, Bd, Cd, C0d
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
-        rows = min(args.baseline_sample, w.m)
-        cols = min(args.baseline_sample, w.n)
+        rows = min(args.baseline_rows, w.m)
+        cols = min(args.baseline_cols, w.n)
         log(f"[bench] cpu baseline: oracle on {rows}x{cols} outputs")
         result["cpu_baseline"] = cpu_baseline(A, B, w, rows, cols, cfg)
     else:

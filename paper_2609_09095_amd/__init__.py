@@ -114,13 +114,55 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
 
 
-def _matrix(t, name):
+def _on_gpu(ts):
+    """Every tensor on one CUDA device (checked after the shapes and sizes,
+    so that shape errors are reported first)."""
+    dev = None
+    for name, t in ts:
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be a CUDA tensor")
+        if dev is None:
+            dev = t.device
+        elif t.device != dev:
+            raise ValueError(f"{name} is on {t.device}, not on {dev} like the other operands")
+
+
+def _matrix(t, name, shape=None):
+    """A 2-D float64 row-major matrix; returns (t, leading dimension)."""
     import torch
-    if not (isinstance(t, torch.Tensor) and t.is_cuda and t.dtype == torch.float64 and t.dim() == 2):
-        raise ValueError(f"{name} must be a 2-D float64 CUDA tensor")
+    if not (isinstance(t, torch.Tensor) and t.dtype == torch.float64 and t.dim() == 2):
+        raise ValueError(f"{name} must be a 2-D float64 tensor")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
     if t.stride(1) != 1 and t.shape[1] > 1:
         raise ValueError(f"{name} must be row-major (unit column stride)")
+    if t.shape[0] > 1 and t.stride(0) < t.shape[1]:
+        raise ValueError(f"{name} rows overlap (row stride below the row length)")
     return t, max(t.stride(0), t.shape[1], 1)
+
+
+def _buffer(t, name, dtypes, numel):
+    """A contiguous tensor of one of `dtypes` holding at least `numel` elements."""
+    import torch
+    if not isinstance(t, torch.Tensor) or t.dtype not in dtypes:
+        raise ValueError(f"{name} must be a tensor of dtype {' or '.join(str(d) for d in dtypes)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() < numel:
+        raise ValueError(f"{name} holds {t.numel()} elements, needs at least {numel}")
+    return t
+
+
+def _u8():
+    import torch
+    return (torch.uint8, torch.int8)
+
+
+def _i32():
+    import torch
+    return (torch.int32,)
 
 
 # ----------------------------------------------------------------- host-only
@@ -163,6 +205,8 @@ def ozaki25_deconstruct(side: int, X, planes=None, exps=None, set: int = S12, qu
     planes uint8 [k_pad/128][num_planes][vecs][128] (S12: limbs as OCP e4m3
     bytes; A15: int8 residues as two's complement bytes), exps int32 [vecs]."""
     import torch
+    if side not in (0, 1):
+        raise ValueError(f"side must be 0 (A) or 1 (B), not {side}")
     X, ldx = _matrix(X, "X")
     vecs, k = (X.shape[0], X.shape[1]) if side == 0 else (X.shape[1], X.shape[0])
     kp = ozaki25_k_pad(k)
@@ -173,8 +217,9 @@ def ozaki25_deconstruct(side: int, X, planes=None, exps=None, set: int = S12, qu
         planes = torch.empty((kp // K_ALIGN, npl, vecs, K_ALIGN), dtype=torch.uint8, device=X.device)
     if exps is None:
         exps = torch.empty((vecs,), dtype=torch.int32, device=X.device)
-    if planes.numel() < npl * vecs * kp or exps.numel() < vecs:
-        raise ValueError("output buffers too small")
+    _buffer(planes, "planes", _u8(), npl * vecs * kp)
+    _buffer(exps, "exps", _i32(), vecs)
+    _on_gpu([("X", X), ("planes", planes), ("exps", exps)])
     _check(lib().ozaki25_deconstruct(side, vecs, k, _ptr(X), ldx, set, quantiser, _ptr(planes),
                                      _ptr(exps), _stream(stream)), "ozaki25_deconstruct")
     return planes, exps
@@ -184,14 +229,17 @@ def ozaki25_residue_gemm(m: int, n: int, k: int, planesA, planesB, Cres=None, se
                          stream=None):
     """Centred per-modulus products, int32 [r][m][n]."""
     import torch
-    dev = planesA.device
     r = ozaki25_num_moduli(set)
     if r < 0:
         raise ValueError(f"unknown modulus set {set}")
+    if min(m, n, k) < 0:
+        raise ValueError("negative dimension")
+    _buffer(planesA, "planesA", _u8(), ozaki25_planes_bytes(m, k, set))
+    _buffer(planesB, "planesB", _u8(), ozaki25_planes_bytes(n, k, set))
     if Cres is None:
-        Cres = torch.empty((r, m, n), dtype=torch.int32, device=dev)
-    if Cres.numel() < r * m * n:
-        raise ValueError("Cres too small")
+        Cres = torch.empty((r, m, n), dtype=torch.int32, device=planesA.device)
+    _buffer(Cres, "Cres", _i32(), r * m * n)
+    _on_gpu([("planesA", planesA), ("planesB", planesB), ("Cres", Cres)])
     _check(lib().ozaki25_residue_gemm(m, n, k, _ptr(planesA), _ptr(planesB), set, _ptr(Cres),
                                       _stream(stream)), "ozaki25_residue_gemm")
     return Cres
@@ -201,25 +249,39 @@ def ozaki25_reconstruct(Cres, expsA, expsB, C=None, subtract: bool = False, set:
                         stream=None):
     """C (m x n float64) from int32 residues [r][m][n] and the exponents."""
     import torch
+    r = ozaki25_num_moduli(set)
+    if r < 0:
+        raise ValueError(f"unknown modulus set {set}")
+    _buffer(expsA, "expsA", _i32(), 0)
+    _buffer(expsB, "expsB", _i32(), 0)
     m, n = expsA.numel(), expsB.numel()
+    _buffer(Cres, "Cres", _i32(), r * m * n)
     if C is None:
         C = torch.empty((m, n), dtype=torch.float64, device=Cres.device)
-    C, ldc = _matrix(C, "C")
+    C, ldc = _matrix(C, "C", (m, n))
+    _on_gpu([("Cres", Cres), ("expsA", expsA), ("expsB", expsB), ("C", C)])
     _check(lib().ozaki25_reconstruct(m, n, _ptr(Cres), _ptr(expsA), _ptr(expsB), set, _ptr(C), ldc,
                                      1 if subtract else 0, _stream(stream)), "ozaki25_reconstruct")
     return C
 
 
 # ----------------------------------------------------------------- GEMM
+def _workspace(workspace):
+    if workspace is None:
+        return ctypes.c_void_p(0), 0
+    _buffer(workspace, "workspace", _u8(), 0)
+    return _ptr(workspace), workspace.numel()
+
+
 def ozaki25_dgemm_ex(A, B, C, subtract: bool = False, workspace=None, stage_events=None,
                      set: int = S12, quantiser: int = RN, stream=None):
     A, lda = _matrix(A, "A")
-    B, ldb = _matrix(B, "B")
-    C, ldc = _matrix(C, "C")
     m, k = A.shape
-    k2, n = B.shape
-    if k2 != k or tuple(C.shape) != (m, n):
-        raise ValueError("shape mismatch")
+    B, ldb = _matrix(B, "B")
+    if B.shape[0] != k:
+        raise ValueError(f"B has {B.shape[0]} rows, A has {k} columns")
+    n = B.shape[1]
+    C, ldc = _matrix(C, "C", (m, n))
     ev = None
     if stage_events is not None:
         handles = []
@@ -227,9 +289,11 @@ def ozaki25_dgemm_ex(A, B, C, subtract: bool = False, workspace=None, stage_even
             if not hasattr(e, "cuda_event") or not e.cuda_event:
                 raise ValueError("stage events must be recorded torch.cuda.Event objects")
             handles.append(e.cuda_event)
+        if len(handles) != NUM_STAGE_EVENTS:
+            raise ValueError(f"need {NUM_STAGE_EVENTS} stage events")
         ev = (ctypes.c_void_p * NUM_STAGE_EVENTS)(*handles)
-    ws_ptr = _ptr(workspace) if workspace is not None else ctypes.c_void_p(0)
-    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    ws_ptr, ws_bytes = _workspace(workspace)
+    _on_gpu([("A", A), ("B", B), ("C", C), ("workspace", workspace)])
     _check(lib().ozaki25_dgemm_ex(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, set, quantiser,
                                   1 if subtract else 0, ws_ptr, ws_bytes,
                                   ctypes.cast(ev, ctypes.c_void_p) if ev is not None else None,
@@ -241,14 +305,15 @@ def ozaki25_dgemm(A, B, C=None, set: int = S12, stream=None):
     """C = A B (float64, row-major CUDA tensors)."""
     import torch
     A, lda = _matrix(A, "A")
-    B, ldb = _matrix(B, "B")
     m, k = A.shape
-    k2, n = B.shape
-    if k2 != k:
-        raise ValueError("shape mismatch")
+    B, ldb = _matrix(B, "B")
+    if B.shape[0] != k:
+        raise ValueError(f"B has {B.shape[0]} rows, A has {k} columns")
+    n = B.shape[1]
     if C is None:
         C = torch.empty((m, n), dtype=torch.float64, device=A.device)
-    C, ldc = _matrix(C, "C")
+    C, ldc = _matrix(C, "C", (m, n))
+    _on_gpu([("A", A), ("B", B), ("C", C)])
     _check(lib().ozaki25_dgemm(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, set,
                                _stream(stream)), "ozaki25_dgemm")
     return C
@@ -257,10 +322,13 @@ def ozaki25_dgemm(A, B, C=None, set: int = S12, stream=None):
 def ozaki25_dgemm_sub(A, B, C, set: int = S12, stream=None):
     """C <- C - A B in place."""
     A, lda = _matrix(A, "A")
-    B, ldb = _matrix(B, "B")
-    C, ldc = _matrix(C, "C")
     m, k = A.shape
-    _, n = B.shape
+    B, ldb = _matrix(B, "B")
+    if B.shape[0] != k:
+        raise ValueError(f"B has {B.shape[0]} rows, A has {k} columns")
+    n = B.shape[1]
+    C, ldc = _matrix(C, "C", (m, n))
+    _on_gpu([("A", A), ("B", B), ("C", C)])
     _check(lib().ozaki25_dgemm_sub(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, set,
                                    _stream(stream)), "ozaki25_dgemm_sub")
     return C
@@ -276,20 +344,22 @@ def ozaki25_dgemm_planes(k: int, planesA, expsA, planesB, expsB, C=None, subtrac
     exponents from ozaki25_deconstruct of A (side 0) and B (side 1) with this
     k and set.  m and n come from the exponent vectors."""
     import torch
-    m, n = expsA.numel(), expsB.numel()
-    kp = ozaki25_k_pad(k)
     npl = ozaki25_num_planes(set)
     if npl < 0:
         raise ValueError(f"unknown modulus set {set}")
-    if planesA.numel() < npl * m * kp or planesB.numel() < npl * n * kp:
-        raise ValueError("plane buffers too small for this k and set")
+    if k < 0:
+        raise ValueError("negative k")
+    _buffer(expsA, "expsA", _i32(), 0)
+    _buffer(expsB, "expsB", _i32(), 0)
+    m, n = expsA.numel(), expsB.numel()
+    _buffer(planesA, "planesA", _u8(), ozaki25_planes_bytes(m, k, set))
+    _buffer(planesB, "planesB", _u8(), ozaki25_planes_bytes(n, k, set))
     if C is None:
         C = torch.empty((m, n), dtype=torch.float64, device=expsA.device)
-    C, ldc = _matrix(C, "C")
-    if tuple(C.shape) != (m, n):
-        raise ValueError("shape mismatch")
-    ws_ptr = _ptr(workspace) if workspace is not None else ctypes.c_void_p(0)
-    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    C, ldc = _matrix(C, "C", (m, n))
+    ws_ptr, ws_bytes = _workspace(workspace)
+    _on_gpu([("planesA", planesA), ("expsA", expsA), ("planesB", planesB), ("expsB", expsB), ("C", C),
+             ("workspace", workspace)])
     _check(lib().ozaki25_dgemm_planes(m, n, k, _ptr(planesA), _ptr(expsA), _ptr(planesB), _ptr(expsB),
                                       _ptr(C), ldc, set, 1 if subtract else 0, ws_ptr, ws_bytes,
                                       _stream(stream)), "ozaki25_dgemm_planes")

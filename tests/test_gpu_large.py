@@ -1,21 +1,27 @@
-"""Parity at the full workload sizes, through the same entry points the
-benchmark times (ozaki25_dgemm_ex with a caller workspace), on sampled
-outputs that the oracle computes one by one.
+"""Parity at the full workload sizes, through the entry points the benchmark
+times (ozaki25_dgemm_ex with a caller workspace) and the stage API.
 
-Per workload: every exponent of A's rows and B's columns, the planes of a
-sample of rows and columns, the per-modulus products and the final C on the
-sampled rows x columns (which always include the first and last row and
-column, i.e. the ragged tiles), all bit for bit."""
+Per workload and modulus set:
+ * every exponent of A's rows and B's columns, bit for bit;
+ * every byte of both operands' stored planes (padding included), against the
+   oracle's quantiser, residues and limb split, streamed in slabs of 1024
+   vectors (tests/plane_check.py);
+ * the per-modulus products C^(i) (int32, stage API) and the final C of
+   ozaki25_dgemm_ex on a seeded sample of 256 rows x 256 columns (all columns
+   when n < 256) that always includes the first two and last two rows and
+   columns, i.e. the ragged tiles, bit for bit."""
 import numpy as np
 import pytest
 
 import oracle
 import paper_2609_09095_amd as oz
 import workloads
-from gpu_util import (device_layout, assert_bits_equal, assert_int_equal, e4m3_bytes, int8_bytes, log, require_gpu,
-                      sample_indices)
+from gpu_util import assert_bits_equal, assert_int_equal, log, require_gpu, sample_indices
+from plane_check import compare_planes_full
 
 pytestmark = pytest.mark.gpu
+
+NSAMPLE = 256
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -23,15 +29,14 @@ def gpu():
     require_gpu()
 
 
-def _run(name, nsample=96, set=oz.S12):
+def _run(name, set=oz.S12):
     """set: the library's modulus set (the oracle numbers them alike)."""
     import torch
     w = workloads.WORKLOADS[name]
-    plane_bytes = int8_bytes if set == oz.A15 else e4m3_bytes
     log(f"[large] {name} set={set}: generating m={w.m} n={w.n} k={w.k}")
     A, B, C0 = workloads.make_inputs(w)
-    rows = sample_indices(w.m, nsample, 11)
-    cols = sample_indices(w.n, nsample, 12)
+    rows = sample_indices(w.m, NSAMPLE, 11)
+    cols = sample_indices(w.n, NSAMPLE, 12)
     Ad = torch.from_numpy(A).cuda()
     Bd = torch.from_numpy(B).cuda()
     Cd = torch.from_numpy(C0).cuda() if C0 is not None else torch.empty((w.m, w.n), dtype=torch.float64, device="cuda")
@@ -51,22 +56,24 @@ def _run(name, nsample=96, set=oz.S12):
     planesB, expsB = oz.ozaki25_deconstruct(1, Bd, set=set)
     torch.cuda.synchronize()
     del Ad, Bd
-    pA_s = planesA.index_select(2, ri).cpu().numpy()
-    pB_s = planesB.index_select(2, ci).cpu().numpy()
     Cres = oz.ozaki25_residue_gemm(w.m, w.n, w.k, planesA, planesB, set=set)
     torch.cuda.synchronize()
     Cres_s = Cres.index_select(1, ri).index_select(2, ci).cpu().numpy()
-    eA, eB = expsA.cpu().numpy(), expsB.cpu().numpy()
-    del planesA, planesB, Cres
+    del Cres
+    torch.cuda.empty_cache()
+
+    t = oracle.scale_bits(w.k, set)
+    sigma = oracle.exponents(A, 0, t)
+    tau = oracle.exponents(B, 1, t)
+    assert_int_equal(expsA.cpu().numpy(), sigma, "sigma (all rows)")
+    assert_int_equal(expsB.cpu().numpy(), tau, "tau (all columns)")
+    compare_planes_full(planesA, A, 0, sigma, set, f"{name} planes of A")
+    compare_planes_full(planesB, B, 1, tau, set, f"{name} planes of B")
+    del planesA, planesB
     torch.cuda.empty_cache()
 
     log(f"[large] {name}: oracle on {len(rows)} x {len(cols)} outputs")
-    t = oracle.scale_bits(w.k, set)
-    assert_int_equal(eA, oracle.exponents(A, 0, t), "sigma (all rows)")
-    assert_int_equal(eB, oracle.exponents(B, 1, t), "tau (all columns)")
-    r = oracle.dgemm(A, B, C_in=C0, rows=rows, cols=cols, set=set)
-    assert_int_equal(pA_s, device_layout(plane_bytes(r.planesA)), "planes of sampled rows of A")
-    assert_int_equal(pB_s, device_layout(plane_bytes(r.planesB)), "planes of sampled columns of B")
+    r = oracle.dgemm(A, B, C_in=C0, rows=rows, cols=cols, set=set, want_planes=False)
     assert_int_equal(Cres_s, r.Cres, "per-modulus products (sampled)")
     assert_bits_equal(C_s, r.C, "C (sampled)")
     log(f"[large] {name}: ok")
@@ -81,11 +88,11 @@ def test_ragged_8191_8209_7937():
 
 
 def test_hpl_trailing_update_32768_1024():
-    _run("hpl", nsample=64)
+    _run("hpl")
 
 
 def test_block_krylov_262144_128_4096():
-    _run("krylov", nsample=128)
+    _run("krylov")
 
 
 def test_long_k_single_output():
@@ -107,8 +114,8 @@ def test_ragged_8191_8209_7937_all_byte_set():
 
 
 def test_hpl_trailing_update_32768_1024_all_byte_set():
-    _run("hpl", nsample=64, set=oz.A15)
+    _run("hpl", set=oz.A15)
 
 
 def test_krylov_262144_128_4096_all_byte_set():
-    _run("krylov", nsample=64, set=oz.A15)
+    _run("krylov", set=oz.A15)
