@@ -86,6 +86,7 @@ typedef enum { OZAKI25_QUANT_RN = 0, OZAKI25_QUANT_TZ = 1 } ozaki25_quantiser;
 #define OZAKI25_MAX_N 8388608          /* columns of B / C (32-bit offsets inside a tile) */
 #define OZAKI25_EXP_NONFINITE INT32_MIN
 #define OZAKI25_NUM_STAGE_EVENTS 5     /* see ozaki25_dgemm_ex */
+#define OZAKI25_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20) /* see ozaki25_dgemm_noalloc */
 
 /* Text for a status code (static storage, never NULL). */
 const char* ozaki25_status_string(ozaki25_status status);
@@ -229,6 +230,32 @@ ozaki25_status ozaki25_dgemm_planes(int64_t m, int64_t n, int64_t k, const uint8
                                     const int32_t* expsB, double* C, int64_t ldc,
                                     ozaki25_moduli_set set, int subtract, void* workspace,
                                     size_t workspace_bytes, void* stream);
+
+/* For callers that cannot allocate device memory -- work recorded under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc:
+ * ozaki25_dgemm_ex with its workspace taken from a static device array of
+ * OZAKI25_NOALLOC_SCRATCH_BYTES (128 MiB) inside the library instead of an
+ * argument, and no allocation of any kind.  Each GPU the library runs on
+ * holds its own copy of the array from the library's load until the process
+ * ends.  The caller still passes A, B and C (device memory, as for
+ * ozaki25_dgemm_ex); quant and subtract as there.
+ *  - Size limit: ozaki25_dgemm_workspace_size(m, n, k, set) must not exceed
+ *    OZAKI25_NOALLOC_SCRATCH_BYTES (e.g. 1024 x 1024 x 1024 fits both sets);
+ *    larger products return OZAKI25_ERR_WORKSPACE before anything is
+ *    enqueued.
+ *  - Every call on one GPU shares that GPU's array and leaves its planes,
+ *    exponents and residues there; nothing in it needs to start at zero.
+ *    Calls that overlap on one GPU (other streams, other host threads) race
+ *    on the array: order them, e.g. on one stream.
+ *  - The first call on a device resolves the array's device address
+ *    (hipGetSymbolAddress, with that device current) and keeps it; make that
+ *    first call outside graph capture.
+ * m == 0 or n == 0: no-op; k == 0: C = +0 (or unchanged with subtract).
+ * Errors: INVALID_VALUE, UNSUPPORTED, WORKSPACE (beyond the array), HIP. */
+ozaki25_status ozaki25_dgemm_noalloc(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
+                                     const double* B, int64_t ldb, double* C, int64_t ldc,
+                                     ozaki25_moduli_set set, ozaki25_quantiser quant, int subtract,
+                                     void* stream);
 
 #ifdef __cplusplus
 }

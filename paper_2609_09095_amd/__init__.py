@@ -19,7 +19,7 @@ __all__ = [
     "ozaki25_scale_bits", "ozaki25_k_pad", "ozaki25_planes_bytes", "ozaki25_dgemm_workspace_size",
     "ozaki25_deconstruct", "ozaki25_residue_gemm", "ozaki25_reconstruct",
     "ozaki25_dgemm", "ozaki25_dgemm_sub", "ozaki25_dgemm_ex",
-    "ozaki25_dgemm_planes_workspace_size", "ozaki25_dgemm_planes",
+    "ozaki25_dgemm_planes_workspace_size", "ozaki25_dgemm_planes", "ozaki25_dgemm_noalloc",
 ]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -38,6 +38,7 @@ MAX_K = 4194304
 MAX_N = 8388608
 EXP_NONFINITE = -(2 ** 31)
 NUM_STAGE_EVENTS = 5
+NOALLOC_SCRATCH_BYTES = 128 << 20
 
 SUCCESS, ERR_INVALID_VALUE, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
 
@@ -80,6 +81,7 @@ def lib():
             "ozaki25_dgemm_ex": ([i64, i64, i64, P, i64, P, i64, P, i64, i32, i32, i32, P, sz, P, P], i32),
             "ozaki25_dgemm_planes_workspace_size": ([i64, i64, i64, i32], sz),
             "ozaki25_dgemm_planes": ([i64, i64, i64, P, P, P, P, P, i64, i32, i32, P, sz, P], i32),
+            "ozaki25_dgemm_noalloc": ([i64, i64, i64, P, i64, P, i64, P, i64, i32, i32, i32, P], i32),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -363,4 +365,28 @@ def ozaki25_dgemm_planes(k: int, planesA, expsA, planesB, expsB, C=None, subtrac
     _check(lib().ozaki25_dgemm_planes(m, n, k, _ptr(planesA), _ptr(expsA), _ptr(planesB), _ptr(expsB),
                                       _ptr(C), ldc, set, 1 if subtract else 0, ws_ptr, ws_bytes,
                                       _stream(stream)), "ozaki25_dgemm_planes")
+    return C
+
+
+def ozaki25_dgemm_noalloc(A, B, C=None, subtract: bool = False, set: int = S12, quantiser: int = RN,
+                          stream=None):
+    """C = A B (or C -= A B) with the library's static per-GPU workspace of
+    NOALLOC_SCRATCH_BYTES: no device allocation.  Products whose workspace
+    (ozaki25_dgemm_workspace_size) exceeds it raise Ozaki25Error with
+    ERR_WORKSPACE.  Calls that overlap on one GPU race on that workspace."""
+    import torch
+    A, lda = _matrix(A, "A")
+    m, k = A.shape
+    B, ldb = _matrix(B, "B")
+    if B.shape[0] != k:
+        raise ValueError(f"B has {B.shape[0]} rows, A has {k} columns")
+    n = B.shape[1]
+    if C is None:
+        if subtract:
+            raise ValueError("subtract needs C")
+        C = torch.empty((m, n), dtype=torch.float64, device=A.device)
+    C, ldc = _matrix(C, "C", (m, n))
+    _on_gpu([("A", A), ("B", B), ("C", C)])
+    _check(lib().ozaki25_dgemm_noalloc(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, set, quantiser,
+                                       1 if subtract else 0, _stream(stream)), "ozaki25_dgemm_noalloc")
     return C

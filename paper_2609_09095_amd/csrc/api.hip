@@ -5,6 +5,7 @@
 
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 
 #include "kernels.hpp"
 #include "moduli.hpp"
@@ -127,6 +128,36 @@ hipError_t scan_and_deconstruct(ozaki25_moduli_set set, ozaki25_quantiser quant,
                                  planes + v0 * oz::kKAlign, s);
   }
   return e;
+}
+
+// The allocation-free entry point's workspace: one static array per GPU
+// (each device's code object holds its own copy).  In host code `scratch`
+// names a host-side stand-in, never the device memory: its device address is
+// resolved per device with hipGetSymbolAddress and only that address is used.
+constexpr size_t kNoallocBytes = OZAKI25_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) unsigned char scratch[kNoallocBytes];
+
+constexpr int kMaxDevices = 256;
+std::mutex scratch_mu;
+void* scratch_ptr[kMaxDevices];
+
+// Device address of the current device's scratch array (resolved once per
+// device, under a lock).
+hipError_t scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p || ((uintptr_t)p & (kAlign - 1))) return hipErrorInvalidSymbol;
+    scratch_ptr[dev] = p;
+  }
+  *out = scratch_ptr[dev];
+  return hipSuccess;
 }
 
 }  // namespace
@@ -335,6 +366,26 @@ ozaki25_status ozaki25_dgemm_planes(int64_t m, int64_t n, int64_t k, const uint8
     if (e == hipSuccess) e = f;
   }
   return hip_status(e);
+}
+
+ozaki25_status ozaki25_dgemm_noalloc(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
+                                     const double* B, int64_t ldb, double* C, int64_t ldc,
+                                     ozaki25_moduli_set set, ozaki25_quantiser quant, int subtract,
+                                     void* stream) {
+  if (!known_set(set) || !known_quantiser(quant) || m < 0 || n < 0 || k < 0)
+    return OZAKI25_ERR_INVALID_VALUE;
+  if (k > OZAKI25_MAX_K || n > OZAKI25_MAX_N) return OZAKI25_ERR_UNSUPPORTED;
+  if (m == 0 || n == 0) return OZAKI25_SUCCESS;
+  // k == 0 fills (or keeps) C without a workspace: ozaki25_dgemm_ex returns
+  // before its allocation
+  if (k == 0)
+    return ozaki25_dgemm_ex(m, n, k, A, lda, B, ldb, C, ldc, set, quant, subtract, nullptr, 0, nullptr,
+                            stream);
+  if (layout(m, n, k, set).total > kNoallocBytes) return OZAKI25_ERR_WORKSPACE;
+  void* ws = nullptr;
+  if (scratch_address(&ws) != hipSuccess) return OZAKI25_ERR_HIP;
+  return ozaki25_dgemm_ex(m, n, k, A, lda, B, ldb, C, ldc, set, quant, subtract, ws, kNoallocBytes,
+                          nullptr, stream);
 }
 
 ozaki25_status ozaki25_dgemm(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,

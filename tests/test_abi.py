@@ -158,3 +158,21 @@ def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
     monkeypatch.setattr(oz, "_lib", None)
     with pytest.raises(ImportError):
         oz.lib()
+
+
+def test_noalloc_limit_is_checked_on_the_host():
+    """ozaki25_dgemm_noalloc refuses a product whose workspace exceeds its
+    static array before any HIP call (so this runs without a GPU), and the
+    header's constant matches the binding's."""
+    L = oz.lib()
+    assert oz.NOALLOC_SCRATCH_BYTES == 128 << 20
+    fake = ctypes.c_void_p(1 << 20)
+    m = n = k = 2048
+    assert oz.ozaki25_dgemm_workspace_size(m, n, k) > oz.NOALLOC_SCRATCH_BYTES
+    st = L.ozaki25_dgemm_noalloc(m, n, k, fake, k, fake, n, fake, n, oz.S12, oz.RN, 0, None)
+    assert st == oz.ERR_WORKSPACE
+    assert L.ozaki25_dgemm_noalloc(-1, n, k, fake, k, fake, n, fake, n, oz.S12, oz.RN, 0, None) == oz.ERR_INVALID_VALUE
+    assert L.ozaki25_dgemm_noalloc(m, n, k, fake, k, fake, n, fake, n, 5, oz.RN, 0, None) == oz.ERR_INVALID_VALUE
+    assert L.ozaki25_dgemm_noalloc(0, n, k, fake, k, fake, n, fake, n, oz.S12, oz.RN, 0, None) == oz.SUCCESS
+    for s in (oz.S12, oz.A15):
+        assert oz.ozaki25_dgemm_workspace_size(1024, 1024, 1024, s) <= oz.NOALLOC_SCRATCH_BYTES
