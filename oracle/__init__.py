@@ -40,7 +40,8 @@ def build(force: bool = True) -> str:
     """Compile the oracle with gcc (plain -O2, single thread)."""
     if force or not os.path.exists(_LIB):
         tmp = _LIB + ".tmp%d" % os.getpid()
-        subprocess.check_call(["gcc", "-O2", "-std=gnu11", "-shared", "-fPIC", "-o", tmp, _SRC, "-lm"])
+        subprocess.check_call(["gcc", "-O2", "-std=gnu11", "-ffp-contract=off", "-shared", "-fPIC", "-o", tmp,
+                               _SRC, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -87,6 +88,7 @@ def lib():
         L.oracle_round_scaled.argtypes = [i64, ctypes.c_uint64, ctypes.c_int]
         L.oracle_round_scaled.restype = ctypes.c_double
         L.oracle_reconstruct.argtypes = [i64, i64, P, P, P, P, ctypes.c_int, P, i64]
+        L.oracle_native_fallback.argtypes = [i64, i64, i64, P, i64, P, i64, P, P, P, P, i64]
         ci = ctypes.c_int
         L.oracle_set_num_moduli.argtypes = [ci]
         L.oracle_set_modulus.argtypes = [ci, ci]
@@ -290,6 +292,27 @@ def reconstruct(Xhi, Xlo, expsA, expsB, C_in: np.ndarray | None = None) -> np.nd
     return C
 
 
+def native_fallback(A: np.ndarray, B: np.ndarray, expsA, expsB, C: np.ndarray,
+                    C_in: np.ndarray | None = None) -> np.ndarray:
+    """Alg. 1's last step: outputs whose row of A or column of B is flagged
+    non-finite by the exponent scan are overwritten, in place in C, by the
+    index-order FP64 dot product (C_in minus it when C_in is given)."""
+    A = np.ascontiguousarray(A, dtype=np.float64)
+    B = np.ascontiguousarray(B, dtype=np.float64)
+    expsA = np.ascontiguousarray(expsA, dtype=np.int32)
+    expsB = np.ascontiguousarray(expsB, dtype=np.int32)
+    m, k = A.shape
+    _, n = B.shape
+    assert C.shape == (m, n) and C.flags.c_contiguous and C.dtype == np.float64
+    cin = None
+    if C_in is not None:
+        cin = np.ascontiguousarray(C_in, dtype=np.float64)
+        assert cin.shape == (m, n)
+    lib().oracle_native_fallback(m, n, k, _p(A), k, _p(B), n, _p(expsA), _p(expsB),
+                                 _p(cin) if cin is not None else None, _p(C), n)
+    return C
+
+
 def to_int(hi, lo) -> np.ndarray:
     """Object array of Python ints from (hi, lo) words."""
     hi = np.asarray(hi)
@@ -310,13 +333,16 @@ class Result:
 
 def dgemm(A: np.ndarray, B: np.ndarray, C_in: np.ndarray | None = None,
           rows=None, cols=None, want_planes: bool = True, check_exact: bool = True,
-          set: int = 0, quant: int = RN) -> Result:
+          set: int = 0, quant: int = RN, fallback: bool = True) -> Result:
     """Oracle emulated DGEMM on the full k, for all outputs or for the sampled
     rows of A and columns of B (each output depends only on its row and
     column).  Steps in the order of Alg. 1: exponent scan, quantise, residues
     and limbs, per-modulus products, Garner, single rounding.  With
     ``check_exact`` the CRT result is compared with the direct integer
-    product (they must be equal, since |A'B'| < M/2)."""
+    product (they must be equal, since |A'B'| < M/2).  With ``fallback``
+    (Alg. 1's last step) outputs of rows / columns holding a NaN or an
+    infinity are re-issued on the native FP64 path (``native_fallback``);
+    without it they stay NaN, as the stage-wise reconstruction leaves them."""
     m, k = A.shape
     k2, n = B.shape
     assert k == k2
@@ -339,6 +365,8 @@ def dgemm(A: np.ndarray, B: np.ndarray, C_in: np.ndarray | None = None,
             raise AssertionError("oracle: CRT reconstruction differs from the exact integer product")
     Cs = None if C_in is None else np.ascontiguousarray(C_in[np.ix_(rows, cols)])
     C = reconstruct(Xhi, Xlo, sigma, tau, Cs)
+    if fallback:
+        native_fallback(As, Bs, sigma, tau, C, Cs)
     r = Result(t=t, sigma=sigma, tau=tau, ZA=ZA, ZB=ZB, Cres=Cres, Xhi=Xhi, Xlo=Xlo, C=C,
                rows=rows, cols=cols)
     if want_planes:

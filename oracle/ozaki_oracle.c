@@ -432,3 +432,30 @@ void oracle_reconstruct(int64_t m, int64_t n, const int64_t* Xhi, const uint64_t
       else C[r * ldc + c] = v;
     }
 }
+
+/* Alg. 1's last step and the range check that closes Alg. 3 (reading of this
+ * build: the paper names the check and the native re-issue but does not
+ * define the range): an output whose row of A or column of B holds a NaN or
+ * an infinity is outside what the integer quantiser of Eq. (scale) can
+ * represent, so it is re-issued on the native FP64 path -- the plain dot
+ * product in index order l = 0..k-1 from +0, each product rounded, then
+ * added (no fused multiply-add; the oracle is compiled with
+ * -ffp-contract=off).  Every other output keeps the emulated value.  Such
+ * outputs are always an infinity or a NaN, with the IEEE semantics of that
+ * order of operations (Inf * 0, Inf - Inf and intermediate overflow
+ * included).  With Cin, C_ij = Cin_ij - (that sum). */
+void oracle_native_fallback(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
+                            const double* B, int64_t ldb, const int32_t* expsA,
+                            const int32_t* expsB, const double* Cin, double* C, int64_t ldc) {
+  for (int64_t r = 0; r < m; ++r)
+    for (int64_t c = 0; c < n; ++c) {
+      if (expsA[r] != OR_NONFINITE && expsB[c] != OR_NONFINITE) continue;
+      double s = 0.0;
+      for (int64_t l = 0; l < k; ++l) {
+        double p = A[r * lda + l] * B[l * ldb + c];
+        s = s + p;
+      }
+      C[r * ldc + c] = Cin ? Cin[r * ldc + c] - s : s;
+    }
+}
+

@@ -433,17 +433,74 @@ def test_dgemm_special_cases():
     assert np.all(res.C == 0) and not np.any(np.signbit(res.C))
 
 
-def test_dgemm_nonfinite_contract():
-    A = workloads.random_matrix(5, 8, 1.0, 1)
-    B = workloads.random_matrix(8, 4, 1.0, 2)
-    A[1, 3] = np.nan
-    B[6, 2] = np.inf
+def _py_dot(a_row, b_col) -> float:
+    """The index-order FP64 dot product in plain Python floats (IEEE binary64
+    products and sums, each rounded; no fused multiply-add)."""
+    s = 0.0
+    for x, y in zip(a_row, b_col):
+        s = s + float(x) * float(y)
+    return s
+
+
+def _same(x: float, y: float) -> bool:
+    return (math.isnan(x) and math.isnan(y)) or (x == y and math.copysign(1, x) == math.copysign(1, y))
+
+
+def _nonfinite_inputs():
+    A = workloads.random_matrix(7, 8, 1.0, 1)
+    B = workloads.random_matrix(8, 6, 1.0, 2)
+    A[1, 3] = np.nan                       # NaN row
+    A[2, 0] = np.inf                       # +Inf row; B[0, 4] = 0 below gives Inf * 0
+    A[3, 2], A[3, 5] = np.inf, -np.inf     # Inf - Inf
+    A[4, :2] = 1e308                       # finite terms overflow to +Inf ...
+    A[4, 7] = -np.inf                      # ... then meet -Inf: NaN in this order
+    B[6, 2] = np.inf                       # +Inf column
+    B[0, 4] = 0.0
+    B[:2, 5] = 1.0                         # column 5 drives row 4's overflow
+    B[7, 5] = 2.0
+    return A, B
+
+
+def test_dgemm_nonfinite_rows_reissued_natively():
+    """Alg. 1's last step (range check, native FP64 re-issue): every output
+    of a row of A or column of B holding a NaN or infinity equals the
+    index-order dot product in plain Python floats; every other output is the
+    emulated value (the same as without the re-issue, and finite)."""
+    A, B = _nonfinite_inputs()
     res = oracle.dgemm(A, B, check_exact=True)
-    for i in range(5):
-        for j in range(4):
-            assert np.isnan(res.C[i, j]) == (i == 1 or j == 2)
+    emu = oracle.dgemm(A, B, fallback=False).C
+    flagged_rows = {1, 2, 3, 4}
+    flagged_cols = {2}
+    kinds = set()
+    for i in range(A.shape[0]):
+        for j in range(B.shape[1]):
+            if i in flagged_rows or j in flagged_cols:
+                want = _py_dot(A[i], B[:, j])
+                assert _same(res.C[i, j], want), (i, j, res.C[i, j], want)
+                assert not math.isfinite(want)
+                kinds.add("nan" if math.isnan(want) else "inf")
+                assert math.isnan(emu[i, j])          # the stage-wise reconstruction's NaN
+            else:
+                assert res.C[i, j] == emu[i, j] and math.isfinite(res.C[i, j])
+    assert kinds == {"nan", "inf"}
+    assert math.isnan(res.C[2, 4]) and math.isnan(res.C[3, 0]) and math.isnan(res.C[4, 5])
+    assert res.C[2, 0] == _py_dot(A[2], B[:, 0]) and math.isinf(res.C[2, 0])
     # a flagged row quantises to zero planes
     assert not res.planesA[:, 1].any()
+
+
+def test_dgemm_sub_nonfinite_rows_reissued_natively():
+    A, B = _nonfinite_inputs()
+    C0 = workloads.random_matrix(7, 6, 1.0, 3)
+    C0[0, 2] = np.inf
+    res = oracle.dgemm(A, B, C_in=C0)
+    emu = oracle.dgemm(A, B, C_in=C0, fallback=False).C
+    for i in range(7):
+        for j in range(6):
+            if i in (1, 2, 3, 4) or j == 2:
+                assert _same(res.C[i, j], float(C0[i, j]) - _py_dot(A[i], B[:, j])), (i, j)
+            else:
+                assert res.C[i, j] == emu[i, j]
 
 
 def test_dgemm_subtract_is_two_roundings():
