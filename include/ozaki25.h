@@ -30,8 +30,16 @@
  *  - Exponents: sigma_i = t(k) - e_i where e_i is the frexp exponent of
  *    max_l |a_il| (max in [2^(e-1), 2^e); e = 0 for a zero row); likewise
  *    tau_j for the columns of B.  A row or column holding a NaN or an infinity
- *    gets OZAKI25_EXP_NONFINITE, its planes are zero and every output it
- *    touches is NaN (the non-finite contract of the validation plan, Sec. 7).
+ *    gets OZAKI25_EXP_NONFINITE and zero planes: it is out of the range the
+ *    integer quantiser can represent (the range check that ends Alg. 1 and
+ *    Alg. 3).  The GEMM entry points, which see A and B (ozaki25_dgemm,
+ *    ozaki25_dgemm_sub, ozaki25_dgemm_ex, ozaki25_dgemm_noalloc), re-issue
+ *    every output such a row or column touches on the native FP64 path: the
+ *    dot product sum_l a_il b_lj in index order l = 0..k-1 from +0, each
+ *    product rounded and then added, no fused multiply-add -- so those
+ *    outputs (always an infinity or a NaN) follow IEEE semantics for that
+ *    order of operations.  ozaki25_reconstruct and ozaki25_dgemm_planes, which
+ *    do not see A and B, write NaN there.
  *  - Rounding: the quantiser of Eq. (scale) rounds to nearest, ties to even
  *    (Ozaki-II-RN), or, where an entry point takes an ozaki25_quantiser and
  *    OZAKI25_QUANT_TZ is passed, truncates toward zero (Ozaki-II-TZ of Table
@@ -160,7 +168,8 @@ ozaki25_status ozaki25_residue_gemm(int64_t m, int64_t n, int64_t k, const uint8
 /* Reconstruction (Alg. 3, Eq. (garner), Eq. (horner)): Garner's mixed-radix
  * digits of the r centred residues (12 or 15), the integer X in [-M/2, M/2), and
  * C_ij = RN(X 2^(-sigma_i - tau_j)) rounded once; NaN where expsA[i] or
- * expsB[j] is OZAKI25_EXP_NONFINITE.  With subtract != 0:
+ * expsB[j] is OZAKI25_EXP_NONFINITE (the GEMM entry points re-issue those
+ * outputs natively instead; see the conventions above).  With subtract != 0:
  * C_ij <- C_ij - RN(X 2^(-sigma_i - tau_j)) (the product rounded, then the
  * IEEE subtraction).
  *  Cres: int32 [r][m][n]; expsA: int32 [m]; expsB: int32 [n]; C: m x n, ldc.
@@ -220,7 +229,9 @@ size_t ozaki25_dgemm_planes_workspace_size(int64_t m, int64_t n, int64_t k, ozak
  *  planesB, expsB: side 1 of a k x n B -- both with this k and set (either
  *    quantiser; the result is that of ozaki25_dgemm_ex with the same
  *    quantiser, bit for bit).
- *  C, ldc, subtract: as in ozaki25_dgemm_ex.
+ *  C, ldc, subtract: as in ozaki25_dgemm_ex, except that outputs on a row or
+ *    column flagged OZAKI25_EXP_NONFINITE are NaN (A and B are not at hand
+ *    for the native re-issue).
  *  workspace: NULL to allocate stream-ordered, else at least
  *    ozaki25_dgemm_planes_workspace_size(m, n, k, set) bytes, 256-byte aligned.
  * m == 0 or n == 0: no-op; k == 0: C = +0 (or unchanged with subtract).

@@ -305,9 +305,11 @@ ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A
                                             w.splits, s);
   if (ev && e == hipSuccess) e = hipEventRecord(ev[3], s);
   const int sub = subtract ? 1 : 0;
+  // outputs on rows / columns flagged non-finite are re-issued natively
+  const oz::NativeOperands nat{A, lda, B, ldb, k};
   if (e == hipSuccess)
-    e = bytes ? oz::launch_reconstruct_bytes_i8(m, n, (const int8_t*)cres, ea, eb, C, ldc, sub, s)
-              : oz::launch_reconstruct_i16(m, n, (const int16_t*)cres, ea, eb, C, ldc, sub, s);
+    e = bytes ? oz::launch_reconstruct_bytes_i8(m, n, (const int8_t*)cres, ea, eb, C, ldc, sub, nat, s)
+              : oz::launch_reconstruct_i16(m, n, (const int16_t*)cres, ea, eb, C, ldc, sub, nat, s);
   if (ev && e == hipSuccess) e = hipEventRecord(ev[4], s);
   if (owned) {
     const hipError_t f = hipFreeAsync(ws, s);
@@ -355,11 +357,13 @@ ozaki25_status ozaki25_dgemm_planes(int64_t m, int64_t n, int64_t k, const uint8
   if (bytes_set(set)) {
     int8_t* cres = (int8_t*)ws;
     e = oz::launch_residue_gemm_bytes_i8(m, n, kp, pa, pb, cres, (int8_t*)part, splits, s);
-    if (e == hipSuccess) e = oz::launch_reconstruct_bytes_i8(m, n, cres, expsA, expsB, C, ldc, sub, s);
+    if (e == hipSuccess)
+      e = oz::launch_reconstruct_bytes_i8(m, n, cres, expsA, expsB, C, ldc, sub, oz::NativeOperands{}, s);
   } else {
     int16_t* cres = (int16_t*)ws;
     e = oz::launch_residue_gemm_i16(m, n, kp, pa, pb, cres, (int16_t*)part, splits, s);
-    if (e == hipSuccess) e = oz::launch_reconstruct_i16(m, n, cres, expsA, expsB, C, ldc, sub, s);
+    if (e == hipSuccess)
+      e = oz::launch_reconstruct_i16(m, n, cres, expsA, expsB, C, ldc, sub, oz::NativeOperands{}, s);
   }
   if (owned) {
     const hipError_t f = hipFreeAsync(ws, s);

@@ -52,20 +52,33 @@ hipError_t launch_residue_gemm_bytes_i8(int64_t m, int64_t n, int64_t kp, const 
                                         const int8_t* pb, int8_t* cres, int8_t* part, int splits,
                                         hipStream_t stream);
 
+// The operands of Alg. 1's last step (range check, native FP64 re-issue):
+// outputs whose row of A or column of B was flagged non-finite by the
+// exponent scan become the index-order FP64 dot product of that row and
+// column (rounded product, then sum; no FMA).  A == nullptr (the stage API,
+// stored planes): those outputs are NaN instead.
+struct NativeOperands {
+  const double* A = nullptr;
+  int64_t lda = 0;
+  const double* B = nullptr;
+  int64_t ldb = 0;
+  int64_t k = 0;
+};
+
 // Alg. 3: Garner, Horner, lift, single rounding (C = or C -= ).
 hipError_t launch_reconstruct_i32(int64_t m, int64_t n, const int32_t* cres, const int32_t* ea,
                                   const int32_t* eb, double* C, int64_t ldc, int subtract,
                                   hipStream_t stream);
 hipError_t launch_reconstruct_i16(int64_t m, int64_t n, const int16_t* cres, const int32_t* ea,
                                   const int32_t* eb, double* C, int64_t ldc, int subtract,
-                                  hipStream_t stream);
+                                  const NativeOperands& nat, hipStream_t stream);
 // the same for the fifteen residues of the all-byte set
 hipError_t launch_reconstruct_bytes_i32(int64_t m, int64_t n, const int32_t* cres,
                                         const int32_t* ea, const int32_t* eb, double* C,
                                         int64_t ldc, int subtract, hipStream_t stream);
 hipError_t launch_reconstruct_bytes_i8(int64_t m, int64_t n, const int8_t* cres, const int32_t* ea,
                                        const int32_t* eb, double* C, int64_t ldc, int subtract,
-                                       hipStream_t stream);
+                                       const NativeOperands& nat, hipStream_t stream);
 
 // C = +0.0 over an m x n block (the k == 0 product).
 hipError_t launch_zero_c(int64_t m, int64_t n, double* C, int64_t ldc, hipStream_t stream);

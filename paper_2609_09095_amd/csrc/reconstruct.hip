@@ -134,10 +134,12 @@ __device__ __forceinline__ int load_residue(const RT* rowbase, int n, int col) {
 
 // rowq: residues of this output row for modulus 0 (row-uniform); the
 // modulus-q row sits mn elements further per q.
+// fill: the value of an output on a row or column flagged non-finite (NaN,
+// or +0 when the native re-issue supplies those outputs)
 template <typename RT>
 __device__ __forceinline__ double reconstruct_one(const RT* rowq, int64_t mn, int n, int col, int sa,
-                                                  int sb) {
-  if (sa == INT32_MIN || sb == INT32_MIN) return __builtin_nan("");
+                                                  int sb, double fill) {
+  if (sa == INT32_MIN || sb == INT32_MIN) return fill;
   int c[kR], v[kR];
   uint32_t packed[kR / 2];
 #pragma unroll
@@ -211,8 +213,8 @@ __device__ __forceinline__ int garner_digit_a(const int (&c)[kRA], uint32_t (&pa
 
 template <typename RT>
 __device__ __forceinline__ double reconstruct_one_a(const RT* rowq, int64_t mn, int n, int col,
-                                                    int sa, int sb) {
-  if (sa == INT32_MIN || sb == INT32_MIN) return __builtin_nan("");
+                                                    int sa, int sb, double fill) {
+  if (sa == INT32_MIN || sb == INT32_MIN) return fill;
   int c[kRA], v[kRA];
 #pragma unroll
   for (int q = 0; q < kRA; ++q) c[q] = load_residue(rowq + q * mn, n, col);
@@ -234,16 +236,68 @@ __global__ __launch_bounds__(256) void reconstruct_kernel(int64_t m, int64_t n,
                                                           const int32_t* __restrict__ ea,
                                                           const int32_t* __restrict__ eb,
                                                           double* __restrict__ C, int64_t ldc,
-                                                          int subtract) {
+                                                          int subtract, double fill) {
   const int64_t col = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (col >= n) return;
   const int64_t mn = m * n;
   const int sb = eb[col];
   for (int64_t row = blockIdx.y; row < m; row += gridDim.y) {
-    const double r = BYTES ? reconstruct_one_a(cres + row * n, mn, (int)n, (int)col, ea[row], sb)
-                           : reconstruct_one(cres + row * n, mn, (int)n, (int)col, ea[row], sb);
+    const double r = BYTES ? reconstruct_one_a(cres + row * n, mn, (int)n, (int)col, ea[row], sb, fill)
+                           : reconstruct_one(cres + row * n, mn, (int)n, (int)col, ea[row], sb, fill);
     double* out = C + row * ldc + col;
     *out = subtract ? *out - r : r;
+  }
+}
+
+// Alg. 1's last step, the native FP64 re-issue: an output whose row of A or
+// column of B holds a NaN or an infinity (exponent INT32_MIN) has no
+// emulated value, and becomes the dot product of that row and column in
+// index order from +0, each product rounded and then added (the library is
+// built with -ffp-contract=off; contraction is also switched off here).
+// Such a value is always an infinity or a NaN.
+__device__ __forceinline__ double native_dot(const double* __restrict__ a, const double* __restrict__ b,
+                                             int64_t ldb, int64_t k) {
+#pragma clang fp contract(off)
+  double s = 0.0;
+  for (int64_t l = 0; l < k; ++l) {
+    const double p = a[l] * b[l * ldb];
+    s = s + p;
+  }
+  return s;
+}
+
+// One block per 256 x 256 output tile (row tiles strided by gridDim.y):
+// the flags of the tile's rows and columns are loaded coalesced and OR-ed
+// across the block, so a tile with none -- every tile, on finite inputs --
+// costs two loads and a barrier.  Otherwise each thread walks its column of
+// the tile and re-issues the flagged outputs: C = dot, or C = C - dot.
+// It runs apart from the reconstruction (whose loop it would slow), which
+// then fills those outputs with +0: after it for C = AB, before it for
+// C -= AB (C - (+0) leaves every value, NaN and infinities included, as it is).
+__global__ __launch_bounds__(256) void native_reissue_kernel(int64_t m, int64_t n,
+                                                             const int32_t* __restrict__ ea,
+                                                             const int32_t* __restrict__ eb,
+                                                             NativeOperands nat, double* C,
+                                                             int64_t ldc, int subtract) {
+  __shared__ int rowflag[256];
+  const int64_t col = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const bool colflag = col < n && eb[col] == INT32_MIN;
+  const int64_t tiles = (m + 255) / 256;
+  for (int64_t t = blockIdx.y; t < tiles; t += gridDim.y) {
+    const int64_t row0 = t * 256, r = row0 + threadIdx.x;
+    const bool rf = r < m && ea[r] == INT32_MIN;
+    rowflag[threadIdx.x] = rf;
+    if (__syncthreads_or(rf || colflag) && col < n) {
+      const int rows = m - row0 < 256 ? (int)(m - row0) : 256;
+      for (int i = 0; i < rows; ++i) {
+        if (!rowflag[i] && !colflag) continue;
+        const int64_t row = row0 + i;
+        const double d = native_dot(nat.A + row * nat.lda, nat.B + col, nat.ldb, nat.k);
+        double* out = C + row * ldc + col;
+        *out = subtract ? *out - d : d;
+      }
+    }
+    __syncthreads();
   }
 }
 
@@ -259,10 +313,24 @@ dim3 grid_for(int64_t m, int64_t n) {
 
 template <bool BYTES, typename RT>
 hipError_t launch_rec(int64_t m, int64_t n, const RT* cres, const int32_t* ea, const int32_t* eb,
-                      double* C, int64_t ldc, int subtract, hipStream_t stream) {
+                      double* C, int64_t ldc, int subtract, const NativeOperands& nat,
+                      hipStream_t stream) {
   if (m <= 0 || n <= 0) return hipSuccess;
-  hipLaunchKernelGGL((reconstruct_kernel<BYTES, RT>), grid_for(m, n), dim3(256), 0, stream, m, n,
-                     cres, ea, eb, C, ldc, subtract);
+  const dim3 grid = grid_for(m, n);
+  if (nat.A && subtract) {
+    hipLaunchKernelGGL(native_reissue_kernel, dim3(grid.x, (unsigned)(m < 16776960 ? (m + 255) / 256 : 65535)),
+                       dim3(256), 0, stream, m, n, ea, eb, nat, C, ldc, subtract);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL((reconstruct_kernel<BYTES, RT>), grid, dim3(256), 0, stream, m, n, cres, ea, eb, C,
+                     ldc, subtract, nat.A ? 0.0 : __builtin_nan(""));
+  if (nat.A && !subtract) {
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(native_reissue_kernel, dim3(grid.x, (unsigned)(m < 16776960 ? (m + 255) / 256 : 65535)),
+                       dim3(256), 0, stream, m, n, ea, eb, nat, C, ldc, subtract);
+  }
   return hipGetLastError();
 }
 
@@ -271,25 +339,25 @@ hipError_t launch_rec(int64_t m, int64_t n, const RT* cres, const int32_t* ea, c
 hipError_t launch_reconstruct_i32(int64_t m, int64_t n, const int32_t* cres, const int32_t* ea,
                                   const int32_t* eb, double* C, int64_t ldc, int subtract,
                                   hipStream_t stream) {
-  return launch_rec<false, int32_t>(m, n, cres, ea, eb, C, ldc, subtract, stream);
+  return launch_rec<false, int32_t>(m, n, cres, ea, eb, C, ldc, subtract, NativeOperands{}, stream);
 }
 
 hipError_t launch_reconstruct_i16(int64_t m, int64_t n, const int16_t* cres, const int32_t* ea,
                                   const int32_t* eb, double* C, int64_t ldc, int subtract,
-                                  hipStream_t stream) {
-  return launch_rec<false, int16_t>(m, n, cres, ea, eb, C, ldc, subtract, stream);
+                                  const NativeOperands& nat, hipStream_t stream) {
+  return launch_rec<false, int16_t>(m, n, cres, ea, eb, C, ldc, subtract, nat, stream);
 }
 
 hipError_t launch_reconstruct_bytes_i32(int64_t m, int64_t n, const int32_t* cres,
                                         const int32_t* ea, const int32_t* eb, double* C,
                                         int64_t ldc, int subtract, hipStream_t stream) {
-  return launch_rec<true, int32_t>(m, n, cres, ea, eb, C, ldc, subtract, stream);
+  return launch_rec<true, int32_t>(m, n, cres, ea, eb, C, ldc, subtract, NativeOperands{}, stream);
 }
 
 hipError_t launch_reconstruct_bytes_i8(int64_t m, int64_t n, const int8_t* cres, const int32_t* ea,
                                        const int32_t* eb, double* C, int64_t ldc, int subtract,
-                                       hipStream_t stream) {
-  return launch_rec<true, int8_t>(m, n, cres, ea, eb, C, ldc, subtract, stream);
+                                       const NativeOperands& nat, hipStream_t stream) {
+  return launch_rec<true, int8_t>(m, n, cres, ea, eb, C, ldc, subtract, nat, stream);
 }
 
 hipError_t launch_zero_c(int64_t m, int64_t n, double* C, int64_t ldc, hipStream_t stream) {

@@ -293,7 +293,8 @@ def test_dgemm_edge_values():
     r = oracle.dgemm(A, B, want_planes=False, set=OSET)
     assert_bits_equal(C.cpu().numpy(), r.C, "C")
     got = C.cpu().numpy()
-    assert np.all(np.isnan(got[3])) and np.all(np.isnan(got[:, 4]))
+    assert np.all(np.isnan(got[3])) and np.all(np.isnan(got[:, 3]))
+    assert not np.any(np.isfinite(got[4])) and not np.any(np.isfinite(got[:, 4]))
 
 
 def test_dgemm_integer_inputs_are_exact():
