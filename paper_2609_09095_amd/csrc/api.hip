@@ -110,23 +110,38 @@ Workspace layout(int64_t m, int64_t n, int64_t k, ozaki25_moduli_set set) {
 // MI355X last-level cache): each run's deconstruction reads the run right
 // after its scan, from that cache rather than HBM (8192 x 8192: 1.21 ->
 // 0.94 ms for both operands).  Each run writes its part of the full plane
-// layout.
+// layout.  Columns of B: their exponent keys are cleared once (or, with
+// keys_cleared, were cleared by A's scan on the side), each run's
+// deconstruction reads the keys directly, and one launch turns all of them
+// into tau at the end.  zero / nzero (side 0): keys to clear on the side.
 hipError_t scan_and_deconstruct(ozaki25_moduli_set set, ozaki25_quantiser quant, int side, int64_t vecs,
                                 int64_t k, const double* X, int64_t ldx, int t, int32_t* exps,
-                                int8_t* planes, hipStream_t s) {
+                                int8_t* planes, hipStream_t s, int32_t* zero = nullptr,
+                                int64_t nzero = 0, bool keys_cleared = false) {
   const int64_t kp = k_pad(k);
   constexpr int64_t kRunBytes = (int64_t)256 << 20, kTile = 256;
   const int64_t per_run = kRunBytes / (kp * (int64_t)sizeof(double)) / kTile * kTile;
   const int64_t run = per_run > kTile ? per_run : kTile;
   hipError_t e = hipSuccess;
+  if (side == 1 && !keys_cleared) e = oz::launch_clear_keys(vecs, exps, s);
   for (int64_t v0 = 0; v0 < vecs && e == hipSuccess; v0 += run) {
     const int64_t nv = vecs - v0 < run ? vecs - v0 : run;
     const double* Xr = side == 0 ? X + v0 * ldx : X + v0;
-    e = oz::launch_scan(side, nv, k, Xr, ldx, t, exps + v0, s);
+    if (side == 0) {
+      // the first run's blocks also clear the keys (one per row: enough
+      // when there are at least as many rows as keys / 256)
+      const bool side_job = v0 == 0 && zero && (nzero + 255) / 256 <= nv;
+      e = oz::launch_scan_rows(nv, k, Xr, ldx, t, exps + v0, side_job ? zero : nullptr,
+                               side_job ? nzero : 0, s);
+      if (e == hipSuccess && v0 == 0 && zero && !side_job) e = oz::launch_clear_keys(nzero, zero, s);
+    } else {
+      e = oz::launch_scan_cols(nv, k, Xr, ldx, exps + v0, s);
+    }
     if (e == hipSuccess)
       e = oz::launch_deconstruct((int)set, (int)quant, side, nv, vecs, k, kp, t, Xr, ldx, exps + v0,
-                                 planes + v0 * oz::kKAlign, s);
+                                 side == 1, planes + v0 * oz::kKAlign, s);
   }
+  if (side == 1 && e == hipSuccess) e = oz::launch_keys_to_sigma(vecs, t, exps, s);
   return e;
 }
 
@@ -295,8 +310,9 @@ ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A
   // the scans run interleaved with the deconstruction (scan_and_deconstruct),
   // so the scan stage is empty and the deconstruct stage holds both
   if (ev && e == hipSuccess) e = hipEventRecord(ev[1], s);
-  if (e == hipSuccess) e = scan_and_deconstruct(set, quant, 0, m, k, A, lda, t, ea, pa, s);
-  if (e == hipSuccess) e = scan_and_deconstruct(set, quant, 1, n, k, B, ldb, t, eb, pb, s);
+  // A's row scan clears B's column keys on the side
+  if (e == hipSuccess) e = scan_and_deconstruct(set, quant, 0, m, k, A, lda, t, ea, pa, s, eb, n);
+  if (e == hipSuccess) e = scan_and_deconstruct(set, quant, 1, n, k, B, ldb, t, eb, pb, s, nullptr, 0, true);
   if (ev && e == hipSuccess) e = hipEventRecord(ev[2], s);
   if (e == hipSuccess)
     e = bytes ? oz::launch_residue_gemm_bytes_i8(m, n, kp, pa, pb, (int8_t*)cres, (int8_t*)part,

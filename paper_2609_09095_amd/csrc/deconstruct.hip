@@ -16,6 +16,7 @@
 #include <utility>
 
 #include "device_math.hpp"
+#include "exponent_key.hpp"
 #include "kernels.hpp"
 #include "moduli.hpp"
 
@@ -213,11 +214,13 @@ __device__ __forceinline__ int64_t plane_offset(int64_t vecs, int nplanes, int64
 // addresses, then the mask, so no branches sit around the loads; zeros past
 // k, for inactive threads and for a non-finite vector.  Returns sigma (0 for
 // a non-finite vector).
+// keys_in: exps holds the column scan's exponent keys, turned into sigma here.
 template <int SIDE>
 __device__ __forceinline__ int load_group(int64_t vecs, int64_t k, const double* __restrict__ X,
-                                          int64_t ldx, const int32_t* __restrict__ exps, int64_t v,
-                                          int64_t k0, bool active, double (&x)[kElems]) {
-  int sigma = active ? exps[v] : 0;
+                                          int64_t ldx, const int32_t* __restrict__ exps, bool keys_in,
+                                          int t, int64_t v, int64_t k0, bool active, double (&x)[kElems]) {
+  const int raw = active ? exps[v] : 0;
+  int sigma = keys_in ? key_to_sigma((uint32_t)raw, t) : raw;
   const bool finite = sigma != INT32_MIN;
   sigma = finite ? sigma : 0;
   // lim = last valid c of this group
@@ -253,13 +256,14 @@ template <int SIDE, bool EXACT, bool TZ>
 __global__ __launch_bounds__(256) void deconstruct_kernel(int64_t vecs, int64_t vstride, int64_t k,
                                                           int64_t kp, const double* __restrict__ X,
                                                           int64_t ldx, const int32_t* __restrict__ exps,
+                                                          bool keys_in, int t,
                                                           int8_t* __restrict__ planes) {
   int64_t v, g;
   group_of(vecs, v, g);
   const bool active = v < vecs && g < kp / kElems;
   const int64_t k0 = g * kElems;
   double x[kElems];
-  const int sigma = load_group<SIDE>(vecs, k, X, ldx, exps, v, k0, active, x);
+  const int sigma = load_group<SIDE>(vecs, k, X, ldx, exps, keys_in, t, v, k0, active, x);
   // the split table, built while the loads are in flight
   __shared__ uint32_t lut[kSplitTable];
   for (int i = threadIdx.x; i < kSplitTable; i += 256) lut[i] = split_16_codes(i - 256);
@@ -317,6 +321,7 @@ __global__ __launch_bounds__(256) void deconstruct_bytes_kernel(int64_t vecs, in
                                                                 int64_t kp, const double* __restrict__ X,
                                                                 int64_t ldx,
                                                                 const int32_t* __restrict__ exps,
+                                                                bool keys_in, int t,
                                                                 int8_t* __restrict__ planes) {
   int64_t v, g;
   group_of(vecs, v, g);
@@ -325,34 +330,41 @@ __global__ __launch_bounds__(256) void deconstruct_bytes_kernel(int64_t vecs, in
   const int64_t k0 = g * kElems;
   double x[kElems], y[kElems];
   uint32_t ylo[kElems];
-  const int sigma = load_group<SIDE>(vecs, k, X, ldx, exps, v, k0, true, x);
+  const int sigma = load_group<SIDE>(vecs, k, X, ldx, exps, keys_in, t, v, k0, true, x);
   scale_round<TZ, EXACT>(x, sigma, y, ylo);
   emit_all_bytes<EXACT>(std::make_integer_sequence<int, kRA>{}, y, ylo, planes, vstride * 128,
                         plane_offset(vstride, kRA, v, g));
 }
 
+struct DecArgs {
+  int64_t blocks, vecs, vstride, k, kp;
+  const double* X;
+  int64_t ldx;
+  const int32_t* exps;
+  bool keys_in;
+  int t;
+  int8_t* planes;
+};
+
 template <int SIDE, bool BYTES, bool EXACT, bool TZ>
-void launch_one(int64_t blocks, int64_t vecs, int64_t vstride, int64_t k, int64_t kp, const double* X,
-                int64_t ldx,
-                const int32_t* exps, int8_t* planes, hipStream_t stream) {
+void launch_one(const DecArgs& a, hipStream_t stream) {
   if constexpr (BYTES)
-    hipLaunchKernelGGL((deconstruct_bytes_kernel<SIDE, EXACT, TZ>), dim3((unsigned)blocks), dim3(256),
-                       0, stream, vecs, vstride, k, kp, X, ldx, exps, planes);
+    hipLaunchKernelGGL((deconstruct_bytes_kernel<SIDE, EXACT, TZ>), dim3((unsigned)a.blocks), dim3(256),
+                       0, stream, a.vecs, a.vstride, a.k, a.kp, a.X, a.ldx, a.exps, a.keys_in, a.t,
+                       a.planes);
   else
-    hipLaunchKernelGGL((deconstruct_kernel<SIDE, EXACT, TZ>), dim3((unsigned)blocks), dim3(256), 0,
-                       stream, vecs, vstride, k, kp, X, ldx, exps, planes);
+    hipLaunchKernelGGL((deconstruct_kernel<SIDE, EXACT, TZ>), dim3((unsigned)a.blocks), dim3(256), 0,
+                       stream, a.vecs, a.vstride, a.k, a.kp, a.X, a.ldx, a.exps, a.keys_in, a.t, a.planes);
 }
 
 template <int SIDE, bool BYTES>
-void launch_side(int64_t blocks, bool exact, bool tz, int64_t vecs, int64_t vstride, int64_t k, int64_t kp,
-                 const double* X, int64_t ldx, const int32_t* exps, int8_t* planes,
-                 hipStream_t stream) {
+void launch_side(bool exact, bool tz, const DecArgs& a, hipStream_t stream) {
   if (exact) {
-    if (tz) launch_one<SIDE, BYTES, true, true>(blocks, vecs, vstride, k, kp, X, ldx, exps, planes, stream);
-    else launch_one<SIDE, BYTES, true, false>(blocks, vecs, vstride, k, kp, X, ldx, exps, planes, stream);
+    if (tz) launch_one<SIDE, BYTES, true, true>(a, stream);
+    else launch_one<SIDE, BYTES, true, false>(a, stream);
   } else {
-    if (tz) launch_one<SIDE, BYTES, false, true>(blocks, vecs, vstride, k, kp, X, ldx, exps, planes, stream);
-    else launch_one<SIDE, BYTES, false, false>(blocks, vecs, vstride, k, kp, X, ldx, exps, planes, stream);
+    if (tz) launch_one<SIDE, BYTES, false, true>(a, stream);
+    else launch_one<SIDE, BYTES, false, false>(a, stream);
   }
 }
 
@@ -360,7 +372,7 @@ void launch_side(int64_t blocks, bool exact, bool tz, int64_t vecs, int64_t vstr
 
 hipError_t launch_deconstruct(int set, int quant, int side, int64_t vecs, int64_t vstride, int64_t k,
                               int64_t kp, int t, const double* X, int64_t ldx, const int32_t* exps,
-                              int8_t* planes, hipStream_t stream) {
+                              bool keys_in, int8_t* planes, hipStream_t stream) {
   if (vstride < vecs) return hipErrorInvalidValue;
   if (vecs <= 0 || kp <= 0) return hipSuccess;
   const bool bytes = set == kSetBytes;
@@ -368,13 +380,13 @@ hipError_t launch_deconstruct(int set, int quant, int side, int64_t vecs, int64_
   // |y| <= 2^t: the quotient needs no correction (the two bounds of
   // centred_residue; the all-byte set takes the sharper one)
   const bool exact = t <= (bytes ? 51 : 50);
-  const int64_t blocks = ((vecs + 31) / 32) * (kp / 128);
+  const DecArgs a{((vecs + 31) / 32) * (kp / 128), vecs, vstride, k, kp, X, ldx, exps, keys_in, t, planes};
   if (side == 0) {
-    if (bytes) launch_side<0, true>(blocks, exact, tz, vecs, vstride, k, kp, X, ldx, exps, planes, stream);
-    else launch_side<0, false>(blocks, exact, tz, vecs, vstride, k, kp, X, ldx, exps, planes, stream);
+    if (bytes) launch_side<0, true>(exact, tz, a, stream);
+    else launch_side<0, false>(exact, tz, a, stream);
   } else {
-    if (bytes) launch_side<1, true>(blocks, exact, tz, vecs, vstride, k, kp, X, ldx, exps, planes, stream);
-    else launch_side<1, false>(blocks, exact, tz, vecs, vstride, k, kp, X, ldx, exps, planes, stream);
+    if (bytes) launch_side<1, true>(exact, tz, a, stream);
+    else launch_side<1, false>(exact, tz, a, stream);
   }
   return hipGetLastError();
 }

@@ -15,19 +15,33 @@ constexpr int kSetBytes = 1;      // Sec. 5.1 candidate A, int8 route
 constexpr int kQuantRN = 0;  // round to nearest, ties to even
 constexpr int kQuantTZ = 1;  // toward zero
 
-// Exponent scan of A's rows (side 0) or B's columns (side 1), Alg. 1 setup:
-// exps[v] = t - e_v, or INT32_MIN for a vector holding a NaN or infinity.
-hipError_t launch_scan(int side, int64_t vecs, int64_t k, const double* X, int64_t ldx, int t,
-                       int32_t* exps, hipStream_t stream);
+// Exponent scan (Alg. 1 setup): sigma_v = t - e_v, or INT32_MIN for a vector
+// holding a NaN or an infinity.
+//  - rows of A: exps[v] = sigma directly; `zero` (nzero int32, may be null)
+//    is cleared on the side -- B's column keys, so that their scan needs no
+//    clearing launch;
+//  - columns of B in three steps: keys cleared to 0 (launch_clear_keys, or
+//    the side job above), an atomic max of order-preserving exponent keys
+//    per column (launch_scan_cols, any number of column ranges), and the
+//    keys turned into sigma (launch_keys_to_sigma).  The deconstruction can
+//    read the keys directly (keys_in).
+hipError_t launch_scan_rows(int64_t vecs, int64_t k, const double* X, int64_t ldx, int t, int32_t* exps,
+                            int32_t* zero, int64_t nzero, hipStream_t stream);
+hipError_t launch_clear_keys(int64_t vecs, int32_t* keys, hipStream_t stream);
+hipError_t launch_scan_cols(int64_t vecs, int64_t k, const double* X, int64_t ldx, int32_t* keys,
+                            hipStream_t stream);
+hipError_t launch_keys_to_sigma(int64_t vecs, int t, int32_t* exps, hipStream_t stream);
 
 // Alg. 2: scale, quantise, residues and the planes of one operand, given exps
-// and the scale bits t: e4m3 limb planes (published set) or int8 residue
-// planes (all-byte set).  vecs vectors of X, written into a plane layout of
-// vstride >= vecs vectors (planes points at the first one's bytes), so that
-// a run of vectors can fill its part of a larger operand's planes.
+// (sigma, or with keys_in the column scan's exponent keys, turned into sigma
+// on load) and the scale bits t: e4m3 limb planes (published set) or int8
+// residue planes (all-byte set).  vecs vectors of X, written into a plane
+// layout of vstride >= vecs vectors (planes points at the first one's
+// bytes), so that a run of vectors can fill its part of a larger operand's
+// planes.
 hipError_t launch_deconstruct(int set, int quant, int side, int64_t vecs, int64_t vstride, int64_t k,
                               int64_t kp, int t, const double* X, int64_t ldx, const int32_t* exps,
-                              int8_t* planes, hipStream_t stream);
+                              bool keys_in, int8_t* planes, hipStream_t stream);
 
 // Eq. (residueprod): r centred per-modulus products [r][m][n], on FP8 MFMA
 // from limb planes (published set) or int8 MFMA from residue planes

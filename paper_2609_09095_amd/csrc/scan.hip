@@ -1,65 +1,67 @@
 // Exponent scan (the once-per-call setup of Alg. 1; Eq. (scale)): for every
 // row of A / column of B the frexp exponent e of its largest magnitude, and
-// sigma = t - e.  HBM-bound: one FP64 read per element.
-//
-// The reduction runs on the magnitude's bit pattern (|x| as uint64 is
-// monotone in |x|, NaN and infinity sort above every finite value), then on
-// a 32-bit order-preserving key: 0 for zero, e + 2048 for finite nonzero
-// values, all ones for non-finite.
+// sigma = t - e.  HBM-bound: one FP64 read per element.  The reduction key
+// is in exponent_key.hpp.
+#include "exponent_key.hpp"
 #include "kernels.hpp"
 
 namespace oz {
 namespace {
 
-constexpr uint32_t kKeyNonfinite = 0xFFFFFFFFu;
-constexpr uint64_t kAbsMask = 0x7FFFFFFFFFFFFFFFull;
-
-__device__ __forceinline__ uint32_t exponent_key(uint64_t absbits) {
-  if (absbits >= 0x7FF0000000000000ull) return kKeyNonfinite;
-  if (absbits == 0) return 0;
-  const int biased = (int)(absbits >> 52);
-  // normal: |x| in [2^(b-1023), 2^(b-1022)); subnormal: mantissa bit p set,
-  // |x| in [2^(p-1074), 2^(p-1073)).
-  const int e = biased ? biased - 1022 : (63 - __builtin_clzll(absbits)) - 1073;
-  return (uint32_t)(e + 2048);
-}
-
-__device__ __forceinline__ int32_t key_to_sigma(uint32_t key, int t) {
-  if (key == kKeyNonfinite) return INT32_MIN;
-  if (key == 0) return t;  // frexp(0) has exponent 0
-  return t - ((int)key - 2048);
-}
-
-__device__ __forceinline__ uint32_t wave_max(uint32_t v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    const uint32_t o = (uint32_t)__shfl_xor((int)v, off, 64);
-    v = o > v ? o : v;
-  }
-  return v;
-}
-
 // One block of four wavefronts per row of A; rows are contiguous, so loads
 // coalesce, and short matrices (few rows, long k) still spread over the
-// chip.  The waves' maxima meet in LDS.
+// chip.  Each lane reads 16-byte pairs, eight independent loads in flight
+// (a 64 KiB row is one unrolled sweep), from the row's first 16-byte
+// boundary; the element before it (a row starting at an odd double) and
+// the odd tail are read singly.  The waves' maxima meet in LDS.
+//
+// zero / nzero: the column keys of B to clear on the side (the first blocks
+// write one zero per thread), so that B's column scan needs no launch of
+// its own for that.
 __global__ __launch_bounds__(256) void scan_rows_kernel(int64_t vecs, int64_t k, const double* X,
-                                                        int64_t ldx, int t, int32_t* exps) {
+                                                        int64_t ldx, int t, int32_t* exps,
+                                                        int32_t* zero, int64_t nzero) {
   __shared__ uint32_t part[4];
+  if (zero) {
+    const int64_t z = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (z < nzero) zero[z] = 0;
+  }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t v = blockIdx.x;
   const uint64_t* row = reinterpret_cast<const uint64_t*>(X + v * ldx);
-  uint64_t mx0 = 0, mx1 = 0;
-  int64_t l = threadIdx.x;
-  for (; l + 256 < k; l += 512) {
-    const uint64_t a = row[l] & kAbsMask, b = row[l + 256] & kAbsMask;
-    mx0 = a > mx0 ? a : mx0;
-    mx1 = b > mx1 ? b : mx1;
+  const int64_t head = ((uintptr_t)row & 15) ? 1 : 0;  // elements before the 16-byte boundary
+  const int64_t pairs = (k - head) / 2;
+  const ulonglong2* body = reinterpret_cast<const ulonglong2*>(row + head);
+  uint64_t mx[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  int64_t p = threadIdx.x;
+  for (; p + 7 * 256 < pairs; p += 8 * 256) {
+    ulonglong2 q[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) q[u] = body[p + u * 256];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint64_t a = q[u].x & kAbsMask, b = q[u].y & kAbsMask;
+      mx[u] = a > mx[u] ? a : mx[u];
+      mx[u] = b > mx[u] ? b : mx[u];
+    }
   }
-  if (l < k) {
-    const uint64_t a = row[l] & kAbsMask;
-    mx0 = a > mx0 ? a : mx0;
+  for (; p < pairs; p += 256) {
+    const ulonglong2 q = body[p];
+    const uint64_t a = q.x & kAbsMask, b = q.y & kAbsMask;
+    mx[0] = a > mx[0] ? a : mx[0];
+    mx[1] = b > mx[1] ? b : mx[1];
   }
-  const uint32_t key = wave_max(exponent_key(mx0 > mx1 ? mx0 : mx1));
+  if (threadIdx.x == 0 && head) {
+    const uint64_t a = row[0] & kAbsMask;
+    mx[2] = a > mx[2] ? a : mx[2];
+  }
+  if (threadIdx.x == 1 && head + 2 * pairs < k) {
+    const uint64_t a = row[k - 1] & kAbsMask;
+    mx[3] = a > mx[3] ? a : mx[3];
+  }
+#pragma unroll
+  for (int u = 1; u < 8; ++u) mx[0] = mx[u] > mx[0] ? mx[u] : mx[0];
+  const uint32_t key = wave_max(exponent_key(mx[0]));
   if (lane == 0) part[wave] = key;
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -110,25 +112,41 @@ __global__ __launch_bounds__(256) void keys_to_sigma_kernel(int64_t vecs, int t,
 
 }  // namespace
 
-hipError_t launch_scan(int side, int64_t vecs, int64_t k, const double* X, int64_t ldx, int t,
-                       int32_t* exps, hipStream_t stream) {
+hipError_t launch_scan_rows(int64_t vecs, int64_t k, const double* X, int64_t ldx, int t, int32_t* exps,
+                            int32_t* zero, int64_t nzero, hipStream_t stream) {
   if (vecs <= 0) return hipSuccess;
-  if (side == 0) {
-    if (vecs > (int64_t)UINT32_MAX) return hipErrorInvalidValue;  // one block per row
-    hipLaunchKernelGGL(scan_rows_kernel, dim3((unsigned)vecs), dim3(256), 0, stream, vecs, k, X, ldx,
-                       t, exps);
-    return hipGetLastError();
-  }
-  const unsigned vb = (unsigned)((vecs + 255) / 256);
-  hipLaunchKernelGGL(clear_keys_kernel, dim3(vb), dim3(256), 0, stream, vecs, exps);
+  // one block per row; the blocks also cover the keys to clear
+  const int64_t zb = zero ? (nzero + 255) / 256 : 0;
+  if (vecs > (int64_t)UINT32_MAX || zb > vecs) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(scan_rows_kernel, dim3((unsigned)vecs), dim3(256), 0, stream, vecs, k, X, ldx, t,
+                     exps, zero, nzero);
+  return hipGetLastError();
+}
+
+hipError_t launch_clear_keys(int64_t vecs, int32_t* keys, hipStream_t stream) {
+  if (vecs <= 0) return hipSuccess;
+  hipLaunchKernelGGL(clear_keys_kernel, dim3((unsigned)((vecs + 255) / 256)), dim3(256), 0, stream, vecs,
+                     keys);
+  return hipGetLastError();
+}
+
+hipError_t launch_scan_cols(int64_t vecs, int64_t k, const double* X, int64_t ldx, int32_t* keys,
+                            hipStream_t stream) {
+  if (vecs <= 0) return hipSuccess;
   // k blocks of 256 rows, or of 64 when that leaves fewer than 1024 blocks
   const int64_t strips = (vecs + 63) / 64;
   const int64_t rows_per_block = strips * ((k + 255) / 256) < 1024 ? 64 : 256;
   const int64_t kblocks = (k + rows_per_block - 1) / rows_per_block;
   if (kblocks > 0)
     hipLaunchKernelGGL(scan_cols_kernel, dim3((unsigned)(strips * kblocks)), dim3(256), 0, stream,
-                       vecs, k, X, ldx, rows_per_block, exps);
-  hipLaunchKernelGGL(keys_to_sigma_kernel, dim3(vb), dim3(256), 0, stream, vecs, t, exps);
+                       vecs, k, X, ldx, rows_per_block, keys);
+  return hipGetLastError();
+}
+
+hipError_t launch_keys_to_sigma(int64_t vecs, int t, int32_t* exps, hipStream_t stream) {
+  if (vecs <= 0) return hipSuccess;
+  hipLaunchKernelGGL(keys_to_sigma_kernel, dim3((unsigned)((vecs + 255) / 256)), dim3(256), 0, stream,
+                     vecs, t, exps);
   return hipGetLastError();
 }
 
