@@ -81,15 +81,24 @@ size_t products_bytes(int64_t m, int64_t n, int64_t k, ozaki25_moduli_set set, i
   return align_up(one) + (sp > 1 ? align_up(one * sp) : 0);
 }
 
+// Storage mode F for A (the all-byte set, at most 128 columns, at least
+// kFusedMinRows rows): A is converted inside the product kernel, so the
+// workspace holds no planes of A and the products need no split of k.
+constexpr int64_t kFusedMinRows = 1024;
+bool fused_a(int64_t m, int64_t n, ozaki25_moduli_set set) {
+  return bytes_set(set) && n <= 128 && m >= kFusedMinRows;
+}
+
 // planes of A and B, exponents, and the residue products: int16 for the
 // published set (|c| <= 0.51 m <= 556), int8 for the all-byte set (|c| <= 128)
 Workspace layout(int64_t m, int64_t n, int64_t k, ozaki25_moduli_set set) {
   Workspace w;
   const int64_t kp = k_pad(k);
   const size_t np = (size_t)num_planes(set);
+  const bool fused = fused_a(m, n, set);
   size_t off = 0;
   w.planes_a = off;
-  off = align_up(off + np * m * kp);
+  off = fused ? off : align_up(off + np * m * kp);
   w.planes_b = off;
   off = align_up(off + np * n * kp);
   w.exps_a = off;
@@ -98,7 +107,8 @@ Workspace layout(int64_t m, int64_t n, int64_t k, ozaki25_moduli_set set) {
   off = align_up(off + (size_t)n * sizeof(int32_t));
   w.cres = off;
   const size_t one = align_up((size_t)num_moduli(set) * m * n * cres_elem(set));
-  const size_t prod = products_bytes(m, n, k, set, &w.splits);
+  const size_t prod = fused ? one : products_bytes(m, n, k, set, &w.splits);
+  if (fused) w.splits = 1;
   w.part = off + one;
   off += prod;
   w.total = off;
@@ -307,6 +317,25 @@ ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A
   const int64_t kp = k_pad(k);
 
   if (ev) e = hipEventRecord(ev[0], s);
+  if (fused_a(m, n, set)) {
+    // storage mode F for A: its exponent scan (clearing B's column keys on
+    // the side), B's scan and planes, then the products straight from FP64 A
+    if (e == hipSuccess) e = oz::launch_scan_rows(m, k, A, lda, t, ea, eb, n, s);
+    if (ev && e == hipSuccess) e = hipEventRecord(ev[1], s);
+    if (e == hipSuccess) e = scan_and_deconstruct(set, quant, 1, n, k, B, ldb, t, eb, pb, s, nullptr, 0, true);
+    if (ev && e == hipSuccess) e = hipEventRecord(ev[2], s);
+    if (e == hipSuccess) e = oz::launch_fused_bytes((int)quant, m, n, k, kp, t, A, lda, ea, pb, (int8_t*)cres, s);
+    if (ev && e == hipSuccess) e = hipEventRecord(ev[3], s);
+    const oz::NativeOperands nat{A, lda, B, ldb, k};
+    if (e == hipSuccess)
+      e = oz::launch_reconstruct_bytes_i8(m, n, (const int8_t*)cres, ea, eb, C, ldc, subtract ? 1 : 0, nat, s);
+    if (ev && e == hipSuccess) e = hipEventRecord(ev[4], s);
+    if (owned) {
+      const hipError_t f = hipFreeAsync(ws, s);
+      if (e == hipSuccess) e = f;
+    }
+    return hip_status(e);
+  }
   // the scans run interleaved with the deconstruction (scan_and_deconstruct),
   // so the scan stage is empty and the deconstruct stage holds both
   if (ev && e == hipSuccess) e = hipEventRecord(ev[1], s);

@@ -1,0 +1,333 @@
+// Storage mode F for A in tall/skinny products (Alg. 1's storage modes,
+// Sec. 6.2: the hybrid of a materialised small operand and a streamed large
+// one), all-byte set: B's residue planes are stored once, while A is read
+// as FP64 inside the product kernel -- scaled by 2^sigma, quantised and
+// reduced to its byte residues per K stage (Eq. (scale), Alg. 2) straight
+// into LDS, never written to HBM as planes.  For at most 128 columns one
+// output tile spans all of B (lambda_A = 1: every element of A is converted
+// once per modulus it serves).
+//
+// A block owns 128 rows of A, all (at most 128) columns and G moduli; its
+// 8 wavefronts convert a 128 x 64 slab per stage (coalesced: 16 lanes per
+// row, 4 consecutive k each), then multiply it with B's slabs on v_mfma_i32_32x32x32_i8
+// (64 x 32 outputs per wavefront), the next slab's FP64 loads in flight
+// meanwhile.  The blocks of one row strip (15 / G of them) are dealt to the
+// same XCD back to back, so the strip's FP64 comes from HBM once and from
+// that XCD's L2 for the others.
+#include "device_math.hpp"
+#include "kernels.hpp"
+#include "moduli.hpp"
+
+namespace oz {
+namespace {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+
+constexpr int FBN = 128;   // columns of B (all of them)
+constexpr int FBK = 64;    // k per stage
+constexpr int kSegF = 1024;  // stages (65536 k) between reductions of the int32 sums
+
+__constant__ int kModF[kRA] = {kModulusA[0],  kModulusA[1],  kModulusA[2],  kModulusA[3],
+                               kModulusA[4],  kModulusA[5],  kModulusA[6],  kModulusA[7],
+                               kModulusA[8],  kModulusA[9],  kModulusA[10], kModulusA[11],
+                               kModulusA[12], kModulusA[13], kModulusA[14]};
+// RN(1/m) for the quotient of the EXACT path; 0 for m = 256, whose residue
+// byte is the low byte of y itself
+__constant__ double kInvQ[kRA] = {
+    0.0,                 1.0 / kModulusA[1],  1.0 / kModulusA[2],  1.0 / kModulusA[3],
+    1.0 / kModulusA[4],  1.0 / kModulusA[5],  1.0 / kModulusA[6],  1.0 / kModulusA[7],
+    1.0 / kModulusA[8],  1.0 / kModulusA[9],  1.0 / kModulusA[10], 1.0 / kModulusA[11],
+    1.0 / kModulusA[12], 1.0 / kModulusA[13], 1.0 / kModulusA[14]};
+static_assert(kModulusA[0] == 256, "the power of two comes first");
+// RN(1/m) for the general quotient and the reductions of the int32 sums
+__constant__ double kInvF[kRA] = {
+    1.0 / kModulusA[0],  1.0 / kModulusA[1],  1.0 / kModulusA[2],  1.0 / kModulusA[3],
+    1.0 / kModulusA[4],  1.0 / kModulusA[5],  1.0 / kModulusA[6],  1.0 / kModulusA[7],
+    1.0 / kModulusA[8],  1.0 / kModulusA[9],  1.0 / kModulusA[10], 1.0 / kModulusA[11],
+    1.0 / kModulusA[12], 1.0 / kModulusA[13], 1.0 / kModulusA[14]};
+
+constexpr double kMagicF = 6755399441055744.0;  // 1.5 * 2^52
+__device__ __forceinline__ uint32_t lo32(double v) { return (uint32_t)__builtin_bit_cast(uint64_t, v); }
+
+// The centred residue of the integer-valued y modulo M, modulo 2^8 (its low
+// byte is the two's complement byte; the higher bits are not defined).
+//  EXACT (|y| <= 2^51, ylo = y mod 2^32): the FMA rounds y RN(1/M) + 1.5 2^52
+//  once to 1.5 2^52 + q, q the nearest quotient (|y RN(1/M) - y/M| <= 1/(4M)
+//  against the 1/(2M) that separates y/M from a half integer), so
+//  ylo - q M = y - q M (mod 2^32) is the centred residue, |r| < 128, and its
+//  low byte is the two's complement byte; for M = 256 (RN(1/M) taken as 0)
+//  q = 0 and the low byte of y is the residue byte.  24-bit products
+//  suffice: only the low 8 bits are kept.
+//  Otherwise: the nearest quotient by rint, the exact remainder by FMA, and
+//  the corrections of cmod_f64.
+template <bool EXACT>
+__device__ __forceinline__ uint32_t residue_byte(double y, uint32_t ylo, int M, double qinv, double inv) {
+  if constexpr (EXACT) {
+    const uint32_t q = lo32(__builtin_fma(y, qinv, kMagicF));
+    // spelled out: left to itself the compiler uses a quarter-rate 32-bit
+    // multiply; sext24(q) (-M) + ylo is y - q M modulo 2^24
+    uint32_t r;
+    asm("v_mad_i32_i24 %0, %1, %2, %3" : "=v"(r) : "v"(q), "s"(-M), "v"(ylo));
+    return r;  // the caller keeps the low byte
+  } else {
+    const double q = __builtin_rint(y * inv);
+    int r = (int)__builtin_fma(-q, (double)M, y);
+    const int hi = (M - 1) / 2;
+    r = r > hi ? r - M : r;
+    r = r < hi - M + 1 ? r + M : r;
+    return (uint32_t)r;  // the caller keeps the low byte
+  }
+}
+
+// LDS slabs: rows of 64 bytes (one stage), the 16-byte chunk index XOR-ed
+// with bits 1-2 of the row, so that the fragment reads of 8 consecutive rows
+// at one chunk hit 8 distinct 16-byte bank groups.
+__device__ __forceinline__ int fswz(int row) { return (row >> 1) & 3; }
+
+// int8 fragment of a 32-row block for one 32-byte K step of a 64-byte stage:
+// lane half fh takes chunk 2 ks + fh of its row
+__device__ __forceinline__ v4i ffrag(const int8_t* base, int r, int ks, int fh) {
+  return *reinterpret_cast<const v4i*>(base + r * FBK + (((2 * ks + fh) ^ fswz(r)) << 4));
+}
+
+__device__ __forceinline__ const int8_t* uniform_ptr_f(const int8_t* p) {
+  const uint64_t v = (uint64_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return (const int8_t*)(((uint64_t)hi << 32) | lo);
+}
+
+using lds_ptr_f = __attribute__((address_space(3))) void*;
+
+// Centred residue of an int32 sum modulo m (as cmod_i32 in the residue GEMM).
+__device__ __forceinline__ int cmod_sum(int x, int m, double minv) {
+  const double xd = (double)x;
+  const double q = __builtin_rint(xd * minv);
+  return (int)__builtin_fma(-q, (double)m, xd);
+}
+
+// 128 rows of A per block, 16 wavefronts: wavefront w converts rows
+// 8 w .. 8 w + 7 of each slab and owns the 32 x 32 outputs (w / 4, w % 4) of
+// every modulus of its group (one MFMA block each, so that G = 5 moduli fit
+// the registers: the FP64 slab then feeds five times the matrix work).
+constexpr int FBM = 128;
+template <int G, bool EXACT, bool TZ, bool VEC>
+__global__ __launch_bounds__(1024, 1) void fused_bytes_kernel(
+    int64_t m, int64_t n, int64_t k, int64_t kp, const double* __restrict__ A, int64_t lda,
+    const int32_t* __restrict__ sigma, const int8_t* __restrict__ pb, int8_t* __restrict__ cres,
+    int64_t strips) {
+  static_assert(kRA % G == 0, "modulus groups");
+  constexpr int NG = kRA / G;
+  __shared__ __attribute__((aligned(1024))) int8_t lds_a[2][G][FBM * FBK];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_b[2][G][FBN * FBK];
+  // block -> (strip, group): the NG blocks of a strip go to one XCD (block b
+  // runs on XCD b % 8), one after the other
+  const uint32_t b = blockIdx.x, o = b >> 3;
+  const int64_t strip = (int64_t)(o / NG) * 8 + (b & 7);
+  const int grp = (int)(o % NG);
+  if (strip >= strips) return;
+  const int64_t row0 = strip * FBM;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wr = wave >> 2, wc = wave & 3;  // 4 x 4 wavefronts of 32 x 32 outputs
+  const int fr = lane & 31, fh = lane >> 5;
+
+  // conversion: lane l takes 4 consecutive k (4 (l % 16) ..) of row
+  // 8 wave + 4 i + l / 16, i = 0, 1: 16 lanes sweep a row's 512 bytes
+  const int ck = 4 * (lane & 15);
+  int sg[2];
+  uint32_t keep[2];  // all ones for a live row, 0 past m or for a non-finite row
+  const double* arow_p[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = 8 * wave + 4 * i + (lane >> 4);
+    const int64_t arow = row0 + r;
+    const bool ok = arow < m;
+    const int sv = ok ? sigma[arow] : 0;
+    const bool live = ok && sv != INT32_MIN;
+    keep[i] = live ? 0xFFFFFFFFu : 0u;
+    sg[i] = live ? sv : 0;
+    arow_p[i] = A + (ok ? arow : m - 1) * lda;
+  }
+
+  int mods[G];
+  double qinv[G], inv[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    mods[g] = kModF[grp * G + g];
+    qinv[g] = kInvQ[grp * G + g];
+    inv[g] = kInvF[grp * G + g];
+  }
+
+  const int nstage = (int)(kp / FBK);
+  // two register sets x0, x1: stage j's values live in x(j % 2), loaded two
+  // stages ahead; x[4 i + c] is row 8 wave + 4 i + lane / 16, k = ck + c
+  double x0[8], x1[8];
+  // x holds the raw values (rows past m or holding a NaN or an infinity
+  // are masked after the conversion); whole stages take the 16-byte loads,
+  // the last, partial one clamped single loads
+  auto load_a = [&](int s, double (&x)[8]) {
+    const int64_t k0 = (int64_t)s * FBK + ck;
+    if (VEC && (int64_t)s * FBK + FBK <= k) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const double2 p = *reinterpret_cast<const double2*>(arow_p[i] + k0);
+        const double2 q = *reinterpret_cast<const double2*>(arow_p[i] + k0 + 2);
+        x[4 * i] = p.x;
+        x[4 * i + 1] = p.y;
+        x[4 * i + 2] = q.x;
+        x[4 * i + 3] = q.y;
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const int64_t kk = k0 + c < k ? k0 + c : k - 1;
+          const double v = arow_p[i][kk];
+          x[4 * i + c] = k0 + c < k ? v : 0.0;
+        }
+    }
+  };
+  // one dword (4 residue bytes) per row and modulus, written at chunk
+  // ck / 16 of the row, swizzled
+  auto convert = [&](int buf, const double (&x)[8]) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int r = 8 * wave + 4 * i + (lane >> 4);
+      double y[4];
+      uint32_t ylo[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const double v = __builtin_ldexp(x[4 * i + c], sg[i]);
+        y[c] = TZ ? __builtin_trunc(v) : __builtin_rint(v);
+        ylo[c] = EXACT ? lo32(y[c] + kMagicF) : 0u;
+      }
+      const int at = r * FBK + (((ck >> 4) ^ fswz(r)) << 4) + (ck & 15);
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        // low bytes of the four residues into one dword (v_perm_b32: bytes
+        // 0-3 of the second operand, 4-7 of the first)
+        const uint32_t r01 =
+            __builtin_amdgcn_perm(residue_byte<EXACT>(y[1], ylo[1], mods[g], qinv[g], inv[g]),
+                                  residue_byte<EXACT>(y[0], ylo[0], mods[g], qinv[g], inv[g]), 0x0c0c0400u);
+        const uint32_t r23 =
+            __builtin_amdgcn_perm(residue_byte<EXACT>(y[3], ylo[3], mods[g], qinv[g], inv[g]),
+                                  residue_byte<EXACT>(y[2], ylo[2], mods[g], qinv[g], inv[g]), 0x0c0c0400u);
+        const uint32_t word = __builtin_amdgcn_perm(r23, r01, 0x05040100u);
+        *reinterpret_cast<uint32_t*>(&lds_a[buf][g][at]) = word & keep[i];
+      }
+    }
+  };
+  // B's slabs of stage s: for each of the G moduli, 128 rows x 64 bytes,
+  // by LDS-DMA (eight 1 KiB loads per modulus, spread over the wavefronts):
+  // lane l lands at row 16 d + l / 4, physical chunk l % 4, and fetches
+  // the global chunk that the swizzle puts there; columns past n read zero.
+  const int brecs = __builtin_amdgcn_readfirstlane((int)(n * 128));
+  auto load_b = [&](int s, int buf) {
+    const int64_t kb = s >> 1, h = s & 1;
+    for (int d = wave; d < 8 * G; d += 16) {
+      const int g = d >> 3, dd = d & 7;
+      const int mod = grp * G + g;
+      const int8_t* piece = uniform_ptr_f(pb + ((kb * kRA + mod) * n) * 128 + h * 64);
+      const __amdgpu_buffer_rsrc_t rs =
+          __builtin_amdgcn_make_buffer_rsrc((void*)piece, (short)0, brecs, 0x00020000);
+      const int row = 16 * dd + (lane >> 2);
+      const int gchunk = (lane & 3) ^ fswz(row);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_f)(&lds_b[buf][g][16 * dd * FBK]), 16,
+                                               row * 128 + gchunk * 16, 0, 0, 0);
+    }
+  };
+
+  v16i acc[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) acc[g] = v16i{};
+
+  // stage s: the loads of stage s + 2 go out, the MFMAs of stage s run on
+  // the LDS buffers s % 2, and stage s + 1 (loaded during stage s - 1) is
+  // converted into the other buffers
+  auto step = [&](int s, double (&xs)[8], double (&xn)[8]) {
+    const int cur = s & 1, nxt = cur ^ 1;
+    if (s + 2 < nstage) load_a(s + 2, xs);
+    if (s + 1 < nstage) load_b(s + 1, nxt);
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const int8_t* la = lds_a[cur][g];
+      const int8_t* lb = lds_b[cur][g];
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+        acc[g] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ffrag(la, wr * 32 + fr, ks, fh),
+                                                       ffrag(lb, wc * 32 + fr, ks, fh), acc[g], 0, 0, 0);
+      // one modulus's fragments at a time in registers
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (s + 1 < nstage) convert(nxt, xn);
+    if (((s + 1) % kSegF) == 0 && s + 1 < nstage) {
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[g][v] = cmod_sum(acc[g][v], mods[g], inv[g]);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  };
+
+  if (nstage > 0) {
+    load_a(0, x0);
+    load_b(0, 0);
+    if (nstage > 1) load_a(1, x1);
+    convert(0, x0);
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  for (int s = 0; s < nstage; s += 2) {
+    step(s, x0, x1);
+    if (s + 1 < nstage) step(s + 1, x1, x0);
+  }
+
+  // epilogue: centred residues (+m/2 of m = 256 stores as -128), int8, into
+  // the compact [15][m][n] layout of the materialised path
+  const int64_t col = wc * 32 + fr;
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    int8_t* out = cres + (int64_t)(grp * G + g) * m * n;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int64_t row = row0 + wr * 32 + 8 * (v >> 2) + 4 * fh + (v & 3);
+      if (row < m && col < n) out[row * n + col] = (int8_t)cmod_sum(acc[g][v], mods[g], inv[g]);
+    }
+  }
+}
+
+template <int G, bool EXACT, bool TZ>
+hipError_t launch_fused_g(int64_t m, int64_t n, int64_t k, int64_t kp, const double* A, int64_t lda,
+                          const int32_t* sigma, const int8_t* pb, int8_t* cres, hipStream_t stream) {
+  const int64_t strips = (m + FBM - 1) / FBM;
+  const int64_t blocks = (strips + 7) / 8 * 8 * (kRA / G);
+  if (blocks > (int64_t)UINT32_MAX) return hipErrorInvalidValue;
+  // 16-byte loads when every row starts 16-byte aligned
+  if ((((uintptr_t)A) & 15) == 0 && (lda & 1) == 0)
+    hipLaunchKernelGGL((fused_bytes_kernel<G, EXACT, TZ, true>), dim3((unsigned)blocks), dim3(1024), 0,
+                       stream, m, n, k, kp, A, lda, sigma, pb, cres, strips);
+  else
+    hipLaunchKernelGGL((fused_bytes_kernel<G, EXACT, TZ, false>), dim3((unsigned)blocks), dim3(1024), 0,
+                       stream, m, n, k, kp, A, lda, sigma, pb, cres, strips);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_fused_bytes(int quant, int64_t m, int64_t n, int64_t k, int64_t kp, int t,
+                              const double* A, int64_t lda, const int32_t* sigma, const int8_t* pb,
+                              int8_t* cres, hipStream_t stream) {
+  if (n > FBN || kp % FBK || m <= 0 || n <= 0) return hipErrorInvalidValue;
+  const bool exact = t <= 51, tz = quant == kQuantTZ;
+  if (exact) return tz ? launch_fused_g<3, true, true>(m, n, k, kp, A, lda, sigma, pb, cres, stream)
+                       : launch_fused_g<3, true, false>(m, n, k, kp, A, lda, sigma, pb, cres, stream);
+  return tz ? launch_fused_g<3, false, true>(m, n, k, kp, A, lda, sigma, pb, cres, stream)
+            : launch_fused_g<3, false, false>(m, n, k, kp, A, lda, sigma, pb, cres, stream);
+}
+
+}  // namespace oz

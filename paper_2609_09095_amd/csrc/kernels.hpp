@@ -66,6 +66,15 @@ hipError_t launch_residue_gemm_bytes_i8(int64_t m, int64_t n, int64_t kp, const 
                                         const int8_t* pb, int8_t* cres, int8_t* part, int splits,
                                         hipStream_t stream);
 
+// Storage mode F for A (tall/skinny, at most 128 columns; all-byte set):
+// the per-modulus products [15][m][n] (compact int8, as
+// launch_residue_gemm_bytes_i8 writes them) straight from FP64 A, its row
+// exponents sigma (launch_scan_rows) and B's stored planes; A is quantised
+// and reduced inside the kernel.  k == 0 is not handled here.
+hipError_t launch_fused_bytes(int quant, int64_t m, int64_t n, int64_t k, int64_t kp, int t,
+                              const double* A, int64_t lda, const int32_t* sigma, const int8_t* pb,
+                              int8_t* cres, hipStream_t stream);
+
 // The operands of Alg. 1's last step (range check, native FP64 re-issue):
 // outputs whose row of A or column of B was flagged non-finite by the
 // exponent scan become the index-order FP64 dot product of that row and
