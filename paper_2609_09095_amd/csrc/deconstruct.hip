@@ -61,7 +61,9 @@ constexpr int log2_exact(int m) { return m <= 1 ? 0 : 1 + log2_exact(m / 2); }
 // kMagic + the integer nearest y RN(1/M); that product is within
 // |y| 2^-53 / M <= 1/(4M) of y / M, while y / M is at least 1/(2M) away from
 // a half integer, so the integer is the nearest quotient q and the low word
-// of the sum is q mod 2^32.  The 24-bit multiply-add then gives
+// of the sum is q mod 2^32.  For the odd byte moduli (M <= 255, RN(1/M)
+// within 2^-61 of 1/M) this holds up to |y| <= 2^52: the error is at most
+// 2^-9 < 1/510.  The 24-bit multiply-add then gives
 // y - q M mod 2^24, and |y - q M| <= (M-1)/2.  For a power of two M, y itself
 // (mod 2^24) serves: its low log2(M) bits are the residue.
 template <int M>
@@ -240,15 +242,20 @@ __device__ __forceinline__ int load_group(int64_t vecs, int64_t k, const double*
 
 // |x 2^sigma| < 2^t: the scaling is exact, and the quantiser of Eq. (scale)
 // is the one rounding: to nearest even (RN), or toward zero (TZ).  EXACT
-// (t <= 51) also forms ylo = y mod 2^32 from y + kMagic.
-template <bool TZ, bool EXACT>
+// also forms ylo = y mod 2^32: from y + kMagic (t <= 51), or with SPLIT
+// (|y| <= 2^52, where that sum is no longer exact) as y - h 2^32 with
+// h = floor(y 2^-32), one exact FMA.
+template <bool TZ, bool EXACT, bool SPLIT = false>
 __device__ __forceinline__ void scale_round(const double (&x)[kElems], int sigma,
                                             double (&y)[kElems], uint32_t (&ylo)[kElems]) {
 #pragma unroll
   for (int c = 0; c < kElems; ++c) {
     const double v = __builtin_ldexp(x[c], sigma);
     y[c] = TZ ? __builtin_trunc(v) : __builtin_rint(v);
-    ylo[c] = EXACT ? low_word(y[c] + kMagic) : 0u;
+    if constexpr (EXACT && SPLIT)
+      ylo[c] = (uint32_t)__builtin_fma(-__builtin_floor(y[c] * 0x1p-32), 0x1p32, y[c]);
+    else
+      ylo[c] = EXACT ? low_word(y[c] + kMagic) : 0u;
   }
 }
 
@@ -316,7 +323,11 @@ __device__ __forceinline__ void emit_all_bytes(std::integer_sequence<int, I...>,
   (emit_byte_modulus<I, EXACT>(y, ylo, planes, plane_stride, off), ...);
 }
 
-template <int SIDE, bool EXACT, bool TZ>
+// MODE 1: quotient route with ylo from y + kMagic (t <= 51); 2: the same
+// with ylo split off (t = 52: for odd m <= 255 the FMA quotient of
+// residue_low errs by at most 2^52 2^-61 = 2^-9 < 1/(2m), so it is still the
+// nearest); 0: cmod_f64.
+template <int SIDE, int MODE, bool TZ>
 __global__ __launch_bounds__(256) void deconstruct_bytes_kernel(int64_t vecs, int64_t vstride, int64_t k,
                                                                 int64_t kp, const double* __restrict__ X,
                                                                 int64_t ldx,
@@ -331,9 +342,9 @@ __global__ __launch_bounds__(256) void deconstruct_bytes_kernel(int64_t vecs, in
   double x[kElems], y[kElems];
   uint32_t ylo[kElems];
   const int sigma = load_group<SIDE>(vecs, k, X, ldx, exps, keys_in, t, v, k0, true, x);
-  scale_round<TZ, EXACT>(x, sigma, y, ylo);
-  emit_all_bytes<EXACT>(std::make_integer_sequence<int, kRA>{}, y, ylo, planes, vstride * 128,
-                        plane_offset(vstride, kRA, v, g));
+  scale_round<TZ, MODE != 0, MODE == 2>(x, sigma, y, ylo);
+  emit_all_bytes<MODE != 0>(std::make_integer_sequence<int, kRA>{}, y, ylo, planes, vstride * 128,
+                            plane_offset(vstride, kRA, v, g));
 }
 
 struct DecArgs {
@@ -346,25 +357,30 @@ struct DecArgs {
   int8_t* planes;
 };
 
-template <int SIDE, bool BYTES, bool EXACT, bool TZ>
+// mode: 0 general residues, 1 quotient route (ylo by kMagic), 2 quotient
+// route with ylo split off (the all-byte set at t = 52)
+template <int SIDE, bool BYTES, int MODE, bool TZ>
 void launch_one(const DecArgs& a, hipStream_t stream) {
   if constexpr (BYTES)
-    hipLaunchKernelGGL((deconstruct_bytes_kernel<SIDE, EXACT, TZ>), dim3((unsigned)a.blocks), dim3(256),
+    hipLaunchKernelGGL((deconstruct_bytes_kernel<SIDE, MODE, TZ>), dim3((unsigned)a.blocks), dim3(256),
                        0, stream, a.vecs, a.vstride, a.k, a.kp, a.X, a.ldx, a.exps, a.keys_in, a.t,
                        a.planes);
   else
-    hipLaunchKernelGGL((deconstruct_kernel<SIDE, EXACT, TZ>), dim3((unsigned)a.blocks), dim3(256), 0,
+    hipLaunchKernelGGL((deconstruct_kernel<SIDE, MODE != 0, TZ>), dim3((unsigned)a.blocks), dim3(256), 0,
                        stream, a.vecs, a.vstride, a.k, a.kp, a.X, a.ldx, a.exps, a.keys_in, a.t, a.planes);
 }
 
 template <int SIDE, bool BYTES>
-void launch_side(bool exact, bool tz, const DecArgs& a, hipStream_t stream) {
-  if (exact) {
-    if (tz) launch_one<SIDE, BYTES, true, true>(a, stream);
-    else launch_one<SIDE, BYTES, true, false>(a, stream);
+void launch_side(int mode, bool tz, const DecArgs& a, hipStream_t stream) {
+  if (mode == 1) {
+    if (tz) launch_one<SIDE, BYTES, 1, true>(a, stream);
+    else launch_one<SIDE, BYTES, 1, false>(a, stream);
+  } else if (BYTES && mode == 2) {
+    if (tz) launch_one<SIDE, BYTES, 2, true>(a, stream);
+    else launch_one<SIDE, BYTES, 2, false>(a, stream);
   } else {
-    if (tz) launch_one<SIDE, BYTES, false, true>(a, stream);
-    else launch_one<SIDE, BYTES, false, false>(a, stream);
+    if (tz) launch_one<SIDE, BYTES, 0, true>(a, stream);
+    else launch_one<SIDE, BYTES, 0, false>(a, stream);
   }
 }
 
@@ -378,15 +394,16 @@ hipError_t launch_deconstruct(int set, int quant, int side, int64_t vecs, int64_
   const bool bytes = set == kSetBytes;
   const bool tz = quant == kQuantTZ;
   // |y| <= 2^t: the quotient needs no correction (the two bounds of
-  // centred_residue; the all-byte set takes the sharper one)
-  const bool exact = t <= (bytes ? 51 : 50);
+  // centred_residue; the all-byte set takes the sharper one, up to t = 52
+  // with ylo split off)
+  const int mode = t <= (bytes ? 51 : 50) ? 1 : (bytes && t == 52 ? 2 : 0);
   const DecArgs a{((vecs + 31) / 32) * (kp / 128), vecs, vstride, k, kp, X, ldx, exps, keys_in, t, planes};
   if (side == 0) {
-    if (bytes) launch_side<0, true>(exact, tz, a, stream);
-    else launch_side<0, false>(exact, tz, a, stream);
+    if (bytes) launch_side<0, true>(mode, tz, a, stream);
+    else launch_side<0, false>(mode, tz, a, stream);
   } else {
-    if (bytes) launch_side<1, true>(exact, tz, a, stream);
-    else launch_side<1, false>(exact, tz, a, stream);
+    if (bytes) launch_side<1, true>(mode, tz, a, stream);
+    else launch_side<1, false>(mode, tz, a, stream);
   }
   return hipGetLastError();
 }

@@ -50,11 +50,20 @@ __constant__ double kInvF[kRA] = {
 constexpr double kMagicF = 6755399441055744.0;  // 1.5 * 2^52
 __device__ __forceinline__ uint32_t lo32(double v) { return (uint32_t)__builtin_bit_cast(uint64_t, v); }
 
+// y mod 2^32 of an integer-valued y with |y| <= 2^52, where y + 1.5 2^52 is
+// no longer exact: h = floor(y 2^-32) (the scaling is exact), y - h 2^32 in
+// [0, 2^32) by one exact FMA, converted.
+__device__ __forceinline__ uint32_t low32_split(double y) {
+  const double h = __builtin_floor(y * 0x1p-32);
+  return (uint32_t)__builtin_fma(-h, 0x1p32, y);
+}
+
 // The centred residue of the integer-valued y modulo M, modulo 2^8 (its low
 // byte is the two's complement byte; the higher bits are not defined).
-//  EXACT (|y| <= 2^51, ylo = y mod 2^32): the FMA rounds y RN(1/M) + 1.5 2^52
-//  once to 1.5 2^52 + q, q the nearest quotient (|y RN(1/M) - y/M| <= 1/(4M)
-//  against the 1/(2M) that separates y/M from a half integer), so
+//  EXACT (|y| <= 2^52, ylo = y mod 2^32): the FMA rounds y RN(1/M) + 1.5 2^52
+//  once to 1.5 2^52 + q, q the nearest quotient: for odd M <= 255,
+//  |y RN(1/M) - y/M| <= 2^52 2^-61 = 2^-9, below the 1/(2M) >= 1/510 that
+//  separates y/M from a half integer, so
 //  ylo - q M = y - q M (mod 2^32) is the centred residue, |r| < 128, and its
 //  low byte is the two's complement byte; for M = 256 (RN(1/M) taken as 0)
 //  q = 0 and the low byte of y is the residue byte.  24-bit products
@@ -112,7 +121,10 @@ __device__ __forceinline__ int cmod_sum(int x, int m, double minv) {
 // every modulus of its group (one MFMA block each, so that G = 5 moduli fit
 // the registers: the FP64 slab then feeds five times the matrix work).
 constexpr int FBM = 128;
-template <int G, bool EXACT, bool TZ, bool VEC>
+// MODE: how y mod 2^32 is formed for the quotient route -- 1: y + 1.5 2^52
+// (|y| <= 2^51), 2: low32_split (|y| <= 2^52), 0: no quotient route (the
+// general residue).
+template <int G, int MODE, bool TZ, bool VEC>
 __global__ __launch_bounds__(1024, 1) void fused_bytes_kernel(
     int64_t m, int64_t n, int64_t k, int64_t kp, const double* __restrict__ A, int64_t lda,
     const int32_t* __restrict__ sigma, const int8_t* __restrict__ pb, int8_t* __restrict__ cres,
@@ -203,7 +215,7 @@ __global__ __launch_bounds__(1024, 1) void fused_bytes_kernel(
       for (int c = 0; c < 4; ++c) {
         const double v = __builtin_ldexp(x[4 * i + c], sg[i]);
         y[c] = TZ ? __builtin_trunc(v) : __builtin_rint(v);
-        ylo[c] = EXACT ? lo32(y[c] + kMagicF) : 0u;
+        ylo[c] = MODE == 1 ? lo32(y[c] + kMagicF) : (MODE == 2 ? low32_split(y[c]) : 0u);
       }
       const int at = r * FBK + (((ck >> 4) ^ fswz(r)) << 4) + (ck & 15);
 #pragma unroll
@@ -211,11 +223,11 @@ __global__ __launch_bounds__(1024, 1) void fused_bytes_kernel(
         // low bytes of the four residues into one dword (v_perm_b32: bytes
         // 0-3 of the second operand, 4-7 of the first)
         const uint32_t r01 =
-            __builtin_amdgcn_perm(residue_byte<EXACT>(y[1], ylo[1], mods[g], qinv[g], inv[g]),
-                                  residue_byte<EXACT>(y[0], ylo[0], mods[g], qinv[g], inv[g]), 0x0c0c0400u);
+            __builtin_amdgcn_perm(residue_byte<MODE != 0>(y[1], ylo[1], mods[g], qinv[g], inv[g]),
+                                  residue_byte<MODE != 0>(y[0], ylo[0], mods[g], qinv[g], inv[g]), 0x0c0c0400u);
         const uint32_t r23 =
-            __builtin_amdgcn_perm(residue_byte<EXACT>(y[3], ylo[3], mods[g], qinv[g], inv[g]),
-                                  residue_byte<EXACT>(y[2], ylo[2], mods[g], qinv[g], inv[g]), 0x0c0c0400u);
+            __builtin_amdgcn_perm(residue_byte<MODE != 0>(y[3], ylo[3], mods[g], qinv[g], inv[g]),
+                                  residue_byte<MODE != 0>(y[2], ylo[2], mods[g], qinv[g], inv[g]), 0x0c0c0400u);
         const uint32_t word = __builtin_amdgcn_perm(r23, r01, 0x05040100u);
         *reinterpret_cast<uint32_t*>(&lds_a[buf][g][at]) = word & keep[i];
       }
@@ -301,7 +313,7 @@ __global__ __launch_bounds__(1024, 1) void fused_bytes_kernel(
   }
 }
 
-template <int G, bool EXACT, bool TZ>
+template <int G, int MODE, bool TZ>
 hipError_t launch_fused_g(int64_t m, int64_t n, int64_t k, int64_t kp, const double* A, int64_t lda,
                           const int32_t* sigma, const int8_t* pb, int8_t* cres, hipStream_t stream) {
   const int64_t strips = (m + FBM - 1) / FBM;
@@ -309,10 +321,10 @@ hipError_t launch_fused_g(int64_t m, int64_t n, int64_t k, int64_t kp, const dou
   if (blocks > (int64_t)UINT32_MAX) return hipErrorInvalidValue;
   // 16-byte loads when every row starts 16-byte aligned
   if ((((uintptr_t)A) & 15) == 0 && (lda & 1) == 0)
-    hipLaunchKernelGGL((fused_bytes_kernel<G, EXACT, TZ, true>), dim3((unsigned)blocks), dim3(1024), 0,
+    hipLaunchKernelGGL((fused_bytes_kernel<G, MODE, TZ, true>), dim3((unsigned)blocks), dim3(1024), 0,
                        stream, m, n, k, kp, A, lda, sigma, pb, cres, strips);
   else
-    hipLaunchKernelGGL((fused_bytes_kernel<G, EXACT, TZ, false>), dim3((unsigned)blocks), dim3(1024), 0,
+    hipLaunchKernelGGL((fused_bytes_kernel<G, MODE, TZ, false>), dim3((unsigned)blocks), dim3(1024), 0,
                        stream, m, n, k, kp, A, lda, sigma, pb, cres, strips);
   return hipGetLastError();
 }
@@ -323,11 +335,16 @@ hipError_t launch_fused_bytes(int quant, int64_t m, int64_t n, int64_t k, int64_
                               const double* A, int64_t lda, const int32_t* sigma, const int8_t* pb,
                               int8_t* cres, hipStream_t stream) {
   if (n > FBN || kp % FBK || m <= 0 || n <= 0) return hipErrorInvalidValue;
-  const bool exact = t <= 51, tz = quant == kQuantTZ;
-  if (exact) return tz ? launch_fused_g<3, true, true>(m, n, k, kp, A, lda, sigma, pb, cres, stream)
-                       : launch_fused_g<3, true, false>(m, n, k, kp, A, lda, sigma, pb, cres, stream);
-  return tz ? launch_fused_g<3, false, true>(m, n, k, kp, A, lda, sigma, pb, cres, stream)
-            : launch_fused_g<3, false, false>(m, n, k, kp, A, lda, sigma, pb, cres, stream);
+  const bool tz = quant == kQuantTZ;
+  // |y| <= 2^t: the quotient route holds up to 2^52
+  const int mode = t <= 51 ? 1 : (t == 52 ? 2 : 0);
+#define OZ_FUSED(MODE)                                                                           \
+  return tz ? launch_fused_g<3, MODE, true>(m, n, k, kp, A, lda, sigma, pb, cres, stream)       \
+            : launch_fused_g<3, MODE, false>(m, n, k, kp, A, lda, sigma, pb, cres, stream)
+  if (mode == 1) OZ_FUSED(1);
+  if (mode == 2) OZ_FUSED(2);
+  OZ_FUSED(0);
+#undef OZ_FUSED
 }
 
 }  // namespace oz

@@ -60,7 +60,8 @@ def _edge_matrix(rows, k, seed):
 # ------------------------------------------------------------ deconstruction
 @pytest.mark.parametrize("shape,s,seed", [((64, 64), 0.5, 1), ((5, 70), 1.0, 2), ((130, 129), 2.0, 3),
                                           ((1, 1), 1.0, 4), ((33, 1000), 0.5, 5), ((9, 8192), 1.0, 6),
-                                          ((3, 9000), 4.0, 7)])
+                                          ((3, 9000), 4.0, 7), ((17, 4096), 1.0, 8), ((9, 1800), 2.0, 9),
+                                          ((5, 7000), 0.5, 10)])
 @pytest.mark.parametrize("side", [0, 1])
 def test_deconstruct_matches_oracle(shape, s, seed, side):
     X = workloads.random_matrix(shape[0], shape[1], s, seed)
@@ -89,20 +90,27 @@ def test_deconstruct_edge_values(side, k):
     assert exps.cpu().numpy()[3] == oz.EXP_NONFINITE and exps.cpu().numpy()[4] == oz.EXP_NONFINITE
 
 
-def test_deconstruct_boundary_residues():
+@pytest.mark.parametrize("k", [8192, 4096])
+def test_deconstruct_boundary_residues(k):
     """Rows whose scaled integers sit on every residue boundary: multiples of
     each modulus plus and minus half of it (the -128 endpoint of 256, the
-    +-(m-1)/2 ends of the odd moduli), at the top of the scale range."""
-    log("[A15] deconstruct boundary residues")
-    k = 8192
+    +-(m-1)/2 ends of the odd moduli), at the top of the scale range; at
+    k = 4096 (t = 52) a second set of rows reaches |y| just below 2^52."""
     t = oracle.scale_bits(k, OSET)
+    log(f"[A15] deconstruct boundary residues k={k} t={t}")
     rng = np.random.default_rng(5)
-    X = np.zeros((2 * 15, k))
+    X = np.zeros((4 * 15, k))
     for i, m in enumerate(oracle.moduli(OSET)):
         q = rng.integers(-(1 << (t - 9)), 1 << (t - 9), size=k)
         X[2 * i] = (q * m + m // 2).astype(np.float64)
         X[2 * i + 1] = (q * m - m // 2).astype(np.float64)
         X[2 * i, 0] = X[2 * i + 1, 0] = 2.0 ** (t - 1)   # sets the scale to 2^0
+        top = (1 << t) // m
+        q = rng.integers(top - 1024, top, size=k) * rng.choice([-1, 1], size=k)
+        X[30 + 2 * i] = (q * m + m // 2).astype(np.float64)
+        X[30 + 2 * i + 1] = (q * m - m // 2).astype(np.float64)
+        X[30 + 2 * i, 0] = X[30 + 2 * i + 1, 0] = float((1 << t) - 1)   # scale 2^0, |y| < 2^t
+    assert np.all(np.abs(X) < 2.0 ** t)
     planes, exps = gpu_deconstruct(X, 0, SET)
     e, P = _oracle_side(X, 0)
     assert_int_equal(exps.cpu().numpy(), e, "exponents")
