@@ -89,6 +89,11 @@ def lib():
         L.oracle_round_scaled.restype = ctypes.c_double
         L.oracle_reconstruct.argtypes = [i64, i64, P, P, P, P, ctypes.c_int, P, i64]
         L.oracle_native_fallback.argtypes = [i64, i64, i64, P, i64, P, i64, P, P, P, P, i64]
+        L.oracle_mag_digit.argtypes = [ctypes.c_double, ctypes.c_int]
+        L.oracle_mag_digits.argtypes = [i64, i64, P, i64, i64, P, P]
+        L.oracle_bound_gemm.argtypes = [i64, i64, i64, P, P, P]
+        L.oracle_acc_total.argtypes = [ctypes.c_int, i64]
+        L.oracle_acc_shifts.argtypes = [ctypes.c_int, i64, i64, P, P, P, P, P]
         ci = ctypes.c_int
         L.oracle_set_num_moduli.argtypes = [ci]
         L.oracle_set_modulus.argtypes = [ci, ci]
@@ -313,6 +318,72 @@ def native_fallback(A: np.ndarray, B: np.ndarray, expsA, expsB, C: np.ndarray,
     return C
 
 
+# ---------------------------------------------------------------- accurate mode
+ACC_CAP = 58
+ACC_INF = 100000
+
+
+def frexp_exponents(X: np.ndarray, side: int) -> np.ndarray:
+    """e of each row (side 0) / column (side 1): the frexp exponent of its
+    largest magnitude (0 for a zero vector), NONFINITE for a non-finite one
+    (the exponent scan at t = 0 gives -e)."""
+    sig = exponents(X, side, 0).astype(np.int64)
+    return np.where(sig == NONFINITE, NONFINITE, -sig).astype(np.int32)
+
+
+def mag_digit(x: float, e: int) -> int:
+    return int(lib().oracle_mag_digit(x, e))
+
+
+def mag_digits(X: np.ndarray, side: int, e: np.ndarray) -> np.ndarray:
+    """ceil(16 |x| 2^-e) per element, [vecs][k] uint8 (0 on non-finite vectors)."""
+    X, nvec, k, sv, sk = _vec_view(X, side)
+    e = np.ascontiguousarray(e, dtype=np.int32)
+    D = np.zeros((nvec, k), np.uint8)
+    lib().oracle_mag_digits(nvec, k, _p(X), sv, sk, _p(e), _p(D))
+    return D
+
+
+def bound_gemm(DA: np.ndarray, DB: np.ndarray) -> np.ndarray:
+    DA = np.ascontiguousarray(DA, dtype=np.uint8)
+    DB = np.ascontiguousarray(DB, dtype=np.uint8)
+    m, k = DA.shape
+    n = DB.shape[0]
+    U = np.zeros((m, n), np.int64)
+    lib().oracle_bound_gemm(m, n, k, _p(DA), _p(DB), _p(U))
+    return U
+
+
+def acc_total(Uij: int, set: int = 0) -> int:
+    return int(lib().oracle_acc_total(set, int(Uij)))
+
+
+def acc_shifts(U: np.ndarray, flagA, flagB, set: int = 0):
+    U = np.ascontiguousarray(U, dtype=np.int64)
+    m, n = U.shape
+    fa = np.ascontiguousarray(flagA, dtype=np.int32)
+    fb = np.ascontiguousarray(flagB, dtype=np.int32)
+    s = np.zeros(m, np.int32)
+    u = np.zeros(n, np.int32)
+    if lib().oracle_acc_shifts(set, m, n, _p(U), _p(fa), _p(fb), _p(s), _p(u)) != 0:
+        raise ValueError("accurate-mode shift below 4")
+    return s, u
+
+
+def accurate_exponents(A: np.ndarray, B: np.ndarray, set: int = 0):
+    """sigma (rows of A) and tau (columns of B) of the accurate mode (the
+    magnitude digits, the bound GEMM, the shifts), for the whole of A and B:
+    every sigma_i depends on all columns of B and every tau_j on all rows of A."""
+    eA = frexp_exponents(A, 0)
+    eB = frexp_exponents(B, 1)
+    U = bound_gemm(mag_digits(A, 0, eA), mag_digits(B, 1, eB))
+    fa, fb = (eA == NONFINITE), (eB == NONFINITE)
+    s, u = acc_shifts(U, fa, fb, set)
+    sigma = np.where(fa, NONFINITE, s.astype(np.int64) - eA).astype(np.int32)
+    tau = np.where(fb, NONFINITE, u.astype(np.int64) - eB).astype(np.int32)
+    return sigma, tau, U, s, u
+
+
 def to_int(hi, lo) -> np.ndarray:
     """Object array of Python ints from (hi, lo) words."""
     hi = np.asarray(hi)
@@ -333,13 +404,15 @@ class Result:
 
 def dgemm(A: np.ndarray, B: np.ndarray, C_in: np.ndarray | None = None,
           rows=None, cols=None, want_planes: bool = True, check_exact: bool = True,
-          set: int = 0, quant: int = RN, fallback: bool = True) -> Result:
+          set: int = 0, quant: int = RN, fallback: bool = True, accurate: bool = False) -> Result:
     """Oracle emulated DGEMM on the full k, for all outputs or for the sampled
     rows of A and columns of B (each output depends only on its row and
     column).  Steps in the order of Alg. 1: exponent scan, quantise, residues
     and limbs, per-modulus products, Garner, single rounding.  With
     ``check_exact`` the CRT result is compared with the direct integer
-    product (they must be equal, since |A'B'| < M/2).  With ``fallback``
+    product (they must be equal, since |A'B'| < M/2).  ``accurate`` takes
+    sigma and tau from the accurate mode (accurate_exponents) instead of
+    the fast rule t(k).  With ``fallback``
     (Alg. 1's last step) outputs of rows / columns holding a NaN or an
     infinity are re-issued on the native FP64 path (``native_fallback``);
     without it they stay NaN, as the stage-wise reconstruction leaves them."""
@@ -351,8 +424,12 @@ def dgemm(A: np.ndarray, B: np.ndarray, C_in: np.ndarray | None = None,
     t = scale_bits(k, set)
     As = np.ascontiguousarray(A[rows])
     Bs = np.ascontiguousarray(B[:, cols])
-    sigma = exponents(As, 0, t)
-    tau = exponents(Bs, 1, t)
+    if accurate:
+        sig_all, tau_all, _, _, _ = accurate_exponents(A, B, set)
+        sigma, tau = sig_all[rows], tau_all[cols]
+    else:
+        sigma = exponents(As, 0, t)
+        tau = exponents(Bs, 1, t)
     ZA = quantise_vectors(As, 0, sigma, quant)
     ZB = quantise_vectors(Bs, 1, tau, quant)
     resA = residues(ZA, set)

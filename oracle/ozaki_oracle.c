@@ -459,3 +459,99 @@ void oracle_native_fallback(int64_t m, int64_t n, int64_t k, const double* A, in
     }
 }
 
+
+/* ---- accurate-mode scaling (reading of this build) ----------------------
+ * Sec. 2 (Eq. (alpha), alpha = 3r + 1) says only that the accurate mode runs
+ * one additional low-precision GEMM that estimates an input magnitude
+ * bound.  This build reads it as follows:
+ *  1. magnitude digits: alpha_il = ceil(16 |a_il| 2^{-e_i}) in {0..16}, e_i
+ *     the frexp exponent of row i's largest magnitude, so that
+ *     |a_il| <= alpha_il 2^{e_i - 4}; likewise beta_lj for the columns of B;
+ *     0 on non-finite rows / columns (they take the native path);
+ *  2. the bound GEMM: U_ij = sum_l alpha_il beta_lj (exact integers);
+ *  3. shifts: for s_i >= 4, alpha_il 2^{s_i - 4} is an integer at least
+ *     |a_il| 2^{s_i - e_i}, so RN (or truncation) of the scaled value cannot
+ *     pass it: |a'_il| <= alpha_il 2^{s_i - 4}, and
+ *     |sum_l a'_il b'_lj| <= 2^{s_i + u_j - 8} U_ij.  The admissible total
+ *     L_ij is the largest L with 2^L U_ij <= 2^8 (M/2 - 1) (unbounded for
+ *     U_ij = 0); u_j = min(58, floor(min_i L_ij / 2)) and
+ *     s_i = min(58, min_j (L_ij - u_j)), so that s_i + u_j <= L_ij for every
+ *     pair and every entry of A'B' stays below M/2, as Eq. (moduli) needs.
+ *     58 is the largest t(k) of either modulus set (the all-byte set at
+ *     k = 1): the scaled integers stay in the range the fast mode reaches;
+ *  4. sigma_i = s_i - e_i, tau_j = u_j - f_j; the rest as in fast mode.
+ * With U_ij <= 256 k, L_ij >= 2 t(k), so s_i, u_j >= t(k): never fewer bits
+ * than the fast rule. */
+
+#define OR_ACC_CAP 58
+#define OR_ACC_INF 100000
+
+/* Step 1 for one value: ceil(16 |x| 2^{-e}); |x| < 2^e, so the result is at
+ * most 16, and the scaling by 2^{4-e} is exact. */
+int oracle_mag_digit(double x, int e) {
+  return (int)ceil(ldexp(fabs(x), 4 - e));
+}
+
+/* Step 1 for vectors: D[v][l] for vector v (element l at X[v*sv + l*sk]), with
+ * the vector's frexp exponent e[v] (INT32_MIN: a non-finite vector, digits 0). */
+void oracle_mag_digits(int64_t nvec, int64_t k, const double* X, int64_t sv, int64_t sk,
+                       const int32_t* e, uint8_t* D) {
+  for (int64_t v = 0; v < nvec; ++v)
+    for (int64_t l = 0; l < k; ++l)
+      D[v * k + l] = e[v] == OR_NONFINITE ? 0 : (uint8_t)oracle_mag_digit(X[v * sv + l * sk], e[v]);
+}
+
+/* Step 2: U[i][j] = sum_l DA[i][l] DB[j][l], plain int64 loops. */
+void oracle_bound_gemm(int64_t m, int64_t n, int64_t k, const uint8_t* DA, const uint8_t* DB,
+                       int64_t* U) {
+  for (int64_t i = 0; i < m; ++i)
+    for (int64_t j = 0; j < n; ++j) {
+      int64_t acc = 0;
+      for (int64_t l = 0; l < k; ++l) acc += (int64_t)DA[i * k + l] * DB[j * k + l];
+      U[i * n + j] = acc;
+    }
+}
+
+/* Step 3 for one entry: the largest L with 2^L U <= 2^8 (M/2 - 1). */
+int oracle_acc_total(int set, int64_t Uij) {
+  if (Uij <= 0) return OR_ACC_INF;
+  u128 M = 1;
+  for (int i = 0; i < or_set_r(set); ++i) M *= (u128)or_set_m(set)[i];
+  const u128 T = (M / 2 - 1) << 8;
+  const u128 U = (u128)Uij;
+  int L = 0;
+  while ((U << (L + 1)) <= T && ((U << (L + 1)) >> (L + 1)) == U) ++L;
+  return L;
+}
+
+/* Step 3: the shifts s[m] and u[n] from U (flagA / flagB nonzero: a
+ * non-finite row / column, left out of the minima -- its digits are zero,
+ * so its L is unbounded anyway).  Returns 0, or -1 if a shift falls below 4
+ * (outside the bound of step 3; needs k near 2^100). */
+int oracle_acc_shifts(int set, int64_t m, int64_t n, const int64_t* U, const int32_t* flagA,
+                      const int32_t* flagB, int32_t* s, int32_t* u) {
+  for (int64_t j = 0; j < n; ++j) {
+    int mn = OR_ACC_INF;
+    for (int64_t i = 0; i < m; ++i) {
+      if (flagA[i]) continue;
+      const int L = oracle_acc_total(set, U[i * n + j]);
+      if (L < mn) mn = L;
+    }
+    const int uj = mn / 2;
+    u[j] = uj < OR_ACC_CAP ? uj : OR_ACC_CAP;
+  }
+  for (int64_t i = 0; i < m; ++i) {
+    int mn = OR_ACC_INF;
+    for (int64_t j = 0; j < n; ++j) {
+      if (flagB[j]) continue;
+      const int L = oracle_acc_total(set, U[i * n + j]) - u[j];
+      if (L < mn) mn = L;
+    }
+    s[i] = mn < OR_ACC_CAP ? mn : OR_ACC_CAP;
+  }
+  for (int64_t i = 0; i < m; ++i)
+    if (!flagA[i] && s[i] < 4) return -1;
+  for (int64_t j = 0; j < n; ++j)
+    if (!flagB[j] && u[j] < 4) return -1;
+  return 0;
+}
