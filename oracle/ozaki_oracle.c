@@ -487,9 +487,13 @@ void oracle_native_fallback(int64_t m, int64_t n, int64_t k, const double* A, in
 #define OR_ACC_INF 100000
 
 /* Step 1 for one value: ceil(16 |x| 2^{-e}); |x| < 2^e, so the result is at
- * most 16, and the scaling by 2^{4-e} is exact. */
+ * most 16.  The scaling by 2^{4-e} is exact unless it lands below the
+ * normal range (x far below its vector's maximum), where the true value lies
+ * in (0, 1) and its ceiling is 1. */
 int oracle_mag_digit(double x, int e) {
-  return (int)ceil(ldexp(fabs(x), 4 - e));
+  if (x == 0.0) return 0;
+  const double d = ceil(ldexp(fabs(x), 4 - e));
+  return d < 1.0 ? 1 : (int)d;
 }
 
 /* Step 1 for vectors: D[v][l] for vector v (element l at X[v*sv + l*sk]), with

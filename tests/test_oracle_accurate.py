@@ -63,10 +63,18 @@ def test_mag_digit_vs_fraction():
             x = math.copysign(math.ldexp(1 - 2.0 ** -53, e), x)
         if rng.random() < 0.05:  # exact multiples of 2^{e-4}
             x = math.ldexp(int(rng.integers(0, 16)), e - 4)
+        if rng.random() < 0.05:  # scaled value below the normal range
+            x = math.ldexp(1.0, int(rng.integers(-1074, -1000))) * (1 if rng.random() < 0.5 else -1)
+            e = int(rng.integers(-20, 1020))
         d = oracle.mag_digit(x, e)
         assert d == _digit(x, e) and 0 <= d <= 16
         assert (d == 0) == (x == 0)
         assert abs(Fraction(x)) <= d * Fraction(2) ** (e - 4) < abs(Fraction(x)) + Fraction(2) ** (e - 4)
+
+
+def test_mag_digit_far_below_the_maximum():
+    for x, e in [(5e-324, 1000), (-5e-324, 4), (2.0 ** -1000, 80), (2.0 ** -1022, 60)]:
+        assert oracle.mag_digit(x, e) == _digit(x, e) == 1
 
 
 def test_mag_digits_vectors_and_flags():
