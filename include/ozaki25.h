@@ -245,6 +245,60 @@ ozaki25_status ozaki25_dgemm_planes(int64_t m, int64_t n, int64_t k, const uint8
                                     ozaki25_moduli_set set, int subtract, void* workspace,
                                     size_t workspace_bytes, void* stream);
 
+/* Accurate mode (Sec. 2, Eq. (alpha): one more low-precision product, an
+ * estimate of the input magnitudes, so alpha = 3r + 1 products for S12).
+ * Instead of the fixed t(k) of the fast mode, each row of A and column of B
+ * gets its own shift from a bound on the outputs it feeds:
+ *   1. digits alpha_il = ceil(16 |a_il| 2^-e_i) in {0..16} (e_i as in the
+ *      conventions above), likewise beta_lj for B -- so |a_il| is at most
+ *      alpha_il 2^(e_i - 4);
+ *   2. U = alpha beta on int8 MFMA (exact: U <= 256 k < 2^31);
+ *   3. L_ij = the largest L with 2^L U_ij <= 2^8 (M/2 - 1); column shifts
+ *      u_j = min(58, floor(min_i L_ij / 2)), row shifts
+ *      s_i = min(58, min_j (L_ij - u_j)); sigma_i = s_i - e_i and
+ *      tau_j = u_j - f_j.
+ * Since |a'_il| <= alpha_il 2^(s_i - 4), every |A'B'|_ij stays below M/2
+ * (Eq. (moduli)); and since U_ij <= 256 k, s_i and u_j are never below the
+ * fast mode's t(k): the accurate mode never keeps fewer bits, and on data
+ * whose magnitudes vary within a row or column it keeps several more per
+ * operand.  The shifts depend on all of A and all of B (a row's shift on
+ * every column it meets), so they are computed per call; non-finite rows /
+ * columns keep OZAKI25_EXP_NONFINITE and are re-issued natively as in the
+ * fast mode.  The cap of 58 is the largest t(k) the fast mode itself uses
+ * (A15 at k = 1). */
+
+/* Device workspace of ozaki25_accurate_exponents: the digit planes of A and
+ * B ((m + n) k_pad bytes), the totals L (m n bytes), n int32, and for few
+ * output tiles the split bound product's int32 partials. */
+size_t ozaki25_accurate_exponents_workspace_size(int64_t m, int64_t n, int64_t k);
+
+/* The accurate mode's sigma (expsA, m int32) and tau (expsB, n int32) for
+ * C = A B, device memory; the two must not overlap.  workspace: NULL to
+ * allocate stream-ordered, else at least
+ * ozaki25_accurate_exponents_workspace_size() bytes, 256-byte aligned.
+ * m, n or k == 0: no-op.  Errors: INVALID_VALUE, UNSUPPORTED, WORKSPACE, HIP. */
+ozaki25_status ozaki25_accurate_exponents(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
+                                          const double* B, int64_t ldb, ozaki25_moduli_set set,
+                                          int32_t* expsA, int32_t* expsB, void* workspace,
+                                          size_t workspace_bytes, void* stream);
+
+/* Device workspace of ozaki25_dgemm_accurate: that of ozaki25_dgemm_ex plus
+ * that of ozaki25_accurate_exponents. */
+size_t ozaki25_dgemm_accurate_workspace_size(int64_t m, int64_t n, int64_t k, ozaki25_moduli_set set);
+
+/* Emulated DGEMM in the accurate mode: ozaki25_dgemm_ex's arguments and
+ * conventions (quantiser, subtract, workspace, the five stage events -- the
+ * second recorded after the accurate exponents, the third after both
+ * operands' planes), with the exponents of ozaki25_accurate_exponents.
+ * The result is that of the fast mode's pipeline run with those exponents,
+ * bit for bit.  k == 0: C = +0 (or unchanged with subtract).
+ * Errors: INVALID_VALUE, UNSUPPORTED, WORKSPACE, HIP. */
+ozaki25_status ozaki25_dgemm_accurate(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
+                                      const double* B, int64_t ldb, double* C, int64_t ldc,
+                                      ozaki25_moduli_set set, ozaki25_quantiser quant, int subtract,
+                                      void* workspace, size_t workspace_bytes,
+                                      void* const* stage_events, void* stream);
+
 /* For callers that cannot allocate device memory -- work recorded under HIP
  * graph capture, tight serving loops, harnesses that forbid hipMalloc:
  * ozaki25_dgemm_ex with its workspace taken from a static device array of

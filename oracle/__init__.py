@@ -344,11 +344,18 @@ def mag_digits(X: np.ndarray, side: int, e: np.ndarray) -> np.ndarray:
     return D
 
 
-def bound_gemm(DA: np.ndarray, DB: np.ndarray) -> np.ndarray:
+def bound_gemm(DA: np.ndarray, DB: np.ndarray, loops: bool | None = None) -> np.ndarray:
+    """U = DA DB^T of the digit planes.  Plain int64 loops in C, or (large
+    products, or loops=False) numpy's FP64 matmul: every partial sum is an
+    integer at most 256 k < 2^53, so that product is exact in any order."""
     DA = np.ascontiguousarray(DA, dtype=np.uint8)
     DB = np.ascontiguousarray(DB, dtype=np.uint8)
     m, k = DA.shape
     n = DB.shape[0]
+    if loops is None:
+        loops = m * n * k <= (1 << 26)
+    if not loops:
+        return (DA.astype(np.float64) @ DB.astype(np.float64).T).astype(np.int64)
     U = np.zeros((m, n), np.int64)
     lib().oracle_bound_gemm(m, n, k, _p(DA), _p(DB), _p(U))
     return U
@@ -365,7 +372,10 @@ def acc_shifts(U: np.ndarray, flagA, flagB, set: int = 0):
     fb = np.ascontiguousarray(flagB, dtype=np.int32)
     s = np.zeros(m, np.int32)
     u = np.zeros(n, np.int32)
-    if lib().oracle_acc_shifts(set, m, n, _p(U), _p(fa), _p(fb), _p(s), _p(u)) != 0:
+    rc = lib().oracle_acc_shifts(set, m, n, _p(U), _p(fa), _p(fb), _p(s), _p(u))
+    if rc == -2:
+        raise MemoryError("oracle_acc_shifts: no host memory for the totals")
+    if rc != 0:
         raise ValueError("accurate-mode shift below 4")
     return s, u
 
@@ -404,7 +414,8 @@ class Result:
 
 def dgemm(A: np.ndarray, B: np.ndarray, C_in: np.ndarray | None = None,
           rows=None, cols=None, want_planes: bool = True, check_exact: bool = True,
-          set: int = 0, quant: int = RN, fallback: bool = True, accurate: bool = False) -> Result:
+          set: int = 0, quant: int = RN, fallback: bool = True, accurate: bool = False,
+          accurate_exps=None) -> Result:
     """Oracle emulated DGEMM on the full k, for all outputs or for the sampled
     rows of A and columns of B (each output depends only on its row and
     column).  Steps in the order of Alg. 1: exponent scan, quantise, residues
@@ -412,7 +423,8 @@ def dgemm(A: np.ndarray, B: np.ndarray, C_in: np.ndarray | None = None,
     ``check_exact`` the CRT result is compared with the direct integer
     product (they must be equal, since |A'B'| < M/2).  ``accurate`` takes
     sigma and tau from the accurate mode (accurate_exponents) instead of
-    the fast rule t(k).  With ``fallback``
+    the fast rule t(k); ``accurate_exps`` may hand in the (sigma, tau) that
+    accurate_exponents already gave for the whole of A and B.  With ``fallback``
     (Alg. 1's last step) outputs of rows / columns holding a NaN or an
     infinity are re-issued on the native FP64 path (``native_fallback``);
     without it they stay NaN, as the stage-wise reconstruction leaves them."""
@@ -425,7 +437,10 @@ def dgemm(A: np.ndarray, B: np.ndarray, C_in: np.ndarray | None = None,
     As = np.ascontiguousarray(A[rows])
     Bs = np.ascontiguousarray(B[:, cols])
     if accurate:
-        sig_all, tau_all, _, _, _ = accurate_exponents(A, B, set)
+        if accurate_exps is None:
+            sig_all, tau_all, _, _, _ = accurate_exponents(A, B, set)
+        else:
+            sig_all, tau_all = accurate_exps
         sigma, tau = sig_all[rows], tau_all[cols]
     else:
         sigma = exponents(As, 0, t)

@@ -29,6 +29,7 @@
  */
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 
 #define OR_R 12
@@ -516,17 +517,34 @@ void oracle_bound_gemm(int64_t m, int64_t n, int64_t k, const uint8_t* DA, const
     }
 }
 
-/* Step 3 for one entry: the largest L with 2^L U <= 2^8 (M/2 - 1). */
-int oracle_acc_total(int set, int64_t Uij) {
-  if (Uij <= 0) return OR_ACC_INF;
+/* 2^8 (M/2 - 1) of a set. */
+static u128 or_acc_limit(int set) {
   u128 M = 1;
   for (int i = 0; i < or_set_r(set); ++i) M *= (u128)or_set_m(set)[i];
-  const u128 T = (M / 2 - 1) << 8;
+  return (M / 2 - 1) << 8;
+}
+
+static int or_bitlen(u128 x) {
+  int b = 0;
+  while (x) {
+    ++b;
+    x >>= 1;
+  }
+  return b;
+}
+
+/* Step 3 for one entry: the largest L with 2^L U <= T = 2^8 (M/2 - 1),
+ * searched upward from bitlen(T) - bitlen(U) - 1, which always qualifies
+ * (2^L U < 2^(bitlen(T) - 1) <= T there). */
+static int or_acc_total_T(u128 T, int64_t Uij) {
+  if (Uij <= 0) return OR_ACC_INF;
   const u128 U = (u128)Uij;
-  int L = 0;
-  while ((U << (L + 1)) <= T && ((U << (L + 1)) >> (L + 1)) == U) ++L;
+  int L = or_bitlen(T) - or_bitlen(U) - 1;
+  while ((U << (L + 1)) <= T) ++L;
   return L;
 }
+
+int oracle_acc_total(int set, int64_t Uij) { return or_acc_total_T(or_acc_limit(set), Uij); }
 
 /* Step 3: the shifts s[m] and u[n] from U (flagA / flagB nonzero: a
  * non-finite row / column, left out of the minima -- its digits are zero,
@@ -534,13 +552,14 @@ int oracle_acc_total(int set, int64_t Uij) {
  * (outside the bound of step 3; needs k near 2^100). */
 int oracle_acc_shifts(int set, int64_t m, int64_t n, const int64_t* U, const int32_t* flagA,
                       const int32_t* flagB, int32_t* s, int32_t* u) {
+  const u128 T = or_acc_limit(set);
+  int32_t* L = (int32_t*)malloc((size_t)(m * n > 0 ? m * n : 1) * sizeof(int32_t));
+  if (!L) return -2; /* out of host memory */
+  for (int64_t q = 0; q < m * n; ++q) L[q] = or_acc_total_T(T, U[q]);
   for (int64_t j = 0; j < n; ++j) {
     int mn = OR_ACC_INF;
-    for (int64_t i = 0; i < m; ++i) {
-      if (flagA[i]) continue;
-      const int L = oracle_acc_total(set, U[i * n + j]);
-      if (L < mn) mn = L;
-    }
+    for (int64_t i = 0; i < m; ++i)
+      if (!flagA[i] && L[i * n + j] < mn) mn = L[i * n + j];
     const int uj = mn / 2;
     u[j] = uj < OR_ACC_CAP ? uj : OR_ACC_CAP;
   }
@@ -548,11 +567,12 @@ int oracle_acc_shifts(int set, int64_t m, int64_t n, const int64_t* U, const int
     int mn = OR_ACC_INF;
     for (int64_t j = 0; j < n; ++j) {
       if (flagB[j]) continue;
-      const int L = oracle_acc_total(set, U[i * n + j]) - u[j];
-      if (L < mn) mn = L;
+      const int d = L[i * n + j] - u[j];
+      if (d < mn) mn = d;
     }
     s[i] = mn < OR_ACC_CAP ? mn : OR_ACC_CAP;
   }
+  free(L);
   for (int64_t i = 0; i < m; ++i)
     if (!flagA[i] && s[i] < 4) return -1;
   for (int64_t j = 0; j < n; ++j)

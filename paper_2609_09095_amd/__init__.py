@@ -20,6 +20,8 @@ __all__ = [
     "ozaki25_deconstruct", "ozaki25_residue_gemm", "ozaki25_reconstruct",
     "ozaki25_dgemm", "ozaki25_dgemm_sub", "ozaki25_dgemm_ex",
     "ozaki25_dgemm_planes_workspace_size", "ozaki25_dgemm_planes", "ozaki25_dgemm_noalloc",
+    "ozaki25_accurate_exponents_workspace_size", "ozaki25_accurate_exponents",
+    "ozaki25_dgemm_accurate_workspace_size", "ozaki25_dgemm_accurate",
 ]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -82,6 +84,11 @@ def lib():
             "ozaki25_dgemm_planes_workspace_size": ([i64, i64, i64, i32], sz),
             "ozaki25_dgemm_planes": ([i64, i64, i64, P, P, P, P, P, i64, i32, i32, P, sz, P], i32),
             "ozaki25_dgemm_noalloc": ([i64, i64, i64, P, i64, P, i64, P, i64, i32, i32, i32, P], i32),
+            "ozaki25_accurate_exponents_workspace_size": ([i64, i64, i64], sz),
+            "ozaki25_accurate_exponents": ([i64, i64, i64, P, i64, P, i64, i32, P, P, P, sz, P], i32),
+            "ozaki25_dgemm_accurate_workspace_size": ([i64, i64, i64, i32], sz),
+            "ozaki25_dgemm_accurate": ([i64, i64, i64, P, i64, P, i64, P, i64, i32, i32, i32, P, sz, P, P],
+                                       i32),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -275,31 +282,87 @@ def _workspace(workspace):
     return _ptr(workspace), workspace.numel()
 
 
-def ozaki25_dgemm_ex(A, B, C, subtract: bool = False, workspace=None, stage_events=None,
-                     set: int = S12, quantiser: int = RN, stream=None):
+def _events(stage_events):
+    if stage_events is None:
+        return None
+    handles = []
+    for e in stage_events:
+        if not hasattr(e, "cuda_event") or not e.cuda_event:
+            raise ValueError("stage events must be recorded torch.cuda.Event objects")
+        handles.append(e.cuda_event)
+    if len(handles) != NUM_STAGE_EVENTS:
+        raise ValueError(f"need {NUM_STAGE_EVENTS} stage events")
+    return ctypes.cast((ctypes.c_void_p * NUM_STAGE_EVENTS)(*handles), ctypes.c_void_p)
+
+
+def _operands(A, B):
     A, lda = _matrix(A, "A")
     m, k = A.shape
     B, ldb = _matrix(B, "B")
     if B.shape[0] != k:
         raise ValueError(f"B has {B.shape[0]} rows, A has {k} columns")
-    n = B.shape[1]
+    return A, lda, B, ldb, m, B.shape[1], k
+
+
+def ozaki25_dgemm_ex(A, B, C, subtract: bool = False, workspace=None, stage_events=None,
+                     set: int = S12, quantiser: int = RN, stream=None):
+    A, lda, B, ldb, m, n, k = _operands(A, B)
     C, ldc = _matrix(C, "C", (m, n))
-    ev = None
-    if stage_events is not None:
-        handles = []
-        for e in stage_events:
-            if not hasattr(e, "cuda_event") or not e.cuda_event:
-                raise ValueError("stage events must be recorded torch.cuda.Event objects")
-            handles.append(e.cuda_event)
-        if len(handles) != NUM_STAGE_EVENTS:
-            raise ValueError(f"need {NUM_STAGE_EVENTS} stage events")
-        ev = (ctypes.c_void_p * NUM_STAGE_EVENTS)(*handles)
+    ev = _events(stage_events)
     ws_ptr, ws_bytes = _workspace(workspace)
     _on_gpu([("A", A), ("B", B), ("C", C), ("workspace", workspace)])
     _check(lib().ozaki25_dgemm_ex(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, set, quantiser,
-                                  1 if subtract else 0, ws_ptr, ws_bytes,
-                                  ctypes.cast(ev, ctypes.c_void_p) if ev is not None else None,
-                                  _stream(stream)), "ozaki25_dgemm_ex")
+                                  1 if subtract else 0, ws_ptr, ws_bytes, ev, _stream(stream)),
+           "ozaki25_dgemm_ex")
+    return C
+
+
+def ozaki25_accurate_exponents_workspace_size(m: int, n: int, k: int) -> int:
+    return lib().ozaki25_accurate_exponents_workspace_size(m, n, k)
+
+
+def ozaki25_accurate_exponents(A, B, expsA=None, expsB=None, set: int = S12, workspace=None,
+                               stream=None):
+    """The accurate mode's sigma (rows of A) and tau (columns of B): the
+    magnitude digits, their int8 bound product and the shifts it admits.
+    Returns (expsA, expsB), int32 CUDA tensors."""
+    import torch
+    A, lda, B, ldb, m, n, k = _operands(A, B)
+    if expsA is None:
+        expsA = torch.empty(m, dtype=torch.int32, device=A.device)
+    if expsB is None:
+        expsB = torch.empty(n, dtype=torch.int32, device=A.device)
+    _buffer(expsA, "expsA", _i32(), m)
+    _buffer(expsB, "expsB", _i32(), n)
+    ws_ptr, ws_bytes = _workspace(workspace)
+    _on_gpu([("A", A), ("B", B), ("expsA", expsA), ("expsB", expsB), ("workspace", workspace)])
+    _check(lib().ozaki25_accurate_exponents(m, n, k, _ptr(A), lda, _ptr(B), ldb, set, _ptr(expsA),
+                                            _ptr(expsB), ws_ptr, ws_bytes, _stream(stream)),
+           "ozaki25_accurate_exponents")
+    return expsA, expsB
+
+
+def ozaki25_dgemm_accurate_workspace_size(m: int, n: int, k: int, set: int = S12) -> int:
+    return lib().ozaki25_dgemm_accurate_workspace_size(m, n, k, set)
+
+
+def ozaki25_dgemm_accurate(A, B, C=None, subtract: bool = False, workspace=None, stage_events=None,
+                           set: int = S12, quantiser: int = RN, stream=None):
+    """C = A B (or C -= A B) in the accurate mode: per-row and per-column
+    shifts from the magnitude-bound product instead of the fixed t(k)."""
+    import torch
+    A, lda, B, ldb, m, n, k = _operands(A, B)
+    if C is None:
+        if subtract:
+            raise ValueError("subtract needs C")
+        C = torch.empty((m, n), dtype=torch.float64, device=A.device)
+    C, ldc = _matrix(C, "C", (m, n))
+    ev = _events(stage_events)
+    ws_ptr, ws_bytes = _workspace(workspace)
+    _on_gpu([("A", A), ("B", B), ("C", C), ("workspace", workspace)])
+    _check(lib().ozaki25_dgemm_accurate(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, set, quantiser,
+                                        1 if subtract else 0, ws_ptr, ws_bytes, ev, _stream(stream)),
+           "ozaki25_dgemm_accurate")
     return C
 
 

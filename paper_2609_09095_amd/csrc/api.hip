@@ -155,6 +155,74 @@ hipError_t scan_and_deconstruct(ozaki25_moduli_set set, ozaki25_quantiser quant,
   return e;
 }
 
+// ---- accurate mode (Sec. 2, Eq. (alpha)) ---------------------------------
+// Scratch of the exponent stage: the digit planes of A and B, the totals L
+// (int8 m x n), the column shifts, and the split bound product's partials.
+struct AccWorkspace {
+  size_t dig_a, dig_b, total, colmin, part, bytes;
+  int splits;
+};
+
+AccWorkspace acc_layout(int64_t m, int64_t n, int64_t k) {
+  AccWorkspace w;
+  const int64_t kp = k_pad(k);
+  w.splits = oz::bound_gemm_splits(m, n, kp);
+  size_t off = 0;
+  w.dig_a = off;
+  off = align_up(off + (size_t)m * kp);
+  w.dig_b = off;
+  off = align_up(off + (size_t)n * kp);
+  w.total = off;
+  off = align_up(off + (size_t)m * n);
+  w.colmin = off;
+  off = align_up(off + (size_t)n * sizeof(int32_t));
+  w.part = off;
+  off = w.splits > 1 ? align_up(off + (size_t)w.splits * m * n * sizeof(int32_t)) : off;
+  w.bytes = off;
+  return w;
+}
+
+// T = 2^8 (M/2 - 1): its bit length and its top 33 bits
+void bound_limit(ozaki25_moduli_set set, int* bt, uint64_t* ttop) {
+  u128 M = 1;
+  for (int i = 0; i < num_moduli(set); ++i) M *= (u128)modulus(set, i);
+  const u128 T = (M / 2 - 1) << 8;
+  int b = 0;
+  while (b < 128 && (T >> b) != 0) ++b;
+  *bt = b;
+  *ttop = (uint64_t)(T >> (b - 33));
+}
+
+// The accurate mode's exponents into ea / eb: the scans at t = 0 (A's row
+// scan clears B's column keys on the side), the magnitude digits, the bound
+// product and its totals, then the shifts.
+hipError_t accurate_exponents(ozaki25_moduli_set set, int64_t m, int64_t n, int64_t k, const double* A,
+                              int64_t lda, const double* B, int64_t ldb, int32_t* ea, int32_t* eb,
+                              char* aux, const AccWorkspace& w, hipStream_t s) {
+  const int64_t kp = k_pad(k);
+  int8_t* da = (int8_t*)(aux + w.dig_a);
+  int8_t* db = (int8_t*)(aux + w.dig_b);
+  int8_t* total = (int8_t*)(aux + w.total);
+  int32_t* colmin = (int32_t*)(aux + w.colmin);
+  int32_t* part = w.splits > 1 ? (int32_t*)(aux + w.part) : nullptr;
+  int bt = 0;
+  uint64_t ttop = 0;
+  bound_limit(set, &bt, &ttop);
+  const bool side_job = (n + 255) / 256 <= m;
+  hipError_t e = oz::launch_scan_rows(m, k, A, lda, 0, ea, side_job ? eb : nullptr, side_job ? n : 0, s);
+  if (e == hipSuccess && !side_job) e = oz::launch_clear_keys(n, eb, s);
+  if (e == hipSuccess) e = oz::launch_scan_cols(n, k, B, ldb, eb, s);
+  if (e == hipSuccess) e = oz::launch_digits(0, m, k, kp, A, lda, ea, false, da, s);
+  if (e == hipSuccess) e = oz::launch_digits(1, n, k, kp, B, ldb, eb, true, db, s);
+  if (e == hipSuccess) e = oz::launch_bound_gemm(m, n, kp, da, db, total, part, w.splits, bt, ttop, s);
+  if (e == hipSuccess) e = oz::launch_accurate_shifts(m, n, total, colmin, ea, eb, s);
+  return e;
+}
+
+// The largest shift of the accurate mode: |A' 2^...| < 2^58, the range of the
+// general residue path (the deconstruction runs it at this t).
+constexpr int kAccurateT = 58;
+
 // The allocation-free entry point's workspace: one static array per GPU
 // (each device's code object holds its own copy).  In host code `scratch`
 // names a host-side stand-in, never the device memory: its device address is
@@ -352,6 +420,120 @@ ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A
   const int sub = subtract ? 1 : 0;
   // outputs on rows / columns flagged non-finite are re-issued natively
   const oz::NativeOperands nat{A, lda, B, ldb, k};
+  if (e == hipSuccess)
+    e = bytes ? oz::launch_reconstruct_bytes_i8(m, n, (const int8_t*)cres, ea, eb, C, ldc, sub, nat, s)
+              : oz::launch_reconstruct_i16(m, n, (const int16_t*)cres, ea, eb, C, ldc, sub, nat, s);
+  if (ev && e == hipSuccess) e = hipEventRecord(ev[4], s);
+  if (owned) {
+    const hipError_t f = hipFreeAsync(ws, s);
+    if (e == hipSuccess) e = f;
+  }
+  return hip_status(e);
+}
+
+size_t ozaki25_accurate_exponents_workspace_size(int64_t m, int64_t n, int64_t k) {
+  if (m < 0 || n < 0 || k < 0) return 0;
+  return acc_layout(m, n, k).bytes;
+}
+
+ozaki25_status ozaki25_accurate_exponents(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
+                                          const double* B, int64_t ldb, ozaki25_moduli_set set,
+                                          int32_t* expsA, int32_t* expsB, void* workspace,
+                                          size_t workspace_bytes, void* stream) {
+  if (!known_set(set) || m < 0 || n < 0 || k < 0) return OZAKI25_ERR_INVALID_VALUE;
+  if (k > OZAKI25_MAX_K || n > OZAKI25_MAX_N) return OZAKI25_ERR_UNSUPPORTED;
+  if (m == 0 || n == 0 || k == 0) return OZAKI25_SUCCESS;
+  if (!A || !B || !expsA || !expsB || lda < k || ldb < n) return OZAKI25_ERR_INVALID_VALUE;
+  if (((uintptr_t)A & 7) || ((uintptr_t)B & 7) || ((uintptr_t)expsA & 3) || ((uintptr_t)expsB & 3))
+    return OZAKI25_ERR_INVALID_VALUE;
+  if (overlaps(expsA, (size_t)m * 4, expsB, (size_t)n * 4)) return OZAKI25_ERR_INVALID_VALUE;
+  const AccWorkspace w = acc_layout(m, n, k);
+  hipStream_t s = (hipStream_t)stream;
+  void* ws = workspace;
+  bool owned = false;
+  if (ws) {
+    if (workspace_bytes < w.bytes || ((uintptr_t)ws & (kAlign - 1))) return OZAKI25_ERR_WORKSPACE;
+  } else {
+    if (hipMallocAsync(&ws, w.bytes, s) != hipSuccess || !ws) return OZAKI25_ERR_WORKSPACE;
+    owned = true;
+  }
+  hipError_t e = accurate_exponents(set, m, n, k, A, lda, B, ldb, expsA, expsB, (char*)ws, w, s);
+  if (owned) {
+    const hipError_t f = hipFreeAsync(ws, s);
+    if (e == hipSuccess) e = f;
+  }
+  return hip_status(e);
+}
+
+size_t ozaki25_dgemm_accurate_workspace_size(int64_t m, int64_t n, int64_t k, ozaki25_moduli_set set) {
+  if (!known_set(set) || m < 0 || n < 0 || k < 0) return 0;
+  return layout(m, n, k, set).total + acc_layout(m, n, k).bytes;
+}
+
+ozaki25_status ozaki25_dgemm_accurate(int64_t m, int64_t n, int64_t k, const double* A, int64_t lda,
+                                      const double* B, int64_t ldb, double* C, int64_t ldc,
+                                      ozaki25_moduli_set set, ozaki25_quantiser quant, int subtract,
+                                      void* workspace, size_t workspace_bytes,
+                                      void* const* stage_events, void* stream) {
+  if (!known_set(set) || !known_quantiser(quant) || m < 0 || n < 0 || k < 0)
+    return OZAKI25_ERR_INVALID_VALUE;
+  if (k > OZAKI25_MAX_K || n > OZAKI25_MAX_N) return OZAKI25_ERR_UNSUPPORTED;
+  if (m == 0 || n == 0) return OZAKI25_SUCCESS;
+  if (!C || ldc < n || ((uintptr_t)C & 7)) return OZAKI25_ERR_INVALID_VALUE;
+  // k == 0 needs no scaling: C = +0 (or unchanged), as in the fast mode
+  if (k == 0)
+    return ozaki25_dgemm_ex(m, n, k, A, lda, B, ldb, C, ldc, set, quant, subtract, nullptr, 0, stage_events,
+                            stream);
+  if (!A || !B || lda < k || ldb < n || ((uintptr_t)A & 7) || ((uintptr_t)B & 7))
+    return OZAKI25_ERR_INVALID_VALUE;
+  const size_t cb = matrix_bytes(m, n, ldc);
+  if (overlaps(A, matrix_bytes(m, k, lda), C, cb) || overlaps(B, matrix_bytes(k, n, ldb), C, cb))
+    return OZAKI25_ERR_INVALID_VALUE;
+
+  const Workspace w = layout(m, n, k, set);
+  const AccWorkspace aw = acc_layout(m, n, k);
+  const size_t need = w.total + aw.bytes;
+  hipStream_t s = (hipStream_t)stream;
+  hipEvent_t* ev = (hipEvent_t*)stage_events;
+  void* ws = workspace;
+  bool owned = false;
+  if (ws) {
+    if (workspace_bytes < need || ((uintptr_t)ws & (kAlign - 1))) return OZAKI25_ERR_WORKSPACE;
+  } else {
+    if (hipMallocAsync(&ws, need, s) != hipSuccess || !ws) return OZAKI25_ERR_WORKSPACE;
+    owned = true;
+  }
+  char* base = (char*)ws;
+  int8_t* pa = (int8_t*)(base + w.planes_a);
+  int8_t* pb = (int8_t*)(base + w.planes_b);
+  int32_t* ea = (int32_t*)(base + w.exps_a);
+  int32_t* eb = (int32_t*)(base + w.exps_b);
+  void* cres = base + w.cres;
+  void* part = w.splits > 1 ? base + w.part : nullptr;
+  const bool bytes = bytes_set(set);
+  const bool fused = fused_a(m, n, set);
+  const int64_t kp = k_pad(k);
+  const int sub = subtract ? 1 : 0;
+  const oz::NativeOperands nat{A, lda, B, ldb, k};
+
+  hipError_t e = hipSuccess;
+  if (ev) e = hipEventRecord(ev[0], s);
+  if (e == hipSuccess) e = accurate_exponents(set, m, n, k, A, lda, B, ldb, ea, eb, base + w.total, aw, s);
+  if (ev && e == hipSuccess) e = hipEventRecord(ev[1], s);
+  if (e == hipSuccess && !fused)
+    e = oz::launch_deconstruct((int)set, (int)quant, 0, m, m, k, kp, kAccurateT, A, lda, ea, false, pa, s);
+  if (e == hipSuccess)
+    e = oz::launch_deconstruct((int)set, (int)quant, 1, n, n, k, kp, kAccurateT, B, ldb, eb, false, pb, s);
+  if (ev && e == hipSuccess) e = hipEventRecord(ev[2], s);
+  if (e == hipSuccess) {
+    if (fused)
+      e = oz::launch_fused_bytes((int)quant, m, n, k, kp, kAccurateT, A, lda, ea, pb, (int8_t*)cres, s);
+    else if (bytes)
+      e = oz::launch_residue_gemm_bytes_i8(m, n, kp, pa, pb, (int8_t*)cres, (int8_t*)part, w.splits, s);
+    else
+      e = oz::launch_residue_gemm_i16(m, n, kp, pa, pb, (int16_t*)cres, (int16_t*)part, w.splits, s);
+  }
+  if (ev && e == hipSuccess) e = hipEventRecord(ev[3], s);
   if (e == hipSuccess)
     e = bytes ? oz::launch_reconstruct_bytes_i8(m, n, (const int8_t*)cres, ea, eb, C, ldc, sub, nat, s)
               : oz::launch_reconstruct_i16(m, n, (const int16_t*)cres, ea, eb, C, ldc, sub, nat, s);

@@ -347,6 +347,37 @@ __global__ __launch_bounds__(256) void deconstruct_bytes_kernel(int64_t vecs, in
                             plane_offset(vstride, kRA, v, g));
 }
 
+// ---- accurate mode (Sec. 2, Eq. (alpha)): the magnitude digit of every
+// element, ceil(16 |x| 2^-e) in {0..16} with e the vector's frexp exponent,
+// as one int8 plane in the plane layout (the operand of the bound product).
+// exps holds -e (the exponent scan at t = 0; with keys_in the column scan's
+// keys).  16 |x| 2^-e is exact in FP64 unless it falls below the normal
+// range, where its ceiling is 1; a non-finite vector gets zero digits.
+template <int SIDE>
+__global__ __launch_bounds__(256) void digits_kernel(int64_t vecs, int64_t k, int64_t kp,
+                                                     const double* __restrict__ X, int64_t ldx,
+                                                     const int32_t* __restrict__ exps, bool keys_in,
+                                                     int8_t* __restrict__ digits) {
+  int64_t v, g;
+  group_of(vecs, v, g);
+  if (v >= vecs || g >= kp / kElems) return;
+  double x[kElems];
+  const int ne = load_group<SIDE>(vecs, k, X, ldx, exps, keys_in, 0, v, g * kElems, true, x);
+  int d[kElems];
+#pragma unroll
+  for (int c = 0; c < kElems; ++c) {
+    const double a = __builtin_fabs(x[c]);
+    const double u = __builtin_ceil(__builtin_ldexp(a, 4 + ne));
+    d[c] = a == 0.0 ? 0 : (u < 1.0 ? 1 : (int)u);
+  }
+  uint4 w;
+  w.x = pack_bytes(d[0], d[1], d[2], d[3]);
+  w.y = pack_bytes(d[4], d[5], d[6], d[7]);
+  w.z = pack_bytes(d[8], d[9], d[10], d[11]);
+  w.w = pack_bytes(d[12], d[13], d[14], d[15]);
+  put16(digits + plane_offset(vecs, 1, v, g), w);
+}
+
 struct DecArgs {
   int64_t blocks, vecs, vstride, k, kp;
   const double* X;
@@ -385,6 +416,20 @@ void launch_side(int mode, bool tz, const DecArgs& a, hipStream_t stream) {
 }
 
 }  // namespace
+
+hipError_t launch_digits(int side, int64_t vecs, int64_t k, int64_t kp, const double* X, int64_t ldx,
+                         const int32_t* exps, bool keys_in, int8_t* digits, hipStream_t stream) {
+  if (vecs <= 0 || kp <= 0) return hipSuccess;
+  const int64_t blocks = ((vecs + 31) / 32) * (kp / 128);
+  if (blocks > (int64_t)UINT32_MAX) return hipErrorInvalidValue;
+  if (side == 0)
+    hipLaunchKernelGGL(digits_kernel<0>, dim3((unsigned)blocks), dim3(256), 0, stream, vecs, k, kp, X, ldx,
+                       exps, keys_in, digits);
+  else
+    hipLaunchKernelGGL(digits_kernel<1>, dim3((unsigned)blocks), dim3(256), 0, stream, vecs, k, kp, X, ldx,
+                       exps, keys_in, digits);
+  return hipGetLastError();
+}
 
 hipError_t launch_deconstruct(int set, int quant, int side, int64_t vecs, int64_t vstride, int64_t k,
                               int64_t kp, int t, const double* X, int64_t ldx, const int32_t* exps,

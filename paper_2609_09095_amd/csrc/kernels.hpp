@@ -103,6 +103,26 @@ hipError_t launch_reconstruct_bytes_i8(int64_t m, int64_t n, const int8_t* cres,
                                        const int32_t* eb, double* C, int64_t ldc, int subtract,
                                        const NativeOperands& nat, hipStream_t stream);
 
+// Accurate mode (Sec. 2, Eq. (alpha)).
+//  - launch_digits: the magnitude digits ceil(16 |x| 2^-e) of one operand as
+//    a single int8 plane [kp/128][vecs][128]; exps holds -e (the scan at
+//    t = 0, or with keys_in the column scan's keys);
+//  - launch_bound_gemm: U = digitsA digitsB^T on int8 MFMA and, per output,
+//    the total shift L (int8 [m][n]) with 2^L U <= T, T = 2^8 (M/2 - 1) of
+//    bit length bt and ttop = T >> (bt - 33); `splits` from
+//    bound_gemm_splits, with splits * m * n int32 of `part` when above 1;
+//  - launch_accurate_shifts: from L the column shifts (into colmin, n int32
+//    of scratch), tau = u - f into eb_keys (the column scan's keys) and
+//    sigma = s - e into ea (the row scan at t = 0).
+hipError_t launch_digits(int side, int64_t vecs, int64_t k, int64_t kp, const double* X, int64_t ldx,
+                         const int32_t* exps, bool keys_in, int8_t* digits, hipStream_t stream);
+int bound_gemm_splits(int64_t m, int64_t n, int64_t kp);
+hipError_t launch_bound_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* da, const int8_t* db,
+                             int8_t* total, int32_t* part, int splits, int bt, uint64_t ttop,
+                             hipStream_t stream);
+hipError_t launch_accurate_shifts(int64_t m, int64_t n, const int8_t* L, int32_t* colmin, int32_t* ea,
+                                  int32_t* eb_keys, hipStream_t stream);
+
 // C = +0.0 over an m x n block (the k == 0 product).
 hipError_t launch_zero_c(int64_t m, int64_t n, double* C, int64_t ldc, hipStream_t stream);
 

@@ -608,14 +608,35 @@ __device__ __forceinline__ void stage_mma_dma_i8(const int8_t* la, const int8_t*
   __builtin_amdgcn_sched_group_barrier(0x008, 8 * NB - 3 * ND > 0 ? 8 * NB - 3 * ND : 0, 0);
 }
 
-template <typename OT, int S>
+// Accurate mode (Sec. 2, Eq. (alpha)): the admissible total shift of one
+// output from its magnitude bound U (the exact product of the digit
+// planes): the largest L with U 2^L <= T = 2^8 (M/2 - 1).  bt is the bit
+// length of T and ttop = T >> (bt - 33).  For U of b bits, T >> (bt - b) =
+// ttop >> (33 - b) has b bits as well, so L is bt - b when U is at most
+// that and bt - b - 1 otherwise.  U = 0 stores 127, and so does any L above
+// it: no shift up to the cap of 58 is then constrained.
+__device__ __forceinline__ int bound_total(int u, int bt, uint64_t ttop) {
+  if (u <= 0) return 127;
+  const int b = 32 - __builtin_clz((unsigned)u);
+  const int L = (uint64_t)u <= (ttop >> (33 - b)) ? bt - b : bt - b - 1;
+  return L < 127 ? L : 127;
+}
+
+// BOUND: the bound product of the accurate mode on the same pipeline -- one
+// plane of digits (0..16) per operand, the plain int32 sum (at most
+// 256 k <= 2^30, no reduction), stored as the total L (int8 OT) or, for a
+// split k range, as the raw partial sums (int32 OT; bound_totals_kernel
+// adds them up).
+template <typename OT, int S, bool BOUND = false>
 __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, int64_t n,
                                                                     int64_t kp,
                                                                     const int8_t* __restrict__ pa,
                                                                     const int8_t* __restrict__ pb,
                                                                     OT* __restrict__ cres,
-                                                                    int splits, int group) {
+                                                                    int splits, int group,
+                                                                    int bt = 0, uint64_t ttop = 0) {
   constexpr int BM = Tile<S>::BM, BN = Tile<S>::BN, NB = Tile<S>::BB, WC = Tile<S>::WC;
+  constexpr int NPL = BOUND ? 1 : kRA;  // planes in the layout
   __shared__ __attribute__((aligned(1024))) int8_t lds_a0[BM * BK];
   __shared__ __attribute__((aligned(1024))) int8_t lds_b0[BN * BK];
   __shared__ __attribute__((aligned(1024))) int8_t lds_a1[BM * BK];
@@ -627,7 +648,7 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
   block_coords(blockIdx.x / (unsigned)splits, (uint32_t)tiles_m, (uint32_t)tiles_n, (uint32_t)group, mod,
                tm, tn);
   const int mm = kModA[mod];
-  cres += (int64_t)split * kRA * m * n;
+  cres += (int64_t)split * NPL * m * n;
   const double minv = kInvA[mod];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -658,9 +679,9 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
   const int nstage = (int)((uint32_t)nstage_all * (uint32_t)(split + 1) / (uint32_t)splits);  // one past the last
   // look-ahead cursor: stage ls and its A and B pieces, one K stage of the
   // plane layout apart (it stays on the panel's last stage)
-  const int64_t step_a = (int64_t)kRA * m * BK, step_b = (int64_t)kRA * n * BK;
-  const int8_t* const first_a = pa + (((int64_t)sbeg * kRA + mod) * m + tm * BM) * BK;
-  const int8_t* const first_b = pb + (((int64_t)sbeg * kRA + mod) * n + tn * BN) * BK;
+  const int64_t step_a = (int64_t)NPL * m * BK, step_b = (int64_t)NPL * n * BK;
+  const int8_t* const first_a = pa + (((int64_t)sbeg * NPL + mod) * m + tm * BM) * BK;
+  const int8_t* const first_b = pb + (((int64_t)sbeg * NPL + mod) * n + tn * BN) * BK;
   int ls = sbeg;
   const int8_t* la = first_a;
   const int8_t* lb = first_b;
@@ -671,8 +692,10 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
       lb += step_b;
     }
   };
-  for (int s0 = sbeg; s0 < nstage; s0 += kSegA) {
-    const int s1 = s0 + kSegA < nstage ? s0 + kSegA : nstage;
+  // the bound product needs no reduction: one segment
+  const int seg = BOUND ? nstage - sbeg : kSegA;
+  for (int s0 = sbeg; s0 < nstage; s0 += seg) {
+    const int s1 = s0 + seg < nstage ? s0 + seg : nstage;
     ls = s0;
     la = first_a + (int64_t)(s0 - sbeg) * step_a;
     lb = first_b + (int64_t)(s0 - sbeg) * step_b;
@@ -695,7 +718,7 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
     }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();  // every wave is done with the buffers before the next segment loads
-    if (s1 < nstage) {
+    if (!BOUND && s1 < nstage) {
 #pragma unroll
       for (int a = 0; a < 2; ++a)
 #pragma unroll
@@ -708,8 +731,25 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
   OT* out = (OT*)uniform_ptr((const int8_t*)(cres + (int64_t)mod * m * n + tm * BM * n + tn * BN));
   store_tile<false, OT, S>(out, (int)n, (int)(m - tm * BM), (int)(n - tn * BN), wr, wc, fr, fh,
                             [&](int a, int b, int v) {
-                              return cmod_i32<sizeof(OT) == 4>(acc[a][b][v], mm, minv);
+                              if constexpr (BOUND)
+                                return sizeof(OT) == 1 ? bound_total(acc[a][b][v], bt, ttop)
+                                                       : acc[a][b][v];
+                              else
+                                return cmod_i32<sizeof(OT) == 4>(acc[a][b][v], mm, minv);
                             });
+}
+
+// The split bound product's partial sums [splits][m][n], added and turned
+// into totals.
+__global__ __launch_bounds__(256) void bound_totals_kernel(int64_t mn, int splits,
+                                                           const int32_t* __restrict__ part,
+                                                           int8_t* __restrict__ total, int bt,
+                                                           uint64_t ttop) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= mn) return;
+  int sum = 0;
+  for (int sp = 0; sp < splits; ++sp) sum += part[sp * mn + i];
+  total[i] = (int8_t)bound_total(sum, bt, ttop);
 }
 
 // Sum of the splits' centred partial products, reduced to the centred
@@ -791,18 +831,16 @@ hipError_t launch_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* pa, const
 
 }  // namespace
 
-int residue_gemm_splits(int set, int64_t m, int64_t n, int64_t kp) {
-  // Split the k range when the tiles of all moduli leave most of the chip
-  // idle.  A block holds a whole CU, so blocks run in rounds of kCUs; the
-  // split count minimises rounds x (fixed cost of a block + its stages),
-  // the fixed cost (prologue, carries, epilogue) measured at about seven
-  // stage times, with at least 2 stages of each product per block (4 for
-  // the single-product int8 kernel).
+namespace {
+
+// Split the k range when the output tiles leave most of the chip idle.  A
+// block holds a whole CU, so blocks run in rounds of kCUs; the split count
+// minimises rounds x (fixed cost of a block + its stages), the fixed cost
+// (prologue, carries, epilogue) measured at about seven stage times, with
+// at least 2 stages of each product per block (4 for the single-product
+// int8 kernel).
+int best_splits(int64_t blocks, int64_t nstage, bool bytes) {
   constexpr int64_t kCUs = 256, kFixedStages = 7;
-  if (m <= 0 || n <= 0) return 1;
-  const bool bytes = set == kSetBytes;
-  const int64_t blocks = gemm_blocks(bytes, m, n);
-  const int64_t nstage = kp / BK;
   if (blocks >= 512) return 1;
   int64_t cap = nstage / (bytes ? 4 : 2);
   if (cap > kMaxSplits) cap = kMaxSplits;
@@ -817,6 +855,52 @@ int residue_gemm_splits(int set, int64_t m, int64_t n, int64_t kp) {
     }
   }
   return (int)best_s;
+}
+
+}  // namespace
+
+int residue_gemm_splits(int set, int64_t m, int64_t n, int64_t kp) {
+  if (m <= 0 || n <= 0) return 1;
+  const bool bytes = set == kSetBytes;
+  return best_splits(gemm_blocks(bytes, m, n), kp / BK, bytes);
+}
+
+int bound_gemm_splits(int64_t m, int64_t n, int64_t kp) {
+  if (m <= 0 || n <= 0) return 1;
+  return best_splits(gemm_blocks(true, m, n) / kRA, kp / BK, true);
+}
+
+hipError_t launch_bound_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* da, const int8_t* db,
+                             int8_t* total, int32_t* part, int splits, int bt, uint64_t ttop,
+                             hipStream_t stream) {
+  if (m <= 0 || n <= 0) return hipSuccess;
+  if (n > kMaxResidueCols) return hipErrorInvalidValue;
+  const int nstage = (int)(kp / BK);
+  if (nstage < 1 || splits < 1 || splits > nstage || (splits > 1 && !part)) return hipErrorInvalidValue;
+  const int shape = gemm_shape(true, n);
+  const int group = kp <= 16 * BK ? 4 : 2;
+  const int64_t blocks = gemm_blocks(true, m, n) / kRA;
+  if (blocks * splits > (int64_t)UINT32_MAX) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)(blocks * splits));
+  if (splits == 1) {
+    if (shape == 3)
+      hipLaunchKernelGGL((residue_gemm_bytes_kernel<int8_t, 3, true>), grid, dim3(1024), 0, stream, m, n,
+                         kp, da, db, total, 1, group, bt, ttop);
+    else
+      hipLaunchKernelGGL((residue_gemm_bytes_kernel<int8_t, 2, true>), grid, dim3(1024), 0, stream, m, n,
+                         kp, da, db, total, 1, group, bt, ttop);
+  } else {
+    if (shape == 3)
+      hipLaunchKernelGGL((residue_gemm_bytes_kernel<int32_t, 3, true>), grid, dim3(1024), 0, stream, m, n,
+                         kp, da, db, part, splits, group, bt, ttop);
+    else
+      hipLaunchKernelGGL((residue_gemm_bytes_kernel<int32_t, 2, true>), grid, dim3(1024), 0, stream, m, n,
+                         kp, da, db, part, splits, group, bt, ttop);
+    const int64_t mn = m * n;
+    hipLaunchKernelGGL(bound_totals_kernel, dim3((unsigned)((mn + 255) / 256)), dim3(256), 0, stream, mn,
+                       splits, part, total, bt, ttop);
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_residue_gemm_i32(int64_t m, int64_t n, int64_t kp, const int8_t* pa,

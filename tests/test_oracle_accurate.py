@@ -104,6 +104,11 @@ def test_bound_gemm_vs_numpy():
     DB = rng.integers(0, 17, size=(7, 301)).astype(np.uint8)
     U = oracle.bound_gemm(DA, DB)
     assert np.array_equal(U, DA.astype(np.int64) @ DB.astype(np.int64).T)
+    # the FP64 matmul route of large products agrees with the C loops
+    DA = np.full((40, 5000), 16, np.uint8)
+    DA[1::2] = rng.integers(0, 17, size=(20, 5000))
+    DB = rng.integers(0, 17, size=(30, 5000)).astype(np.uint8)
+    assert np.array_equal(oracle.bound_gemm(DA, DB, loops=True), oracle.bound_gemm(DA, DB, loops=False))
 
 
 @pytest.mark.parametrize("set", [0, 1])
