@@ -208,6 +208,43 @@ def time_set(oz, torch, w, Ad, Bd, Cd, cfg, steps, warmup, quant):
     return ms, stage.mean(axis=0).tolist(), median
 
 
+def time_accurate(oz, torch, w, Ad, Bd, Cd, C0d, cfg, steps, warmup, quant):
+    """ms per step and per stage of ozaki25_dgemm_accurate (the accurate
+    mode: magnitude digits, bound product and shifts, then the same stages
+    as the fast mode with those exponents)."""
+    ws = torch.empty(oz.ozaki25_dgemm_accurate_workspace_size(w.m, w.n, w.k, cfg["id"]), dtype=torch.uint8,
+                     device=Ad.device)
+
+    def step(events=None):
+        oz.ozaki25_dgemm_accurate(Ad, Bd, Cd, subtract=w.subtract, workspace=ws, stage_events=events,
+                                  set=cfg["id"], quantiser=quant)
+
+    if C0d is not None:
+        Cd.copy_(C0d)
+    for _ in range(warmup):
+        step()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(oz.NUM_STAGE_EVENTS)] for _ in range(steps)]
+    for row in ev:
+        for e in row:
+            e.record()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(steps):
+        step(ev[i])
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / steps
+    stage = np.array([[row[j].elapsed_time(row[j + 1]) for j in range(oz.NUM_STAGE_EVENTS - 1)] for row in ev])
+    del ws
+    st = stage.mean(axis=0).tolist()
+    return {"ms_per_step": round(ms, 4), "value": round(w.flops / (ms * 1e-3) / 1e12, 3), "unit": "TFLOPS",
+            "stage_ms": dict(zip(("exponents", "deconstruct", "residue_gemm", "reconstruct"),
+                                 [round(x, 4) for x in st])),
+            "note": "ozaki25_dgemm_accurate: per-row/column shifts from the int8 magnitude-bound "
+                    "product (one extra product) instead of the fixed t(k)"}
+
+
 def time_planes(oz, torch, w, Ad, Bd, Cd, cfg, steps, quant):
     """Storage mode P: ms per ozaki25_dgemm_planes call on planes made once."""
     planesA, expsA = oz.ozaki25_deconstruct(0, Ad, set=cfg["id"], quantiser=quant)
@@ -368,11 +405,17 @@ def main():
         pms = time_planes(oz, torch, w, Ad, Bd, Cd, ocfg, args.steps, quant)
         other["stored_planes"] = {"ms_per_call": round(pms, 4), "value": round(w.flops / (pms * 1e-3) / 1e12, 3),
                                   "unit": "TFLOPS"}
+        log(f"[bench] {ocfg['moduli']}: accurate mode")
+        other["accurate_mode"] = time_accurate(oz, torch, w, Ad, Bd, Cd, C0d, ocfg, args.steps, args.warmup,
+                                               quant)
 
     if C0d is not None:
         Cd.copy_(C0d)
     log("[bench] stored planes (mode P)")
     pms = time_planes(oz, torch, w, Ad, Bd, Cd, cfg, args.steps, quant)
+    log(f"[bench] {cfg['moduli']}: accurate mode")
+    acc = time_accurate(oz, torch, w, Ad, Bd, Cd, C0d, cfg, args.steps, args.warmup, quant)
+    log(f"[bench] accurate mode {acc['ms_per_step']:.3f} ms/step; stages {acc['stage_ms']}")
     if C0d is not None:
         Cd.copy_(C0d)
     log("[bench] graph replay")
@@ -445,6 +488,7 @@ def main():
                           "unit": "TFLOPS",
                           "note": "storage mode P: ozaki25_dgemm_planes on planes deconstructed once "
                                   "(residue products + reconstruction per call)"},
+        "accurate_mode": acc,
         "graph_replay": {"ms_per_call": round(gms, 4), "value": round(w.flops / (gms * 1e-3) / 1e12, 3),
                          "unit": "TFLOPS",
                          "note": "one ozaki25_dgemm_ex call captured in a HIP graph, replayed"},

@@ -194,8 +194,8 @@ void bound_limit(ozaki25_moduli_set set, int* bt, uint64_t* ttop) {
 }
 
 // The accurate mode's exponents into ea / eb: the scans at t = 0 (A's row
-// scan clears B's column keys on the side), the magnitude digits, the bound
-// product and its totals, then the shifts.
+// scan clears B's column keys on the side and writes A's magnitude digits),
+// B's digits, the bound product and its totals, then the shifts.
 hipError_t accurate_exponents(ozaki25_moduli_set set, int64_t m, int64_t n, int64_t k, const double* A,
                               int64_t lda, const double* B, int64_t ldb, int32_t* ea, int32_t* eb,
                               char* aux, const AccWorkspace& w, hipStream_t s) {
@@ -209,19 +209,20 @@ hipError_t accurate_exponents(ozaki25_moduli_set set, int64_t m, int64_t n, int6
   uint64_t ttop = 0;
   bound_limit(set, &bt, &ttop);
   const bool side_job = (n + 255) / 256 <= m;
-  hipError_t e = oz::launch_scan_rows(m, k, A, lda, 0, ea, side_job ? eb : nullptr, side_job ? n : 0, s);
+  // the row scan writes A's digits too
+  hipError_t e =
+      oz::launch_scan_rows(m, k, A, lda, 0, ea, side_job ? eb : nullptr, side_job ? n : 0, s, da, kp);
   if (e == hipSuccess && !side_job) e = oz::launch_clear_keys(n, eb, s);
   if (e == hipSuccess) e = oz::launch_scan_cols(n, k, B, ldb, eb, s);
-  if (e == hipSuccess) e = oz::launch_digits(0, m, k, kp, A, lda, ea, false, da, s);
   if (e == hipSuccess) e = oz::launch_digits(1, n, k, kp, B, ldb, eb, true, db, s);
   if (e == hipSuccess) e = oz::launch_bound_gemm(m, n, kp, da, db, total, part, w.splits, bt, ttop, s);
   if (e == hipSuccess) e = oz::launch_accurate_shifts(m, n, total, colmin, ea, eb, s);
   return e;
 }
 
-// The largest shift of the accurate mode: |A' 2^...| < 2^58, the range of the
-// general residue path (the deconstruction runs it at this t).
-constexpr int kAccurateT = 58;
+// The accurate mode's shifts are at most 58: the deconstruction runs at that
+// t (the residue route with one correction).
+constexpr int kAccurateT = oz::kMaxScaleBits;
 
 // The allocation-free entry point's workspace: one static array per GPU
 // (each device's code object holds its own copy).  In host code `scratch`

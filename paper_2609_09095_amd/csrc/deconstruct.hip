@@ -15,7 +15,6 @@
 //  - B (side 1): every FP64 load reads 64 contiguous bytes of 8 rows of B.
 #include <utility>
 
-#include "device_math.hpp"
 #include "exponent_key.hpp"
 #include "kernels.hpp"
 #include "moduli.hpp"
@@ -56,16 +55,29 @@ __device__ __forceinline__ uint32_t low_word(double v) {
 }
 constexpr int log2_exact(int m) { return m <= 1 ? 0 : 1 + log2_exact(m / 2); }
 
-// y - q M modulo 2^24 for the nearest quotient q (EXACT path, |y| <= 2^51,
-// ylo = y mod 2^32).  For odd M the FMA rounds y RN(1/M) + kMagic once, to
-// kMagic + the integer nearest y RN(1/M); that product is within
-// |y| 2^-53 / M <= 1/(4M) of y / M, while y / M is at least 1/(2M) away from
-// a half integer, so the integer is the nearest quotient q and the low word
-// of the sum is q mod 2^32.  For the odd byte moduli (M <= 255, RN(1/M)
-// within 2^-61 of 1/M) this holds up to |y| <= 2^52: the error is at most
-// 2^-9 < 1/510.  The 24-bit multiply-add then gives
-// y - q M mod 2^24, and |y - q M| <= (M-1)/2.  For a power of two M, y itself
-// (mod 2^24) serves: its low log2(M) bits are the residue.
+// Residue modes (the template parameter RM below), by the range of the
+// scaled integers y = RN(x 2^sigma), |y| <= 2^t:
+//  1: nearest quotient, ylo = y mod 2^32 from y + kMagic      (|y| <= 2^51)
+//  2: nearest quotient, ylo split off by one exact FMA        (|y| <= 2^52,
+//     the odd byte moduli only)
+//  3: quotient within one of the nearest, ylo split off, one correction
+//     each way                                                (|y| <= 2^58)
+// 2^58 bounds every scale the library uses (t(k) <= 58 for both sets, and
+// the accurate mode's shifts are capped there).
+//
+// y - q M modulo 2^24 for the FMA quotient q (ylo = y mod 2^32).  For odd M
+// the FMA rounds y RN(1/M) + kMagic once, to kMagic + the integer nearest
+// y RN(1/M) (|y / M| < 2^51, so the sum lies in [2^52, 2^53), where the
+// spacing is 1); that product is within |y| ulp(1/M) / 2 of y / M.  For
+// |y| <= 2^51 that is at most 1/(4M), while y / M is at least 1/(2M) away
+// from a half integer, so the integer is the nearest quotient q and the low
+// word of the sum is q mod 2^32.  For the odd byte moduli (M <= 255,
+// ulp(1/M) / 2 = 2^-61) this holds up to |y| <= 2^52: the error is at most
+// 2^-9 < 1/510.  Up to |y| <= 2^58 (every odd modulus here has
+// ulp(1/M) / 2 <= 2^-61) the error is at most 1/8, so q is within 5/8 of
+// y / M: |y - q M| <= 5 M / 8, one correction from the centred range.  The
+// 24-bit multiply-add gives y - q M mod 2^24.  For a power of two M, y
+// itself (mod 2^24) serves: its low log2(M) bits are the residue.
 template <int M>
 __device__ __forceinline__ int residue_low(double y, uint32_t ylo) {
   if constexpr ((M & (M - 1)) == 0) {
@@ -81,20 +93,24 @@ __device__ __forceinline__ int residue_low(double y, uint32_t ylo) {
 }
 
 // Centred residue of the integer-valued y modulo M, in [-(M/2), (M-1)/2]
-// (an int, |residue| <= 544).  EXACT: sign-extend the low bits of
-// residue_low -- 24 bits for odd M (already centred: q is the nearest
-// quotient), log2(M) bits for a power of two (the two's complement field is
-// [-M/2, M/2) by itself).  Otherwise the general FP64 form with its two
-// corrections.
-template <int M, bool EXACT>
+// (an int, |residue| <= 544): the low bits of residue_low, sign-extended --
+// log2(M) bits for a power of two (the two's complement field is
+// [-M/2, M/2) by itself), 24 bits for odd M, already centred when q is the
+// nearest quotient (RM 1, 2) and after one correction otherwise (RM 3).
+template <int M, int RM>
 __device__ __forceinline__ int centred_residue(double y, uint32_t ylo) {
-  if constexpr (!EXACT) {
-    return cmod_f64<M>(y);
-  } else if constexpr ((M & (M - 1)) == 0) {
+  if constexpr ((M & (M - 1)) == 0) {
     constexpr int sh = 32 - log2_exact(M);
     return (int)(ylo << sh) >> sh;
   } else {
-    return (int)((uint32_t)residue_low<M>(y, ylo) << 8) >> 8;
+    const int r = (int)((uint32_t)residue_low<M>(y, ylo) << 8) >> 8;
+    if constexpr (RM == 3) {
+      constexpr int hi = (M - 1) / 2, lo = hi - M + 1;
+      const int r1 = r > hi ? r - M : r;
+      return r1 < lo ? r1 + M : r1;
+    } else {
+      return r;
+    }
   }
 }
 
@@ -155,7 +171,7 @@ __device__ __forceinline__ void gather_planes(uint32_t x0, uint32_t x1, uint32_t
   p2 = __builtin_amdgcn_perm(u23, u01, 0x05040100u);
 }
 
-template <int I, bool EXACT>
+template <int I, int RM>
 __device__ __forceinline__ void emit_modulus(const double (&y)[kElems], const uint32_t (&ylo)[kElems],
                                              int8_t* planes,
                                              int64_t plane_stride, int64_t off,
@@ -168,13 +184,13 @@ __device__ __forceinline__ void emit_modulus(const double (&y)[kElems], const ui
     float l0[kElems], l1[kElems];
 #pragma unroll
     for (int c = 0; c < kElems; ++c)
-      split_square<S>((float)centred_residue<M, EXACT>(y[c], ylo[c]), l0[c], l1[c]);
+      split_square<S>((float)centred_residue<M, RM>(y[c], ylo[c]), l0[c], l1[c]);
     store16(base, l0);
     store16(base + plane_stride, l1);
   } else {
     uint32_t x[kElems];
 #pragma unroll
-    for (int c = 0; c < kElems; ++c) x[c] = lut[centred_residue<M, EXACT>(y[c], ylo[c]) + 256];
+    for (int c = 0; c < kElems; ++c) x[c] = lut[centred_residue<M, RM>(y[c], ylo[c]) + 256];
     uint4 w0, w1, w2;
     gather_planes(x[0], x[1], x[2], x[3], w0.x, w1.x, w2.x);
     gather_planes(x[4], x[5], x[6], x[7], w0.y, w1.y, w2.y);
@@ -186,11 +202,11 @@ __device__ __forceinline__ void emit_modulus(const double (&y)[kElems], const ui
   }
 }
 
-template <bool EXACT, int... I>
+template <int RM, int... I>
 __device__ __forceinline__ void emit_all(std::integer_sequence<int, I...>, const double (&y)[kElems],
                                          const uint32_t (&ylo)[kElems], int8_t* planes,
                                          int64_t plane_stride, int64_t off, const uint32_t* lut) {
-  (emit_modulus<I, EXACT>(y, ylo, planes, plane_stride, off, lut), ...);
+  (emit_modulus<I, RM>(y, ylo, planes, plane_stride, off, lut), ...);
 }
 
 // Thread -> (vector, 16-k group), both sides: a block covers 32 vectors x
@@ -241,25 +257,25 @@ __device__ __forceinline__ int load_group(int64_t vecs, int64_t k, const double*
 }
 
 // |x 2^sigma| < 2^t: the scaling is exact, and the quantiser of Eq. (scale)
-// is the one rounding: to nearest even (RN), or toward zero (TZ).  EXACT
-// also forms ylo = y mod 2^32: from y + kMagic (t <= 51), or with SPLIT
-// (|y| <= 2^52, where that sum is no longer exact) as y - h 2^32 with
-// h = floor(y 2^-32), one exact FMA.
-template <bool TZ, bool EXACT, bool SPLIT = false>
+// is the one rounding: to nearest even (RN), or toward zero (TZ).  Then
+// ylo = y mod 2^32: from y + kMagic (RM 1, |y| <= 2^51), or (RM 2, 3: past
+// 2^51 that sum is no longer exact) as y - h 2^32 with h = floor(y 2^-32),
+// one exact FMA.
+template <bool TZ, int RM>
 __device__ __forceinline__ void scale_round(const double (&x)[kElems], int sigma,
                                             double (&y)[kElems], uint32_t (&ylo)[kElems]) {
 #pragma unroll
   for (int c = 0; c < kElems; ++c) {
     const double v = __builtin_ldexp(x[c], sigma);
     y[c] = TZ ? __builtin_trunc(v) : __builtin_rint(v);
-    if constexpr (EXACT && SPLIT)
-      ylo[c] = (uint32_t)__builtin_fma(-__builtin_floor(y[c] * 0x1p-32), 0x1p32, y[c]);
+    if constexpr (RM == 1)
+      ylo[c] = low_word(y[c] + kMagic);
     else
-      ylo[c] = EXACT ? low_word(y[c] + kMagic) : 0u;
+      ylo[c] = (uint32_t)__builtin_fma(-__builtin_floor(y[c] * 0x1p-32), 0x1p32, y[c]);
   }
 }
 
-template <int SIDE, bool EXACT, bool TZ>
+template <int SIDE, int RM, bool TZ>
 __global__ __launch_bounds__(256) void deconstruct_kernel(int64_t vecs, int64_t vstride, int64_t k,
                                                           int64_t kp, const double* __restrict__ X,
                                                           int64_t ldx, const int32_t* __restrict__ exps,
@@ -278,8 +294,8 @@ __global__ __launch_bounds__(256) void deconstruct_kernel(int64_t vecs, int64_t 
   if (!active) return;
   double y[kElems];
   uint32_t ylo[kElems];
-  scale_round<TZ, EXACT>(x, sigma, y, ylo);
-  emit_all<EXACT>(std::make_integer_sequence<int, kR>{}, y, ylo, planes, vstride * 128,
+  scale_round<TZ, RM>(x, sigma, y, ylo);
+  emit_all<RM>(std::make_integer_sequence<int, kR>{}, y, ylo, planes, vstride * 128,
                   plane_offset(vstride, kPlanes, v, g), lut);
 }
 
@@ -297,8 +313,8 @@ __device__ __forceinline__ uint32_t pack_bytes(int a, int b, int c, int d) {
 }
 
 // The byte of the centred residue: its low eight bits, which residue_low
-// already holds on the EXACT path.
-template <int I, bool EXACT>
+// already holds when q is the nearest quotient (RM 1, 2).
+template <int I, int RM>
 __device__ __forceinline__ void emit_byte_modulus(const double (&y)[kElems],
                                                   const uint32_t (&ylo)[kElems], int8_t* planes,
                                                   int64_t plane_stride, int64_t off) {
@@ -306,7 +322,7 @@ __device__ __forceinline__ void emit_byte_modulus(const double (&y)[kElems],
   int r[kElems];
 #pragma unroll
   for (int c = 0; c < kElems; ++c)
-    r[c] = EXACT ? residue_low<M>(y[c], ylo[c]) : cmod_f64<M>(y[c]);
+    r[c] = RM == 3 ? centred_residue<M, 3>(y[c], ylo[c]) : residue_low<M>(y[c], ylo[c]);
   uint4 w;
   w.x = pack_bytes(r[0], r[1], r[2], r[3]);
   w.y = pack_bytes(r[4], r[5], r[6], r[7]);
@@ -315,19 +331,16 @@ __device__ __forceinline__ void emit_byte_modulus(const double (&y)[kElems],
   put16(planes + (int64_t)I * plane_stride + off, w);
 }
 
-template <bool EXACT, int... I>
+template <int RM, int... I>
 __device__ __forceinline__ void emit_all_bytes(std::integer_sequence<int, I...>,
                                                const double (&y)[kElems],
                                                const uint32_t (&ylo)[kElems], int8_t* planes,
                                                int64_t plane_stride, int64_t off) {
-  (emit_byte_modulus<I, EXACT>(y, ylo, planes, plane_stride, off), ...);
+  (emit_byte_modulus<I, RM>(y, ylo, planes, plane_stride, off), ...);
 }
 
-// MODE 1: quotient route with ylo from y + kMagic (t <= 51); 2: the same
-// with ylo split off (t = 52: for odd m <= 255 the FMA quotient of
-// residue_low errs by at most 2^52 2^-61 = 2^-9 < 1/(2m), so it is still the
-// nearest); 0: cmod_f64.
-template <int SIDE, int MODE, bool TZ>
+// RM: the residue mode (1, 2 or 3, as for residue_low).
+template <int SIDE, int RM, bool TZ>
 __global__ __launch_bounds__(256) void deconstruct_bytes_kernel(int64_t vecs, int64_t vstride, int64_t k,
                                                                 int64_t kp, const double* __restrict__ X,
                                                                 int64_t ldx,
@@ -342,8 +355,8 @@ __global__ __launch_bounds__(256) void deconstruct_bytes_kernel(int64_t vecs, in
   double x[kElems], y[kElems];
   uint32_t ylo[kElems];
   const int sigma = load_group<SIDE>(vecs, k, X, ldx, exps, keys_in, t, v, k0, true, x);
-  scale_round<TZ, MODE != 0, MODE == 2>(x, sigma, y, ylo);
-  emit_all_bytes<MODE != 0>(std::make_integer_sequence<int, kRA>{}, y, ylo, planes, vstride * 128,
+  scale_round<TZ, RM>(x, sigma, y, ylo);
+  emit_all_bytes<RM>(std::make_integer_sequence<int, kRA>{}, y, ylo, planes, vstride * 128,
                             plane_offset(vstride, kRA, v, g));
 }
 
@@ -388,30 +401,27 @@ struct DecArgs {
   int8_t* planes;
 };
 
-// mode: 0 general residues, 1 quotient route (ylo by kMagic), 2 quotient
-// route with ylo split off (the all-byte set at t = 52)
-template <int SIDE, bool BYTES, int MODE, bool TZ>
+template <int SIDE, bool BYTES, int RM, bool TZ>
 void launch_one(const DecArgs& a, hipStream_t stream) {
   if constexpr (BYTES)
-    hipLaunchKernelGGL((deconstruct_bytes_kernel<SIDE, MODE, TZ>), dim3((unsigned)a.blocks), dim3(256),
-                       0, stream, a.vecs, a.vstride, a.k, a.kp, a.X, a.ldx, a.exps, a.keys_in, a.t,
-                       a.planes);
-  else
-    hipLaunchKernelGGL((deconstruct_kernel<SIDE, MODE != 0, TZ>), dim3((unsigned)a.blocks), dim3(256), 0,
+    hipLaunchKernelGGL((deconstruct_bytes_kernel<SIDE, RM, TZ>), dim3((unsigned)a.blocks), dim3(256), 0,
                        stream, a.vecs, a.vstride, a.k, a.kp, a.X, a.ldx, a.exps, a.keys_in, a.t, a.planes);
+  else if constexpr (RM != 2)  // the nearest-quotient bound of RM 2 holds for byte moduli only
+    hipLaunchKernelGGL((deconstruct_kernel<SIDE, RM, TZ>), dim3((unsigned)a.blocks), dim3(256), 0, stream,
+                       a.vecs, a.vstride, a.k, a.kp, a.X, a.ldx, a.exps, a.keys_in, a.t, a.planes);
 }
 
 template <int SIDE, bool BYTES>
-void launch_side(int mode, bool tz, const DecArgs& a, hipStream_t stream) {
-  if (mode == 1) {
+void launch_side(int rm, bool tz, const DecArgs& a, hipStream_t stream) {
+  if (rm == 1) {
     if (tz) launch_one<SIDE, BYTES, 1, true>(a, stream);
     else launch_one<SIDE, BYTES, 1, false>(a, stream);
-  } else if (BYTES && mode == 2) {
+  } else if (rm == 2) {
     if (tz) launch_one<SIDE, BYTES, 2, true>(a, stream);
     else launch_one<SIDE, BYTES, 2, false>(a, stream);
   } else {
-    if (tz) launch_one<SIDE, BYTES, 0, true>(a, stream);
-    else launch_one<SIDE, BYTES, 0, false>(a, stream);
+    if (tz) launch_one<SIDE, BYTES, 3, true>(a, stream);
+    else launch_one<SIDE, BYTES, 3, false>(a, stream);
   }
 }
 
@@ -434,14 +444,13 @@ hipError_t launch_digits(int side, int64_t vecs, int64_t k, int64_t kp, const do
 hipError_t launch_deconstruct(int set, int quant, int side, int64_t vecs, int64_t vstride, int64_t k,
                               int64_t kp, int t, const double* X, int64_t ldx, const int32_t* exps,
                               bool keys_in, int8_t* planes, hipStream_t stream) {
-  if (vstride < vecs) return hipErrorInvalidValue;
+  if (vstride < vecs || t > kMaxScaleBits) return hipErrorInvalidValue;
   if (vecs <= 0 || kp <= 0) return hipSuccess;
   const bool bytes = set == kSetBytes;
   const bool tz = quant == kQuantTZ;
-  // |y| <= 2^t: the quotient needs no correction (the two bounds of
-  // centred_residue; the all-byte set takes the sharper one, up to t = 52
-  // with ylo split off)
-  const int mode = t <= (bytes ? 51 : 50) ? 1 : (bytes && t == 52 ? 2 : 0);
+  // |y| <= 2^t: the nearest quotient with ylo from kMagic, then (the byte
+  // moduli at t = 52) with ylo split off, else one correction
+  const int mode = t <= (bytes ? 51 : 50) ? 1 : (bytes && t == 52 ? 2 : 3);
   const DecArgs a{((vecs + 31) / 32) * (kp / 128), vecs, vstride, k, kp, X, ldx, exps, keys_in, t, planes};
   if (side == 0) {
     if (bytes) launch_side<0, true>(mode, tz, a, stream);

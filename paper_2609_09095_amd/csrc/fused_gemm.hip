@@ -14,7 +14,6 @@
 // meanwhile.  The blocks of one row strip (15 / G of them) are dealt to the
 // same XCD back to back, so the strip's FP64 comes from HBM once and from
 // that XCD's L2 for the others.
-#include "device_math.hpp"
 #include "kernels.hpp"
 #include "moduli.hpp"
 
@@ -32,7 +31,7 @@ __constant__ int kModF[kRA] = {kModulusA[0],  kModulusA[1],  kModulusA[2],  kMod
                                kModulusA[4],  kModulusA[5],  kModulusA[6],  kModulusA[7],
                                kModulusA[8],  kModulusA[9],  kModulusA[10], kModulusA[11],
                                kModulusA[12], kModulusA[13], kModulusA[14]};
-// RN(1/m) for the quotient of the EXACT path; 0 for m = 256, whose residue
+// RN(1/m) for the quotient route; 0 for m = 256, whose residue
 // byte is the low byte of y itself
 __constant__ double kInvQ[kRA] = {
     0.0,                 1.0 / kModulusA[1],  1.0 / kModulusA[2],  1.0 / kModulusA[3],
@@ -40,7 +39,7 @@ __constant__ double kInvQ[kRA] = {
     1.0 / kModulusA[8],  1.0 / kModulusA[9],  1.0 / kModulusA[10], 1.0 / kModulusA[11],
     1.0 / kModulusA[12], 1.0 / kModulusA[13], 1.0 / kModulusA[14]};
 static_assert(kModulusA[0] == 256, "the power of two comes first");
-// RN(1/m) for the general quotient and the reductions of the int32 sums
+// RN(1/m) for the reductions of the int32 sums
 __constant__ double kInvF[kRA] = {
     1.0 / kModulusA[0],  1.0 / kModulusA[1],  1.0 / kModulusA[2],  1.0 / kModulusA[3],
     1.0 / kModulusA[4],  1.0 / kModulusA[5],  1.0 / kModulusA[6],  1.0 / kModulusA[7],
@@ -59,34 +58,34 @@ __device__ __forceinline__ uint32_t low32_split(double y) {
 }
 
 // The centred residue of the integer-valued y modulo M, modulo 2^8 (its low
-// byte is the two's complement byte; the higher bits are not defined).
-//  EXACT (|y| <= 2^52, ylo = y mod 2^32): the FMA rounds y RN(1/M) + 1.5 2^52
-//  once to 1.5 2^52 + q, q the nearest quotient: for odd M <= 255,
-//  |y RN(1/M) - y/M| <= 2^52 2^-61 = 2^-9, below the 1/(2M) >= 1/510 that
-//  separates y/M from a half integer, so
-//  ylo - q M = y - q M (mod 2^32) is the centred residue, |r| < 128, and its
-//  low byte is the two's complement byte; for M = 256 (RN(1/M) taken as 0)
-//  q = 0 and the low byte of y is the residue byte.  24-bit products
-//  suffice: only the low 8 bits are kept.
-//  Otherwise: the nearest quotient by rint, the exact remainder by FMA, and
-//  the corrections of cmod_f64.
-template <bool EXACT>
-__device__ __forceinline__ uint32_t residue_byte(double y, uint32_t ylo, int M, double qinv, double inv) {
-  if constexpr (EXACT) {
-    const uint32_t q = lo32(__builtin_fma(y, qinv, kMagicF));
-    // spelled out: left to itself the compiler uses a quarter-rate 32-bit
-    // multiply; sext24(q) (-M) + ylo is y - q M modulo 2^24
-    uint32_t r;
-    asm("v_mad_i32_i24 %0, %1, %2, %3" : "=v"(r) : "v"(q), "s"(-M), "v"(ylo));
-    return r;  // the caller keeps the low byte
-  } else {
-    const double q = __builtin_rint(y * inv);
-    int r = (int)__builtin_fma(-q, (double)M, y);
+// byte is the two's complement byte; the higher bits are not defined), with
+// ylo = y mod 2^32.  The FMA rounds y RN(1/M) + 1.5 2^52 once to
+// 1.5 2^52 + q (|y / M| < 2^51: the sum lies where the spacing is 1), and
+// |y RN(1/M) - y/M| <= |y| 2^-61 for the odd M <= 255.
+//  CORR false (|y| <= 2^52): that error is at most 2^-9, below the
+//  1/(2M) >= 1/510 that separates y/M from a half integer, so q is the
+//  nearest quotient and ylo - q M = y - q M (mod 2^32) is the centred
+//  residue, |r| < 128, whose low byte is the two's complement byte.
+//  CORR true (|y| <= 2^58): the error is at most 1/8, so |y - q M| <= 5M/8
+//  and one correction each way centres it (24 bits hold it exactly).
+// For M = 256 (RN(1/M) taken as 0) q = 0 and the low byte of y is the
+// residue byte; the corrections move it by multiples of 256, which leaves
+// that byte alone.  24-bit products suffice.
+template <bool CORR>
+__device__ __forceinline__ uint32_t residue_byte(double y, uint32_t ylo, int M, double qinv) {
+  const uint32_t q = lo32(__builtin_fma(y, qinv, kMagicF));
+  // spelled out: left to itself the compiler uses a quarter-rate 32-bit
+  // multiply; sext24(q) (-M) + ylo is y - q M modulo 2^24
+  uint32_t r;
+  asm("v_mad_i32_i24 %0, %1, %2, %3" : "=v"(r) : "v"(q), "s"(-M), "v"(ylo));
+  if constexpr (CORR) {
     const int hi = (M - 1) / 2;
-    r = r > hi ? r - M : r;
-    r = r < hi - M + 1 ? r + M : r;
-    return (uint32_t)r;  // the caller keeps the low byte
+    int c = (int)(r << 8) >> 8;
+    c = c > hi ? c - M : c;
+    c = c < hi - M + 1 ? c + M : c;
+    return (uint32_t)c;
   }
+  return r;  // the caller keeps the low byte
 }
 
 // LDS slabs: rows of 64 bytes (one stage), the 16-byte chunk index XOR-ed
@@ -121,9 +120,9 @@ __device__ __forceinline__ int cmod_sum(int x, int m, double minv) {
 // every modulus of its group (one MFMA block each, so that G = 5 moduli fit
 // the registers: the FP64 slab then feeds five times the matrix work).
 constexpr int FBM = 128;
-// MODE: how y mod 2^32 is formed for the quotient route -- 1: y + 1.5 2^52
-// (|y| <= 2^51), 2: low32_split (|y| <= 2^52), 0: no quotient route (the
-// general residue).
+// MODE: the residue route by the range of y -- 1: ylo = y + 1.5 2^52
+// (|y| <= 2^51); 2: ylo by low32_split (|y| <= 2^52); 3: low32_split and the
+// corrected quotient (|y| <= 2^58).
 template <int G, int MODE, bool TZ, bool VEC>
 __global__ __launch_bounds__(1024, 1) void fused_bytes_kernel(
     int64_t m, int64_t n, int64_t k, int64_t kp, const double* __restrict__ A, int64_t lda,
@@ -215,7 +214,7 @@ __global__ __launch_bounds__(1024, 1) void fused_bytes_kernel(
       for (int c = 0; c < 4; ++c) {
         const double v = __builtin_ldexp(x[4 * i + c], sg[i]);
         y[c] = TZ ? __builtin_trunc(v) : __builtin_rint(v);
-        ylo[c] = MODE == 1 ? lo32(y[c] + kMagicF) : (MODE == 2 ? low32_split(y[c]) : 0u);
+        ylo[c] = MODE == 1 ? lo32(y[c] + kMagicF) : low32_split(y[c]);
       }
       const int at = r * FBK + (((ck >> 4) ^ fswz(r)) << 4) + (ck & 15);
 #pragma unroll
@@ -223,11 +222,11 @@ __global__ __launch_bounds__(1024, 1) void fused_bytes_kernel(
         // low bytes of the four residues into one dword (v_perm_b32: bytes
         // 0-3 of the second operand, 4-7 of the first)
         const uint32_t r01 =
-            __builtin_amdgcn_perm(residue_byte<MODE != 0>(y[1], ylo[1], mods[g], qinv[g], inv[g]),
-                                  residue_byte<MODE != 0>(y[0], ylo[0], mods[g], qinv[g], inv[g]), 0x0c0c0400u);
+            __builtin_amdgcn_perm(residue_byte<MODE == 3>(y[1], ylo[1], mods[g], qinv[g]),
+                                  residue_byte<MODE == 3>(y[0], ylo[0], mods[g], qinv[g]), 0x0c0c0400u);
         const uint32_t r23 =
-            __builtin_amdgcn_perm(residue_byte<MODE != 0>(y[3], ylo[3], mods[g], qinv[g], inv[g]),
-                                  residue_byte<MODE != 0>(y[2], ylo[2], mods[g], qinv[g], inv[g]), 0x0c0c0400u);
+            __builtin_amdgcn_perm(residue_byte<MODE == 3>(y[3], ylo[3], mods[g], qinv[g]),
+                                  residue_byte<MODE == 3>(y[2], ylo[2], mods[g], qinv[g]), 0x0c0c0400u);
         const uint32_t word = __builtin_amdgcn_perm(r23, r01, 0x05040100u);
         *reinterpret_cast<uint32_t*>(&lds_a[buf][g][at]) = word & keep[i];
       }
@@ -334,16 +333,16 @@ hipError_t launch_fused_g(int64_t m, int64_t n, int64_t k, int64_t kp, const dou
 hipError_t launch_fused_bytes(int quant, int64_t m, int64_t n, int64_t k, int64_t kp, int t,
                               const double* A, int64_t lda, const int32_t* sigma, const int8_t* pb,
                               int8_t* cres, hipStream_t stream) {
-  if (n > FBN || kp % FBK || m <= 0 || n <= 0) return hipErrorInvalidValue;
+  if (n > FBN || kp % FBK || m <= 0 || n <= 0 || t > kMaxScaleBits) return hipErrorInvalidValue;
   const bool tz = quant == kQuantTZ;
-  // |y| <= 2^t: the quotient route holds up to 2^52
-  const int mode = t <= 51 ? 1 : (t == 52 ? 2 : 0);
+  // |y| <= 2^t: the nearest quotient up to 2^52, then the corrected one
+  const int mode = t <= 51 ? 1 : (t == 52 ? 2 : 3);
 #define OZ_FUSED(MODE)                                                                           \
   return tz ? launch_fused_g<3, MODE, true>(m, n, k, kp, A, lda, sigma, pb, cres, stream)       \
             : launch_fused_g<3, MODE, false>(m, n, k, kp, A, lda, sigma, pb, cres, stream)
   if (mode == 1) OZ_FUSED(1);
   if (mode == 2) OZ_FUSED(2);
-  OZ_FUSED(0);
+  OZ_FUSED(3);
 #undef OZ_FUSED
 }
 

@@ -25,12 +25,19 @@ constexpr int kQuantTZ = 1;  // toward zero
 //    per column (launch_scan_cols, any number of column ranges), and the
 //    keys turned into sigma (launch_keys_to_sigma).  The deconstruction can
 //    read the keys directly (keys_in).
+// With digits (the accurate mode) the row scan also writes the rows'
+// magnitude digits as one int8 plane (see launch_digits) of kp per row.
 hipError_t launch_scan_rows(int64_t vecs, int64_t k, const double* X, int64_t ldx, int t, int32_t* exps,
-                            int32_t* zero, int64_t nzero, hipStream_t stream);
+                            int32_t* zero, int64_t nzero, hipStream_t stream, int8_t* digits = nullptr,
+                            int64_t kp = 0);
 hipError_t launch_clear_keys(int64_t vecs, int32_t* keys, hipStream_t stream);
 hipError_t launch_scan_cols(int64_t vecs, int64_t k, const double* X, int64_t ldx, int32_t* keys,
                             hipStream_t stream);
 hipError_t launch_keys_to_sigma(int64_t vecs, int t, int32_t* exps, hipStream_t stream);
+
+// The largest scale t (|A'| <= 2^t) the residue kernels accept: t(k) of
+// either set at k = 1, and the accurate mode's cap.
+constexpr int kMaxScaleBits = 58;
 
 // Alg. 2: scale, quantise, residues and the planes of one operand, given exps
 // (sigma, or with keys_in the column scan's exponent keys, turned into sigma

@@ -27,9 +27,10 @@
 //    the three pairs of a half in 64-bit arithmetic.
 //  - |X| = H P + L with H = |Xh| < 2^53 and |L| < P, formed as a 128-bit
 //    integer and rounded once.
+#include <hip/hip_runtime.h>
+
 #include <utility>
 
-#include "device_math.hpp"
 #include "fp64_round.hpp"
 #include "kernels.hpp"
 #include "moduli.hpp"

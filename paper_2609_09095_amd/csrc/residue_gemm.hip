@@ -48,7 +48,6 @@
 // 20-25 B/clk per CU, which bounds a stage (halving the stream cuts the time
 // by a quarter, halving the LDS fragment reads by 2 %), and the MFMA clock
 // itself drops with the switching activity of dense data.
-#include "device_math.hpp"
 #include "kernels.hpp"
 #include "moduli.hpp"
 

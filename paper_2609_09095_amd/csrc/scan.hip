@@ -18,9 +18,19 @@ namespace {
 // zero / nzero: the column keys of B to clear on the side (the first blocks
 // write one zero per thread), so that B's column scan needs no launch of
 // its own for that.
+//
+// DIGITS (the accurate mode, Sec. 2, Eq. (alpha)): once the row's exponent
+// e is known, the block reads its row a second time -- from cache: it has
+// just streamed it -- and writes the magnitude digits ceil(16 |x| 2^-e) in
+// {0..16} (0 past k and on a non-finite row) as one int8 plane of the plane
+// layout [kp/128][vecs][128]: each wavefront takes 128-element chunks, a
+// lane two elements 64 apart, so loads and byte stores stay contiguous
+// across the wavefront.
+template <bool DIGITS>
 __global__ __launch_bounds__(256) void scan_rows_kernel(int64_t vecs, int64_t k, const double* X,
                                                         int64_t ldx, int t, int32_t* exps,
-                                                        int32_t* zero, int64_t nzero) {
+                                                        int32_t* zero, int64_t nzero, int64_t kp,
+                                                        int8_t* digits) {
   __shared__ uint32_t part[4];
   if (zero) {
     const int64_t z = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -64,10 +74,28 @@ __global__ __launch_bounds__(256) void scan_rows_kernel(int64_t vecs, int64_t k,
   const uint32_t key = wave_max(exponent_key(mx[0]));
   if (lane == 0) part[wave] = key;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t m = part[0];
-    for (int w = 1; w < 4; ++w) m = part[w] > m ? part[w] : m;
-    exps[v] = key_to_sigma(m, t);
+  uint32_t m = part[0];
+  for (int w = 1; w < 4; ++w) m = part[w] > m ? part[w] : m;
+  if (threadIdx.x == 0) exps[v] = key_to_sigma(m, t);
+  if constexpr (DIGITS) {
+    const int32_t ne = key_to_sigma(m, 0);  // -e, or INT32_MIN
+    const bool live = ne != INT32_MIN;
+    const int sh = live ? 4 + ne : 0;
+    const double* xr = X + v * ldx;
+    const int64_t chunks = kp / 128;
+    int8_t* drow = digits + v * 128 + lane;
+    auto digit = [&](int64_t l) -> int {
+      const double a = (live && l < k) ? __builtin_fabs(xr[l < k ? l : 0]) : 0.0;
+      const double u = __builtin_ceil(__builtin_ldexp(a, sh));
+      return a == 0.0 ? 0 : (u < 1.0 ? 1 : (int)u);
+    };
+    for (int64_t c = wave; c < chunks; c += 4) {
+      const int64_t l0 = c * 128 + lane;
+      const int d0 = digit(l0), d1 = digit(l0 + 64);
+      int8_t* dst = drow + c * vecs * 128;
+      dst[0] = (int8_t)d0;
+      dst[64] = (int8_t)d1;
+    }
   }
 }
 
@@ -113,13 +141,19 @@ __global__ __launch_bounds__(256) void keys_to_sigma_kernel(int64_t vecs, int t,
 }  // namespace
 
 hipError_t launch_scan_rows(int64_t vecs, int64_t k, const double* X, int64_t ldx, int t, int32_t* exps,
-                            int32_t* zero, int64_t nzero, hipStream_t stream) {
+                            int32_t* zero, int64_t nzero, hipStream_t stream, int8_t* digits, int64_t kp) {
   if (vecs <= 0) return hipSuccess;
   // one block per row; the blocks also cover the keys to clear
   const int64_t zb = zero ? (nzero + 255) / 256 : 0;
   if (vecs > (int64_t)UINT32_MAX || zb > vecs) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(scan_rows_kernel, dim3((unsigned)vecs), dim3(256), 0, stream, vecs, k, X, ldx, t,
-                     exps, zero, nzero);
+  if (digits) {
+    if (kp < k || kp % 128) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(scan_rows_kernel<true>, dim3((unsigned)vecs), dim3(256), 0, stream, vecs, k, X, ldx,
+                       t, exps, zero, nzero, kp, digits);
+  } else {
+    hipLaunchKernelGGL(scan_rows_kernel<false>, dim3((unsigned)vecs), dim3(256), 0, stream, vecs, k, X, ldx,
+                       t, exps, zero, nzero, kp, digits);
+  }
   return hipGetLastError();
 }
 

@@ -44,6 +44,37 @@ def test_deconstruct_matches_oracle(shape, s, seed, side):
     assert_int_equal(planes.cpu().numpy(), device_layout(e4m3_bytes(P)), "planes")
 
 
+@pytest.mark.parametrize("k", [1024, 128, 64, 16])
+def test_deconstruct_boundary_residues(k):
+    """Rows whose scaled integers are multiples of each modulus plus and
+    minus half of it (the ends of the centred range, quotients next to a
+    half integer), and a second set reaching |y| just below 2^t, for
+    t = 50, 51, 52 and 53: the nearest quotient route and the corrected one."""
+    t = oracle.scale_bits(k)
+    log(f"deconstruct boundary residues k={k} t={t}")
+    rng = np.random.default_rng(7)
+    mods = oracle.moduli()
+    X = np.zeros((4 * len(mods), k))
+    for i, m in enumerate(mods):
+        q = rng.integers(-(1 << (t - 12)), 1 << (t - 12), size=k)
+        X[2 * i] = (q * m + m // 2).astype(np.float64)
+        X[2 * i + 1] = (q * m - m // 2).astype(np.float64)
+        X[2 * i, 0] = X[2 * i + 1, 0] = 2.0 ** (t - 1)   # sets the scale to 2^0
+        top = (1 << t) // m
+        q = rng.integers(top - 1024, top, size=k) * rng.choice([-1, 1], size=k)
+        r = 2 * len(mods) + 2 * i
+        X[r] = (q * m + m // 2).astype(np.float64)
+        X[r + 1] = (q * m - m // 2).astype(np.float64)
+        X[r, 0] = X[r + 1, 0] = float((1 << t) - 1)   # scale 2^0, |y| < 2^t
+    assert np.all(np.abs(X) < 2.0 ** t)
+    for side in (0, 1):
+        Xs = X if side == 0 else np.ascontiguousarray(X.T)
+        planes, exps = gpu_deconstruct(Xs, side)
+        e, P = _oracle_side(Xs, side)
+        assert_int_equal(exps.cpu().numpy(), e, "exponents")
+        assert_int_equal(planes.cpu().numpy(), device_layout(e4m3_bytes(P)), "planes")
+
+
 def _edge_matrix(rows, k, seed):
     rng = np.random.default_rng(seed)
     X = workloads.random_matrix(rows, k, 1.0, seed)

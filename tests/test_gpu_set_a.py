@@ -90,12 +90,14 @@ def test_deconstruct_edge_values(side, k):
     assert exps.cpu().numpy()[3] == oz.EXP_NONFINITE and exps.cpu().numpy()[4] == oz.EXP_NONFINITE
 
 
-@pytest.mark.parametrize("k", [8192, 4096])
+@pytest.mark.parametrize("k", [8192, 4096, 1024, 64])
 def test_deconstruct_boundary_residues(k):
     """Rows whose scaled integers sit on every residue boundary: multiples of
     each modulus plus and minus half of it (the -128 endpoint of 256, the
-    +-(m-1)/2 ends of the odd moduli), at the top of the scale range; at
-    k = 4096 (t = 52) a second set of rows reaches |y| just below 2^52."""
+    +-(m-1)/2 ends of the odd moduli, quotients next to a half integer), at
+    the top of the scale range; a second set of rows reaches |y| just below
+    2^t.  t = 51, 52, 53 and 55: each residue route (the nearest quotient
+    with ylo from the magic sum or split off, and the corrected quotient)."""
     t = oracle.scale_bits(k, OSET)
     log(f"[A15] deconstruct boundary residues k={k} t={t}")
     rng = np.random.default_rng(5)
@@ -110,6 +112,9 @@ def test_deconstruct_boundary_residues(k):
         X[30 + 2 * i] = (q * m + m // 2).astype(np.float64)
         X[30 + 2 * i + 1] = (q * m - m // 2).astype(np.float64)
         X[30 + 2 * i, 0] = X[30 + 2 * i + 1, 0] = float((1 << t) - 1)   # scale 2^0, |y| < 2^t
+    # past 2^53 the integers round to doubles: keep every one below 2^t
+    lim = np.nextafter(2.0 ** t, 0.0)
+    X = np.clip(X, -lim, lim)
     assert np.all(np.abs(X) < 2.0 ** t)
     planes, exps = gpu_deconstruct(X, 0, SET)
     e, P = _oracle_side(X, 0)
