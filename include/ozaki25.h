@@ -268,8 +268,9 @@ ozaki25_status ozaki25_dgemm_planes(int64_t m, int64_t n, int64_t k, const uint8
  * (A15 at k = 1). */
 
 /* Device workspace of ozaki25_accurate_exponents: the digit planes of A and
- * B ((m + n) k_pad bytes), the totals L (m n bytes), n int32, and for few
- * output tiles the split bound product's int32 partials. */
+ * B ((m + n) k_pad bytes), the totals L (m n bytes), their column minima per
+ * 64 rows (ceil(m/64) n bytes), n bytes of column shifts, and for few output
+ * tiles the split bound product's int32 partials. */
 size_t ozaki25_accurate_exponents_workspace_size(int64_t m, int64_t n, int64_t k);
 
 /* The accurate mode's sigma (expsA, m int32) and tau (expsB, n int32) for

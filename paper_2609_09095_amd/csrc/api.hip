@@ -157,9 +157,10 @@ hipError_t scan_and_deconstruct(ozaki25_moduli_set set, ozaki25_quantiser quant,
 
 // ---- accurate mode (Sec. 2, Eq. (alpha)) ---------------------------------
 // Scratch of the exponent stage: the digit planes of A and B, the totals L
-// (int8 m x n), the column shifts, and the split bound product's partials.
+// (int8 m x n), the column minima of each 64-row group of L, the column
+// shifts as bytes, and the split bound product's partials.
 struct AccWorkspace {
-  size_t dig_a, dig_b, total, colmin, part, bytes;
+  size_t dig_a, dig_b, total, colpart, colslice, ub, part, bytes;
   int splits;
 };
 
@@ -174,8 +175,12 @@ AccWorkspace acc_layout(int64_t m, int64_t n, int64_t k) {
   off = align_up(off + (size_t)n * kp);
   w.total = off;
   off = align_up(off + (size_t)m * n);
-  w.colmin = off;
-  off = align_up(off + (size_t)n * sizeof(int32_t));
+  w.colpart = off;
+  off = align_up(off + (size_t)((m + 63) / 64) * n);
+  w.colslice = off;
+  off = align_up(off + (size_t)(m > 0 && n > 0 ? oz::accurate_slices(m, n, nullptr) : 0) * n);
+  w.ub = off;
+  off = align_up(off + (size_t)n);
   w.part = off;
   off = w.splits > 1 ? align_up(off + (size_t)w.splits * m * n * sizeof(int32_t)) : off;
   w.bytes = off;
@@ -203,7 +208,9 @@ hipError_t accurate_exponents(ozaki25_moduli_set set, int64_t m, int64_t n, int6
   int8_t* da = (int8_t*)(aux + w.dig_a);
   int8_t* db = (int8_t*)(aux + w.dig_b);
   int8_t* total = (int8_t*)(aux + w.total);
-  int32_t* colmin = (int32_t*)(aux + w.colmin);
+  int8_t* colpart = (int8_t*)(aux + w.colpart);
+  int8_t* colslice = (int8_t*)(aux + w.colslice);
+  uint8_t* ub = (uint8_t*)(aux + w.ub);
   int32_t* part = w.splits > 1 ? (int32_t*)(aux + w.part) : nullptr;
   int bt = 0;
   uint64_t ttop = 0;
@@ -215,8 +222,9 @@ hipError_t accurate_exponents(ozaki25_moduli_set set, int64_t m, int64_t n, int6
   if (e == hipSuccess && !side_job) e = oz::launch_clear_keys(n, eb, s);
   if (e == hipSuccess) e = oz::launch_scan_cols(n, k, B, ldb, eb, s);
   if (e == hipSuccess) e = oz::launch_digits(1, n, k, kp, B, ldb, eb, true, db, s);
-  if (e == hipSuccess) e = oz::launch_bound_gemm(m, n, kp, da, db, total, part, w.splits, bt, ttop, s);
-  if (e == hipSuccess) e = oz::launch_accurate_shifts(m, n, total, colmin, ea, eb, s);
+  if (e == hipSuccess)
+    e = oz::launch_bound_gemm(m, n, kp, da, db, total, colpart, part, w.splits, bt, ttop, s);
+  if (e == hipSuccess) e = oz::launch_accurate_shifts(m, n, total, colpart, colslice, ub, ea, eb, s);
   return e;
 }
 

@@ -116,19 +116,24 @@ hipError_t launch_reconstruct_bytes_i8(int64_t m, int64_t n, const int8_t* cres,
 //    t = 0, or with keys_in the column scan's keys);
 //  - launch_bound_gemm: U = digitsA digitsB^T on int8 MFMA and, per output,
 //    the total shift L (int8 [m][n]) with 2^L U <= T, T = 2^8 (M/2 - 1) of
-//    bit length bt and ttop = T >> (bt - 33); `splits` from
+//    bit length bt and ttop = T >> (bt - 33), plus the column minima of L
+//    over each 64-row group (colpart, int8 [ceil(m/64)][n]); `splits` from
 //    bound_gemm_splits, with splits * m * n int32 of `part` when above 1;
-//  - launch_accurate_shifts: from L the column shifts (into colmin, n int32
-//    of scratch), tau = u - f into eb_keys (the column scan's keys) and
-//    sigma = s - e into ea (the row scan at t = 0).
+//  - launch_accurate_shifts: from colpart the column shifts (ub, n bytes,
+//    16-byte aligned) and tau = u - f into eb_keys (the column scan's keys),
+//    then from L sigma = s - e into ea (the row scan at t = 0).
 hipError_t launch_digits(int side, int64_t vecs, int64_t k, int64_t kp, const double* X, int64_t ldx,
                          const int32_t* exps, bool keys_in, int8_t* digits, hipStream_t stream);
 int bound_gemm_splits(int64_t m, int64_t n, int64_t kp);
 hipError_t launch_bound_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* da, const int8_t* db,
-                             int8_t* total, int32_t* part, int splits, int bt, uint64_t ttop,
+                             int8_t* total, int8_t* colpart, int32_t* part, int splits, int bt, uint64_t ttop,
                              hipStream_t stream);
-hipError_t launch_accurate_shifts(int64_t m, int64_t n, const int8_t* L, int32_t* colmin, int32_t* ea,
-                                  int32_t* eb_keys, hipStream_t stream);
+// colpart is reduced in two steps: over slices of groups into colslice
+// ([accurate_slices(m, n)][n] bytes), then over the slices.
+int64_t accurate_slices(int64_t m, int64_t n, int64_t* per_slice);
+hipError_t launch_accurate_shifts(int64_t m, int64_t n, const int8_t* L, const int8_t* colpart,
+                                  int8_t* colslice, uint8_t* ub, int32_t* ea, int32_t* eb_keys,
+                                  hipStream_t stream);
 
 // C = +0.0 over an m x n block (the k == 0 product).
 hipError_t launch_zero_c(int64_t m, int64_t n, double* C, int64_t ldc, hipStream_t stream);

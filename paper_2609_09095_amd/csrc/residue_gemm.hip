@@ -623,9 +623,11 @@ __device__ __forceinline__ int bound_total(int u, int bt, uint64_t ttop) {
 
 // BOUND: the bound product of the accurate mode on the same pipeline -- one
 // plane of digits (0..16) per operand, the plain int32 sum (at most
-// 256 k <= 2^30, no reduction), stored as the total L (int8 OT) or, for a
-// split k range, as the raw partial sums (int32 OT; bound_totals_kernel
-// adds them up).
+// 256 k <= 2^30, no reduction), stored as the total L (int8 OT) together
+// with each wavefront's column minima over its 64 rows (colpart
+// [ceil(m/64)][n]: rows past m have zero digits, so their L of 127 never
+// lowers a minimum), or, for a split k range, as the raw partial sums
+// (int32 OT; bound_totals_kernel adds them up).
 template <typename OT, int S, bool BOUND = false>
 __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, int64_t n,
                                                                     int64_t kp,
@@ -633,7 +635,8 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
                                                                     const int8_t* __restrict__ pb,
                                                                     OT* __restrict__ cres,
                                                                     int splits, int group,
-                                                                    int bt = 0, uint64_t ttop = 0) {
+                                                                    int bt = 0, uint64_t ttop = 0,
+                                                                    int8_t* colpart = nullptr) {
   constexpr int BM = Tile<S>::BM, BN = Tile<S>::BN, NB = Tile<S>::BB, WC = Tile<S>::WC;
   constexpr int NPL = BOUND ? 1 : kRA;  // planes in the layout
   __shared__ __attribute__((aligned(1024))) int8_t lds_a0[BM * BK];
@@ -736,19 +739,52 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_kernel(int64_t m, 
                               else
                                 return cmod_i32<sizeof(OT) == 4>(acc[a][b][v], mm, minv);
                             });
+  if constexpr (BOUND && sizeof(OT) == 1) {
+    // lane l holds column l % 32 of each block, rows 4 (l / 32) + ... of
+    // both row blocks: its minimum, then the other half's by a swap
+    const int64_t g = tm * (BM / 64) + wr;
+    if (g * 64 < m) {
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        int mn = 127;
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int L = bound_total(acc[a][b][v], bt, ttop);
+            mn = L < mn ? L : mn;
+          }
+        const int o = __shfl_xor(mn, 32, 64);
+        mn = o < mn ? o : mn;
+        const int64_t col = tn * BN + wc * 32 * NB + b * 32 + fr;
+        if (fh == 0 && col < n) colpart[g * n + col] = (int8_t)mn;
+      }
+    }
+  }
 }
 
 // The split bound product's partial sums [splits][m][n], added and turned
-// into totals.
-__global__ __launch_bounds__(256) void bound_totals_kernel(int64_t mn, int splits,
+// into totals and the column minima of each 64-row group: a thread per
+// column (consecutive threads, consecutive columns), a block row per group.
+__global__ __launch_bounds__(256) void bound_totals_kernel(int64_t m, int64_t n, int splits,
                                                            const int32_t* __restrict__ part,
-                                                           int8_t* __restrict__ total, int bt,
+                                                           int8_t* __restrict__ total,
+                                                           int8_t* __restrict__ colpart, int bt,
                                                            uint64_t ttop) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= mn) return;
-  int sum = 0;
-  for (int sp = 0; sp < splits; ++sp) sum += part[sp * mn + i];
-  total[i] = (int8_t)bound_total(sum, bt, ttop);
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t g = blockIdx.y;
+  if (j >= n) return;
+  const int64_t mn = m * n;
+  const int64_t i1 = g * 64 + 64 < m ? g * 64 + 64 : m;
+  int low = 127;
+  for (int64_t i = g * 64; i < i1; ++i) {
+    int sum = 0;
+    for (int sp = 0; sp < splits; ++sp) sum += part[sp * mn + i * n + j];
+    const int L = bound_total(sum, bt, ttop);
+    total[i * n + j] = (int8_t)L;
+    low = L < low ? L : low;
+  }
+  colpart[g * n + j] = (int8_t)low;
 }
 
 // Sum of the splits' centred partial products, reduced to the centred
@@ -870,7 +906,7 @@ int bound_gemm_splits(int64_t m, int64_t n, int64_t kp) {
 }
 
 hipError_t launch_bound_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* da, const int8_t* db,
-                             int8_t* total, int32_t* part, int splits, int bt, uint64_t ttop,
+                             int8_t* total, int8_t* colpart, int32_t* part, int splits, int bt, uint64_t ttop,
                              hipStream_t stream) {
   if (m <= 0 || n <= 0) return hipSuccess;
   if (n > kMaxResidueCols) return hipErrorInvalidValue;
@@ -884,10 +920,10 @@ hipError_t launch_bound_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* da,
   if (splits == 1) {
     if (shape == 3)
       hipLaunchKernelGGL((residue_gemm_bytes_kernel<int8_t, 3, true>), grid, dim3(1024), 0, stream, m, n,
-                         kp, da, db, total, 1, group, bt, ttop);
+                         kp, da, db, total, 1, group, bt, ttop, colpart);
     else
       hipLaunchKernelGGL((residue_gemm_bytes_kernel<int8_t, 2, true>), grid, dim3(1024), 0, stream, m, n,
-                         kp, da, db, total, 1, group, bt, ttop);
+                         kp, da, db, total, 1, group, bt, ttop, colpart);
   } else {
     if (shape == 3)
       hipLaunchKernelGGL((residue_gemm_bytes_kernel<int32_t, 3, true>), grid, dim3(1024), 0, stream, m, n,
@@ -895,9 +931,10 @@ hipError_t launch_bound_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* da,
     else
       hipLaunchKernelGGL((residue_gemm_bytes_kernel<int32_t, 2, true>), grid, dim3(1024), 0, stream, m, n,
                          kp, da, db, part, splits, group, bt, ttop);
-    const int64_t mn = m * n;
-    hipLaunchKernelGGL(bound_totals_kernel, dim3((unsigned)((mn + 255) / 256)), dim3(256), 0, stream, mn,
-                       splits, part, total, bt, ttop);
+    const int64_t groups = (m + 63) / 64;
+    if ((n + 255) / 256 > (int64_t)UINT32_MAX || groups > 65535) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(bound_totals_kernel, dim3((unsigned)((n + 255) / 256), (unsigned)groups), dim3(256), 0,
+                       stream, m, n, splits, part, total, colpart, bt, ttop);
   }
   return hipGetLastError();
 }
