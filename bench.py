@@ -46,11 +46,13 @@ SETS = {
                 peak=FP8_PEAK_TOPS, dtype="fp8", moduli="published 12-modulus set",
                 route="e4m3 MFMA, fp32 accumulate", gemm_kernel="residue_gemm_kernel<int16>",
                 dec_kernel="deconstruct_kernel<0>+<1>",
+                fused_kernel="fused_pub_kernel", fused_products=42,
                 note="fp8 ops (1 MAC = 2 ops): 36 limb products x 2mnk per launch; peak is the dense fp8 rate"),
     "a15": dict(id=1, oracle_set=1, r=15, products=15, plane_bytes=15, cres_bytes=15,
                 peak=INT8_PEAK_TOPS, dtype="int8", moduli="all-byte 15-modulus set (Sec. 5.1 candidate A)",
                 route="int8 MFMA, int32 accumulate", gemm_kernel="residue_gemm_bytes_kernel<int8>",
                 dec_kernel="deconstruct_bytes_kernel<0>+<1>",
+                fused_kernel="fused_bytes_kernel", fused_products=15,
                 note="int8 ops (1 MAC = 2 ops): 15 residue products x 2mnk per launch; peak is the dense int8 rate"),
 }
 COUNTER_FILES = {"s12": os.path.join(ROOT, "profiles", "residue_gemm_square_counters.txt"),
@@ -301,18 +303,51 @@ def time_graph(oz, torch, w, Ad, Bd, Cd, cfg, steps, quant):
     return ms
 
 
+def fused(w):
+    """Storage mode F for A (the library's choice for at most 128 columns and
+    at least 1024 rows): A is quantised inside the product kernel, so there
+    is no deconstruction stage to price against HBM."""
+    return w.n <= 128 and w.m >= 1024
+
+
 def rates(w, cfg, ms, stages):
     scan_ms, dec_ms, gemm_ms, rec_ms = stages
     elems = w.m * w.k + w.k * w.n
     dec_bytes = elems * (8 + cfg["plane_bytes"])
     rec_bytes = w.m * w.n * (cfg["cres_bytes"] + 8 + (8 if w.subtract else 0))
-    gemm_ops = 2.0 * cfg["products"] * w.m * w.n * w.k
+    gemm_ops = 2.0 * (cfg["fused_products"] if fused(w) else cfg["products"]) * w.m * w.n * w.k
     return dict(tflops=w.flops / (ms * 1e-3) / 1e12, gemm_ops=gemm_ops,
                 gemm_tops=gemm_ops / (gemm_ms * 1e-3) / 1e12, dec_bytes=dec_bytes,
                 dec_gbs=dec_bytes / (dec_ms * 1e-3) / 1e9,
                 stage_gbs=(dec_bytes + elems * 8) / ((dec_ms + scan_ms) * 1e-3) / 1e9,
                 rec_gbs=rec_bytes / (rec_ms * 1e-3) / 1e9,
                 roof=cfg["peak"] / cfg["products"])
+
+
+def dec_roofline(w, cfg, rt, moduli, scan_ms, dec_ms):
+    if fused(w):
+        return {"bound": "hbm", "kernel": None, "achieved": None, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": None, "bytes_per_call": None,
+                "note": "storage mode F for A: no planes of A are made (the product kernel " + cfg["fused_kernel"]
+                        + " quantises A); the scan stage holds A's exponent scan, the deconstruct stage B's"}
+    return {"bound": "hbm", "kernel": cfg["dec_kernel"], "achieved": round(rt["dec_gbs"], 1),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(rt["dec_gbs"] / HBM_PEAK_GBS, 4),
+            "bytes_per_call": rt["dec_bytes"], "stage_with_scan_gbs": round(rt["stage_gbs"], 1),
+            **measured_deconstruction(w, moduli, scan_ms, dec_ms)}
+
+
+def gemm_roofline(w, cfg, rt, moduli):
+    unit = "TFLOP/s" if cfg["dtype"] == "fp8" else "TOP/s"
+    r = {"bound": "mfma", "kernel": cfg["fused_kernel"] if fused(w) else cfg["gemm_kernel"],
+         "achieved": round(rt["gemm_tops"], 2), "peak": cfg["peak"], "unit": unit,
+         "frac": round(rt["gemm_tops"] / cfg["peak"], 4),
+         "traffic": None if fused(w) else measured_traffic(w, moduli), "ops_per_launch": rt["gemm_ops"],
+         "note": cfg["note"]}
+    if fused(w):
+        r["note"] = (f"storage mode F: {cfg['fused_products']} products x 2mnk per launch "
+                     "(the published set's digit products: 3 per square and 4 per nonsquare modulus); "
+                     "the kernel is bound by converting A (VALU), not by the matrix cores")
+    return r
 
 
 def main():
@@ -392,16 +427,8 @@ def main():
             "value": round(ort["tflops"], 3), "unit": "TFLOPS", "ms_per_step": round(oms, 4),
             "stage_ms": dict(zip(("scan", "deconstruct", "residue_gemm", "reconstruct"),
                                  [round(x, 4) for x in ostages])),
-            "roofline": {"bound": "mfma", "kernel": ocfg["gemm_kernel"], "achieved": round(ort["gemm_tops"], 2),
-                         "peak": ocfg["peak"], "unit": "TFLOP/s" if ocfg["dtype"] == "fp8" else "TOP/s",
-                         "frac": round(ort["gemm_tops"] / ocfg["peak"], 4),
-                         "traffic": measured_traffic(w, name), "ops_per_launch": ort["gemm_ops"],
-                         "note": ocfg["note"]},
-            "roofline_deconstruct": {"bound": "hbm", "kernel": ocfg["dec_kernel"],
-                                     "achieved": round(ort["dec_gbs"], 1), "peak": HBM_PEAK_GBS,
-                                     "unit": "GB/s", "frac": round(ort["dec_gbs"] / HBM_PEAK_GBS, 4),
-                                     "bytes_per_call": ort["dec_bytes"],
-                                     **measured_deconstruction(w, name, ostages[0], ostages[1])},
+            "roofline": gemm_roofline(w, ocfg, ort, name),
+            "roofline_deconstruct": dec_roofline(w, ocfg, ort, name, ostages[0], ostages[1]),
             "emulation_roof_tflops": round(ort["roof"], 2),
             "emulation_roof_frac": round(ort["tflops"] / ort["roof"], 4),
         }
@@ -454,7 +481,6 @@ def main():
             per_product = rt["gemm_tops"]
             vendor["residue_gemm_over_vendor"] = round(per_product / vendor["achieved"], 4)
 
-    peak_unit = "TFLOP/s" if cfg["dtype"] == "fp8" else "TOP/s"
     result = {
         "metric": "emulated FP64 TFLOPS (2mnk/s) + deconstruction GB/s vs HBM/MFMA roofs",
         "value": round(rt["tflops"], 3),
@@ -473,18 +499,8 @@ def main():
                                f"entries (U-0.5)exp({w.s} N), seed {w.seed}",
                    "m": w.m, "n": w.n, "k": w.k, "moduli": cfg["moduli"], "quantiser": args.quantiser.upper(),
                    "route": cfg["route"]},
-        "roofline": {"bound": "mfma", "kernel": cfg["gemm_kernel"],
-                     "achieved": round(rt["gemm_tops"], 2), "peak": cfg["peak"], "unit": peak_unit,
-                     "frac": round(rt["gemm_tops"] / cfg["peak"], 4),
-                     "traffic": measured_traffic(w, args.moduli),
-                     "ops_per_launch": rt["gemm_ops"],
-                     "note": cfg["note"]},
-        "roofline_deconstruct": {"bound": "hbm", "kernel": cfg["dec_kernel"],
-                                 "achieved": round(rt["dec_gbs"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                                 "frac": round(rt["dec_gbs"] / HBM_PEAK_GBS, 4),
-                                 "bytes_per_call": rt["dec_bytes"],
-                                 "stage_with_scan_gbs": round(rt["stage_gbs"], 1),
-                                 **measured_deconstruction(w, args.moduli, scan_ms, dec_ms)},
+        "roofline": gemm_roofline(w, cfg, rt, args.moduli),
+        "roofline_deconstruct": dec_roofline(w, cfg, rt, args.moduli, scan_ms, dec_ms),
         "roofline_reconstruct": {"bound": "hbm", "achieved": round(rt["rec_gbs"], 1), "peak": HBM_PEAK_GBS,
                                  "unit": "GB/s", "frac": round(rt["rec_gbs"] / HBM_PEAK_GBS, 4)},
         "stage_ms": {"scan": round(scan_ms, 4), "deconstruct": round(dec_ms, 4), "residue_gemm": round(gemm_ms, 4),

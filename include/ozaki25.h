@@ -184,10 +184,11 @@ size_t ozaki25_dgemm_workspace_size(int64_t m, int64_t n, int64_t k, ozaki25_mod
 
 /* Emulated DGEMM C = A B (Alg. 1): both operands deconstructed once into
  * planes in the workspace (storage mode M), the residue products, then the
- * reconstruction.  For the all-byte set with n <= 128 and m >= 1024 (tall
- * and skinny: one output tile spans all of B) only B's planes are stored
- * and A is quantised and reduced inside the product kernel (storage mode F
- * for A -- the hybrid of Sec. 6.2); the result is the same bit for bit.  The workspace is allocated and released stream-ordered on
+ * reconstruction.  With n <= 128 and m >= 1024 (tall and skinny: one output
+ * tile spans all of B), either set, only B's planes are stored and A is
+ * quantised and reduced inside the product kernel (storage mode F for A --
+ * the hybrid of Sec. 6.2); the result is the same bit for bit.  The
+ * workspace is allocated and released stream-ordered on
  * `stream` (hipMallocAsync / hipFreeAsync).  m == 0 or n == 0: no-op;
  * k == 0: C = +0.  A and B must not overlap C.  Errors: INVALID_VALUE,
  * UNSUPPORTED, WORKSPACE (allocation failed), HIP. */

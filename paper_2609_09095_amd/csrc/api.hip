@@ -81,12 +81,14 @@ size_t products_bytes(int64_t m, int64_t n, int64_t k, ozaki25_moduli_set set, i
   return align_up(one) + (sp > 1 ? align_up(one * sp) : 0);
 }
 
-// Storage mode F for A (the all-byte set, at most 128 columns, at least
-// kFusedMinRows rows): A is converted inside the product kernel, so the
-// workspace holds no planes of A and the products need no split of k.
+// Storage mode F for A (at most 128 columns, at least kFusedMinRows rows;
+// either set): A is converted inside the product kernel, so the workspace
+// holds no planes of A and the products need no split of k.  B's planes
+// there: the all-byte set's residue planes, or for the published set the
+// 24 digit planes of its fused product (fewer bytes than its 30 planes).
 constexpr int64_t kFusedMinRows = 1024;
 bool fused_a(int64_t m, int64_t n, ozaki25_moduli_set set) {
-  return bytes_set(set) && n <= 128 && m >= kFusedMinRows;
+  return known_set(set) && n <= 128 && m >= kFusedMinRows;
 }
 
 // planes of A and B, exponents, and the residue products: int16 for the
@@ -396,16 +398,26 @@ ozaki25_status ozaki25_dgemm_ex(int64_t m, int64_t n, int64_t k, const double* A
   if (ev) e = hipEventRecord(ev[0], s);
   if (fused_a(m, n, set)) {
     // storage mode F for A: its exponent scan (clearing B's column keys on
-    // the side), B's scan and planes, then the products straight from FP64 A
+    // the side), B's scan and planes (for the published set B's scan only:
+    // its digit planes come with the product), then the products straight
+    // from FP64 A
     if (e == hipSuccess) e = oz::launch_scan_rows(m, k, A, lda, t, ea, eb, n, s);
     if (ev && e == hipSuccess) e = hipEventRecord(ev[1], s);
-    if (e == hipSuccess) e = scan_and_deconstruct(set, quant, 1, n, k, B, ldb, t, eb, pb, s, nullptr, 0, true);
+    if (bytes) {
+      if (e == hipSuccess) e = scan_and_deconstruct(set, quant, 1, n, k, B, ldb, t, eb, pb, s, nullptr, 0, true);
+    } else {
+      if (e == hipSuccess) e = oz::launch_scan_cols(n, k, B, ldb, eb, s);
+      if (e == hipSuccess) e = oz::launch_keys_to_sigma(n, t, eb, s);
+    }
     if (ev && e == hipSuccess) e = hipEventRecord(ev[2], s);
-    if (e == hipSuccess) e = oz::launch_fused_bytes((int)quant, m, n, k, kp, t, A, lda, ea, pb, (int8_t*)cres, s);
+    if (e == hipSuccess)
+      e = bytes ? oz::launch_fused_bytes((int)quant, m, n, k, kp, t, A, lda, ea, pb, (int8_t*)cres, s)
+                : oz::launch_fused_pub((int)quant, m, n, k, kp, t, A, lda, ea, B, ldb, eb, pb, (int16_t*)cres, s);
     if (ev && e == hipSuccess) e = hipEventRecord(ev[3], s);
     const oz::NativeOperands nat{A, lda, B, ldb, k};
     if (e == hipSuccess)
-      e = oz::launch_reconstruct_bytes_i8(m, n, (const int8_t*)cres, ea, eb, C, ldc, subtract ? 1 : 0, nat, s);
+      e = bytes ? oz::launch_reconstruct_bytes_i8(m, n, (const int8_t*)cres, ea, eb, C, ldc, subtract ? 1 : 0, nat, s)
+                : oz::launch_reconstruct_i16(m, n, (const int16_t*)cres, ea, eb, C, ldc, subtract ? 1 : 0, nat, s);
     if (ev && e == hipSuccess) e = hipEventRecord(ev[4], s);
     if (owned) {
       const hipError_t f = hipFreeAsync(ws, s);
@@ -531,12 +543,15 @@ ozaki25_status ozaki25_dgemm_accurate(int64_t m, int64_t n, int64_t k, const dou
   if (ev && e == hipSuccess) e = hipEventRecord(ev[1], s);
   if (e == hipSuccess && !fused)
     e = oz::launch_deconstruct((int)set, (int)quant, 0, m, m, k, kp, kAccurateT, A, lda, ea, false, pa, s);
-  if (e == hipSuccess)
+  // (the published set's fused product makes B's digit planes itself)
+  if (e == hipSuccess && (bytes || !fused))
     e = oz::launch_deconstruct((int)set, (int)quant, 1, n, n, k, kp, kAccurateT, B, ldb, eb, false, pb, s);
   if (ev && e == hipSuccess) e = hipEventRecord(ev[2], s);
   if (e == hipSuccess) {
-    if (fused)
+    if (fused && bytes)
       e = oz::launch_fused_bytes((int)quant, m, n, k, kp, kAccurateT, A, lda, ea, pb, (int8_t*)cres, s);
+    else if (fused)
+      e = oz::launch_fused_pub((int)quant, m, n, k, kp, kAccurateT, A, lda, ea, B, ldb, eb, pb, (int16_t*)cres, s);
     else if (bytes)
       e = oz::launch_residue_gemm_bytes_i8(m, n, kp, pa, pb, (int8_t*)cres, (int8_t*)part, w.splits, s);
     else

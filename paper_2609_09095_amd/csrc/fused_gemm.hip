@@ -328,6 +328,394 @@ hipError_t launch_fused_g(int64_t m, int64_t n, int64_t k, int64_t kp, const dou
   return hipGetLastError();
 }
 
+// ---- published set (twelve moduli) on FP8 MFMA -----------------------------
+// The same storage mode F for the published moduli, in six pairs: square g
+// (m = s^2) and nonsquare 6 + g.  Operand digits, every one an e4m3-exact
+// integer:
+//  - square: the balanced base-s digits (d0, d1) of the centred residue x,
+//    x = d0 + s d1, |d0|, |d1| <= 16; mod s^2 the product is
+//    d0 e0 + s (d0 e1 + d1 e0) (d1 e1 carries the factor s^2), summed in two
+//    FP32 accumulator sets (weights 1 and s);
+//  - nonsquare: balanced base-16 digits kept as (d0, 16 d1), |d0| <= 8,
+//    |16 d1| <= 256 (multiples of 16 up to 256 are e4m3-exact), so the four
+//    products of (d0 + 16 d1)(e0 + 16 e1) sum x y in one FP32 set.
+// Every partial sum is an integer kept below 2^24: per k the nonsquare terms
+// add up to at most 257^2 in magnitude, so that set is reduced every 2
+// stages (128 k); the square sets (at most 256 and 512 per k) every
+// kSegS stages.  The outputs are the compact residues of the published
+// set's product path (the true ones times compact_scale(i)^-1 mod m_i,
+// |c| <= 0.51 m_i), so its reconstruction takes them as they stand.
+// B's digits come from fused_b_digits_kernel: [kp/128][24][n][128], planes
+// 2 g, 2 g + 1 for square g and 12 + 2 g, 13 + 2 g for nonsquare 6 + g.
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+constexpr int kPairs = 6;
+constexpr int kSegS = 256;  // stages between reductions of the square sets
+
+struct PairConst {
+  int ms, s, mn;         // square modulus, its root, nonsquare modulus
+  double qs, qn;         // RN(1/m) for the quotient route
+  float is, ims, imn;    // RN(1/s), RN(1/ms), RN(1/mn)
+  float inv16;           // 16^-1 mod mn
+};
+constexpr PairConst make_pair(int g) {
+  return PairConst{kModulus[g],
+                   root_of(g),
+                   kModulus[kPairs + g],
+                   1.0 / kModulus[g],
+                   1.0 / kModulus[kPairs + g],
+                   1.0f / (float)root_of(g),
+                   1.0f / (float)kModulus[g],
+                   1.0f / (float)kModulus[kPairs + g],
+                   (float)inverse_mod(16, kModulus[kPairs + g])};
+}
+constexpr bool pairs_are_square_nonsquare() {
+  for (int g = 0; g < kPairs; ++g)
+    if (!root_of(g) || root_of(kPairs + g) || root_of(g) > 33 || kModulus[kPairs + g] > 511) return false;
+  return true;
+}
+static_assert(kR == 2 * kPairs && pairs_are_square_nonsquare(),
+              "six squares (s <= 33) first, then six nonsquares below 512");
+static_assert(compact_scale(0) == 1 && compact_scale(kPairs) == 16, "compact scales of the product path");
+__constant__ PairConst kPair[kPairs] = {make_pair(0), make_pair(1), make_pair(2),
+                                        make_pair(3), make_pair(4), make_pair(5)};
+
+// Centred residue of the integer-valued y modulo M (ylo = y mod 2^32), as a
+// 24-bit signed value: the FMA quotient of y RN(1/M) + 1.5 2^52 (exact
+// for M = 1024) and one 24-bit multiply-add.  MODE 1 (|y| <= 2^51): the
+// quotient is the nearest one (|y| ulp(1/M) / 2 <= 2^-11 for these moduli,
+// below the 1/(2M) that separates y/M from a half integer; for M = 1024 a
+// tie may give +512, as good a representative).  MODE 3 (|y| <= 2^58): the
+// quotient is within 5/8 of y/M, one correction each way.
+template <int MODE>
+__device__ __forceinline__ int residue_pub(double y, uint32_t ylo, int M, double qinv) {
+  const uint32_t q = lo32(__builtin_fma(y, qinv, kMagicF));
+  uint32_t r;
+  asm("v_mad_i32_i24 %0, %1, %2, %3" : "=v"(r) : "v"(q), "s"(-M), "v"(ylo));
+  int c = (int)(r << 8) >> 8;
+  if constexpr (MODE == 3) {
+    const int hi = (M - 1) / 2;
+    c = c > hi ? c - M : c;
+    c = c < hi - M + 1 ? c + M : c;
+  }
+  return c;
+}
+
+// four values (e4m3-exact integers) as OCP E4M3FN bytes, the first lowest
+__device__ __forceinline__ uint32_t e4m3x4(float a, float b, float c, float d) {
+  const int lo = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+  return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(c, d, lo, true);
+}
+
+// Digits of four residues: square (base s; q = rint(x / s) by one FP32
+// product, which never lands on the wrong side of a half integer: x / s is
+// either an exact tie -- s = 32, product exact -- or at least 1/(2s) from
+// one) and nonsquare (base 16, kept as d0 and 16 d1).  Each output dword
+// holds four bytes, the first value lowest.
+__device__ __forceinline__ void square_digits(const int (&x)[4], float s, float is, uint32_t& w0,
+                                              uint32_t& w1) {
+  float d0[4], d1[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const float xf = (float)x[c];
+    d1[c] = __builtin_rintf(xf * is);
+    d0[c] = __builtin_fmaf(-d1[c], s, xf);
+  }
+  w0 = e4m3x4(d0[0], d0[1], d0[2], d0[3]);
+  w1 = e4m3x4(d1[0], d1[1], d1[2], d1[3]);
+}
+__device__ __forceinline__ void nonsquare_digits(const int (&x)[4], uint32_t& w0, uint32_t& w1) {
+  float d0[4], h[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const float xf = (float)x[c];
+    h[c] = 16.0f * __builtin_rintf(xf * 0.0625f);
+    d0[c] = xf - h[c];
+  }
+  w0 = e4m3x4(d0[0], d0[1], d0[2], d0[3]);
+  w1 = e4m3x4(h[0], h[1], h[2], h[3]);
+}
+
+__device__ __forceinline__ float reduce_pf(float x, float m, float minv) {
+  return __builtin_fmaf(-__builtin_rintf(x * minv), m, x);
+}
+
+// fp8 fragment of a 32-row block for the 64-byte K step of a stage: lane
+// half fh takes chunks fh and 2 + fh of its row (the same on both operands,
+// so the MFMA pairs equal k)
+__device__ __forceinline__ v8i ffrag8(const int8_t* base, int r, int fh) {
+  const int8_t* row = base + r * FBK;
+  const v4i lo = *reinterpret_cast<const v4i*>(row + ((fh ^ fswz(r)) << 4));
+  const v4i hi = *reinterpret_cast<const v4i*>(row + (((2 + fh) ^ fswz(r)) << 4));
+  return v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+}
+
+__device__ __forceinline__ v16f mma8(v8i a, v8i b, v16f c) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+}
+
+// B's digits for the fused product: thread (lane, wave) of block
+// (column block, 64-k group) takes column 64 cb + lane and the 16 k from
+// 64 kg + 16 wave; every plane gets one 16-byte store.  tau: the columns'
+// exponents (OZAKI25_EXP_NONFINITE: zero digits).
+template <int MODE, bool TZ>
+__global__ __launch_bounds__(256) void fused_b_digits_kernel(int64_t n, int64_t k, int64_t kp,
+                                                             const double* __restrict__ B, int64_t ldb,
+                                                             const int32_t* __restrict__ tau,
+                                                             int8_t* __restrict__ digits) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t cbs = (n + 63) / 64;
+  const int64_t j = (int64_t)(blockIdx.x % cbs) * 64 + lane;
+  const int64_t k0 = (int64_t)(blockIdx.x / cbs) * 64 + wave * 16;
+  if (j >= n || k0 >= kp) return;
+  const int tj = tau[j];
+  const bool live = tj != INT32_MIN;
+  double y[16];
+  uint32_t ylo[16];
+#pragma unroll
+  for (int c = 0; c < 16; ++c) {
+    const double b = (live && k0 + c < k) ? B[(k0 + c) * ldb + j] : 0.0;
+    const double v = __builtin_ldexp(b, live ? tj : 0);
+    y[c] = TZ ? __builtin_trunc(v) : __builtin_rint(v);
+    ylo[c] = MODE == 1 ? lo32(y[c] + kMagicF) : low32_split(y[c]);
+  }
+  int8_t* out = digits + ((k0 / 128) * (2 * kR)) * n * 128 + j * 128 + (k0 % 128);
+  const int64_t pstride = n * 128;
+  for (int g = 0; g < kPairs; ++g) {
+    const PairConst pc = kPair[g];
+    uint32_t ws[2][4], wn[2][4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      int xs[4], xn[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        xs[c] = residue_pub<MODE>(y[4 * q + c], ylo[4 * q + c], pc.ms, pc.qs);
+        xn[c] = residue_pub<MODE>(y[4 * q + c], ylo[4 * q + c], pc.mn, pc.qn);
+      }
+      square_digits(xs, (float)pc.s, pc.is, ws[0][q], ws[1][q]);
+      nonsquare_digits(xn, wn[0][q], wn[1][q]);
+    }
+#pragma unroll
+    for (int d = 0; d < 2; ++d) {
+      *reinterpret_cast<uint4*>(out + (2 * g + d) * pstride) = uint4{ws[d][0], ws[d][1], ws[d][2], ws[d][3]};
+      *reinterpret_cast<uint4*>(out + (2 * kPairs + 2 * g + d) * pstride) =
+          uint4{wn[d][0], wn[d][1], wn[d][2], wn[d][3]};
+    }
+  }
+}
+
+// 128 rows of A per block and one pair of moduli; 16 wavefronts: wavefront
+// w converts rows 8 w .. 8 w + 7 of each 128 x 64 slab into the four digit
+// planes of the pair and owns the 32 x 32 outputs (w / 4, w % 4) of both
+// moduli.  The six blocks of a row strip go to one XCD back to back.
+// MODE: the residue route (1: |y| <= 2^51, ylo by 1.5 2^52; 3: |y| <= 2^58).
+template <int MODE, bool TZ, bool VEC>
+__global__ __launch_bounds__(1024, 1) void fused_pub_kernel(
+    int64_t m, int64_t n, int64_t k, int64_t kp, const double* __restrict__ A, int64_t lda,
+    const int32_t* __restrict__ sigma, const int8_t* __restrict__ pb, int16_t* __restrict__ cres,
+    int64_t strips) {
+  // [buffer][plane][slab]: planes 0, 1 the square digits, 2, 3 the nonsquare ones
+  __shared__ __attribute__((aligned(1024))) int8_t lds_a[2][4][FBM * FBK];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_b[2][4][FBN * FBK];
+  const uint32_t b = blockIdx.x, o = b >> 3;
+  const int64_t strip = (int64_t)(o / kPairs) * 8 + (b & 7);
+  const int grp = (int)(o % kPairs);
+  if (strip >= strips) return;
+  const int64_t row0 = strip * FBM;
+  const PairConst pc = kPair[grp];
+  const float fs = (float)pc.s, fms = (float)pc.ms, fmn = (float)pc.mn;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wr = wave >> 2, wc = wave & 3;
+  const int fr = lane & 31, fh = lane >> 5;
+
+  // conversion: lane l takes 4 consecutive k (4 (l % 16) ..) of row
+  // 8 wave + 4 i + l / 16, i = 0, 1
+  const int ck = 4 * (lane & 15);
+  int sg[2];
+  uint32_t keep[2];
+  const double* arow_p[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = 8 * wave + 4 * i + (lane >> 4);
+    const int64_t arow = row0 + r;
+    const bool ok = arow < m;
+    const int sv = ok ? sigma[arow] : 0;
+    const bool live = ok && sv != INT32_MIN;
+    keep[i] = live ? 0xFFFFFFFFu : 0u;
+    sg[i] = live ? sv : 0;
+    arow_p[i] = A + (ok ? arow : m - 1) * lda;
+  }
+
+  const int nstage = (int)(kp / FBK);
+  double x0[8], x1[8];
+  auto load_a = [&](int s, double (&x)[8]) {
+    const int64_t k0 = (int64_t)s * FBK + ck;
+    if (VEC && (int64_t)s * FBK + FBK <= k) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const double2 p = *reinterpret_cast<const double2*>(arow_p[i] + k0);
+        const double2 q = *reinterpret_cast<const double2*>(arow_p[i] + k0 + 2);
+        x[4 * i] = p.x;
+        x[4 * i + 1] = p.y;
+        x[4 * i + 2] = q.x;
+        x[4 * i + 3] = q.y;
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const int64_t kk = k0 + c < k ? k0 + c : k - 1;
+          const double v = arow_p[i][kk];
+          x[4 * i + c] = k0 + c < k ? v : 0.0;
+        }
+    }
+  };
+  // one dword (4 digit bytes) per row and plane, at chunk ck / 16 of the
+  // row, swizzled
+  auto convert = [&](int buf, const double (&x)[8]) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int r = 8 * wave + 4 * i + (lane >> 4);
+      double y[4];
+      uint32_t ylo[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const double v = __builtin_ldexp(x[4 * i + c], sg[i]);
+        y[c] = TZ ? __builtin_trunc(v) : __builtin_rint(v);
+        ylo[c] = MODE == 1 ? lo32(y[c] + kMagicF) : low32_split(y[c]);
+      }
+      int xs[4], xn[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        xs[c] = residue_pub<MODE>(y[c], ylo[c], pc.ms, pc.qs);
+        xn[c] = residue_pub<MODE>(y[c], ylo[c], pc.mn, pc.qn);
+      }
+      uint32_t w[4];
+      square_digits(xs, fs, pc.is, w[0], w[1]);
+      nonsquare_digits(xn, w[2], w[3]);
+      const int at = r * FBK + (((ck >> 4) ^ fswz(r)) << 4) + (ck & 15);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) *reinterpret_cast<uint32_t*>(&lds_a[buf][q][at]) = w[q] & keep[i];
+    }
+  };
+  // B's four digit slabs of stage s (128 columns x 64 bytes each) by
+  // LDS-DMA, eight 1 KiB loads per slab spread over the wavefronts; columns
+  // past n read zero
+  const int brecs = __builtin_amdgcn_readfirstlane((int)(n * 128));
+  auto load_b = [&](int s, int buf) {
+    const int64_t kb = s >> 1, h = s & 1;
+    for (int d = wave; d < 32; d += 16) {
+      const int q = d >> 3, dd = d & 7;
+      const int plane = q < 2 ? 2 * grp + q : 2 * kPairs + 2 * grp + (q - 2);
+      const int8_t* piece = uniform_ptr_f(pb + ((kb * (2 * kR) + plane) * n) * 128 + h * 64);
+      const __amdgpu_buffer_rsrc_t rs =
+          __builtin_amdgcn_make_buffer_rsrc((void*)piece, (short)0, brecs, 0x00020000);
+      const int row = 16 * dd + (lane >> 2);
+      const int gchunk = (lane & 3) ^ fswz(row);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_f)(&lds_b[buf][q][16 * dd * FBK]), 16,
+                                               row * 128 + gchunk * 16, 0, 0, 0);
+    }
+  };
+
+  v16f acc1 = v16f{}, accs = v16f{}, accn = v16f{};
+  auto step = [&](int s, double (&xs)[8], double (&xn)[8]) {
+    const int cur = s & 1, nxt = cur ^ 1;
+    if (s + 2 < nstage) load_a(s + 2, xs);
+    if (s + 1 < nstage) load_b(s + 1, nxt);
+    // at most three fragments live at a time (registers are short here)
+    const int ar = wr * 32 + fr, br = wc * 32 + fr;
+    {
+      const v8i a0 = ffrag8(lds_a[cur][0], ar, fh), b0 = ffrag8(lds_b[cur][0], br, fh);
+      acc1 = mma8(a0, b0, acc1);
+      const v8i b1 = ffrag8(lds_b[cur][1], br, fh);
+      accs = mma8(a0, b1, accs);
+      const v8i a1 = ffrag8(lds_a[cur][1], ar, fh);
+      accs = mma8(a1, b0, accs);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    {
+      const v8i a0 = ffrag8(lds_a[cur][2], ar, fh), b0 = ffrag8(lds_b[cur][2], br, fh);
+      accn = mma8(a0, b0, accn);
+      const v8i b1 = ffrag8(lds_b[cur][3], br, fh);
+      accn = mma8(a0, b1, accn);
+      const v8i a1 = ffrag8(lds_a[cur][3], ar, fh);
+      accn = mma8(a1, b0, accn);
+      accn = mma8(a1, b1, accn);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    if (s + 1 < nstage) convert(nxt, xn);
+    if ((s & 1) && s + 1 < nstage) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) accn[v] = reduce_pf(accn[v], fmn, pc.imn);
+    }
+    if (((s + 1) % kSegS) == 0 && s + 1 < nstage) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        acc1[v] = reduce_pf(acc1[v], fms, pc.ims);
+        accs[v] = reduce_pf(accs[v], fms, pc.ims);
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  };
+
+  if (nstage > 0) {
+    load_a(0, x0);
+    load_b(0, 0);
+    if (nstage > 1) load_a(1, x1);
+    convert(0, x0);
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  for (int s = 0; s < nstage; s += 2) {
+    step(s, x0, x1);
+    if (s + 1 < nstage) step(s + 1, x1, x0);
+  }
+
+  // epilogue: the compact residues -- square (acc1 + s accs) mod m; nonsquare
+  // (x y summed) 16^-1 mod m -- each reduced to |c| <= 0.51 m (every value
+  // here is an integer below 2^24 in magnitude), as int16 in [12][m][n]
+  const int64_t col = wc * 32 + fr;
+  int16_t* outs = cres + (int64_t)grp * m * n;
+  int16_t* outn = cres + (int64_t)(kPairs + grp) * m * n;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int64_t row = row0 + wr * 32 + 8 * (v >> 2) + 4 * fh + (v & 3);
+    const float sv = reduce_pf(reduce_pf(acc1[v], fms, pc.ims) + fs * reduce_pf(accs[v], fms, pc.ims), fms,
+                               pc.ims);
+    const float nv = reduce_pf(reduce_pf(accn[v], fmn, pc.imn) * pc.inv16, fmn, pc.imn);
+    if (row < m && col < n) {
+      outs[row * n + col] = (int16_t)(int)sv;
+      outn[row * n + col] = (int16_t)(int)nv;
+    }
+  }
+}
+
+template <int MODE, bool TZ>
+hipError_t launch_fused_pub_m(int64_t m, int64_t n, int64_t k, int64_t kp, const double* A, int64_t lda,
+                              const int32_t* sigma, const double* B, int64_t ldb, const int32_t* tau,
+                              int8_t* pb, int16_t* cres, hipStream_t stream) {
+  const int64_t cbs = (n + 63) / 64, kgs = kp / 64;
+  if (cbs * kgs > (int64_t)UINT32_MAX) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((fused_b_digits_kernel<MODE, TZ>), dim3((unsigned)(cbs * kgs)), dim3(256), 0, stream, n, k,
+                     kp, B, ldb, tau, pb);
+  const int64_t strips = (m + FBM - 1) / FBM;
+  const int64_t blocks = (strips + 7) / 8 * 8 * kPairs;
+  if (blocks > (int64_t)UINT32_MAX) return hipErrorInvalidValue;
+  if ((((uintptr_t)A) & 15) == 0 && (lda & 1) == 0)
+    hipLaunchKernelGGL((fused_pub_kernel<MODE, TZ, true>), dim3((unsigned)blocks), dim3(1024), 0, stream, m, n,
+                       k, kp, A, lda, sigma, pb, cres, strips);
+  else
+    hipLaunchKernelGGL((fused_pub_kernel<MODE, TZ, false>), dim3((unsigned)blocks), dim3(1024), 0, stream, m,
+                       n, k, kp, A, lda, sigma, pb, cres, strips);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_fused_bytes(int quant, int64_t m, int64_t n, int64_t k, int64_t kp, int t,
@@ -344,6 +732,24 @@ hipError_t launch_fused_bytes(int quant, int64_t m, int64_t n, int64_t k, int64_
   if (mode == 2) OZ_FUSED(2);
   OZ_FUSED(3);
 #undef OZ_FUSED
+}
+
+}  // namespace oz
+
+namespace oz {
+
+hipError_t launch_fused_pub(int quant, int64_t m, int64_t n, int64_t k, int64_t kp, int t, const double* A,
+                            int64_t lda, const int32_t* sigma, const double* B, int64_t ldb,
+                            const int32_t* tau, int8_t* pb, int16_t* cres, hipStream_t stream) {
+  if (n > FBN || kp % 128 || m <= 0 || n <= 0 || t > kMaxScaleBits) return hipErrorInvalidValue;
+  const bool tz = quant == kQuantTZ;
+  // |y| <= 2^t: the nearest quotient with ylo from 1.5 2^52 up to 2^50, the
+  // corrected one beyond (as in the deconstruction of the published set)
+  if (t <= 50)
+    return tz ? launch_fused_pub_m<1, true>(m, n, k, kp, A, lda, sigma, B, ldb, tau, pb, cres, stream)
+              : launch_fused_pub_m<1, false>(m, n, k, kp, A, lda, sigma, B, ldb, tau, pb, cres, stream);
+  return tz ? launch_fused_pub_m<3, true>(m, n, k, kp, A, lda, sigma, B, ldb, tau, pb, cres, stream)
+            : launch_fused_pub_m<3, false>(m, n, k, kp, A, lda, sigma, B, ldb, tau, pb, cres, stream);
 }
 
 }  // namespace oz

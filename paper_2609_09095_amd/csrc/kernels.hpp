@@ -82,6 +82,15 @@ hipError_t launch_fused_bytes(int quant, int64_t m, int64_t n, int64_t k, int64_
                               const double* A, int64_t lda, const int32_t* sigma, const int8_t* pb,
                               int8_t* cres, hipStream_t stream);
 
+// Storage mode F for A, published set (at most 128 columns): B's digit
+// planes for the fused product (24 planes [kp/128][24][n][128] into pb, from
+// B and its column exponents tau), then the per-modulus products [12][m][n]
+// as the compact int16 residues launch_reconstruct_i16 takes, straight from
+// FP64 A and its row exponents sigma.  k == 0 is not handled here.
+hipError_t launch_fused_pub(int quant, int64_t m, int64_t n, int64_t k, int64_t kp, int t, const double* A,
+                            int64_t lda, const int32_t* sigma, const double* B, int64_t ldb,
+                            const int32_t* tau, int8_t* pb, int16_t* cres, hipStream_t stream);
+
 // The operands of Alg. 1's last step (range check, native FP64 re-issue):
 // outputs whose row of A or column of B was flagged non-finite by the
 // exponent scan become the index-order FP64 dot product of that row and

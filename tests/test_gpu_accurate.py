@@ -121,16 +121,17 @@ def test_accurate_subtract_tz_and_nonfinite(set):
     assert_bits_equal(_dgemm(A, B, set, quant=oz.TZ), want, "C (TZ)")
 
 
+@pytest.mark.parametrize("set", [0, 1])
 @pytest.mark.parametrize("m,n,k,s,seed", [(1100, 90, 300, 3.0, 41), (2049, 128, 4096, 1.0, 42)])
-def test_accurate_fused_path(m, n, k, s, seed):
-    """The all-byte set with at most 128 columns and at least 1024 rows
-    converts A inside the product kernel (storage mode F)."""
-    log(f"accurate fused A15 m={m} n={n} k={k}")
+def test_accurate_fused_path(set, m, n, k, s, seed):
+    """At most 128 columns and at least 1024 rows: A is converted inside the
+    product kernel (storage mode F), here at the accurate mode's shifts."""
+    log(f"accurate fused set={set} m={m} n={n} k={k}")
     A = workloads.random_matrix(m, k, s, seed)
     B = workloads.random_matrix(k, n, s, seed + 100)
     A[3, 3] = -np.inf
-    want = oracle.dgemm(A, B, set=1, accurate=True, want_planes=False).C
-    assert_bits_equal(_dgemm(A, B, 1), want, "C")
+    want = oracle.dgemm(A, B, set=set, accurate=True, want_planes=False).C
+    assert_bits_equal(_dgemm(A, B, set), want, "C")
 
 
 def test_accurate_k_zero_and_errors():

@@ -1,10 +1,11 @@
-"""Storage mode F for A (the all-byte set, at most 128 columns, at least 1024
-rows): ozaki25_dgemm_ex converts A inside the product kernel instead of
-storing its planes.  Every output is compared with the oracle bit for bit
+"""Storage mode F for A (at most 128 columns, at least 1024 rows, both
+modulus sets): ozaki25_dgemm_ex converts A inside the product kernel instead
+of storing its planes.  Every output is compared with the oracle bit for bit
 (any NaN matching any NaN): ragged rows, columns and k, one column, k past
-the 65536-long segments of the int32 sums, C -= AB, the truncating
-quantiser, rows and columns with non-finite values (native re-issue), and
-a wide exponent range."""
+the segments after which the sums are reduced (65536 k for the all-byte
+set's int32 sums, 16384 k for the published set's square digit sums), C -=
+AB, the truncating quantiser, rows and columns with non-finite values
+(native re-issue), and a wide exponent range."""
 import numpy as np
 import pytest
 
@@ -21,29 +22,34 @@ def gpu():
     require_gpu()
 
 
-def _run(A, B, C0=None, quant=oz.RN):
+SETS = [pytest.param(oz.S12, id="S12"), pytest.param(oz.A15, id="A15")]
+
+
+def _run(A, B, set, C0=None, quant=oz.RN):
     import torch
     m, k = A.shape
     n = B.shape[1]
-    ws = torch.empty(oz.ozaki25_dgemm_workspace_size(m, n, k, oz.A15), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(oz.ozaki25_dgemm_workspace_size(m, n, k, set), dtype=torch.uint8, device="cuda")
     C = to_dev(C0) if C0 is not None else torch.empty((m, n), dtype=torch.float64, device="cuda")
-    oz.ozaki25_dgemm_ex(to_dev(A), to_dev(B), C, subtract=C0 is not None, workspace=ws, set=oz.A15,
+    oz.ozaki25_dgemm_ex(to_dev(A), to_dev(B), C, subtract=C0 is not None, workspace=ws, set=set,
                         quantiser=quant)
     torch.cuda.synchronize()
     return C.cpu().numpy()
 
 
+@pytest.mark.parametrize("set", SETS)
 @pytest.mark.parametrize("m,n,k,s,seed", [(1024, 128, 64, 1.0, 1), (1300, 70, 1000, 1.0, 2),
                                           (2049, 1, 257, 2.0, 3), (4096, 128, 4096, 1.0, 4),
-                                          (1500, 100, 130, 4.0, 5)])
-def test_fused_matches_oracle(m, n, k, s, seed):
-    log(f"fused A15 m={m} n={n} k={k} s={s}")
+                                          (1500, 100, 130, 4.0, 5), (1030, 128, 8, 0.5, 6)])
+def test_fused_matches_oracle(set, m, n, k, s, seed):
+    log(f"fused set={set} m={m} n={n} k={k} s={s}")
     A = workloads.random_matrix(m, k, s, seed)
     B = workloads.random_matrix(k, n, s, seed + 100)
-    assert_bits_equal(_run(A, B), oracle.dgemm(A, B, set=1, want_planes=False).C, "C")
+    assert_bits_equal(_run(A, B, set), oracle.dgemm(A, B, set=set, want_planes=False).C, "C")
 
 
-def test_fused_subtract_tz_and_nonfinite():
+@pytest.mark.parametrize("set", SETS)
+def test_fused_subtract_tz_and_nonfinite(set):
     m, n, k = 1100, 90, 300
     A = workloads.random_matrix(m, k, 1.0, 11)
     B = workloads.random_matrix(k, n, 1.0, 12)
@@ -51,21 +57,42 @@ def test_fused_subtract_tz_and_nonfinite():
     A[5, 7] = np.nan
     A[1090, 0] = -np.inf
     B[3, 40] = np.inf
-    log("fused A15 C -= AB with non-finite rows and columns")
-    assert_bits_equal(_run(A, B, C0), oracle.dgemm(A, B, C_in=C0, set=1, want_planes=False).C, "C -= AB")
-    log("fused A15 truncating quantiser")
+    log(f"fused set={set} C -= AB with non-finite rows and columns")
+    assert_bits_equal(_run(A, B, set, C0), oracle.dgemm(A, B, C_in=C0, set=set, want_planes=False).C,
+                      "C -= AB")
+    log(f"fused set={set} truncating quantiser")
     A[5, 7], A[1090, 0], B[3, 40] = 1.0, 2.0, 3.0
-    assert_bits_equal(_run(A, B, quant=oz.TZ),
-                      oracle.dgemm(A, B, set=1, want_planes=False, quant=oracle.TZ).C, "C (TZ)")
+    assert_bits_equal(_run(A, B, set, quant=oz.TZ),
+                      oracle.dgemm(A, B, set=set, want_planes=False, quant=oracle.TZ).C, "C (TZ)")
 
 
-def test_fused_long_k_segments():
-    """k = 70000 crosses the 65536-long segment after which the int32 sums
-    are reduced mod m."""
+@pytest.mark.parametrize("set", SETS)
+def test_fused_long_k_segments(set):
+    """k = 70000 crosses the segments after which the sums are reduced mod
+    m (65536 k for the all-byte set, 16384 k for the published set's square
+    digit sums)."""
     m, n, k = 1024, 3, 70000
     A = workloads.random_matrix(m, k, 1.0, 21)
     B = workloads.random_matrix(k, n, 1.0, 22)
     rows = sample_indices(m, 64, 23)
-    got = _run(A, B)[rows]
-    want = oracle.dgemm(A, B, rows=rows, set=1, want_planes=False).C
+    log(f"fused set={set} k={k}")
+    got = _run(A, B, set)[rows]
+    want = oracle.dgemm(A, B, rows=rows, set=set, want_planes=False).C
     assert_bits_equal(got, want, "C (sampled rows)")
+
+
+def test_fused_published_constant_vectors():
+    """Published set: constant rows of A and columns of B, so that every
+    term of a sum has the same residue product and the FP32 sums grow
+    without cancellation between reductions (their largest magnitudes for
+    those residues), beside random rows and columns."""
+    m, n, k = 1024, 8, 2048
+    A = workloads.random_matrix(m, k, 1.0, 32)
+    B = workloads.random_matrix(k, n, 1.0, 33)
+    A[:16, :] = np.ldexp(1.0, -3) * (1 - 2.0 ** -40)
+    A[16:32, :] = -1.0
+    A[32:48, :] = 3.0 * (1 + 2.0 ** -30)
+    B[:, :2] = 7.0 * (1 - 2.0 ** -45)
+    B[:, 2] = -3.0
+    log("fused S12 constant rows and columns")
+    assert_bits_equal(_run(A, B, oz.S12), oracle.dgemm(A, B, set=0, want_planes=False).C, "C")
