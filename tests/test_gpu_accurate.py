@@ -134,6 +134,24 @@ def test_accurate_fused_path(set, m, n, k, s, seed):
     assert_bits_equal(_dgemm(A, B, set), want, "C")
 
 
+@pytest.mark.parametrize("set", [0, 1])
+def test_accurate_fused_subtract_tz(set):
+    """Storage mode F at the accurate mode's shifts with C -= AB, the
+    truncating quantiser, a non-finite column and a zero row."""
+    m, n, k = 1200, 64, 520
+    A = workloads.random_matrix(m, k, 2.0, 51)
+    B = workloads.random_matrix(k, n, 2.0, 52)
+    C0 = workloads.random_matrix(m, n, 1.0, 53)
+    B[9, 33] = np.nan
+    A[77] = 0.0
+    log(f"accurate fused C -= AB, set={set}")
+    want = oracle.dgemm(A, B, C_in=C0, set=set, accurate=True, want_planes=False).C
+    assert_bits_equal(_dgemm(A, B, set, C0=C0), want, "C -= AB")
+    log(f"accurate fused, truncating quantiser, set={set}")
+    want = oracle.dgemm(A, B, set=set, accurate=True, want_planes=False, quant=oracle.TZ).C
+    assert_bits_equal(_dgemm(A, B, set, quant=oz.TZ), want, "C (TZ)")
+
+
 def test_accurate_k_zero_and_errors():
     import torch
     A = torch.zeros((4, 0), dtype=torch.float64, device="cuda")
