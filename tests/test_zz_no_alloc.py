@@ -72,6 +72,22 @@ def test_noalloc_split_k_then_smaller():
         assert_bits_equal(got, _ex(A, B, None, False, oz.S12), f"call {call}: noalloc vs dgemm_ex")
 
 
+@pytest.mark.parametrize("set", [oz.S12, oz.A15])
+def test_noalloc_tall_skinny_then_smaller(set):
+    """Tall and skinny products (storage mode F for A: B's planes and the
+    products in the array, A converted inside the product kernel), the
+    second one smaller."""
+    for call, (m, n, k) in enumerate([(2048, 100, 700), (1024, 64, 130)]):
+        log(f"noalloc tall/skinny set={set} call {call}: m={m} n={n} k={k}")
+        A = workloads.random_matrix(m, k, 1.0, 500 + call)
+        B = workloads.random_matrix(k, n, 1.0, 510 + call)
+        got = _noalloc(A, B, None, False, set)
+        assert_bits_equal(got, _ex(A, B, None, False, set), f"call {call}: noalloc vs dgemm_ex")
+        if call == 1:
+            want = oracle.dgemm(A, B, set=set, want_planes=False).C
+            assert_bits_equal(got, want, f"call {call}: noalloc vs oracle")
+
+
 def test_noalloc_refuses_beyond_its_array():
     import torch
     m = n = k = 2048
