@@ -108,6 +108,32 @@ __device__ __forceinline__ const int8_t* uniform_ptr_f(const int8_t* p) {
 
 using lds_ptr_f = __attribute__((address_space(3))) void*;
 
+// The lane index, computed afresh where it is used. The all-byte kernel runs
+// at the register limit, and a lane offset held across its k loop is spilled;
+// its reload from scratch waits on the vector-memory counter and so drains
+// the look-ahead loads with it. A volatile asm is neither hoisted nor merged.
+__device__ __forceinline__ int lane_now() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
+// End of a pipeline stage. Each wave waits for its own LDS writes and its
+// LDS-DMA, then the workgroup meets at the barrier. When keep_a is set, the
+// last four vector loads (A's FP64 values for the stage after next, issued
+// after the DMA) may stay outstanding: vmcnt(4) expcnt(0) lgkmcnt(0). Any
+// other load path issues at least four loads there, and the counter retires
+// in issue order. The barrier is a bare instruction behind a compiler memory
+// barrier, because the release fence of __syncthreads() drains every
+// outstanding vector load.
+__device__ __forceinline__ void stage_barrier(bool keep_a) {
+  if (keep_a)
+    __builtin_amdgcn_s_waitcnt(0x0004);
+  else
+    __builtin_amdgcn_s_waitcnt(0);
+  asm volatile("s_barrier" ::: "memory");
+}
+
 // Centred residue of an int32 sum modulo m (as cmod_i32 in the residue GEMM).
 __device__ __forceinline__ int cmod_sum(int x, int m, double minv) {
   const double xd = (double)x;
@@ -130,8 +156,13 @@ __global__ __launch_bounds__(1024, 1) void fused_bytes_kernel(
     int64_t strips) {
   static_assert(kRA % G == 0, "modulus groups");
   constexpr int NG = kRA / G;
-  __shared__ __attribute__((aligned(1024))) int8_t lds_a[2][G][FBM * FBK];
-  __shared__ __attribute__((aligned(1024))) int8_t lds_b[2][G][FBN * FBK];
+  // two buffers of each, every buffer its own LDS object: the compiler then
+  // tells the buffer that LDS-DMA fills from the one being read, and does
+  // not wait for the DMA before the reads
+  __shared__ __attribute__((aligned(1024))) int8_t lds_a0[G][FBM * FBK];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_a1[G][FBM * FBK];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_b0[G][FBN * FBK];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_b1[G][FBN * FBK];
   // block -> (strip, group): the NG blocks of a strip go to one XCD (block b
   // runs on XCD b % 8), one after the other
   const uint32_t b = blockIdx.x, o = b >> 3;
@@ -176,12 +207,13 @@ __global__ __launch_bounds__(1024, 1) void fused_bytes_kernel(
   // two register sets x0, x1: stage j's values live in x(j % 2), loaded two
   // stages ahead; x[4 i + c] is row 8 wave + 4 i + lane / 16, k = ck + c
   double x0[8], x1[8];
-  // x holds the raw values (rows past m or holding a NaN or an infinity
-  // are masked after the conversion); whole stages take the 16-byte loads,
-  // the last, partial one clamped single loads
-  auto load_a = [&](int s, double (&x)[8]) {
-    const int64_t k0 = (int64_t)s * FBK + ck;
-    if (VEC && (int64_t)s * FBK + FBK <= k) {
+  // x holds the raw values (rows past m or holding a NaN or an infinity,
+  // and k past the end, are masked after the conversion); whole stages take
+  // the 16-byte loads, the last, partial one clamped single loads; full:
+  // stage s is known to lie inside k
+  auto load_a = [&](int s, double (&x)[8], bool full) __attribute__((always_inline)) {
+    const int64_t k0 = (int64_t)s * FBK + 4 * (lane_now() & 15);
+    if (VEC && (full || (int64_t)s * FBK + FBK <= k)) {
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
         const double2 p = *reinterpret_cast<const double2*>(arow_p[i] + k0);
@@ -196,15 +228,21 @@ __global__ __launch_bounds__(1024, 1) void fused_bytes_kernel(
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-          const int64_t kk = k0 + c < k ? k0 + c : k - 1;
-          const double v = arow_p[i][kk];
-          x[4 * i + c] = k0 + c < k ? v : 0.0;
+          // clamped into the row; convert zeroes the digits past k
+          x[4 * i + c] = arow_p[i][k0 + c < k ? k0 + c : k - 1];
         }
     }
   };
   // one dword (4 residue bytes) per row and modulus, written at chunk
   // ck / 16 of the row, swizzled
-  auto convert = [&](int buf, const double (&x)[8]) {
+  auto convert = [&](int buf, const double (&x)[8], int t) __attribute__((always_inline)) {
+    // byte c of a digit word is element k0 + c: the bytes at or past k of
+    // the last (partial) stage t are cleared with the dead rows'
+    uint32_t kmask = 0xFFFFFFFFu;
+    if ((int64_t)(t + 1) * FBK > k) {
+      const int64_t rem = k - ((int64_t)t * FBK + ck);
+      kmask = rem >= 4 ? 0xFFFFFFFFu : rem <= 0 ? 0u : 0xFFFFFFFFu >> (32 - 8 * (int)rem);
+    }
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int r = 8 * wave + 4 * i + (lane >> 4);
@@ -228,7 +266,7 @@ __global__ __launch_bounds__(1024, 1) void fused_bytes_kernel(
             __builtin_amdgcn_perm(residue_byte<MODE == 3>(y[3], ylo[3], mods[g], qinv[g]),
                                   residue_byte<MODE == 3>(y[2], ylo[2], mods[g], qinv[g]), 0x0c0c0400u);
         const uint32_t word = __builtin_amdgcn_perm(r23, r01, 0x05040100u);
-        *reinterpret_cast<uint32_t*>(&lds_a[buf][g][at]) = word & keep[i];
+        *reinterpret_cast<uint32_t*>(&(buf ? lds_a1 : lds_a0)[g][at]) = word & (keep[i] & kmask);
       }
     }
   };
@@ -237,7 +275,7 @@ __global__ __launch_bounds__(1024, 1) void fused_bytes_kernel(
   // lane l lands at row 16 d + l / 4, physical chunk l % 4, and fetches
   // the global chunk that the swizzle puts there; columns past n read zero.
   const int brecs = __builtin_amdgcn_readfirstlane((int)(n * 128));
-  auto load_b = [&](int s, int buf) {
+  auto load_b = [&](int s, int buf) __attribute__((always_inline)) {
     const int64_t kb = s >> 1, h = s & 1;
     for (int d = wave; d < 8 * G; d += 16) {
       const int g = d >> 3, dd = d & 7;
@@ -247,7 +285,7 @@ __global__ __launch_bounds__(1024, 1) void fused_bytes_kernel(
           __builtin_amdgcn_make_buffer_rsrc((void*)piece, (short)0, brecs, 0x00020000);
       const int row = 16 * dd + (lane >> 2);
       const int gchunk = (lane & 3) ^ fswz(row);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_f)(&lds_b[buf][g][16 * dd * FBK]), 16,
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_f)(&(buf ? lds_b1 : lds_b0)[g][16 * dd * FBK]), 16,
                                                row * 128 + gchunk * 16, 0, 0, 0);
     }
   };
@@ -257,16 +295,25 @@ __global__ __launch_bounds__(1024, 1) void fused_bytes_kernel(
   for (int g = 0; g < G; ++g) acc[g] = v16i{};
 
   // stage s: the loads of stage s + 2 go out, the MFMAs of stage s run on
-  // the LDS buffers s % 2, and stage s + 1 (loaded during stage s - 1) is
-  // converted into the other buffers
-  auto step = [&](int s, double (&xs)[8], double (&xn)[8]) {
-    const int cur = s & 1, nxt = cur ^ 1;
-    if (s + 2 < nstage) load_a(s + 2, xs);
-    if (s + 1 < nstage) load_b(s + 1, nxt);
+  // the LDS buffers cur = s % 2, and stage s + 1 (loaded during stage
+  // s - 1) is converted into the other buffers.
+  // inner: a stage of the main loop, whose next stage exists and whose
+  // look-ahead stage lies inside k. The look-ahead there is unconditional
+  // and takes one load path, so that the compiler sees every look-ahead
+  // register consumed and keeps the loads in flight across the barrier.
+  // B's DMA goes out before A's loads, so that the end-of-stage wait can
+  // leave the latter outstanding.
+  auto step = [&](int s, double (&xs)[8], double (&xn)[8], int cur, bool inner)
+                  __attribute__((always_inline)) {
+    const int nxt = cur ^ 1;
+    const bool next = inner || s + 1 < nstage;
+    const bool more = inner || s + 2 < nstage;
+    if (next) load_b(s + 1, nxt);
+    if (more) load_a(s + 2, xs, inner);
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      const int8_t* la = lds_a[cur][g];
-      const int8_t* lb = lds_b[cur][g];
+      const int8_t* la = (cur ? lds_a1 : lds_a0)[g];
+      const int8_t* lb = (cur ? lds_b1 : lds_b0)[g];
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks)
         acc[g] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ffrag(la, wr * 32 + fr, ks, fh),
@@ -274,28 +321,35 @@ __global__ __launch_bounds__(1024, 1) void fused_bytes_kernel(
       // one modulus's fragments at a time in registers
       __builtin_amdgcn_sched_barrier(0);
     }
-    if (s + 1 < nstage) convert(nxt, xn);
-    if (((s + 1) % kSegF) == 0 && s + 1 < nstage) {
+    if (next) convert(nxt, xn, s + 1);
+    if (((s + 1) % kSegF) == 0 && next) {
 #pragma unroll
       for (int g = 0; g < G; ++g)
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[g][v] = cmod_sum(acc[g][v], mods[g], inv[g]);
     }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+    stage_barrier(more);
   };
 
   if (nstage > 0) {
-    load_a(0, x0);
+    load_a(0, x0, false);
     load_b(0, 0);
-    if (nstage > 1) load_a(1, x1);
-    convert(0, x0);
+    if (nstage > 1) load_a(1, x1, false);
+    convert(0, x0, 0);
   }
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  for (int s = 0; s < nstage; s += 2) {
-    step(s, x0, x1);
-    if (s + 1 < nstage) step(s + 1, x1, x0);
+  // the main loop runs while both look-ahead stages are full; the last
+  // (at most four) stages take the guarded steps
+  const int nfull = (int)(k / FBK);
+  int s = 0;
+  for (; s + 3 < nfull; s += 2) {
+    step(s, x0, x1, 0, true);
+    step(s + 1, x1, x0, 1, true);
+  }
+  for (; s < nstage; s += 2) {
+    step(s, x0, x1, 0, false);
+    if (s + 1 < nstage) step(s + 1, x1, x0, 1, false);
   }
 
   // epilogue: centred residues (+m/2 of m = 256 stores as -128), int8, into
