@@ -393,10 +393,11 @@ hipError_t launch_fused_g(int64_t m, int64_t n, int64_t k, int64_t kp, const dou
 //  - nonsquare: balanced base-16 digits kept as (d0, 16 d1), |d0| <= 8,
 //    |16 d1| <= 256 (multiples of 16 up to 256 are e4m3-exact), so the four
 //    products of (d0 + 16 d1)(e0 + 16 e1) sum x y in one FP32 set.
-// Every partial sum is an integer kept below 2^24: per k the nonsquare terms
-// add up to at most 257^2 in magnitude, so that set is reduced every 2
-// stages (128 k); the square sets (at most 256 and 512 per k) every
-// kSegS stages.  The outputs are the compact residues of the published
+// Every partial sum is an integer kept below 2^24: per k the nonsquare digit
+// products add up to at most 264^2 in magnitude (|d0| + |16 d1| <= 264, at
+// x = 248), so that set is reduced every 3 stages (192 k: 13 381 632, plus
+// at most 256 left by the last reduction); the square sets (at most 256 and
+// 512 per k) every kSegS stages.  The outputs are the compact residues of the published
 // set's product path (the true ones times compact_scale(i)^-1 mod m_i,
 // |c| <= 0.51 m_i), so its reconstruction takes them as they stand.
 // B's digits come from fused_b_digits_kernel: [kp/128][24][n][128], planes
@@ -591,7 +592,6 @@ __global__ __launch_bounds__(1024, 1) void fused_pub_kernel(
   const int ck = 4 * (lane & 15);
   int sg[2];
   uint32_t keep[2];
-  const double* arow_p[2];
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int r = 8 * wave + 4 * i + (lane >> 4);
@@ -601,13 +601,22 @@ __global__ __launch_bounds__(1024, 1) void fused_pub_kernel(
     const bool live = ok && sv != INT32_MIN;
     keep[i] = live ? 0xFFFFFFFFu : 0u;
     sg[i] = live ? sv : 0;
-    arow_p[i] = A + (ok ? arow : m - 1) * lda;
   }
 
   const int nstage = (int)(kp / FBK);
   double x0[8], x1[8];
   auto load_a = [&](int s, double (&x)[8]) {
-    const int64_t k0 = (int64_t)s * FBK + ck;
+    // the lane's k offset and row pointers recomputed here, not held
+    // across the loop (the kernel is at the register limit, and a spilled
+    // copy would be reloaded from scratch at the start of every stage)
+    const int l = lane_now();
+    const int64_t k0 = (int64_t)s * FBK + 4 * (l & 15);
+    const double* arow_p[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int64_t arow = row0 + 8 * wave + 4 * i + (l >> 4);
+      arow_p[i] = A + (arow < m ? arow : m - 1) * lda;
+    }
     if (VEC && (int64_t)s * FBK + FBK <= k) {
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
@@ -703,7 +712,7 @@ __global__ __launch_bounds__(1024, 1) void fused_pub_kernel(
     }
     __builtin_amdgcn_sched_barrier(0);
     if (s + 1 < nstage) convert(nxt, xn);
-    if ((s & 1) && s + 1 < nstage) {
+    if ((s % 3) == 2 && s + 1 < nstage) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) accn[v] = reduce_pf(accn[v], fmn, pc.imn);
     }
