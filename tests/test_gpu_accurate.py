@@ -152,6 +152,18 @@ def test_accurate_fused_subtract_tz(set):
     assert_bits_equal(_dgemm(A, B, set, quant=oz.TZ), want, "C (TZ)")
 
 
+@pytest.mark.parametrize("set", [0, 1])
+def test_accurate_fused_edge_rows(set):
+    """Storage mode F at the accurate mode's shifts with zero, subnormal,
+    huge, tie, boundary and non-finite rows of A and columns of B."""
+    m, n, k = 1040, 24, 600
+    A = workloads.edge_rows(workloads.random_matrix(m, k, 1.0, 71), 72)
+    B = np.ascontiguousarray(workloads.edge_rows(workloads.random_matrix(n, k, 1.0, 73), 74).T)
+    log(f"accurate fused edge rows and columns, set={set}")
+    want = oracle.dgemm(A, B, set=set, accurate=True, want_planes=False).C
+    assert_bits_equal(_dgemm(A, B, set), want, "C")
+
+
 def test_accurate_k_zero_and_errors():
     import torch
     A = torch.zeros((4, 0), dtype=torch.float64, device="cuda")

@@ -5,7 +5,8 @@ of storing its planes.  Every output is compared with the oracle bit for bit
 the segments after which the sums are reduced (65536 k for the all-byte
 set's int32 sums, 16384 k for the published set's square digit sums), C -=
 AB, the truncating quantiser, rows and columns with non-finite values
-(native re-issue), and a wide exponent range."""
+(native re-issue), a wide exponent range, and zero, subnormal, huge and
+tie rows."""
 import numpy as np
 import pytest
 
@@ -79,6 +80,23 @@ def test_fused_long_k_segments(set):
     got = _run(A, B, set)[rows]
     want = oracle.dgemm(A, B, rows=rows, set=set, want_planes=False).C
     assert_bits_equal(got, want, "C (sampled rows)")
+
+
+@pytest.mark.parametrize("set", SETS)
+@pytest.mark.parametrize("quant", [pytest.param(oz.RN, id="RN"), pytest.param(oz.TZ, id="TZ")])
+def test_fused_edge_rows(set, quant):
+    """Zero, subnormal, huge, tie, boundary and non-finite rows of A and
+    columns of B, converted inside the product kernel with their own row
+    scales (k = 600: whole stages, then a partial one)."""
+    m, n, k = 1040, 24, 600
+    A = workloads.edge_rows(workloads.random_matrix(m, k, 1.0, 61), 62)
+    B = np.ascontiguousarray(workloads.edge_rows(workloads.random_matrix(n, k, 1.0, 63), 64).T)
+    log(f"fused set={set} edge rows and columns, quantiser {quant}")
+    want = oracle.dgemm(A, B, set=set, want_planes=False, quant=oracle.TZ if quant == oz.TZ else oracle.RN).C
+    got = _run(A, B, set, quant=quant)
+    assert_bits_equal(got, want, "C")
+    # row 3 of A and column 3 of B hold a NaN: re-issued natively
+    assert np.all(np.isnan(got[3])) and np.all(np.isnan(got[:, 3]))
 
 
 def test_fused_published_constant_vectors():

@@ -78,6 +78,31 @@ def random_matrix(rows: int, cols: int, s: float, seed: int) -> np.ndarray:
     return draw(np.random.default_rng(seed), rows, cols, s)
 
 
+def edge_rows(X: np.ndarray, seed: int) -> np.ndarray:
+    """Overwrite the first eleven rows of X (it needs at least eleven) with
+    edge cases: zeros, subnormals, a lone smallest subnormal, a NaN, an
+    infinity, huge values up to 1.7e308, small integers, one dominant entry,
+    values that tie once scaled, negative zeros, and values at the
+    normal/subnormal boundary.  Returns X."""
+    rng = np.random.default_rng(seed)
+    k = X.shape[1]
+    X[0] = 0.0
+    X[1] = rng.standard_normal(k) * 1e-310
+    X[2] = 0.0
+    X[2, k // 2] = 5e-324
+    X[3, 3 % k] = np.nan
+    X[4, 1 % k] = -np.inf
+    X[5] = rng.standard_normal(k) * 1e300
+    X[5, 0] = 1.7e308
+    X[6] = np.round(rng.standard_normal(k) * 1000)
+    X[7, 0] = 1e6
+    X[8] = (rng.integers(-64, 64, size=k) + 0.5) * 2.0 ** -50
+    X[8, 0] = 1.0
+    X[9] = -0.0
+    X[10] = rng.standard_normal(k) * 2.0 ** -1020
+    return X
+
+
 def boundary_values(M: int, P: int) -> list:
     """Integers in [-M/2, M/2) at or next to FP64 rounding boundaries at
     every magnitude from 2^54 up: powers of two and midpoints between
