@@ -50,6 +50,21 @@ def test_fused_matches_oracle(set, m, n, k, s, seed):
 
 
 @pytest.mark.parametrize("set", SETS)
+def test_fused_k_sweep(set):
+    """k around the points where the all-byte kernel's main loop (both
+    look-ahead stages whole) hands over to its guarded steps, and where the
+    last stage turns partial or lies past k: each multiple of 64 from 256
+    to 576 and its two neighbours."""
+    m, n = 1024, 3
+    ks = sorted({kk + d for kk in range(256, 577, 64) for d in (-1, 0, 1)})
+    for i, k in enumerate(ks):
+        A = workloads.random_matrix(m, k, 1.0, 300 + i)
+        B = workloads.random_matrix(k, n, 1.0, 400 + i)
+        log(f"fused set={set} k={k}")
+        assert_bits_equal(_run(A, B, set), oracle.dgemm(A, B, set=set, want_planes=False).C, f"C (k={k})")
+
+
+@pytest.mark.parametrize("set", SETS)
 def test_fused_subtract_tz_and_nonfinite(set):
     m, n, k = 1100, 90, 300
     A = workloads.random_matrix(m, k, 1.0, 11)
