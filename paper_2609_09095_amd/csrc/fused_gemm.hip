@@ -382,29 +382,31 @@ hipError_t launch_fused_g(int64_t m, int64_t n, int64_t k, int64_t kp, const dou
   return hipGetLastError();
 }
 
-// ---- published set (twelve moduli) on FP8 MFMA -----------------------------
+// ---- published set (twelve moduli) on FP8 and FP16 MFMA ---------------------
 // The same storage mode F for the published moduli, in six pairs: square g
-// (m = s^2) and nonsquare 6 + g.  Operand digits, every one an e4m3-exact
-// integer:
+// (m = s^2) and nonsquare 6 + g.  Operands, every one exact in its format:
 //  - square: the balanced base-s digits (d0, d1) of the centred residue x,
-//    x = d0 + s d1, |d0|, |d1| <= 16; mod s^2 the product is
+//    x = d0 + s d1, |d0|, |d1| <= 16, as e4m3; mod s^2 the product is
 //    d0 e0 + s (d0 e1 + d1 e0) (d1 e1 carries the factor s^2), summed in two
-//    FP32 accumulator sets (weights 1 and s);
-//  - nonsquare: balanced base-16 digits kept as (d0, 16 d1), |d0| <= 8,
-//    |16 d1| <= 256 (multiples of 16 up to 256 are e4m3-exact), so the four
-//    products of (d0 + 16 d1)(e0 + 16 e1) sum x y in one FP32 set.
-// Every partial sum is an integer kept below 2^24: per k the nonsquare digit
-// products add up to at most 264^2 in magnitude (|d0| + |16 d1| <= 264, at
-// x = 248), so that set is reduced every 3 stages (192 k: 13 381 632, plus
-// at most 256 left by the last reduction); the square sets (at most 256 and
-// 512 per k) every kSegS stages.  The outputs are the compact residues of the published
-// set's product path (the true ones times compact_scale(i)^-1 mod m_i,
-// |c| <= 0.51 m_i), so its reconstruction takes them as they stand.
-// B's digits come from fused_b_digits_kernel: [kp/128][24][n][128], planes
-// 2 g, 2 g + 1 for square g and 12 + 2 g, 13 + 2 g for nonsquare 6 + g.
+//    FP32 accumulator sets (weights 1 and s) on FP8 MFMA;
+//  - nonsquare (m <= 511): the centred residue itself, |x| <= 255, as fp16,
+//    one product x y per k on FP16 MFMA into one FP32 set.
+// Every partial sum is an integer kept below 2^24: per k the nonsquare
+// products reach 255^2, so that set is reduced every 4 stages (256 k:
+// 16 646 400, plus at most 256 left by the last reduction); the square sets
+// (at most 256 and 512 per k) every kSegS stages.  The outputs are the
+// compact residues of the published set's product path (the true ones times
+// compact_scale(i)^-1 mod m_i, |c| <= 0.51 m_i), so its reconstruction takes
+// them as they stand.  B's operands come from fused_b_digits_kernel in
+// [kp/128][24][n][128] bytes: planes 2 g, 2 g + 1 hold square g's digits
+// (the 128 k of the block, one byte each); planes 12 + 2 g + h hold
+// nonsquare 6 + g's residues for k 64 h .. 64 h + 63 of the block (fp16, in
+// k order).
 
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+typedef __fp16 h2x __attribute__((ext_vector_type(2)));
 
 constexpr int kPairs = 6;
 constexpr int kSegS = 256;  // stages between reductions of the square sets
@@ -464,11 +466,10 @@ __device__ __forceinline__ uint32_t e4m3x4(float a, float b, float c, float d) {
   return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(c, d, lo, true);
 }
 
-// Digits of four residues: square (base s; q = rint(x / s) by one FP32
+// Digits of four square residues (base s; q = rint(x / s) by one FP32
 // product, which never lands on the wrong side of a half integer: x / s is
 // either an exact tie -- s = 32, product exact -- or at least 1/(2s) from
-// one) and nonsquare (base 16, kept as d0 and 16 d1).  Each output dword
-// holds four bytes, the first value lowest.
+// one).  Each output dword holds four bytes, the first value lowest.
 __device__ __forceinline__ void square_digits(const int (&x)[4], float s, float is, uint32_t& w0,
                                               uint32_t& w1) {
   float d0[4], d1[4];
@@ -481,16 +482,12 @@ __device__ __forceinline__ void square_digits(const int (&x)[4], float s, float 
   w0 = e4m3x4(d0[0], d0[1], d0[2], d0[3]);
   w1 = e4m3x4(d1[0], d1[1], d1[2], d1[3]);
 }
-__device__ __forceinline__ void nonsquare_digits(const int (&x)[4], uint32_t& w0, uint32_t& w1) {
-  float d0[4], h[4];
-#pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    const float xf = (float)x[c];
-    h[c] = 16.0f * __builtin_rintf(xf * 0.0625f);
-    d0[c] = xf - h[c];
-  }
-  w0 = e4m3x4(d0[0], d0[1], d0[2], d0[3]);
-  w1 = e4m3x4(h[0], h[1], h[2], h[3]);
+// four nonsquare residues (|x| <= 255, exact in fp16) as fp16, the first in
+// the low half of the first dword
+__device__ __forceinline__ uint2 fp16x4(const int (&x)[4]) {
+  const h2x lo = __builtin_amdgcn_cvt_pkrtz((float)x[0], (float)x[1]);
+  const h2x hi = __builtin_amdgcn_cvt_pkrtz((float)x[2], (float)x[3]);
+  return uint2{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
 }
 
 __device__ __forceinline__ float reduce_pf(float x, float m, float minv) {
@@ -511,10 +508,25 @@ __device__ __forceinline__ v16f mma8(v8i a, v8i b, v16f c) {
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
 }
 
-// B's digits for the fused product: thread (lane, wave) of block
+// The fp16 slabs: 64 k (128 bytes) per row at a row stride of 144 bytes, so
+// that the rows read at one chunk by 16 lanes fall on distinct banks with
+// no swizzle, and a lane's four fragments sit at immediate offsets from one
+// address.  Fragment for the 16-k step ks of a stage: lane half fh takes
+// chunk 2 ks + fh of its row (the same on both operands, so the MFMA pairs
+// equal k).
+constexpr int kNS = 144;
+__device__ __forceinline__ v8h ffrag16(const int8_t* base, int r, int ks, int fh) {
+  return *reinterpret_cast<const v8h*>(base + r * kNS + (2 * ks + fh) * 16);
+}
+__device__ __forceinline__ v16f mma16(v8h a, v8h b, v16f c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+
+// B's operands for the fused product: thread (lane, wave) of block
 // (column block, 64-k group) takes column 64 cb + lane and the 16 k from
-// 64 kg + 16 wave; every plane gets one 16-byte store.  tau: the columns'
-// exponents (OZAKI25_EXP_NONFINITE: zero digits).
+// 64 kg + 16 wave; every square plane gets one 16-byte store, every
+// nonsquare residue slab two.  tau: the columns' exponents
+// (OZAKI25_EXP_NONFINITE: zeros).
 template <int MODE, bool TZ>
 __global__ __launch_bounds__(256) void fused_b_digits_kernel(int64_t n, int64_t k, int64_t kp,
                                                              const double* __restrict__ B, int64_t ldb,
@@ -536,11 +548,15 @@ __global__ __launch_bounds__(256) void fused_b_digits_kernel(int64_t n, int64_t 
     y[c] = TZ ? __builtin_trunc(v) : __builtin_rint(v);
     ylo[c] = MODE == 1 ? lo32(y[c] + kMagicF) : low32_split(y[c]);
   }
-  int8_t* out = digits + ((k0 / 128) * (2 * kR)) * n * 128 + j * 128 + (k0 % 128);
   const int64_t pstride = n * 128;
+  int8_t* out = digits + ((k0 / 128) * (2 * kR)) * pstride + j * 128 + (k0 % 128);
+  // nonsquare g: plane 12 + 2 g + (k0 % 128) / 64, fp16 at 2 (k0 % 64)
+  int8_t* outn = digits + ((k0 / 128) * (2 * kR) + 2 * kPairs + (k0 % 128) / 64) * pstride + j * 128 +
+                 2 * (k0 % 64);
   for (int g = 0; g < kPairs; ++g) {
     const PairConst pc = kPair[g];
-    uint32_t ws[2][4], wn[2][4];
+    uint32_t ws[2][4];
+    uint2 wn[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       int xs[4], xn[4];
@@ -550,30 +566,34 @@ __global__ __launch_bounds__(256) void fused_b_digits_kernel(int64_t n, int64_t 
         xn[c] = residue_pub<MODE>(y[4 * q + c], ylo[4 * q + c], pc.mn, pc.qn);
       }
       square_digits(xs, (float)pc.s, pc.is, ws[0][q], ws[1][q]);
-      nonsquare_digits(xn, wn[0][q], wn[1][q]);
+      wn[q] = fp16x4(xn);
     }
+    *reinterpret_cast<uint4*>(outn + 2 * g * pstride) = uint4{wn[0].x, wn[0].y, wn[1].x, wn[1].y};
+    *reinterpret_cast<uint4*>(outn + 2 * g * pstride + 16) = uint4{wn[2].x, wn[2].y, wn[3].x, wn[3].y};
 #pragma unroll
     for (int d = 0; d < 2; ++d) {
       *reinterpret_cast<uint4*>(out + (2 * g + d) * pstride) = uint4{ws[d][0], ws[d][1], ws[d][2], ws[d][3]};
-      *reinterpret_cast<uint4*>(out + (2 * kPairs + 2 * g + d) * pstride) =
-          uint4{wn[d][0], wn[d][1], wn[d][2], wn[d][3]};
     }
   }
 }
 
 // 128 rows of A per block and one pair of moduli; 16 wavefronts: wavefront
-// w converts rows 8 w .. 8 w + 7 of each 128 x 64 slab into the four digit
-// planes of the pair and owns the 32 x 32 outputs (w / 4, w % 4) of both
-// moduli.  The six blocks of a row strip go to one XCD back to back.
+// w converts rows 8 w .. 8 w + 7 of each 128 x 64 slab into the square
+// modulus's two digit planes and the nonsquare one's fp16 residues, and
+// owns the 32 x 32 outputs (w / 4, w % 4) of both moduli.  The six blocks
+// of a row strip go to one XCD back to back.
 // MODE: the residue route (1: |y| <= 2^51, ylo by 1.5 2^52; 3: |y| <= 2^58).
 template <int MODE, bool TZ, bool VEC>
 __global__ __launch_bounds__(1024, 1) void fused_pub_kernel(
     int64_t m, int64_t n, int64_t k, int64_t kp, const double* __restrict__ A, int64_t lda,
     const int32_t* __restrict__ sigma, const int8_t* __restrict__ pb, int16_t* __restrict__ cres,
     int64_t strips) {
-  // [buffer][plane][slab]: planes 0, 1 the square digits, 2, 3 the nonsquare ones
-  __shared__ __attribute__((aligned(1024))) int8_t lds_a[2][4][FBM * FBK];
-  __shared__ __attribute__((aligned(1024))) int8_t lds_b[2][4][FBN * FBK];
+  // [buffer][plane][slab]: the square digits; [buffer][slab]: the nonsquare
+  // fp16 residues, rows kNS bytes apart (136 KiB in all)
+  __shared__ __attribute__((aligned(1024))) int8_t lds_a[2][2][FBM * FBK];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_b[2][2][FBN * FBK];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_an[2][FBM * kNS];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_bn[2][FBN * kNS];
   const uint32_t b = blockIdx.x, o = b >> 3;
   const int64_t strip = (int64_t)(o / kPairs) * 8 + (b & 7);
   const int grp = (int)(o % kPairs);
@@ -589,7 +609,6 @@ __global__ __launch_bounds__(1024, 1) void fused_pub_kernel(
 
   // conversion: lane l takes 4 consecutive k (4 (l % 16) ..) of row
   // 8 wave + 4 i + l / 16, i = 0, 1
-  const int ck = 4 * (lane & 15);
   int sg[2];
   uint32_t keep[2];
 #pragma unroll
@@ -638,12 +657,15 @@ __global__ __launch_bounds__(1024, 1) void fused_pub_kernel(
         }
     }
   };
-  // one dword (4 digit bytes) per row and plane, at chunk ck / 16 of the
-  // row, swizzled
+  // per row one dword (4 digit bytes) into each square plane, at chunk
+  // ck / 16 of the row (swizzled), and 8 bytes (4 fp16) into the nonsquare
+  // slab, at byte 2 ck of the row
   auto convert = [&](int buf, const double (&x)[8]) {
+    // the lane's row and k offsets recomputed, as in load_a
+    const int l = lane_now(), cl = 4 * (l & 15);
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const int r = 8 * wave + 4 * i + (lane >> 4);
+      const int r = 8 * wave + 4 * i + (l >> 4);
       double y[4];
       uint32_t ylo[4];
 #pragma unroll
@@ -658,30 +680,43 @@ __global__ __launch_bounds__(1024, 1) void fused_pub_kernel(
         xs[c] = residue_pub<MODE>(y[c], ylo[c], pc.ms, pc.qs);
         xn[c] = residue_pub<MODE>(y[c], ylo[c], pc.mn, pc.qn);
       }
-      uint32_t w[4];
+      uint32_t w[2];
       square_digits(xs, fs, pc.is, w[0], w[1]);
-      nonsquare_digits(xn, w[2], w[3]);
-      const int at = r * FBK + (((ck >> 4) ^ fswz(r)) << 4) + (ck & 15);
+      const uint2 h = fp16x4(xn);
+      const int at = r * FBK + (((cl >> 4) ^ fswz(r)) << 4) + (cl & 15);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) *reinterpret_cast<uint32_t*>(&lds_a[buf][q][at]) = w[q] & keep[i];
+      for (int q = 0; q < 2; ++q) *reinterpret_cast<uint32_t*>(&lds_a[buf][q][at]) = w[q] & keep[i];
+      *reinterpret_cast<uint2*>(&lds_an[buf][r * kNS + 2 * cl]) = uint2{h.x & keep[i], h.y & keep[i]};
     }
   };
-  // B's four digit slabs of stage s (128 columns x 64 bytes each) by
-  // LDS-DMA, eight 1 KiB loads per slab spread over the wavefronts; columns
-  // past n read zero
+  // B's slabs of stage s by LDS-DMA, 1 KiB loads spread over the
+  // wavefronts (columns past n read zero): loads 0-15 the two square digit
+  // slabs (128 columns x 64 bytes, 16 columns a load), loads 16-33 the
+  // nonsquare fp16 slab (128 columns at the kNS stride: 1152 16-byte slots
+  // filled in order, slot 8 of each row, the padding, from past the end of
+  // the buffer, which reads zero)
   const int brecs = __builtin_amdgcn_readfirstlane((int)(n * 128));
   auto load_b = [&](int s, int buf) {
     const int64_t kb = s >> 1, h = s & 1;
-    for (int d = wave; d < 32; d += 16) {
-      const int q = d >> 3, dd = d & 7;
-      const int plane = q < 2 ? 2 * grp + q : 2 * kPairs + 2 * grp + (q - 2);
-      const int8_t* piece = uniform_ptr_f(pb + ((kb * (2 * kR) + plane) * n) * 128 + h * 64);
-      const __amdgpu_buffer_rsrc_t rs =
-          __builtin_amdgcn_make_buffer_rsrc((void*)piece, (short)0, brecs, 0x00020000);
-      const int row = 16 * dd + (lane >> 2);
-      const int gchunk = (lane & 3) ^ fswz(row);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_f)(&lds_b[buf][q][16 * dd * FBK]), 16,
-                                               row * 128 + gchunk * 16, 0, 0, 0);
+    for (int d = wave; d < 16 + FBN * kNS / 1024; d += 16) {
+      if (d < 16) {
+        const int q = d >> 3, dd = d & 7;
+        const int8_t* piece = uniform_ptr_f(pb + ((kb * (2 * kR) + 2 * grp + q) * n) * 128 + h * 64);
+        const __amdgpu_buffer_rsrc_t rs =
+            __builtin_amdgcn_make_buffer_rsrc((void*)piece, (short)0, brecs, 0x00020000);
+        const int row = 16 * dd + (lane >> 2);
+        const int gchunk = (lane & 3) ^ fswz(row);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_f)(&lds_b[buf][q][16 * dd * FBK]), 16,
+                                                 row * 128 + gchunk * 16, 0, 0, 0);
+      } else {
+        const int dd = d - 16;
+        const int8_t* piece = uniform_ptr_f(pb + ((kb * (2 * kR) + 2 * kPairs + 2 * grp + h) * n) * 128);
+        const __amdgpu_buffer_rsrc_t rs =
+            __builtin_amdgcn_make_buffer_rsrc((void*)piece, (short)0, brecs, 0x00020000);
+        const int slot = 64 * dd + lane, row = slot / 9, chunk = slot - 9 * row;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_f)(&lds_bn[buf][1024 * dd]), 16,
+                                                 chunk < 8 ? row * 128 + chunk * 16 : brecs, 0, 0, 0);
+      }
     }
   };
 
@@ -701,18 +736,14 @@ __global__ __launch_bounds__(1024, 1) void fused_pub_kernel(
       accs = mma8(a1, b0, accs);
     }
     __builtin_amdgcn_sched_barrier(0);
-    {
-      const v8i a0 = ffrag8(lds_a[cur][2], ar, fh), b0 = ffrag8(lds_b[cur][2], br, fh);
-      accn = mma8(a0, b0, accn);
-      const v8i b1 = ffrag8(lds_b[cur][3], br, fh);
-      accn = mma8(a0, b1, accn);
-      const v8i a1 = ffrag8(lds_a[cur][3], ar, fh);
-      accn = mma8(a1, b0, accn);
-      accn = mma8(a1, b1, accn);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      accn = mma16(ffrag16(lds_an[cur], ar, ks, fh), ffrag16(lds_bn[cur], br, ks, fh), accn);
+      __builtin_amdgcn_sched_barrier(0);  // one fragment pair live at a time
     }
     __builtin_amdgcn_sched_barrier(0);
     if (s + 1 < nstage) convert(nxt, xn);
-    if ((s % 3) == 2 && s + 1 < nstage) {
+    if ((s & 3) == 3 && s + 1 < nstage) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) accn[v] = reduce_pf(accn[v], fmn, pc.imn);
     }
