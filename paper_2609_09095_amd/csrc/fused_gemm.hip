@@ -89,9 +89,10 @@ __device__ __forceinline__ uint32_t residue_byte(double y, uint32_t ylo, int M, 
 }
 
 // LDS slabs: rows of 64 bytes (one stage), the 16-byte chunk index XOR-ed
-// with bits 1-2 of the row, so that the fragment reads of 8 consecutive rows
-// at one chunk hit 8 distinct 16-byte bank groups.
-__device__ __forceinline__ int fswz(int row) { return (row >> 1) & 3; }
+// with bits 1-2 of the row and then with bit 3, so that the fragment reads
+// at one chunk of 8 consecutive rows (128 bytes a cycle) and of 16 (256
+// bytes a cycle) hit distinct 16-byte bank groups.
+__device__ __forceinline__ int fswz(int row) { return ((row >> 1) & 3) ^ ((row >> 3) & 1); }
 
 // int8 fragment of a 32-row block for one 32-byte K step of a 64-byte stage:
 // lane half fh takes chunk 2 ks + fh of its row
