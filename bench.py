@@ -46,7 +46,7 @@ SETS = {
                 peak=FP8_PEAK_TOPS, dtype="fp8", moduli="published 12-modulus set",
                 route="e4m3 MFMA, fp32 accumulate", gemm_kernel="residue_gemm_kernel<int16>",
                 dec_kernel="deconstruct_kernel<0>+<1>",
-                fused_kernel="fused_pub_kernel", fused_products=42,
+                fused_kernel="fused_pub_kernel", fused_products=30,
                 note="fp8 ops (1 MAC = 2 ops): 36 limb products x 2mnk per launch; peak is the dense fp8 rate"),
     "a15": dict(id=1, oracle_set=1, r=15, products=15, plane_bytes=15, cres_bytes=15,
                 peak=INT8_PEAK_TOPS, dtype="int8", moduli="all-byte 15-modulus set (Sec. 5.1 candidate A)",
@@ -344,8 +344,9 @@ def gemm_roofline(w, cfg, rt, moduli):
          "traffic": None if fused(w) else measured_traffic(w, moduli), "ops_per_launch": rt["gemm_ops"],
          "note": cfg["note"]}
     if fused(w):
-        r["note"] = (f"storage mode F: {cfg['fused_products']} products x 2mnk per launch "
-                     "(the published set's digit products: 3 per square and 4 per nonsquare modulus); "
+        r["note"] = (f"storage mode F: {cfg['fused_products']} products x 2mnk per launch, in units of the "
+                     "peak's dtype (the published set: 3 e4m3 digit products per square modulus and one fp16 "
+                     "residue product per nonsquare one, counted twice as fp16 runs at half the fp8 rate); "
                      "the kernel is bound by converting A (VALU), not by the matrix cores")
     return r
 
