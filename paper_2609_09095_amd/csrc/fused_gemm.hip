@@ -393,9 +393,9 @@ hipError_t launch_fused_g(int64_t m, int64_t n, int64_t k, int64_t kp, const dou
 //  - nonsquare (m <= 511): the centred residue itself, |x| <= 255, as fp16,
 //    one product x y per k on FP16 MFMA into one FP32 set.
 // Every partial sum is an integer kept below 2^24: per k the nonsquare
-// products reach 255^2, so that set is reduced every 4 stages (256 k:
-// 16 646 400, plus at most 256 left by the last reduction); the square sets
-// (at most 256 and 512 per k) every kSegS stages.  The outputs are the
+// products reach 255^2, so that set is reduced every kSegN = 4 stages (256
+// k: 16 646 400, plus at most 256 left by the last reduction); the square
+// sets (at most 256 and 512 per k) every kSegS stages.  The outputs are the
 // compact residues of the published set's product path (the true ones times
 // compact_scale(i)^-1 mod m_i, |c| <= 0.51 m_i), so its reconstruction takes
 // them as they stand.  B's operands come from fused_b_digits_kernel in
@@ -411,6 +411,12 @@ typedef __fp16 h2x __attribute__((ext_vector_type(2)));
 
 constexpr int kPairs = 6;
 constexpr int kSegS = 256;  // stages between reductions of the square sets
+constexpr int kSegN = 4;    // stages between reductions of the nonsquare set
+// exact FP32 sums: the products' magnitudes summed over the stages between
+// reductions, plus the largest value a reduction leaves, stay below 2^24
+static_assert((int64_t)kSegS * FBK * 512 + 1089 < (1 << 24), "square sets exact between reductions");
+static_assert((int64_t)kSegN * FBK * 255 * 255 + 256 < (1 << 24), "nonsquare set exact between reductions");
+static_assert((kSegN & (kSegN - 1)) == 0, "the stage test masks");
 
 struct PairConst {
   int ms, s, mn;         // square modulus, its root, nonsquare modulus
@@ -744,7 +750,7 @@ __global__ __launch_bounds__(1024, 1) void fused_pub_kernel(
     }
     __builtin_amdgcn_sched_barrier(0);
     if (s + 1 < nstage) convert(nxt, xn);
-    if ((s & 3) == 3 && s + 1 < nstage) {
+    if ((s & (kSegN - 1)) == kSegN - 1 && s + 1 < nstage) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) accn[v] = reduce_pf(accn[v], fmn, pc.imn);
     }
