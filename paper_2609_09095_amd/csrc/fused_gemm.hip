@@ -26,6 +26,9 @@ typedef int v16i __attribute__((ext_vector_type(16)));
 constexpr int FBN = 128;   // columns of B (all of them)
 constexpr int FBK = 64;    // k per stage
 constexpr int kSegF = 1024;  // stages (65536 k) between reductions of the int32 sums
+// residue bytes in [-128, 127]: products up to 2^14 in magnitude; the sums of
+// kSegF stages, plus the largest value a reduction leaves, fit in int32
+static_assert((int64_t)kSegF * FBK * 128 * 128 + 128 < (int64_t)INT32_MAX, "int32 sums exact between reductions");
 
 __constant__ int kModF[kRA] = {kModulusA[0],  kModulusA[1],  kModulusA[2],  kModulusA[3],
                                kModulusA[4],  kModulusA[5],  kModulusA[6],  kModulusA[7],
