@@ -112,10 +112,11 @@ __device__ __forceinline__ const int8_t* uniform_ptr_f(const int8_t* p) {
 
 using lds_ptr_f = __attribute__((address_space(3))) void*;
 
-// The lane index, computed afresh where it is used. The all-byte kernel runs
-// at the register limit, and a lane offset held across its k loop is spilled;
-// its reload from scratch waits on the vector-memory counter and so drains
-// the look-ahead loads with it. A volatile asm is neither hoisted nor merged.
+// The lane index, computed afresh where it is used. Both fused kernels run
+// at the register limit, and a lane offset held across the k loop is
+// spilled; its reload from scratch waits on the vector-memory counter and
+// so drains the look-ahead loads with it. A volatile asm is neither hoisted
+// nor merged.
 __device__ __forceinline__ int lane_now() {
   int l;
   asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
