@@ -336,9 +336,27 @@ def dec_roofline(w, cfg, rt, moduli, scan_ms, dec_ms):
             **measured_deconstruction(w, moduli, scan_ms, dec_ms)}
 
 
+def gemm_kernel_name(w, cfg):
+    """The residue GEMM kernel the library launches for this shape: the
+    published set's int16 product takes its persistent form (one block per
+    CU walking tiles) at short k, an even count of at most 16 K stages of
+    128, with at least two output tiles per CU (512 x 128 tiles for n <= 128,
+    256 x 256 otherwise, per modulus)."""
+    if cfg["dtype"] != "fp8":
+        return cfg["gemm_kernel"]
+    import torch
+    nstage = -(-w.k // 128)
+    bm, bn = (512, 128) if w.n <= 128 else (256, 256)
+    tiles = cfg["r"] * -(-w.m // bm) * -(-w.n // bn)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count // 8 * 8
+    if 2 <= nstage <= 16 and nstage % 2 == 0 and cus >= 8 and tiles >= 2 * cus:
+        return "residue_gemm_persistent_kernel<int16>"
+    return cfg["gemm_kernel"]
+
+
 def gemm_roofline(w, cfg, rt, moduli):
     unit = "TFLOP/s" if cfg["dtype"] == "fp8" else "TOP/s"
-    r = {"bound": "mfma", "kernel": cfg["fused_kernel"] if fused(w) else cfg["gemm_kernel"],
+    r = {"bound": "mfma", "kernel": cfg["fused_kernel"] if fused(w) else gemm_kernel_name(w, cfg),
          "achieved": round(rt["gemm_tops"], 2), "peak": cfg["peak"], "unit": unit,
          "frac": round(rt["gemm_tops"] / cfg["peak"], 4),
          "traffic": None if fused(w) else measured_traffic(w, moduli), "ops_per_launch": rt["gemm_ops"],

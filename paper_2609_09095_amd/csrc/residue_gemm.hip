@@ -519,6 +519,154 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_kernel(int64_t m, int64_
                            });
 }
 
+// The lane index from a volatile asm: values derived from it inside a loop
+// are neither hoisted out of it nor kept live across it.
+__device__ __forceinline__ int lane_id_now() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
+// Persistent form (one block per CU, no split-k, an even number of stages
+// per tile): a block takes virtual blocks blockIdx.x, + gridDim.x, ... in the
+// order above (gridDim.x a multiple of 8 keeps each on its XCD).  The look-
+// ahead of a tile's last stage is the next tile's first stage, so its loads
+// are in flight while the tile's residues are formed and stored, and the
+// block skips the launch and first-load latency of a fresh block per tile.
+// The next tile's first barrier waits for every load and store (loads and
+// stores share one counter, and their relative completion order is not
+// relied on).  Only the compact int16 output takes this form.
+template <typename OT, int S>
+__global__ __launch_bounds__(1024, 1) void residue_gemm_persistent_kernel(
+    int64_t m, int64_t n, int64_t kp, const int8_t* __restrict__ pa, const int8_t* __restrict__ pb,
+    OT* __restrict__ cres, int group, uint32_t nvirt) {
+  constexpr int BM = Tile<S>::BM, BN = Tile<S>::BN, NB = Tile<S>::BB, WC = Tile<S>::WC;
+  static_assert(sizeof(OT) == 2, "the compact int16 residue output");
+  __shared__ __attribute__((aligned(1024))) int8_t lds_a0[BM * BK];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_b0[BN * BK];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_a1[BM * BK];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_b1[BN * BK];
+  const int64_t tiles_m = (m + BM - 1) / BM, tiles_n = (n + BN - 1) / BN;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wr = wave / WC, wc = wave % WC;
+  const int fr = lane & 31, fh = lane >> 5;
+  const int ra0 = wr * 64 + fr, rb0 = wc * 32 * NB + fr;
+  int voffa[Tile<S>::ADMA], voffb[Tile<S>::BDMA];
+  slab_offsets(wave, lane, voffa);
+  slab_offsets(wave, lane, voffb);
+
+  const int nstage = (int)(kp / BK);
+  const int nseg = (nstage + kSeg - 1) / kSeg;
+  const int total = 3 * nstage;  // even (the host checks)
+  const int64_t step_a = (int64_t)kPlanes * m * BK, step_b = (int64_t)kPlanes * n * BK;
+  auto rsrc = [](const int8_t* p, int nrec) __attribute__((always_inline)) {
+    return __builtin_amdgcn_make_buffer_rsrc((void*)uniform_ptr(p), (short)0, nrec, 0x00020000);
+  };
+  // a tile: modulus, tile row and column, and the bytes its panels hold
+  // (rows past the matrix edge read as zero)
+  struct TileAt {
+    int mod;
+    int64_t tm, tn;
+    int na, nb;
+  };
+  auto tile_at = [&](uint32_t v) __attribute__((always_inline)) {
+    TileAt t;
+    block_coords(v, (uint32_t)tiles_m, (uint32_t)tiles_n, (uint32_t)group, t.mod, t.tm, t.tn);
+    const int64_t rows_a = m - t.tm * BM < BM ? m - t.tm * BM : BM;
+    const int64_t rows_b = n - t.tn * BN < BN ? n - t.tn * BN : BN;
+    t.na = __builtin_amdgcn_readfirstlane((int)(rows_a * BK));
+    t.nb = __builtin_amdgcn_readfirstlane((int)(rows_b * BK));
+    return t;
+  };
+  auto first_a = [&](const TileAt& t, int p) __attribute__((always_inline)) {
+    return pa + ((int64_t)kSched[t.mod].plane_a[p] * m + t.tm * BM) * BK;
+  };
+  auto first_b = [&](const TileAt& t, int p) __attribute__((always_inline)) {
+    return pb + ((int64_t)kSched[t.mod].plane_b[p] * n + t.tn * BN) * BK;
+  };
+
+  uint32_t v = blockIdx.x;
+  if (v >= nvirt) return;
+  TileAt cur = tile_at(v), nxt = cur;
+  bool have_next = false, ahead = false;
+  // look-ahead cursor: product lp, stage ls of the current tile (or, once
+  // ahead, the next tile's first stage), its pieces and their tile's bytes
+  int lp = 0, ls = 0, lna = cur.na, lnb = cur.nb;
+  const int8_t* la = first_a(cur, 0);
+  const int8_t* lb = first_b(cur, 0);
+  auto advance = [&]() __attribute__((always_inline)) {
+    if (ahead) return;
+    if (ls + 1 < nstage) {
+      ++ls;
+      la += step_a;
+      lb += step_b;
+    } else if (lp < 2) {
+      ++lp;
+      ls = 0;
+      la = first_a(cur, lp);
+      lb = first_b(cur, lp);
+    } else if (have_next) {
+      ahead = true;
+      la = first_a(nxt, 0);
+      lb = first_b(nxt, 0);
+      lna = nxt.na;
+      lnb = nxt.nb;
+    }
+  };
+  stage_load<S>(rsrc(la, lna), rsrc(lb, lnb), lds_a0, lds_b0, voffa, voffb, wave);
+  for (;;) {
+    const uint32_t vn = v + gridDim.x;
+    have_next = vn < nvirt;
+    if (have_next) nxt = tile_at(vn);
+    advance();
+    const ModSched sc = kSched[cur.mod];
+    const float fm = (float)sc.m, finv = sc.inv;
+    v16f acc[2][NB];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int b = 0; b < NB; ++b) acc[a][b] = v16f{};
+    int cp = 0, cs = 0;
+    auto carry_step = [&]() __attribute__((always_inline)) {
+      carry<NB, false>(acc, cp, cs, nstage, nseg, cur.mod, fm, finv);
+      if (++cs == nstage) {
+        cs = 0;
+        ++cp;
+      }
+    };
+    for (int G = 0; G < total; G += 2) {
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      stage_mma_dma<S>(lds_a0, lds_b0, ra0, rb0, fh, acc, rsrc(la, lna), rsrc(lb, lnb), lds_a1, lds_b1,
+                        voffa, voffb, wave);
+      advance();
+      carry_step();
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      stage_mma_dma<S>(lds_a1, lds_b1, ra0, rb0, fh, acc, rsrc(la, lna), rsrc(lb, lnb), lds_a0, lds_b0,
+                        voffa, voffb, wave);
+      advance();
+      carry_step();
+    }
+    OT* out = (OT*)uniform_ptr((const int8_t*)(cres + (int64_t)cur.mod * m * n + cur.tm * BM * n +
+                                               cur.tn * BN));
+    const int rows_left = (int)(m - cur.tm * BM), cols_left = (int)(n - cur.tn * BN);
+    // the store offsets from a lane index read here: derived from the
+    // loop-invariant one they would be hoisted and held across the stages
+    const int el = lane_id_now() & 63;
+    store_tile<true, OT, S>(out, (int)n, rows_left, cols_left, wr, wc, el & 31, el >> 5,
+                             [&](int a, int b, int vv) { return (int)acc[a][b][vv]; });
+    if (!have_next) break;
+    v = vn;
+    cur = nxt;
+    lp = 0;
+    ls = 0;
+    ahead = false;
+  }
+  __builtin_amdgcn_s_waitcnt(0);  // the last look-ahead (a repeat) lands before the block ends
+}
+
 // ---- all-byte set (Sec. 5.1, candidate A) on int8 MFMA --------------------
 // The planes hold the centred residues themselves (|r| <= 128), so a modulus
 // is ONE int8 product, accumulated in int32 by v_mfma_i32_32x32x32_i8:
@@ -840,6 +988,27 @@ hipError_t launch_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* pa, const
   // block indices (and block_coords' arithmetic) are 32-bit
   if (blocks * splits > (int64_t)UINT32_MAX) return hipErrorInvalidValue;
   const dim3 grid((unsigned)(blocks * splits));
+  if constexpr (!BYTES && sizeof(OT) == 2) {
+    // the persistent form for short k, where a tile's first-stage load and
+    // its stores are a larger share of its time: one block per CU (a
+    // multiple of 8, so a block keeps its XCD), at least two tiles each,
+    // whole k, a nonzero even stage count (measured on the 32768^2 x 1024
+    // update: 34.7 -> 34.0 ms; no change on 8192^3, which keeps the grid
+    // of one block per tile)
+    int dev = 0, cus = 0;
+    if (splits == 1 && nstage >= 2 && nstage <= 16 && nstage % 2 == 0 && hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        cus >= 8 && blocks >= 2 * (int64_t)(cus / 8 * 8)) {
+      const dim3 pgrid((unsigned)(cus / 8 * 8));
+      if (shape == 3)
+        hipLaunchKernelGGL((residue_gemm_persistent_kernel<OT, 3>), pgrid, dim3(1024), 0, stream, m, n, kp,
+                           pa, pb, dst, group, (uint32_t)blocks);
+      else
+        hipLaunchKernelGGL((residue_gemm_persistent_kernel<OT, 2>), pgrid, dim3(1024), 0, stream, m, n, kp,
+                           pa, pb, dst, group, (uint32_t)blocks);
+      return hipGetLastError();
+    }
+  }
   if constexpr (BYTES) {
     if (shape == 3)
       hipLaunchKernelGGL((residue_gemm_bytes_kernel<OT, 3>), grid, dim3(1024), 0, stream, m, n, kp, pa,
