@@ -994,11 +994,11 @@ hipError_t launch_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* pa, const
     // multiple of 8, so a block keeps its XCD), at least two tiles each,
     // whole k, a nonzero even stage count (measured on the 32768^2 x 1024
     // update: 34.7 -> 34.0 ms; no change on 8192^3, which keeps the grid
-    // of one block per tile)
+    // of one block per tile); the tile ids plus one grid stay below 2^32
     int dev = 0, cus = 0;
     if (splits == 1 && nstage >= 2 && nstage <= 16 && nstage % 2 == 0 && hipGetDevice(&dev) == hipSuccess &&
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-        cus >= 8 && blocks >= 2 * (int64_t)(cus / 8 * 8)) {
+        cus >= 8 && blocks >= 2 * (int64_t)(cus / 8 * 8) && blocks <= (int64_t)UINT32_MAX - cus) {
       const dim3 pgrid((unsigned)(cus / 8 * 8));
       if (shape == 3)
         hipLaunchKernelGGL((residue_gemm_persistent_kernel<OT, 3>), pgrid, dim3(1024), 0, stream, m, n, kp,
