@@ -634,38 +634,46 @@ __global__ __launch_bounds__(1024, 1) void fused_pub_kernel(
   }
 
   const int nstage = (int)(kp / FBK);
+  // whole stages (VEC) read the strip's rows through one buffer resource:
+  // 32-bit byte offsets from its first row, 24-bit products (the host takes
+  // this path for lda < 2^21 only, so 128 rows stay below 2^31 bytes), rows
+  // past m read as zero
+  const int lda8 = (int)(lda * 8);
+  const int arec = VEC ? (int)((m - row0 < FBM ? m - row0 : FBM) * lda8) : 0;
+  const __amdgpu_buffer_rsrc_t ars = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)uniform_ptr_f((const int8_t*)(A + row0 * lda)), (short)0, arec, 0x00020000);
   double x0[8], x1[8];
   auto load_a = [&](int s, double (&x)[8]) {
-    // the lane's k offset and row pointers recomputed here, not held
-    // across the loop (the kernel is at the register limit, and a spilled
-    // copy would be reloaded from scratch at the start of every stage)
+    // the lane's offsets recomputed here, not held across the loop (the
+    // kernel is at the register limit, and a spilled copy would be
+    // reloaded from scratch at the start of every stage)
     const int l = lane_now();
-    const int64_t k0 = (int64_t)s * FBK + 4 * (l & 15);
-    const double* arow_p[2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int64_t arow = row0 + 8 * wave + 4 * i + (l >> 4);
-      arow_p[i] = A + (arow < m ? arow : m - 1) * lda;
-    }
     if (VEC && (int64_t)s * FBK + FBK <= k) {
+      const int kb = (s * FBK + 4 * (l & 15)) * 8;
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
-        const double2 p = *reinterpret_cast<const double2*>(arow_p[i] + k0);
-        const double2 q = *reinterpret_cast<const double2*>(arow_p[i] + k0 + 2);
+        const int off = __mul24(8 * wave + 4 * i + (l >> 4), lda8) + kb;
+        const double2 p = __builtin_bit_cast(double2, __builtin_amdgcn_raw_buffer_load_b128(ars, off, 0, 0));
+        const double2 q =
+            __builtin_bit_cast(double2, __builtin_amdgcn_raw_buffer_load_b128(ars, off + 16, 0, 0));
         x[4 * i] = p.x;
         x[4 * i + 1] = p.y;
         x[4 * i + 2] = q.x;
         x[4 * i + 3] = q.y;
       }
     } else {
+      const int64_t k0 = (int64_t)s * FBK + 4 * (l & 15);
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < 2; ++i) {
+        const int64_t arow = row0 + 8 * wave + 4 * i + (l >> 4);
+        const double* arow_p = A + (arow < m ? arow : m - 1) * lda;
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
           const int64_t kk = k0 + c < k ? k0 + c : k - 1;
-          const double v = arow_p[i][kk];
+          const double v = arow_p[kk];
           x[4 * i + c] = k0 + c < k ? v : 0.0;
         }
+      }
     }
   };
   // per row one dword (4 digit bytes) into each square plane, at chunk
@@ -812,7 +820,7 @@ hipError_t launch_fused_pub_m(int64_t m, int64_t n, int64_t k, int64_t kp, const
   const int64_t strips = (m + FBM - 1) / FBM;
   const int64_t blocks = (strips + 7) / 8 * 8 * kPairs;
   if (blocks > (int64_t)UINT32_MAX) return hipErrorInvalidValue;
-  if ((((uintptr_t)A) & 15) == 0 && (lda & 1) == 0)
+  if ((((uintptr_t)A) & 15) == 0 && (lda & 1) == 0 && lda < (1 << 21))
     hipLaunchKernelGGL((fused_pub_kernel<MODE, TZ, true>), dim3((unsigned)blocks), dim3(1024), 0, stream, m, n,
                        k, kp, A, lda, sigma, pb, cres, strips);
   else
