@@ -45,12 +45,14 @@ SETS = {
     "s12": dict(id=0, oracle_set=0, r=12, products=36, plane_bytes=30, cres_bytes=24,
                 peak=FP8_PEAK_TOPS, dtype="fp8", moduli="published 12-modulus set",
                 route="e4m3 MFMA, fp32 accumulate", gemm_kernel="residue_gemm_kernel<int16>",
+                persistent_kernel="residue_gemm_persistent_kernel<int16>",
                 dec_kernel="deconstruct_kernel<0>+<1>",
                 fused_kernel="fused_pub_kernel", fused_products=30,
                 note="fp8 ops (1 MAC = 2 ops): 36 limb products x 2mnk per launch; peak is the dense fp8 rate"),
     "a15": dict(id=1, oracle_set=1, r=15, products=15, plane_bytes=15, cres_bytes=15,
                 peak=INT8_PEAK_TOPS, dtype="int8", moduli="all-byte 15-modulus set (Sec. 5.1 candidate A)",
                 route="int8 MFMA, int32 accumulate", gemm_kernel="residue_gemm_bytes_kernel<int8>",
+                persistent_kernel="residue_gemm_bytes_persistent_kernel<int8>",
                 dec_kernel="deconstruct_bytes_kernel<0>+<1>",
                 fused_kernel="fused_bytes_kernel", fused_products=15,
                 note="int8 ops (1 MAC = 2 ops): 15 residue products x 2mnk per launch; peak is the dense int8 rate"),
@@ -338,19 +340,17 @@ def dec_roofline(w, cfg, rt, moduli, scan_ms, dec_ms):
 
 def gemm_kernel_name(w, cfg):
     """The residue GEMM kernel the library launches for this shape: the
-    published set's int16 product takes its persistent form (one block per
+    compact product of either set takes its persistent form (one block per
     CU walking tiles) at short k, an even count of at most 16 K stages of
     128, with at least two output tiles per CU (512 x 128 tiles for n <= 128,
     256 x 256 otherwise, per modulus)."""
-    if cfg["dtype"] != "fp8":
-        return cfg["gemm_kernel"]
     import torch
     nstage = -(-w.k // 128)
     bm, bn = (512, 128) if w.n <= 128 else (256, 256)
     tiles = cfg["r"] * -(-w.m // bm) * -(-w.n // bn)
     cus = torch.cuda.get_device_properties(0).multi_processor_count // 8 * 8
     if 2 <= nstage <= 16 and nstage % 2 == 0 and cus >= 8 and tiles >= 2 * cus:
-        return "residue_gemm_persistent_kernel<int16>"
+        return cfg["persistent_kernel"]
     return cfg["gemm_kernel"]
 
 

@@ -967,6 +967,120 @@ constexpr int64_t gemm_blocks(bool bytes, int64_t m, int64_t n) {
   return (int64_t)(bytes ? kRA : kR) * ((m + bm - 1) / bm) * ((n + bn - 1) / bn);
 }
 
+// Persistent form of the int8 product for short k (the compact int8
+// output, one segment: at most 16 stages, an even count), as the FP8 one:
+// one block per CU walking virtual tiles blockIdx.x + j gridDim.x, the next
+// tile's first stage loaded during the current one's last stage and its
+// stores, every barrier a full wait.
+template <typename OT, int S>
+__global__ __launch_bounds__(1024, 1) void residue_gemm_bytes_persistent_kernel(
+    int64_t m, int64_t n, int64_t kp, const int8_t* __restrict__ pa, const int8_t* __restrict__ pb,
+    OT* __restrict__ cres, int group, uint32_t nvirt) {
+  constexpr int BM = Tile<S>::BM, BN = Tile<S>::BN, NB = Tile<S>::BB, WC = Tile<S>::WC;
+  static_assert(sizeof(OT) == 1, "the compact int8 residue output");
+  __shared__ __attribute__((aligned(1024))) int8_t lds_a0[BM * BK];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_b0[BN * BK];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_a1[BM * BK];
+  __shared__ __attribute__((aligned(1024))) int8_t lds_b1[BN * BK];
+  const int64_t tiles_m = (m + BM - 1) / BM, tiles_n = (n + BN - 1) / BN;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wr = wave / WC, wc = wave % WC;
+  const int fr = lane & 31, fh = lane >> 5;
+  const int ra0 = wr * 64 + fr, rb0 = wc * 32 * NB + fr;
+  int voffa[Tile<S>::ADMA], voffb[Tile<S>::BDMA];
+  slab_offsets(wave, lane, voffa);
+  slab_offsets(wave, lane, voffb);
+
+  const int nstage = (int)(kp / BK);  // even, at most 16 (the host checks)
+  const int64_t step_a = (int64_t)kRA * m * BK, step_b = (int64_t)kRA * n * BK;
+  auto rsrc = [](const int8_t* p, int nrec) __attribute__((always_inline)) {
+    return __builtin_amdgcn_make_buffer_rsrc((void*)uniform_ptr(p), (short)0, nrec, 0x00020000);
+  };
+  struct TileAt {
+    int mod;
+    int64_t tm, tn;
+    int na, nb;
+  };
+  auto tile_at = [&](uint32_t v) __attribute__((always_inline)) {
+    TileAt t;
+    block_coords(v, (uint32_t)tiles_m, (uint32_t)tiles_n, (uint32_t)group, t.mod, t.tm, t.tn);
+    const int64_t rows_a = m - t.tm * BM < BM ? m - t.tm * BM : BM;
+    const int64_t rows_b = n - t.tn * BN < BN ? n - t.tn * BN : BN;
+    t.na = __builtin_amdgcn_readfirstlane((int)(rows_a * BK));
+    t.nb = __builtin_amdgcn_readfirstlane((int)(rows_b * BK));
+    return t;
+  };
+  auto first_a = [&](const TileAt& t) __attribute__((always_inline)) {
+    return pa + ((int64_t)t.mod * m + t.tm * BM) * BK;
+  };
+  auto first_b = [&](const TileAt& t) __attribute__((always_inline)) {
+    return pb + ((int64_t)t.mod * n + t.tn * BN) * BK;
+  };
+
+  uint32_t v = blockIdx.x;
+  if (v >= nvirt) return;
+  TileAt cur = tile_at(v), nxt = cur;
+  bool have_next = false, ahead = false;
+  // look-ahead cursor: stage ls of the current tile (or, once ahead, the
+  // next tile's first stage), its pieces and their tile's bytes
+  int ls = 0, lna = cur.na, lnb = cur.nb;
+  const int8_t* la = first_a(cur);
+  const int8_t* lb = first_b(cur);
+  auto advance = [&]() __attribute__((always_inline)) {
+    if (ahead) return;
+    if (ls + 1 < nstage) {
+      ++ls;
+      la += step_a;
+      lb += step_b;
+    } else if (have_next) {
+      ahead = true;
+      la = first_a(nxt);
+      lb = first_b(nxt);
+      lna = nxt.na;
+      lnb = nxt.nb;
+    }
+  };
+  stage_load<S>(rsrc(la, lna), rsrc(lb, lnb), lds_a0, lds_b0, voffa, voffb, wave);
+  for (;;) {
+    const uint32_t vn = v + gridDim.x;
+    have_next = vn < nvirt;
+    if (have_next) nxt = tile_at(vn);
+    advance();
+    v16i acc[2][NB];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int b = 0; b < NB; ++b) acc[a][b] = v16i{};
+    for (int G = 0; G < nstage; G += 2) {
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      stage_mma_dma_i8<S>(lds_a0, lds_b0, ra0, rb0, fh, acc, rsrc(la, lna), rsrc(lb, lnb), lds_a1, lds_b1,
+                           voffa, voffb, wave);
+      advance();
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      stage_mma_dma_i8<S>(lds_a1, lds_b1, ra0, rb0, fh, acc, rsrc(la, lna), rsrc(lb, lnb), lds_a0, lds_b0,
+                           voffa, voffb, wave);
+      advance();
+    }
+    const int mm = kModA[cur.mod];
+    const double minv = kInvA[cur.mod];
+    OT* out = (OT*)uniform_ptr((const int8_t*)(cres + (int64_t)cur.mod * m * n + cur.tm * BM * n +
+                                               cur.tn * BN));
+    // the store offsets from a lane index read here (as in the FP8 form)
+    const int el = lane_id_now() & 63;
+    store_tile<false, OT, S>(out, (int)n, (int)(m - cur.tm * BM), (int)(n - cur.tn * BN), wr, wc, el & 31,
+                              el >> 5, [&](int a, int b, int vv) { return cmod_i32<false>(acc[a][b][vv], mm, minv); });
+    if (!have_next) break;
+    v = vn;
+    cur = nxt;
+    ls = 0;
+    ahead = false;
+  }
+  __builtin_amdgcn_s_waitcnt(0);  // the last look-ahead (a repeat) lands before the block ends
+}
+
 template <bool BYTES, typename OT>
 hipError_t launch_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* pa, const int8_t* pb,
                        OT* cres, OT* part, int splits, hipStream_t stream) {
@@ -988,24 +1102,34 @@ hipError_t launch_gemm(int64_t m, int64_t n, int64_t kp, const int8_t* pa, const
   // block indices (and block_coords' arithmetic) are 32-bit
   if (blocks * splits > (int64_t)UINT32_MAX) return hipErrorInvalidValue;
   const dim3 grid((unsigned)(blocks * splits));
-  if constexpr (!BYTES && sizeof(OT) == 2) {
+  if constexpr (sizeof(OT) < 4) {
     // the persistent form for short k, where a tile's first-stage load and
     // its stores are a larger share of its time: one block per CU (a
     // multiple of 8, so a block keeps its XCD), at least two tiles each,
     // whole k, a nonzero even stage count (measured on the 32768^2 x 1024
-    // update: 34.7 -> 34.0 ms; no change on 8192^3, which keeps the grid
-    // of one block per tile); the tile ids plus one grid stay below 2^32
+    // update: FP8 34.7 -> 34.0 ms, int8 19.8 -> 17.9 ms; no change on
+    // 8192^3, which keeps the grid of one block per tile); the tile ids
+    // plus one grid stay below 2^32
     int dev = 0, cus = 0;
     if (splits == 1 && nstage >= 2 && nstage <= 16 && nstage % 2 == 0 && hipGetDevice(&dev) == hipSuccess &&
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
         cus >= 8 && blocks >= 2 * (int64_t)(cus / 8 * 8) && blocks <= (int64_t)UINT32_MAX - cus) {
       const dim3 pgrid((unsigned)(cus / 8 * 8));
-      if (shape == 3)
-        hipLaunchKernelGGL((residue_gemm_persistent_kernel<OT, 3>), pgrid, dim3(1024), 0, stream, m, n, kp,
-                           pa, pb, dst, group, (uint32_t)blocks);
-      else
-        hipLaunchKernelGGL((residue_gemm_persistent_kernel<OT, 2>), pgrid, dim3(1024), 0, stream, m, n, kp,
-                           pa, pb, dst, group, (uint32_t)blocks);
+      if constexpr (BYTES) {
+        if (shape == 3)
+          hipLaunchKernelGGL((residue_gemm_bytes_persistent_kernel<OT, 3>), pgrid, dim3(1024), 0, stream, m,
+                             n, kp, pa, pb, dst, group, (uint32_t)blocks);
+        else
+          hipLaunchKernelGGL((residue_gemm_bytes_persistent_kernel<OT, 2>), pgrid, dim3(1024), 0, stream, m,
+                             n, kp, pa, pb, dst, group, (uint32_t)blocks);
+      } else {
+        if (shape == 3)
+          hipLaunchKernelGGL((residue_gemm_persistent_kernel<OT, 3>), pgrid, dim3(1024), 0, stream, m, n,
+                             kp, pa, pb, dst, group, (uint32_t)blocks);
+        else
+          hipLaunchKernelGGL((residue_gemm_persistent_kernel<OT, 2>), pgrid, dim3(1024), 0, stream, m, n,
+                             kp, pa, pb, dst, group, (uint32_t)blocks);
+      }
       return hipGetLastError();
     }
   }
