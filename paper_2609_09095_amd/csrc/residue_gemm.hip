@@ -628,8 +628,10 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_persistent_kernel(
 #pragma unroll
       for (int b = 0; b < NB; ++b) acc[a][b] = v16f{};
     int cp = 0, cs = 0;
+    // every carry but the tile's last, which the store epilogue applies as
+    // a bare reduction (the final weight is 1 for compact outputs)
     auto carry_step = [&]() __attribute__((always_inline)) {
-      carry<NB, false>(acc, cp, cs, nstage, nseg, cur.mod, fm, finv);
+      if (cp < 2 || cs + 1 < nstage) carry<NB, false>(acc, cp, cs, nstage, nseg, cur.mod, fm, finv);
       if (++cs == nstage) {
         cs = 0;
         ++cp;
@@ -656,7 +658,7 @@ __global__ __launch_bounds__(1024, 1) void residue_gemm_persistent_kernel(
     // loop-invariant one they would be hoisted and held across the stages
     const int el = lane_id_now() & 63;
     store_tile<true, OT, S>(out, (int)n, rows_left, cols_left, wr, wc, el & 31, el >> 5,
-                             [&](int a, int b, int vv) { return (int)acc[a][b][vv]; });
+                             [&](int a, int b, int vv) { return (int)reduce_f(acc[a][b][vv], fm, finv); });
     if (!have_next) break;
     v = vn;
     cur = nxt;
