@@ -57,3 +57,21 @@ def test_multitile(c, set):
     want = oracle.dgemm(A, B, C_in=C0, rows=rows, cols=cols, set=set, accurate=c["accurate"],
                         want_planes=False, quant=oracle.TZ if c["tz"] else oracle.RN).C
     assert_bits_equal(got, want, "C (sampled)")
+
+
+@pytest.mark.parametrize("set", SETS)
+def test_stored_planes_tall_narrow(set):
+    """Storage mode P at most 128 columns wide (the 512 x 128 tile shape) at
+    short k: 43 tile rows x 12 or 15 moduli, again over two tiles per CU."""
+    import torch
+    m, n, k = 22000, 100, 256
+    log(f"[multitile] mode P set={set} m={m} n={n} k={k}")
+    A = workloads.random_matrix(m, k, 1.0, 8200)
+    B = workloads.random_matrix(k, n, 1.0, 8201)
+    planesA, expsA = oz.ozaki25_deconstruct(0, to_dev(A), set=set)
+    planesB, expsB = oz.ozaki25_deconstruct(1, to_dev(B), set=set)
+    C = oz.ozaki25_dgemm_planes(k, planesA, expsA, planesB, expsB, set=set)
+    torch.cuda.synchronize()
+    rows = sample_indices(m, 128, 8202)
+    want = oracle.dgemm(A, B, rows=rows, set=set, want_planes=False).C
+    assert_bits_equal(C.cpu().numpy()[rows], want, "C (sampled rows)")
