@@ -1,5 +1,6 @@
 """bench.py's command line on a machine without a GPU: more than one GPU is
-refused with a message, and the per-set constants describe the kernels."""
+refused with a message, the per-set constants describe the kernels, and the
+roofline names the kernel the library launches for each workload."""
 import os
 import subprocess
 import sys
@@ -54,3 +55,24 @@ def test_committed_counters_are_plausible():
     if stale:
         import pytest
         pytest.skip(f"counter summaries taken on older kernel sources: {stale}")
+
+
+def test_gemm_kernel_names(monkeypatch):
+    """The kernel named in the roofline object follows the library's rule:
+    the persistent forms at an even count of 2-16 K stages with at least two
+    tiles per CU (256 CUs here), the grid of one block per tile otherwise."""
+    import types
+
+    import torch
+    sys.path.insert(0, ROOT)
+    import bench
+    import workloads
+    monkeypatch.setattr(torch.cuda, "get_device_properties",
+                        lambda i: types.SimpleNamespace(multi_processor_count=256))
+    s12, a15 = bench.SETS["s12"], bench.SETS["a15"]
+    W = workloads.WORKLOADS
+    assert bench.gemm_kernel_name(W["hpl"], s12) == "residue_gemm_persistent_kernel<int16>"
+    assert bench.gemm_kernel_name(W["hpl"], a15) == "residue_gemm_bytes_persistent_kernel<int8>"
+    for name in ("square", "ragged", "reach", "tiny"):
+        assert bench.gemm_kernel_name(W[name], s12) == "residue_gemm_kernel<int16>", name
+        assert bench.gemm_kernel_name(W[name], a15) == "residue_gemm_bytes_kernel<int8>", name
